@@ -16,8 +16,9 @@ Field layout (sign, exponent, mantissa) and special values:
 Encoding (a reading; the paper does not spell out rounding): a binary32 value
 ``v`` is rounded to the nearest representable value with ties to the code
 whose mantissa is even; magnitudes at or above the largest finite value
-(including infinities) saturate to +-FMAX; NaN maps to 0x7F with the input's
-sign bit; the sign of zero is kept.
+(including infinities) saturate to +-FMAX; every NaN maps to the one code 0x7F
+(IEEE 754 leaves the sign of a NaN produced by arithmetic unspecified, so the
+sign of a NaN carries no information); the sign of zero is kept.
 """
 
 import functools
@@ -112,7 +113,7 @@ def _round_to_grid(a, fmt):
 
 
 def encode(v, fmt):
-    """binary32 array -> uint8 FP8 codes (RNE, saturating, NaN -> 0x7F|sign)."""
+    """binary32 array -> uint8 FP8 codes (RNE, saturating, NaN -> 0x7F)."""
     v = np.asarray(v, dtype=np.float32)
     bits = v.view(np.uint32)
     sign = ((bits >> 31) & 1).astype(np.uint8) << 7
@@ -126,7 +127,8 @@ def encode(v, fmt):
     out[sat] = _V2C[fmt][fm]
     r = _round_to_grid(a[reg], fmt)
     out[reg] = _lookup(r, fmt)
-    return out | sign
+    out[~isnan] |= sign[~isnan]
+    return out
 
 
 def _lookup(r, fmt):

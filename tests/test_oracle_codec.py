@@ -68,7 +68,7 @@ def test_every_finite_code_round_trips(fmt):
     back = fp8.encode(vals.astype(np.float32), fmt)
     for c, v, b in zip(codes, vals, back):
         if np.isnan(v):
-            assert b & 0x7F == 0x7F              # a NaN code (sign of the NaN value aside)
+            assert b == 0x7F                     # the canonical NaN code
         elif np.isinf(v):
             assert b == (0x7B | (c & 0x80))     # E5M2 infinities saturate
         else:
@@ -103,12 +103,10 @@ def test_saturation():
     assert list(q) == [0x7B] * 4
 
 
-def test_nan_keeps_sign():
-    nan = np.float32(np.nan)
-    neg = np.array([0xFFC00000], np.uint32).view(np.float32)[0]
+def test_every_nan_maps_to_the_canonical_code():
+    pats = np.array([0x7FC00000, 0xFFC00000, 0x7F800001, 0xFFBFFFFF], np.uint32)
     for fmt in FMTS:
-        assert fp8.encode(np.array([nan], np.float32), fmt)[0] == 0x7F
-        assert fp8.encode(np.array([neg], np.float32), fmt)[0] == 0xFF
+        assert list(fp8.encode(pats.view(np.float32), fmt)) == [0x7F] * 4
 
 
 def test_underflow_and_signed_zero():
@@ -122,7 +120,7 @@ def test_underflow_and_signed_zero():
 
 def _brute_force_encode(v, fmt):
     """Nearest finite code by scanning the whole table; ties -> even mantissa;
-    |v| >= FMAX saturates; NaN -> 0x7F|sign."""
+    |v| >= FMAX saturates; NaN -> 0x7F."""
     t = fp8.decode_table(fmt)
     pos_codes = np.array([c for c in range(128) if np.isfinite(t[c])])
     pos_vals = t[pos_codes]
@@ -142,8 +140,9 @@ def _brute_force_encode(v, fmt):
     pick = np.where((cand & even).any(axis=1), np.argmax(cand & even, axis=1), np.argmax(cand, axis=1))
     out[reg] = pos_codes[pick]
     out[sat] = pos_codes[np.argmax(pos_vals)]
+    out |= sign
     out[nan] = 0x7F
-    return out | sign
+    return out
 
 
 @pytest.mark.parametrize("fmt", FMTS)
