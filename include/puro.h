@@ -1,0 +1,208 @@
+/*
+ * puro.h -- C ABI of the MI355X (gfx950) FP8 linear-layer library (libpuro.so).
+ *
+ * The operations are those of an FP8 linear layer as the paper states it
+ * (Section 3.2, "FP8 Mixed-Precision Training"; Appendix C, "FP8
+ * implementation pipeline" and the precision-flow figure): BF16 inputs and
+ * weights are quantised to FP8 immediately before each GEMM, with scales
+ * computed online from the data; Fprop (Y = X W^T), Dgrad (dX = dY W) and
+ * Wgrad (dW = dY^T X) run on FP8 operands; Y and dX are written in BF16 and
+ * dW accumulates in FP32; the quantised input is kept for Wgrad.
+ *
+ * Conventions for every entry point:
+ *  - All tensor pointers are DEVICE pointers owned by the caller. The library
+ *    never allocates, frees or synchronises; scratch memory is a caller
+ *    workspace (`ws`, `ws_bytes`) sized by the matching *_workspace_size().
+ *  - BF16 tensors are passed as their uint16_t bit patterns, FP8 tensors as
+ *    uint8_t codes (OCP E4M3 "E4M3FN" or E5M2), scales as float.
+ *  - Matrices are row-major; `ld` is the row pitch in elements.
+ *  - Arguments are validated on the host before anything is enqueued; an
+ *    error status means nothing was launched. On success the work is
+ *    enqueued on `stream` and the call returns without waiting.
+ *  - Results are deterministic: the same inputs give the same bytes.
+ *  - Calls on one stream are ordered; calls that share a workspace must not
+ *    run concurrently on different streams.
+ *
+ * Encoding (readings of the paper, which fixes the formats but not the
+ * rounding): a value x is encoded as FP8(fl32(x * r)) with round-to-nearest-
+ * even, saturation of finite and infinite magnitudes above the format's
+ * largest value (448 for E4M3, 57344 for E5M2) and every NaN mapped to 0x7F.
+ * Per-tensor scales: s = fl32(amax / FMAX), r = fl32(FMAX / amax) (s = r = 1
+ * when amax = 0). Power-of-two scales: s = 2^e, r = 2^-e with e the smallest
+ * integer such that amax <= FMAX * 2^e, clamped to [-127, 127] (e = 0 for
+ * amax = 0). The stored scale is always the dequantisation scale s.
+ */
+#ifndef PURO_H
+#define PURO_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    PURO_OK = 0,
+    PURO_ERR_NULL = 1,        /* a required pointer is NULL                              */
+    PURO_ERR_SHAPE = 2,       /* negative size, ld smaller than the row, mismatched dims */
+    PURO_ERR_UNSUPPORTED = 3, /* format / mode / rounding combination not provided       */
+    PURO_ERR_ALIGN = 4,       /* size or pointer not a multiple the kernels need         */
+    PURO_ERR_WORKSPACE = 5,   /* ws_bytes below the matching *_workspace_size()          */
+    PURO_ERR_HIP = 6          /* a kernel launch reported an error                       */
+} puro_status;
+
+typedef enum { PURO_E4M3 = 0, PURO_E5M2 = 1 } puro_fp8_format;
+
+/* Scale granularity (Section 3.2: one scale per tensor, or groups of 128
+ * consecutive values along a GEMM's reduction dimension for activations and
+ * gradients, and 128x128 blocks for weights). */
+typedef enum {
+    PURO_SCALE_TENSOR = 0,        /* one scale                                          */
+    PURO_SCALE_ROW_1x128 = 1,     /* one scale per row per 128 consecutive columns      */
+    PURO_SCALE_COL_128x1 = 2,     /* one scale per column per 128 consecutive rows      */
+    PURO_SCALE_BLOCK_128x128 = 3  /* one scale per 128x128 block                        */
+} puro_scale_mode;
+
+/* Scale value rule. Section 3.2: block scales are powers of two (the
+ * exponent-only E8M0 representation of MXFP8). */
+typedef enum {
+    PURO_SCALE_FP32 = 0, /* s = amax / FMAX in binary32 (per-tensor mode only) */
+    PURO_SCALE_POW2 = 1  /* s = 2^e, the smallest power of two that avoids saturation */
+} puro_scale_rounding;
+
+typedef enum { PURO_OUT_BF16 = 0, PURO_OUT_FP32 = 1 } puro_out_dtype;
+
+/* Static text for a status code (never NULL). */
+const char* puro_status_string(puro_status status);
+
+/* ---------------------------------------------------------------- amax ---
+ * amax = max |x| over the [rows, cols] BF16 tensor x (row pitch ld), written
+ * as one float to the device scalar `amax`. NaN if any element is NaN; 0 for
+ * an empty tensor; -0 counts as 0. Section 3.2 computes scales online from
+ * the data; this is the per-tensor statistic they come from.
+ * Requirements: cols % 8 == 0, ld % 8 == 0, x 16-byte aligned (rows of whole
+ * 16-byte vectors). ws: puro_amax_workspace_size(rows, cols) bytes. */
+size_t puro_amax_workspace_size(int64_t rows, int64_t cols);
+puro_status puro_amax(const uint16_t* x, int64_t rows, int64_t cols, int64_t ld,
+                      float* amax, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------ quantise ---
+ * Quantise the [rows, cols] BF16 tensor x (row pitch ld) to FP8 `fmt`.
+ * Section 3.2: activations and activation gradients in 1x128 groups along the
+ * reduction dimension, weights in 128x128 blocks, or one scale per tensor.
+ *
+ *  mode TENSOR: q [rows, cols] and/or qT [cols, rows] (the same codes,
+ *      transposed); scale[0] = s. rnd FP32 or POW2. If amax_in is not NULL
+ *      the device scalar *amax_in is used instead of the tensor's own amax
+ *      (values beyond it saturate).
+ *  mode ROW_1x128: q [rows, cols], scale [rows, cols/128]. If qT is not NULL
+ *      the same read also writes the column-grouped copy: qT [cols, rows]
+ *      with scaleT [cols, rows/128] (128x1 groups down each column, as
+ *      Wgrad needs; quantised from the BF16 values, not from q).
+ *  mode COL_128x1: only qT [cols, rows] and scaleT [cols, rows/128].
+ *  mode BLOCK_128x128: q [rows, cols] with scale [rows/128, cols/128], and
+ *      if qT is not NULL also qT [cols, rows] with scaleT [cols/128, rows/128]
+ *      (the same codes and scales, transposed).
+ *  Grouped modes require rnd == POW2 and amax_in == NULL.
+ *
+ * Requirements: cols % 16 == 0 and ld % 8 == 0 with x 16-byte aligned;
+ * rows % 16 == 0 when qT is written; the grouped dimension(s) % 128 == 0.
+ * Outputs are dense (row pitch = their column count). ws:
+ * puro_quantize_workspace_size(rows, cols) bytes (used in TENSOR mode). */
+size_t puro_quantize_workspace_size(int64_t rows, int64_t cols);
+puro_status puro_quantize_fp8(const uint16_t* x, int64_t rows, int64_t cols, int64_t ld,
+                              puro_fp8_format fmt, puro_scale_mode mode, puro_scale_rounding rnd,
+                              const float* amax_in, uint8_t* q, float* scale,
+                              uint8_t* qT, float* scaleT, void* ws, size_t ws_bytes,
+                              hipStream_t stream);
+
+/* ---------------------------------------------------------------- GEMM ---
+ * D[m, n] = sum_k A[m, k] * B[n, k] with FP32 accumulation (Section 3.2:
+ * the Fprop, Dgrad and Wgrad GEMMs of a linear layer run on FP8 operands).
+ * Both operands are stored with the reduction index k contiguous: A is
+ * [M, K] with row pitch A->ld bytes, B is [N, K] with row pitch B->ld bytes.
+ * Fprop is A = Xq, B = Wq; Dgrad A = dYq, B = WqT; Wgrad A = dYqT, B = XqT.
+ *
+ * Operand scales (device memory, float):
+ *   TENSOR:          scale[0]
+ *   ROW_1x128:       scale[row * (K/128) + k/128]          ([rows, K/128])
+ *   BLOCK_128x128:   scale[(row/128) * (K/128) + k/128]    ([ceil(rows/128), K/128])
+ * Grouped scales must be powers of two in [2^-127, 2^127] (as written by
+ * puro_quantize_fp8 with POW2); they are applied exactly inside the MFMA.
+ * Per-tensor scales are applied once, in FP32, to the accumulated sum.
+ *
+ * D is BF16 (round-to-nearest-even) or FP32, row pitch ldd elements. With
+ * accumulate != 0, D += result (the old value is read in D's type and the sum
+ * formed in FP32). Requirements: K % 16 == 0 (K % 128 == 0 with grouped
+ * scales), lda and ldb multiples of 16, operand pointers 16-byte aligned,
+ * ldd >= N. ws: puro_fp8_gemm_workspace_size(M, N, K, d_type) bytes. */
+typedef struct {
+    const uint8_t* data;
+    int64_t ld;
+    puro_fp8_format fmt;
+    puro_scale_mode mode;   /* TENSOR, ROW_1x128 or BLOCK_128x128 */
+    const float* scale;
+} puro_fp8_operand;
+
+size_t puro_fp8_gemm_workspace_size(int64_t M, int64_t N, int64_t K, puro_out_dtype d_type);
+puro_status puro_fp8_gemm(int64_t M, int64_t N, int64_t K,
+                          const puro_fp8_operand* A, const puro_fp8_operand* B,
+                          void* D, puro_out_dtype d_type, int64_t ldd, int accumulate,
+                          void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* -------------------------------------------------------- linear layer ---
+ * Y = X W^T with X [M, K] and W [N, K] in BF16 (dense rows), and its backward
+ * pass, as a sequence of the calls above (Section 3.2; Appendix C).
+ *
+ * Recipe: blockwise = 0 -> one scale per tensor (rule `rnd`); blockwise = 1
+ * -> X and dY in 1x128 groups along each GEMM's reduction dimension (row
+ * groups for Fprop and Dgrad, column groups for Wgrad), W in 128x128 blocks,
+ * power-of-two scales (`rnd` ignored). */
+typedef struct {
+    puro_fp8_format x_fmt, w_fmt, dy_fmt;
+    int blockwise;
+    puro_scale_rounding rnd;
+} puro_linear_recipe;
+
+/* What the forward pass keeps for the backward pass (caller-allocated):
+ * the quantised input, transposed for Wgrad (Section 3.2 keeps the quantised
+ * input for Wgrad), and the quantised weight, transposed for Dgrad.
+ *   xq_t    [K, M] FP8;  x_scale: per-tensor [1], blockwise [K, M/128]
+ *   wq_t    [K, N] FP8;  w_scale: per-tensor [1], blockwise [K/128, N/128]  */
+typedef struct {
+    uint8_t* xq_t;
+    float* x_scale;
+    uint8_t* wq_t;
+    float* w_scale;
+} puro_linear_saved;
+
+/* Byte sizes of the four saved buffers (sizes[0..3] in the struct's order);
+ * returns their sum. */
+size_t puro_linear_saved_bytes(int64_t M, int64_t N, int64_t K, const puro_linear_recipe* recipe,
+                               size_t sizes[4]);
+size_t puro_linear_fwd_workspace_size(int64_t M, int64_t N, int64_t K, const puro_linear_recipe* recipe);
+size_t puro_linear_bwd_workspace_size(int64_t M, int64_t N, int64_t K, const puro_linear_recipe* recipe);
+
+/* Forward: quantise X and W, Y [M, N] (BF16) = Fprop, fill `saved`.
+ * Requirements: M, N, K multiples of 16 (of 128 when blockwise). */
+puro_status puro_linear_fwd(const uint16_t* X, const uint16_t* W, int64_t M, int64_t N, int64_t K,
+                            const puro_linear_recipe* recipe, uint16_t* Y,
+                            const puro_linear_saved* saved, void* ws, size_t ws_bytes,
+                            hipStream_t stream);
+
+/* Backward: quantise dY [M, N]; dX [M, K] (BF16) = Dgrad and dW [N, K] (FP32)
+ * = Wgrad (dW += when accumulate_dW != 0). dX or dW may be NULL to skip that
+ * GEMM. */
+puro_status puro_linear_bwd(const uint16_t* dY, const puro_linear_saved* saved,
+                            int64_t M, int64_t N, int64_t K, const puro_linear_recipe* recipe,
+                            uint16_t* dX, float* dW, int accumulate_dW,
+                            void* ws, size_t ws_bytes, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PURO_H */

@@ -1,0 +1,384 @@
+// C ABI of libpuro: argument validation, workspace layout and kernel launches.
+// Declarations and their documentation: include/puro.h.
+
+#include "puro.h"
+
+#include <hip/hip_runtime.h>
+
+#include "kernels.h"
+
+using namespace puro;
+
+namespace {
+
+constexpr int64_t kGroup = 128;
+constexpr size_t kAlign = 256;
+
+inline size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+inline bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+inline bool fmt_ok(puro_fp8_format f) { return f == PURO_E4M3 || f == PURO_E5M2; }
+
+puro_status launched() {
+    return hipGetLastError() == hipSuccess ? PURO_OK : PURO_ERR_HIP;
+}
+
+// Byte offsets of named regions carved from a caller workspace.
+struct Carver {
+    size_t used = 0;
+    size_t take(size_t bytes) {
+        const size_t at = used;
+        used = align_up(used + bytes);
+        return at;
+    }
+};
+
+size_t amax_ws(int64_t rows, int64_t cols) {
+    return (size_t)amax_num_partials(rows, cols) * sizeof(uint32_t);
+}
+
+puro_status check_bf16_matrix(const uint16_t* x, int64_t rows, int64_t cols, int64_t ld) {
+    if (rows < 0 || cols < 0 || ld < cols) return PURO_ERR_SHAPE;
+    if (rows > 0 && cols > 0 && !x) return PURO_ERR_NULL;
+    if ((cols % 8) != 0 || (ld % 8) != 0 || !aligned16(x)) return PURO_ERR_ALIGN;
+    if (rows > (int64_t)65535 * kGroup || cols > ((int64_t)1 << 31)) return PURO_ERR_SHAPE;
+    return PURO_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* puro_status_string(puro_status s) {
+    switch (s) {
+    case PURO_OK: return "ok";
+    case PURO_ERR_NULL: return "a required pointer is NULL";
+    case PURO_ERR_SHAPE: return "invalid or mismatched sizes";
+    case PURO_ERR_UNSUPPORTED: return "unsupported format, scale mode or rounding combination";
+    case PURO_ERR_ALIGN: return "size or pointer alignment not supported";
+    case PURO_ERR_WORKSPACE: return "workspace too small";
+    case PURO_ERR_HIP: return "HIP kernel launch failed";
+    }
+    return "unknown status";
+}
+
+// ------------------------------------------------------------------- amax
+size_t puro_amax_workspace_size(int64_t rows, int64_t cols) {
+    return amax_ws(rows, cols);
+}
+
+puro_status puro_amax(const uint16_t* x, int64_t rows, int64_t cols, int64_t ld, float* amax,
+                      void* ws, size_t ws_bytes, hipStream_t stream) {
+    puro_status st = check_bf16_matrix(x, rows, cols, ld);
+    if (st != PURO_OK) return st;
+    if (!amax) return PURO_ERR_NULL;
+    const int P = amax_num_partials(rows, cols);
+    if (P > 0 && !ws) return PURO_ERR_NULL;
+    if (ws_bytes < (size_t)P * sizeof(uint32_t)) return PURO_ERR_WORKSPACE;
+    uint32_t* partial = reinterpret_cast<uint32_t*>(ws);
+    if (P > 0) launch_amax_partials(x, rows, cols, ld, partial, P, stream);
+    launch_amax_finalize(partial, P, amax, stream);
+    return launched();
+}
+
+// --------------------------------------------------------------- quantise
+size_t puro_quantize_workspace_size(int64_t rows, int64_t cols) {
+    return amax_ws(rows, cols);
+}
+
+puro_status puro_quantize_fp8(const uint16_t* x, int64_t rows, int64_t cols, int64_t ld,
+                              puro_fp8_format fmt, puro_scale_mode mode, puro_scale_rounding rnd,
+                              const float* amax_in, uint8_t* q, float* scale, uint8_t* qT,
+                              float* scaleT, void* ws, size_t ws_bytes, hipStream_t stream) {
+    puro_status st = check_bf16_matrix(x, rows, cols, ld);
+    if (st != PURO_OK) return st;
+    if (!fmt_ok(fmt) || (rnd != PURO_SCALE_FP32 && rnd != PURO_SCALE_POW2)) return PURO_ERR_UNSUPPORTED;
+    if ((cols % 16) != 0) return PURO_ERR_ALIGN;
+    QuantArgs a{};
+    a.x = x; a.rows = rows; a.cols = cols; a.ld = ld;
+    a.q = q; a.scale = scale; a.qT = qT; a.scaleT = scaleT;
+    a.amax_in = amax_in;
+    a.pow2 = rnd == PURO_SCALE_POW2;
+    // outputs of an empty tensor are never written (torch hands out NULL for them)
+    const bool empty = rows == 0 || cols == 0;
+    int qmode;
+    switch (mode) {
+    case PURO_SCALE_TENSOR:
+        if (!empty && !q && !qT) return PURO_ERR_NULL;
+        if (!scale) return PURO_ERR_NULL;
+        if (qT && (rows % 16) != 0) return PURO_ERR_ALIGN;
+        qmode = kQTensor;
+        break;
+    case PURO_SCALE_ROW_1x128:
+        if (!empty && (!q || !scale || (qT && !scaleT))) return PURO_ERR_NULL;
+        if (rnd != PURO_SCALE_POW2 || amax_in) return PURO_ERR_UNSUPPORTED;
+        if ((cols % kGroup) != 0 || (qT && (rows % kGroup) != 0)) return PURO_ERR_ALIGN;
+        qmode = kQRow;
+        break;
+    case PURO_SCALE_COL_128x1:
+        if (!empty && (!qT || !scaleT)) return PURO_ERR_NULL;
+        if (rnd != PURO_SCALE_POW2 || amax_in) return PURO_ERR_UNSUPPORTED;
+        if ((rows % kGroup) != 0) return PURO_ERR_ALIGN;
+        a.q = nullptr; a.scale = nullptr;
+        qmode = kQCol;
+        break;
+    case PURO_SCALE_BLOCK_128x128:
+        if (!empty && (!q || !scale || (qT && !scaleT))) return PURO_ERR_NULL;
+        if (rnd != PURO_SCALE_POW2 || amax_in) return PURO_ERR_UNSUPPORTED;
+        if ((rows % kGroup) != 0 || (cols % kGroup) != 0) return PURO_ERR_ALIGN;
+        qmode = kQBlock;
+        break;
+    default:
+        return PURO_ERR_UNSUPPORTED;
+    }
+    if (qmode == kQTensor && !amax_in) {
+        const int P = amax_num_partials(rows, cols);
+        if (P > 0 && !ws) return PURO_ERR_NULL;
+        if (ws_bytes < (size_t)P * sizeof(uint32_t)) return PURO_ERR_WORKSPACE;
+        a.partial = reinterpret_cast<const uint32_t*>(ws);
+        a.npartial = P;
+        if (P > 0) launch_amax_partials(x, rows, cols, ld, reinterpret_cast<uint32_t*>(ws), P, stream);
+    }
+    // an empty tensor has no groups; its per-tensor scale (amax 0) is 1 and is
+    // written by the single block the launcher uses for it
+    if ((rows == 0 || cols == 0) && qmode != kQTensor) return PURO_OK;
+    launch_quantize(fmt, qmode, a, stream);
+    return launched();
+}
+
+// ------------------------------------------------------------------- GEMM
+size_t puro_fp8_gemm_workspace_size(int64_t M, int64_t N, int64_t K, puro_out_dtype d_type) {
+    if (M <= 0 || N <= 0 || K <= 0) return 0;
+    return gemm_workspace_bytes(M, N, K, d_type == PURO_OUT_FP32 ? kOutF32 : kOutBF16);
+}
+
+static puro_status check_operand(const puro_fp8_operand* o, int64_t rows, int64_t K, int* smode) {
+    if (!o) return PURO_ERR_NULL;
+    // the scale is read whenever the operand has rows (also for K == 0, where
+    // the result is a scaled empty sum); the data only when there is a k
+    if (rows > 0 && (!o->scale || (K > 0 && !o->data))) return PURO_ERR_NULL;
+    if (!fmt_ok(o->fmt)) return PURO_ERR_UNSUPPORTED;
+    if (o->ld < K) return PURO_ERR_SHAPE;
+    if ((o->ld % 16) != 0 || !aligned16(o->data)) return PURO_ERR_ALIGN;
+    // buffer offsets within one tile of 256 rows stay below 2^31
+    if (o->ld > ((int64_t)1 << 22)) return PURO_ERR_SHAPE;
+    switch (o->mode) {
+    case PURO_SCALE_TENSOR: *smode = kSTensor; break;
+    case PURO_SCALE_ROW_1x128: *smode = kSRow; break;
+    case PURO_SCALE_BLOCK_128x128: *smode = kSBlock; break;
+    default: return PURO_ERR_UNSUPPORTED;
+    }
+    if (*smode != kSTensor && (K % kGroup) != 0) return PURO_ERR_ALIGN;
+    return PURO_OK;
+}
+
+puro_status puro_fp8_gemm(int64_t M, int64_t N, int64_t K, const puro_fp8_operand* A,
+                          const puro_fp8_operand* B, void* D, puro_out_dtype d_type, int64_t ldd,
+                          int accumulate, void* ws, size_t ws_bytes, hipStream_t stream) {
+    if (M < 0 || N < 0 || K < 0) return PURO_ERR_SHAPE;
+    if (M > INT32_MAX / 2 || N > INT32_MAX / 2 || K > INT32_MAX / 2) return PURO_ERR_SHAPE;
+    int sa = 0, sb = 0;
+    puro_status st = check_operand(A, M, K, &sa);
+    if (st != PURO_OK) return st;
+    st = check_operand(B, N, K, &sb);
+    if (st != PURO_OK) return st;
+    if (d_type != PURO_OUT_BF16 && d_type != PURO_OUT_FP32) return PURO_ERR_UNSUPPORTED;
+    if ((K % 16) != 0) return PURO_ERR_ALIGN;
+    if (ldd < N) return PURO_ERR_SHAPE;
+    if (M == 0 || N == 0) return PURO_OK;
+    if (!D) return PURO_ERR_NULL;
+    if ((ldd % 4) != 0 || !aligned16(D)) return PURO_ERR_ALIGN;
+    const int out = d_type == PURO_OUT_FP32 ? kOutF32 : kOutBF16;
+    const size_t need = gemm_workspace_bytes(M, N, K, out);
+    if (need > 0 && !ws) return PURO_ERR_NULL;
+    if (ws_bytes < need) return PURO_ERR_WORKSPACE;
+    GemmProblem g{};
+    g.M = M; g.N = N; g.K = K;
+    g.A = A->data; g.lda = A->ld; g.fa = A->fmt; g.sa_mode = sa; g.sa = A->scale;
+    g.B = B->data; g.ldb = B->ld; g.fb = B->fmt; g.sb_mode = sb; g.sb = B->scale;
+    g.D = D; g.ldd = ldd; g.out = out; g.accumulate = accumulate != 0;
+    launch_gemm(g, ws, stream);
+    return launched();
+}
+
+// ----------------------------------------------------------- linear layer
+namespace {
+
+bool recipe_ok(const puro_linear_recipe* r) {
+    return r && fmt_ok(r->x_fmt) && fmt_ok(r->w_fmt) && fmt_ok(r->dy_fmt) &&
+           (r->blockwise == 0 || r->blockwise == 1) &&
+           (r->rnd == PURO_SCALE_FP32 || r->rnd == PURO_SCALE_POW2);
+}
+
+puro_status check_linear_dims(int64_t M, int64_t N, int64_t K, const puro_linear_recipe* r) {
+    if (!recipe_ok(r)) return PURO_ERR_UNSUPPORTED;
+    if (M < 0 || N < 0 || K < 0) return PURO_ERR_SHAPE;
+    const int64_t g = r->blockwise ? kGroup : 16;
+    if ((M % g) != 0 || (N % g) != 0 || (K % g) != 0) return PURO_ERR_ALIGN;
+    return PURO_OK;
+}
+
+struct FwdLayout {
+    size_t xq, wq, xs_row, w_blk, part_x, part_w, gemm, total;
+};
+
+FwdLayout fwd_layout(int64_t M, int64_t N, int64_t K, const puro_linear_recipe* r) {
+    Carver c;
+    FwdLayout l{};
+    l.xq = c.take((size_t)M * K);
+    l.wq = c.take((size_t)N * K);
+    if (r->blockwise) {
+        l.xs_row = c.take((size_t)M * (K / kGroup) * sizeof(float));
+        l.w_blk = c.take((size_t)(N / kGroup) * (K / kGroup) * sizeof(float));
+    } else {
+        l.part_x = c.take(amax_ws(M, K));
+        l.part_w = c.take(amax_ws(N, K));
+    }
+    l.gemm = c.take(gemm_workspace_bytes(M, N, K, kOutBF16));
+    l.total = c.used;
+    return l;
+}
+
+struct BwdLayout {
+    size_t dyq, dyq_t, dy_scale, dy_scale_t, part, gemm, total;
+};
+
+BwdLayout bwd_layout(int64_t M, int64_t N, int64_t K, const puro_linear_recipe* r) {
+    Carver c;
+    BwdLayout l{};
+    l.dyq = c.take((size_t)M * N);
+    l.dyq_t = c.take((size_t)N * M);
+    if (r->blockwise) {
+        l.dy_scale = c.take((size_t)M * (N / kGroup) * sizeof(float));
+        l.dy_scale_t = c.take((size_t)N * (M / kGroup) * sizeof(float));
+    } else {
+        l.dy_scale = c.take(sizeof(float));
+        l.part = c.take(amax_ws(M, N));
+    }
+    const size_t g1 = gemm_workspace_bytes(M, K, N, kOutBF16);
+    const size_t g2 = gemm_workspace_bytes(N, K, M, kOutF32);
+    l.gemm = c.take(g1 > g2 ? g1 : g2);
+    l.total = c.used;
+    return l;
+}
+
+}  // namespace
+
+size_t puro_linear_saved_bytes(int64_t M, int64_t N, int64_t K, const puro_linear_recipe* r,
+                               size_t sizes[4]) {
+    size_t s[4] = {0, 0, 0, 0};
+    if (recipe_ok(r) && M >= 0 && N >= 0 && K >= 0) {
+        s[0] = (size_t)K * M;
+        s[1] = r->blockwise ? (size_t)K * (M / kGroup) * sizeof(float) : sizeof(float);
+        s[2] = (size_t)K * N;
+        s[3] = r->blockwise ? (size_t)(K / kGroup) * (N / kGroup) * sizeof(float) : sizeof(float);
+    }
+    if (sizes)
+        for (int i = 0; i < 4; ++i) sizes[i] = s[i];
+    return s[0] + s[1] + s[2] + s[3];
+}
+
+size_t puro_linear_fwd_workspace_size(int64_t M, int64_t N, int64_t K, const puro_linear_recipe* r) {
+    if (check_linear_dims(M, N, K, r) != PURO_OK) return 0;
+    return fwd_layout(M, N, K, r).total;
+}
+
+size_t puro_linear_bwd_workspace_size(int64_t M, int64_t N, int64_t K, const puro_linear_recipe* r) {
+    if (check_linear_dims(M, N, K, r) != PURO_OK) return 0;
+    return bwd_layout(M, N, K, r).total;
+}
+
+puro_status puro_linear_fwd(const uint16_t* X, const uint16_t* W, int64_t M, int64_t N, int64_t K,
+                            const puro_linear_recipe* r, uint16_t* Y, const puro_linear_saved* saved,
+                            void* ws, size_t ws_bytes, hipStream_t stream) {
+    puro_status st = check_linear_dims(M, N, K, r);
+    if (st != PURO_OK) return st;
+    if (!saved || !X || !W || !Y || !saved->xq_t || !saved->x_scale || !saved->wq_t || !saved->w_scale)
+        return PURO_ERR_NULL;
+    if (!aligned16(X) || !aligned16(W) || !aligned16(Y) || !aligned16(saved->xq_t) ||
+        !aligned16(saved->wq_t))
+        return PURO_ERR_ALIGN;
+    const FwdLayout l = fwd_layout(M, N, K, r);
+    if (!ws) return PURO_ERR_NULL;
+    if (ws_bytes < l.total) return PURO_ERR_WORKSPACE;
+    uint8_t* w8 = reinterpret_cast<uint8_t*>(ws);
+    uint8_t* xq = w8 + l.xq;
+    uint8_t* wq = w8 + l.wq;
+    puro_fp8_operand A{}, B{};
+    if (!r->blockwise) {
+        st = puro_quantize_fp8(X, M, K, K, r->x_fmt, PURO_SCALE_TENSOR, r->rnd, nullptr, xq, saved->x_scale,
+                               saved->xq_t, nullptr, w8 + l.part_x, amax_ws(M, K), stream);
+        if (st != PURO_OK) return st;
+        st = puro_quantize_fp8(W, N, K, K, r->w_fmt, PURO_SCALE_TENSOR, r->rnd, nullptr, wq, saved->w_scale,
+                               saved->wq_t, nullptr, w8 + l.part_w, amax_ws(N, K), stream);
+        if (st != PURO_OK) return st;
+        A = puro_fp8_operand{xq, K, r->x_fmt, PURO_SCALE_TENSOR, saved->x_scale};
+        B = puro_fp8_operand{wq, K, r->w_fmt, PURO_SCALE_TENSOR, saved->w_scale};
+    } else {
+        // X: 1x128 row groups for Fprop and, from the same read, the 128x1
+        // column-grouped transposed copy kept for Wgrad.
+        float* xs_row = reinterpret_cast<float*>(w8 + l.xs_row);
+        float* w_blk = reinterpret_cast<float*>(w8 + l.w_blk);
+        st = puro_quantize_fp8(X, M, K, K, r->x_fmt, PURO_SCALE_ROW_1x128, PURO_SCALE_POW2, nullptr, xq,
+                               xs_row, saved->xq_t, saved->x_scale, nullptr, 0, stream);
+        if (st != PURO_OK) return st;
+        // W: 128x128 blocks, plus the transposed copy (same blocks) kept for Dgrad.
+        st = puro_quantize_fp8(W, N, K, K, r->w_fmt, PURO_SCALE_BLOCK_128x128, PURO_SCALE_POW2, nullptr, wq,
+                               w_blk, saved->wq_t, saved->w_scale, nullptr, 0, stream);
+        if (st != PURO_OK) return st;
+        A = puro_fp8_operand{xq, K, r->x_fmt, PURO_SCALE_ROW_1x128, xs_row};
+        B = puro_fp8_operand{wq, K, r->w_fmt, PURO_SCALE_BLOCK_128x128, w_blk};
+    }
+    return puro_fp8_gemm(M, N, K, &A, &B, Y, PURO_OUT_BF16, N, 0, w8 + l.gemm, ws_bytes - l.gemm, stream);
+}
+
+puro_status puro_linear_bwd(const uint16_t* dY, const puro_linear_saved* saved, int64_t M, int64_t N,
+                            int64_t K, const puro_linear_recipe* r, uint16_t* dX, float* dW,
+                            int accumulate_dW, void* ws, size_t ws_bytes, hipStream_t stream) {
+    puro_status st = check_linear_dims(M, N, K, r);
+    if (st != PURO_OK) return st;
+    if (!saved || !dY || !saved->xq_t || !saved->x_scale || !saved->wq_t || !saved->w_scale)
+        return PURO_ERR_NULL;
+    if (!aligned16(dY) || !aligned16(saved->xq_t) || !aligned16(saved->wq_t) || (dX && !aligned16(dX)) ||
+        (dW && !aligned16(dW)))
+        return PURO_ERR_ALIGN;
+    if (!dX && !dW) return PURO_OK;
+    const BwdLayout l = bwd_layout(M, N, K, r);
+    if (!ws) return PURO_ERR_NULL;
+    if (ws_bytes < l.total) return PURO_ERR_WORKSPACE;
+    uint8_t* w8 = reinterpret_cast<uint8_t*>(ws);
+    uint8_t* dyq = w8 + l.dyq;
+    uint8_t* dyq_t = w8 + l.dyq_t;
+    float* dys = reinterpret_cast<float*>(w8 + l.dy_scale);
+    float* dys_t = reinterpret_cast<float*>(w8 + l.dy_scale_t);
+    void* gws = w8 + l.gemm;
+    const size_t gws_bytes = ws_bytes - l.gemm;
+    puro_fp8_operand dA{}, dB{}, wA{}, wB{};
+    if (!r->blockwise) {
+        st = puro_quantize_fp8(dY, M, N, N, r->dy_fmt, PURO_SCALE_TENSOR, r->rnd, nullptr, dyq, dys, dyq_t,
+                               nullptr, w8 + l.part, amax_ws(M, N), stream);
+        if (st != PURO_OK) return st;
+        dA = puro_fp8_operand{dyq, N, r->dy_fmt, PURO_SCALE_TENSOR, dys};
+        dB = puro_fp8_operand{saved->wq_t, N, r->w_fmt, PURO_SCALE_TENSOR, saved->w_scale};
+        wA = puro_fp8_operand{dyq_t, M, r->dy_fmt, PURO_SCALE_TENSOR, dys};
+        wB = puro_fp8_operand{saved->xq_t, M, r->x_fmt, PURO_SCALE_TENSOR, saved->x_scale};
+    } else {
+        st = puro_quantize_fp8(dY, M, N, N, r->dy_fmt, PURO_SCALE_ROW_1x128, PURO_SCALE_POW2, nullptr, dyq,
+                               dys, dyq_t, dys_t, nullptr, 0, stream);
+        if (st != PURO_OK) return st;
+        dA = puro_fp8_operand{dyq, N, r->dy_fmt, PURO_SCALE_ROW_1x128, dys};
+        dB = puro_fp8_operand{saved->wq_t, N, r->w_fmt, PURO_SCALE_BLOCK_128x128, saved->w_scale};
+        wA = puro_fp8_operand{dyq_t, M, r->dy_fmt, PURO_SCALE_ROW_1x128, dys_t};
+        wB = puro_fp8_operand{saved->xq_t, M, r->x_fmt, PURO_SCALE_ROW_1x128, saved->x_scale};
+    }
+    if (dX) {
+        st = puro_fp8_gemm(M, K, N, &dA, &dB, dX, PURO_OUT_BF16, K, 0, gws, gws_bytes, stream);
+        if (st != PURO_OK) return st;
+    }
+    if (dW) {
+        st = puro_fp8_gemm(N, K, M, &wA, &wB, dW, PURO_OUT_FP32, K, accumulate_dW, gws, gws_bytes, stream);
+        if (st != PURO_OK) return st;
+    }
+    return PURO_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,147 @@
+// Device helpers shared by the quantiser and GEMM kernels (gfx950 only).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace puro {
+
+// FP8 format ids; the values double as the MFMA operand-format selectors of
+// the gfx950 f8f6f4 instructions (0 = E4M3, 1 = E5M2).
+enum : int { kE4M3 = 0, kE5M2 = 1 };
+
+template <int FMT> struct Fp8Traits;
+template <> struct Fp8Traits<kE4M3> {
+    static constexpr float kMax = 448.0f;
+    static constexpr uint32_t kMaxBits = 0x43E00000u;  // 448.0f
+    static constexpr int kEmax = 8;                    // 448 = 1.75 * 2^8
+};
+template <> struct Fp8Traits<kE5M2> {
+    static constexpr float kMax = 57344.0f;
+    static constexpr uint32_t kMaxBits = 0x47600000u;  // 57344.0f
+    static constexpr int kEmax = 15;                   // 57344 = 1.75 * 2^15
+};
+
+__device__ __forceinline__ float bf16lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+
+// Hardware conversion of two binary32 values to two FP8 codes (RNE), written
+// into byte pair HI (false: bytes 0-1, true: bytes 2-3) of `old`. In range it
+// rounds exactly like the encoding this library defines; it does not
+// saturate (too-large values become NaN/Inf) and gives NaN a sign, which the
+// callers below handle.
+template <int FMT, bool HI>
+__device__ __forceinline__ uint32_t cvt_pk(float a, float b, uint32_t old) {
+    if constexpr (FMT == kE4M3)
+        return (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(a, b, (int)old, HI);
+    else
+        return (uint32_t)__builtin_amdgcn_cvt_pk_bf8_f32(a, b, (int)old, HI);
+}
+
+// Four values already known to lie within [-FMAX, FMAX] in magnitude up to
+// one binary32 rounding of the scale (never NaN): hardware path.
+template <int FMT>
+__device__ __forceinline__ uint32_t encode4_fast(float a, float b, float c, float d) {
+    uint32_t w = cvt_pk<FMT, false>(a, b, 0u);
+    return cvt_pk<FMT, true>(c, d, w);
+}
+
+// One value of any kind: saturate finite and infinite magnitudes above FMAX
+// to +-FMAX, map every NaN to 0x7F.
+template <int FMT>
+__device__ __forceinline__ uint32_t encode1_safe(float v) {
+    uint32_t u = __float_as_uint(v);
+    uint32_t m = u & 0x7FFFFFFFu;
+    bool nan = m > 0x7F800000u;
+    m = m < Fp8Traits<FMT>::kMaxBits ? m : Fp8Traits<FMT>::kMaxBits;
+    float c = __uint_as_float((u & 0x80000000u) | m);
+    uint32_t code = cvt_pk<FMT, false>(c, 0.0f, 0u) & 0xFFu;
+    return nan ? 0x7Fu : code;
+}
+
+template <int FMT>
+__device__ __forceinline__ uint32_t encode4_safe(float a, float b, float c, float d) {
+    return encode1_safe<FMT>(a) | (encode1_safe<FMT>(b) << 8) | (encode1_safe<FMT>(c) << 16) |
+           (encode1_safe<FMT>(d) << 24);
+}
+
+// Encode 8 BF16 values (4 packed words) times r into 8 codes (2 words).
+template <int FMT, bool SAFE>
+__device__ __forceinline__ uint2 encode8(const uint32_t w[4], float r) {
+    float v[8];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        v[2 * i] = bf16lo(w[i]) * r;
+        v[2 * i + 1] = bf16hi(w[i]) * r;
+    }
+    uint2 out;
+    if constexpr (SAFE) {
+        out.x = encode4_safe<FMT>(v[0], v[1], v[2], v[3]);
+        out.y = encode4_safe<FMT>(v[4], v[5], v[6], v[7]);
+    } else {
+        out.x = encode4_fast<FMT>(v[0], v[1], v[2], v[3]);
+        out.y = encode4_fast<FMT>(v[4], v[5], v[6], v[7]);
+    }
+    return out;
+}
+
+// Largest BF16 magnitude pattern among 8 values (4 words); as integers the
+// magnitude patterns order like the magnitudes, and NaN patterns exceed Inf.
+__device__ __forceinline__ uint32_t absmax_bits8(const uint32_t w[4]) {
+    uint32_t m = 0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        uint32_t lo = w[i] & 0x7FFFu, hi = (w[i] >> 16) & 0x7FFFu;
+        m = max(m, max(lo, hi));
+    }
+    return m;
+}
+
+// Power-of-two scale exponent: the smallest e with amax <= FMAX * 2^e,
+// clamped to [-127, 127]; amax given as its BF16 magnitude pattern (finite,
+// non-NaN). amax = 0 -> 0. Writing amax = f * 2^E with f in [1, 2):
+// e = E - Emax, plus one when f > 1.75 (FMAX = 1.75 * 2^Emax).
+template <int FMT>
+__device__ __forceinline__ int pow2_exponent_bf16(uint32_t mag) {
+    if (mag == 0) return 0;
+    if (mag >= 0x7F80u) return 127;                 // infinity
+    uint32_t bits = mag << 16;
+    int ef = (int)(bits >> 23);
+    if (ef == 0) return -127;                        // subnormal: far below the clamp
+    int e = ef - 127 - Fp8Traits<FMT>::kEmax + ((bits & 0x7FFFFFu) > 0x600000u ? 1 : 0);
+    return e < -127 ? -127 : (e > 127 ? 127 : e);
+}
+
+// 2^e as binary32 for e in [-127, 127] (2^-127 is subnormal).
+__device__ __forceinline__ float exp2i(int e) {
+    return e >= -126 ? __uint_as_float((uint32_t)(e + 127) << 23) : __uint_as_float(0x00400000u);
+}
+
+// 8x8 byte transpose: in[i] holds row i (bytes 0..7 = columns 0..7, as a
+// uint2), out[j] holds column j (bytes 0..7 = rows 0..7).
+__device__ __forceinline__ void transpose8x8(const uint2 in[8], uint2 out[8]) {
+    // 4x4 byte transpose of four words (rows) -> four words (columns)
+    auto t4 = [](uint32_t a, uint32_t b, uint32_t c, uint32_t d, uint32_t o[4]) {
+        // interleave bytes of (a, b) and (c, d)
+        uint32_t ab_lo = __builtin_amdgcn_perm(b, a, 0x05010400u);  // a0 b0 a1 b1
+        uint32_t ab_hi = __builtin_amdgcn_perm(b, a, 0x07030602u);  // a2 b2 a3 b3
+        uint32_t cd_lo = __builtin_amdgcn_perm(d, c, 0x05010400u);  // c0 d0 c1 d1
+        uint32_t cd_hi = __builtin_amdgcn_perm(d, c, 0x07030602u);  // c2 d2 c3 d3
+        o[0] = __builtin_amdgcn_perm(cd_lo, ab_lo, 0x05040100u);    // a0 b0 c0 d0
+        o[1] = __builtin_amdgcn_perm(cd_lo, ab_lo, 0x07060302u);    // a1 b1 c1 d1
+        o[2] = __builtin_amdgcn_perm(cd_hi, ab_hi, 0x05040100u);    // a2 b2 c2 d2
+        o[3] = __builtin_amdgcn_perm(cd_hi, ab_hi, 0x07060302u);    // a3 b3 c3 d3
+    };
+    uint32_t tl[4], tr[4], bl[4], br[4];
+    t4(in[0].x, in[1].x, in[2].x, in[3].x, tl);  // rows 0-3, cols 0-3
+    t4(in[0].y, in[1].y, in[2].y, in[3].y, tr);  // rows 0-3, cols 4-7
+    t4(in[4].x, in[5].x, in[6].x, in[7].x, bl);  // rows 4-7, cols 0-3
+    t4(in[4].y, in[5].y, in[6].y, in[7].y, br);  // rows 4-7, cols 4-7
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        out[j] = make_uint2(tl[j], bl[j]);
+        out[4 + j] = make_uint2(tr[j], br[j]);
+    }
+}
+
+}  // namespace puro

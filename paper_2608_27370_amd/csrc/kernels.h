@@ -1,0 +1,65 @@
+// Host-side launchers of the HIP kernels (internal to libpuro).
+#pragma once
+
+#include <hip/hip_runtime_api.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace puro {
+
+// ---- amax / quantisation (quant.hip) ----------------------------------------
+
+// Number of per-block partial maxima the amax pass writes for a tensor.
+int amax_num_partials(int64_t rows, int64_t cols);
+
+// Per-block maxima of the BF16 magnitude patterns of x into partial[0..P).
+void launch_amax_partials(const uint16_t* x, int64_t rows, int64_t cols, int64_t ld,
+                          uint32_t* partial, int P, hipStream_t stream);
+// amax = max of partial[0..P) as a float (0 when P == 0).
+void launch_amax_finalize(const uint32_t* partial, int P, float* amax, hipStream_t stream);
+
+enum QuantMode : int { kQTensor = 0, kQRow = 1, kQCol = 2, kQBlock = 3 };
+
+struct QuantArgs {
+    const uint16_t* x;
+    int64_t rows, cols, ld;
+    uint8_t* q;
+    float* scale;
+    uint8_t* qT;
+    float* scaleT;
+    // per-tensor mode: the amax source (amax_in, or the partial maxima) and the rule
+    const uint32_t* partial;
+    int npartial;
+    const float* amax_in;
+    int pow2;
+};
+
+void launch_quantize(int fmt, int mode, const QuantArgs& a, hipStream_t stream);
+
+// ---- GEMM (gemm.hip) ----------------------------------------------------------
+
+enum ScaleMode : int { kSTensor = 0, kSRow = 1, kSBlock = 2 };
+enum OutKind : int { kOutBF16 = 0, kOutF32 = 1 };
+
+struct GemmProblem {
+    int64_t M, N, K;
+    const uint8_t* A;
+    int64_t lda;
+    int fa, sa_mode;
+    const float* sa;
+    const uint8_t* B;
+    int64_t ldb;
+    int fb, sb_mode;
+    const float* sb;
+    void* D;
+    int64_t ldd;
+    int out;
+    int accumulate;
+};
+
+// Workspace the GEMM needs for split-K partial sums (0 when it runs unsplit).
+size_t gemm_workspace_bytes(int64_t M, int64_t N, int64_t K, int out);
+// Enqueue the GEMM; `ws` must hold gemm_workspace_bytes(...) bytes.
+void launch_gemm(const GemmProblem& p, void* ws, hipStream_t stream);
+
+}  // namespace puro

@@ -1,0 +1,403 @@
+// amax and FP8 quantisation kernels for gfx950.
+//
+// Section 3.2 of the paper: each linear layer quantises its BF16 operands to
+// FP8 right before the GEMM, with scales computed online from the data: one
+// per tensor, one per 128 consecutive values along the GEMM's reduction
+// dimension (activations, gradients), or one per 128x128 block (weights),
+// block scales being powers of two.
+//
+// These passes are bound by HBM bandwidth: every element is read once as BF16
+// (16-byte vector loads, coalesced along rows) and written as one FP8 byte
+// per requested copy. Each thread owns an 8x8 sub-block of a 128x128 tile, so
+// a transposed copy is produced by an in-register 8x8 byte transpose and
+// stored as 8-byte runs of the transposed rows, without an LDS round trip.
+// Per-tensor scaling needs the whole tensor's amax first: a first pass writes
+// per-block partial maxima (no atomics, no zero-initialised state), and every
+// block of the quantise pass reduces them before encoding.
+
+#include "device_common.h"
+#include "kernels.h"
+
+namespace puro {
+
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kTile = 128;
+
+__device__ __forceinline__ uint32_t wave_max(uint32_t v) {
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) v = max(v, (uint32_t)__shfl_xor((int)v, o, 64));
+    return v;
+}
+
+// Block-wide max of a per-thread value (256 threads); result in every thread.
+__device__ __forceinline__ uint32_t block_max(uint32_t v, uint32_t* red) {
+    v = wave_max(v);
+    const int w = threadIdx.x >> 6;
+    __syncthreads();
+    if ((threadIdx.x & 63) == 0) red[w] = v;
+    __syncthreads();
+    return max(max(red[0], red[1]), max(red[2], red[3]));
+}
+
+// ---------------------------------------------------------------- amax ---
+template <bool DENSE>
+__global__ __launch_bounds__(kThreads) void amax_partial_kernel(const uint16_t* __restrict__ x,
+                                                                int64_t rows, uint32_t cpr,
+                                                                int64_t ld,
+                                                                uint32_t* __restrict__ partial) {
+    __shared__ uint32_t red[4];
+    const int P = gridDim.x;
+    const int64_t r0 = rows * blockIdx.x / P, r1 = rows * (blockIdx.x + 1) / P;
+    const uint32_t n = (uint32_t)((r1 - r0) * cpr);
+    uint32_t m = 0;
+    constexpr int U = 4;
+    for (uint32_t j0 = threadIdx.x; j0 < n; j0 += kThreads * U) {
+        uint4 v[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const uint32_t j = j0 + u * kThreads;
+            v[u] = make_uint4(0, 0, 0, 0);
+            if (j < n) {
+                const uint16_t* p;
+                if constexpr (DENSE) {
+                    p = x + (r0 * cpr + j) * 8;
+                } else {
+                    const uint32_t rr = j / cpr, cc = j - rr * cpr;
+                    p = x + (r0 + rr) * ld + (int64_t)cc * 8;
+                }
+                v[u] = *reinterpret_cast<const uint4*>(p);
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const uint32_t w[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
+            m = max(m, absmax_bits8(w));
+        }
+    }
+    m = block_max(m, red);
+    if (threadIdx.x == 0) partial[blockIdx.x] = m;
+}
+
+__global__ __launch_bounds__(kThreads) void amax_finalize_kernel(const uint32_t* __restrict__ partial,
+                                                                 int P, float* __restrict__ amax) {
+    __shared__ uint32_t red[4];
+    uint32_t m = 0;
+    for (int i = threadIdx.x; i < P; i += kThreads) m = max(m, partial[i]);
+    m = block_max(m, red);
+    if (threadIdx.x == 0) *amax = __uint_as_float(m << 16);
+}
+
+// ------------------------------------------------------------ quantise ---
+struct Tile {
+    int cc, rg;       // column chunk (8 columns) and row group (8 rows) of this thread
+    int64_t row0;     // first of the thread's 8 rows
+    int64_t col;      // first of the thread's 8 columns
+    bool col_ok;
+};
+
+__device__ __forceinline__ Tile tile_coords(int64_t cols) {
+    Tile t;
+    t.cc = threadIdx.x & 15;
+    t.rg = threadIdx.x >> 4;
+    t.row0 = (int64_t)blockIdx.y * kTile + t.rg * 8;
+    t.col = (int64_t)blockIdx.x * kTile + t.cc * 8;
+    t.col_ok = t.col < cols;
+    return t;
+}
+
+__device__ __forceinline__ void load_8x8(const QuantArgs& a, const Tile& t, uint32_t w[8][4]) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        uint4 v = make_uint4(0, 0, 0, 0);
+        const int64_t r = t.row0 + i;
+        if (t.col_ok && r < a.rows) v = *reinterpret_cast<const uint4*>(a.x + r * a.ld + t.col);
+        w[i][0] = v.x; w[i][1] = v.y; w[i][2] = v.z; w[i][3] = v.w;
+    }
+}
+
+__device__ __forceinline__ void store_rows(const QuantArgs& a, const Tile& t, const uint2 c[8]) {
+    if (!t.col_ok) return;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        const int64_t r = t.row0 + i;
+        if (r < a.rows) *reinterpret_cast<uint2*>(a.q + r * a.cols + t.col) = c[i];
+    }
+}
+
+// qT [cols, rows]: column j of the thread's block becomes 8 bytes of row col+j.
+__device__ __forceinline__ void store_transposed(const QuantArgs& a, const Tile& t, const uint2 c[8]) {
+    if (!t.col_ok || t.row0 >= a.rows) return;
+    uint2 ct[8];
+    transpose8x8(c, ct);
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+        *reinterpret_cast<uint2*>(a.qT + (t.col + j) * a.rows + t.row0) = ct[j];
+}
+
+// Encode with one multiplier per column of the 8x8 block (column-grouped scales).
+template <int FMT, bool SAFE>
+__device__ __forceinline__ uint2 encode8_cols(const uint32_t w[4], const float r[8]) {
+    float v[8];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        v[2 * i] = bf16lo(w[i]) * r[2 * i];
+        v[2 * i + 1] = bf16hi(w[i]) * r[2 * i + 1];
+    }
+    uint2 out;
+    if constexpr (SAFE) {
+        out.x = encode4_safe<FMT>(v[0], v[1], v[2], v[3]);
+        out.y = encode4_safe<FMT>(v[4], v[5], v[6], v[7]);
+    } else {
+        out.x = encode4_fast<FMT>(v[0], v[1], v[2], v[3]);
+        out.y = encode4_fast<FMT>(v[4], v[5], v[6], v[7]);
+    }
+    return out;
+}
+
+__device__ __forceinline__ uint32_t elem_mag(const uint32_t w[8][4], int i, int j) {
+    const uint32_t word = w[i][j >> 1];
+    return ((j & 1) ? (word >> 16) : word) & 0x7FFFu;
+}
+
+// Per-tensor quantisation: scale from amax_in or from the partial maxima.
+template <int FMT>
+__global__ __launch_bounds__(kThreads) void quant_tensor_kernel(QuantArgs a) {
+    __shared__ uint32_t red[4];
+    const Tile t = tile_coords(a.cols);
+    uint32_t w[8][4];
+    load_8x8(a, t, w);
+
+    float amax;
+    bool safe;
+    if (a.amax_in) {
+        amax = *a.amax_in;
+        safe = true;   // values beyond a supplied amax saturate
+    } else {
+        uint32_t m = 0;
+        for (int i = threadIdx.x; i < a.npartial; i += kThreads) m = max(m, a.partial[i]);
+        m = block_max(m, red);
+        amax = __uint_as_float(m << 16);
+        safe = false;
+    }
+    float s, r;
+    constexpr float fm = Fp8Traits<FMT>::kMax;
+    if (a.pow2) {
+        if (amax != amax) {
+            s = r = __uint_as_float(0x7FC00000u);
+        } else {
+            // |amax| as a BF16-or-wider magnitude: reuse the exponent rule on its top bits
+            const uint32_t bits = __float_as_uint(fabsf(amax));
+            int e;
+            if (bits == 0) e = 0;
+            else if (bits >= 0x7F800000u) e = 127;
+            else if ((bits >> 23) == 0) e = -127;
+            else {
+                e = (int)(bits >> 23) - 127 - Fp8Traits<FMT>::kEmax + ((bits & 0x7FFFFFu) > 0x600000u ? 1 : 0);
+                e = e < -127 ? -127 : (e > 127 ? 127 : e);
+            }
+            s = exp2i(e);
+            r = exp2i(-e);
+        }
+    } else if (amax == 0.0f) {
+        s = r = 1.0f;
+    } else {
+        s = amax / fm;
+        r = fm / amax;
+    }
+    safe = safe || !(fabsf(amax) <= 3.4028235e38f) || !(fabsf(r) <= 3.4028235e38f);
+    if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0 && a.scale) a.scale[0] = s;
+
+    uint2 c[8];
+    if (safe) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) c[i] = encode8<FMT, true>(w[i], r);
+    } else {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) c[i] = encode8<FMT, false>(w[i], r);
+    }
+    if (a.q) store_rows(a, t, c);
+    if (a.qT) store_transposed(a, t, c);
+}
+
+// 1x128 row groups (q, scale) and/or 128x1 column groups (qT, scaleT).
+template <int FMT, bool ROWS, bool COLS>
+__global__ __launch_bounds__(kThreads) void quant_groups_kernel(QuantArgs a) {
+    __shared__ uint32_t colmax[4][kTile];
+    const Tile t = tile_coords(a.cols);
+    uint32_t w[8][4];
+    load_8x8(a, t, w);
+
+    if constexpr (ROWS) {
+        uint2 c[8];
+        float srow[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            uint32_t m = absmax_bits8(w[i]);
+#pragma unroll
+            for (int o = 8; o >= 1; o >>= 1) m = max(m, (uint32_t)__shfl_xor((int)m, o, 16));
+            if (m <= 0x7F7Fu) {                      // finite group
+                const int e = pow2_exponent_bf16<FMT>(m);
+                srow[i] = exp2i(e);
+                c[i] = encode8<FMT, false>(w[i], exp2i(-e));
+            } else if (m == 0x7F80u) {               // an infinity: largest scale, saturate
+                srow[i] = exp2i(127);
+                c[i] = encode8<FMT, true>(w[i], exp2i(-127));
+            } else {                                 // a NaN: NaN scale, NaN codes
+                srow[i] = __uint_as_float(0x7FC00000u);
+                c[i] = encode8<FMT, true>(w[i], srow[i]);
+            }
+        }
+        store_rows(a, t, c);
+        if (t.cc == 0) {
+            const int64_t ng = a.cols / kTile;
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                const int64_t r = t.row0 + i;
+                if (r < a.rows) a.scale[r * ng + blockIdx.x] = srow[i];
+            }
+        }
+    }
+    if constexpr (COLS) {
+        // column maxima over the tile's 128 rows: 8 rows in-thread, 4 row
+        // groups per wave (lanes 16 apart), 4 waves through LDS
+        uint32_t cm[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            uint32_t m = 0;
+#pragma unroll
+            for (int i = 0; i < 8; ++i) m = max(m, elem_mag(w, i, j));
+            m = max(m, (uint32_t)__shfl_xor((int)m, 16, 64));
+            m = max(m, (uint32_t)__shfl_xor((int)m, 32, 64));
+            cm[j] = m;
+        }
+        const int wv = threadIdx.x >> 6;
+        if ((threadIdx.x & 63) < 16) {
+#pragma unroll
+            for (int j = 0; j < 8; ++j) colmax[wv][t.cc * 8 + j] = cm[j];
+        }
+        __syncthreads();
+        float rcol[8], scol[8];
+        bool finite = true;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const int k = t.cc * 8 + j;
+            const uint32_t m = max(max(colmax[0][k], colmax[1][k]), max(colmax[2][k], colmax[3][k]));
+            if (m <= 0x7F7Fu) {
+                const int e = pow2_exponent_bf16<FMT>(m);
+                scol[j] = exp2i(e);
+                rcol[j] = exp2i(-e);
+            } else if (m == 0x7F80u) {
+                scol[j] = exp2i(127);
+                rcol[j] = exp2i(-127);
+                finite = false;
+            } else {
+                scol[j] = rcol[j] = __uint_as_float(0x7FC00000u);
+                finite = false;
+            }
+        }
+        uint2 c[8];
+        if (finite) {
+#pragma unroll
+            for (int i = 0; i < 8; ++i) c[i] = encode8_cols<FMT, false>(w[i], rcol);
+        } else {
+#pragma unroll
+            for (int i = 0; i < 8; ++i) c[i] = encode8_cols<FMT, true>(w[i], rcol);
+        }
+        store_transposed(a, t, c);
+        if (t.rg == 0 && t.col_ok) {
+            const int64_t ng = a.rows / kTile;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) a.scaleT[(t.col + j) * ng + blockIdx.y] = scol[j];
+        }
+    }
+}
+
+// One scale per 128x128 block; optional transposed copy with transposed scales.
+template <int FMT>
+__global__ __launch_bounds__(kThreads) void quant_block_kernel(QuantArgs a) {
+    __shared__ uint32_t red[4];
+    const Tile t = tile_coords(a.cols);
+    uint32_t w[8][4];
+    load_8x8(a, t, w);
+    uint32_t m = 0;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) m = max(m, absmax_bits8(w[i]));
+    m = block_max(m, red);
+    float s;
+    uint2 c[8];
+    if (m <= 0x7F7Fu) {
+        const int e = pow2_exponent_bf16<FMT>(m);
+        s = exp2i(e);
+        const float r = exp2i(-e);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) c[i] = encode8<FMT, false>(w[i], r);
+    } else {
+        const bool inf = m == 0x7F80u;
+        s = inf ? exp2i(127) : __uint_as_float(0x7FC00000u);
+        const float r = inf ? exp2i(-127) : s;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) c[i] = encode8<FMT, true>(w[i], r);
+    }
+    store_rows(a, t, c);
+    if (a.qT) store_transposed(a, t, c);
+    if (threadIdx.x == 0) {
+        a.scale[(int64_t)blockIdx.y * (a.cols / kTile) + blockIdx.x] = s;
+        if (a.scaleT) a.scaleT[(int64_t)blockIdx.x * (a.rows / kTile) + blockIdx.y] = s;
+    }
+}
+
+template <int FMT>
+void launch_quantize_fmt(int mode, const QuantArgs& a, hipStream_t stream) {
+    // at least one block, so that an empty tensor still gets its scale written
+    const int64_t gx = (a.cols + kTile - 1) / kTile, gy = (a.rows + kTile - 1) / kTile;
+    const dim3 grid((unsigned)(gx > 0 ? gx : 1), (unsigned)(gy > 0 ? gy : 1));
+    switch (mode) {
+    case kQTensor:
+        quant_tensor_kernel<FMT><<<grid, kThreads, 0, stream>>>(a);
+        break;
+    case kQRow:
+        if (a.qT) quant_groups_kernel<FMT, true, true><<<grid, kThreads, 0, stream>>>(a);
+        else quant_groups_kernel<FMT, true, false><<<grid, kThreads, 0, stream>>>(a);
+        break;
+    case kQCol:
+        quant_groups_kernel<FMT, false, true><<<grid, kThreads, 0, stream>>>(a);
+        break;
+    case kQBlock:
+        quant_block_kernel<FMT><<<grid, kThreads, 0, stream>>>(a);
+        break;
+    }
+}
+
+}  // namespace
+
+int amax_num_partials(int64_t rows, int64_t cols) {
+    if (rows <= 0 || cols <= 0) return 0;
+    const int64_t chunks = rows * (cols / 8);
+    int64_t P = chunks / (kThreads * 16);   // ~16 vector loads per thread
+    if (P < 1) P = 1;
+    if (P > 1024) P = 1024;
+    if (P > rows) P = rows;                 // whole rows per block
+    return (int)P;
+}
+
+void launch_amax_partials(const uint16_t* x, int64_t rows, int64_t cols, int64_t ld,
+                          uint32_t* partial, int P, hipStream_t stream) {
+    const uint32_t cpr = (uint32_t)(cols / 8);
+    if (ld == cols)
+        amax_partial_kernel<true><<<P, kThreads, 0, stream>>>(x, rows, cpr, ld, partial);
+    else
+        amax_partial_kernel<false><<<P, kThreads, 0, stream>>>(x, rows, cpr, ld, partial);
+}
+
+void launch_amax_finalize(const uint32_t* partial, int P, float* amax, hipStream_t stream) {
+    amax_finalize_kernel<<<1, kThreads, 0, stream>>>(partial, P, amax);
+}
+
+void launch_quantize(int fmt, int mode, const QuantArgs& a, hipStream_t stream) {
+    if (fmt == kE4M3) launch_quantize_fmt<kE4M3>(mode, a, stream);
+    else launch_quantize_fmt<kE5M2>(mode, a, stream);
+}
+
+}  // namespace puro

@@ -1,0 +1,275 @@
+"""Thin ctypes binding of libpuro (include/puro.h): argument marshalling only.
+
+Every operation runs in the HIP kernels of ``libpuro.so``; torch supplies
+device memory and the current stream. There is no fallback: if the library
+is missing or a call fails, an exception is raised.
+
+Tensors: BF16 data as ``torch.bfloat16`` (or int16/uint16 holding the bit
+patterns), FP8 codes as ``torch.uint8``, scales as ``torch.float32``, all on
+the GPU; 2-D with unit stride along rows.
+"""
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libpuro.so")
+
+E4M3, E5M2 = 0, 1
+SCALE_TENSOR, SCALE_ROW_1x128, SCALE_COL_128x1, SCALE_BLOCK_128x128 = 0, 1, 2, 3
+SCALE_FP32, SCALE_POW2 = 0, 1
+OUT_BF16, OUT_FP32 = 0, 1
+
+FMAX = {E4M3: 448.0, E5M2: 57344.0}
+
+_i64, _sz, _p, _i = ctypes.c_int64, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_int
+
+
+class PuroError(RuntimeError):
+    def __init__(self, fn, code, msg):
+        super().__init__("%s failed: %s (status %d)" % (fn, msg, code))
+        self.code = code
+
+
+class Operand(ctypes.Structure):
+    """puro_fp8_operand: FP8 codes [rows, K] (row pitch ld bytes) and scales."""
+    _fields_ = [("data", _p), ("ld", _i64), ("fmt", _i), ("mode", _i), ("scale", _p)]
+
+
+class Recipe(ctypes.Structure):
+    """puro_linear_recipe."""
+    _fields_ = [("x_fmt", _i), ("w_fmt", _i), ("dy_fmt", _i), ("blockwise", _i), ("rnd", _i)]
+
+
+class Saved(ctypes.Structure):
+    """puro_linear_saved."""
+    _fields_ = [("xq_t", _p), ("x_scale", _p), ("wq_t", _p), ("w_scale", _p)]
+
+
+_SIGS = {
+    "puro_status_string": (ctypes.c_char_p, [_i]),
+    "puro_amax_workspace_size": (_sz, [_i64, _i64]),
+    "puro_amax": (_i, [_p, _i64, _i64, _i64, _p, _p, _sz, _p]),
+    "puro_quantize_workspace_size": (_sz, [_i64, _i64]),
+    "puro_quantize_fp8": (_i, [_p, _i64, _i64, _i64, _i, _i, _i, _p, _p, _p, _p, _p, _p, _sz, _p]),
+    "puro_fp8_gemm_workspace_size": (_sz, [_i64, _i64, _i64, _i]),
+    "puro_fp8_gemm": (_i, [_i64, _i64, _i64, ctypes.POINTER(Operand), ctypes.POINTER(Operand),
+                           _p, _i, _i64, _i, _p, _sz, _p]),
+    "puro_linear_saved_bytes": (_sz, [_i64, _i64, _i64, ctypes.POINTER(Recipe), ctypes.POINTER(_sz * 4)]),
+    "puro_linear_fwd_workspace_size": (_sz, [_i64, _i64, _i64, ctypes.POINTER(Recipe)]),
+    "puro_linear_bwd_workspace_size": (_sz, [_i64, _i64, _i64, ctypes.POINTER(Recipe)]),
+    "puro_linear_fwd": (_i, [_p, _p, _i64, _i64, _i64, ctypes.POINTER(Recipe), _p, ctypes.POINTER(Saved),
+                             _p, _sz, _p]),
+    "puro_linear_bwd": (_i, [_p, ctypes.POINTER(Saved), _i64, _i64, _i64, ctypes.POINTER(Recipe), _p, _p,
+                             _i, _p, _sz, _p]),
+}
+
+_lib = None
+
+
+def lib():
+    """The loaded libpuro (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError("libpuro.so is not built (run paper_2608_27370_amd/build.py or "
+                              "__graft_entry__.build()); there is no fallback path")
+        l = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in _SIGS.items():
+            f = getattr(l, name)
+            f.restype = res
+            f.argtypes = args
+        _lib = l
+    return _lib
+
+
+def status_string(code):
+    return lib().puro_status_string(code).decode()
+
+
+def _check(fn, code):
+    if code != 0:
+        raise PuroError(fn, code, status_string(code))
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream():
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _ld(t):
+    assert t.dim() == 2, "2-D tensors"
+    if t.numel() == 0:
+        return t.shape[1]          # torch gives empty tensors zero strides
+    assert t.stride(1) == 1, "2-D tensors with unit column stride"
+    return t.stride(0)
+
+
+def _ws(nbytes, ws, device):
+    if nbytes == 0:
+        return None, 0
+    if ws is None:
+        ws = torch.empty(nbytes, dtype=torch.uint8, device=device)
+    assert ws.numel() * ws.element_size() >= nbytes
+    return ws, ws.numel() * ws.element_size()
+
+
+# ------------------------------------------------------------------- amax
+def amax(x, out=None, ws=None):
+    """max |x| of a 2-D BF16 tensor as a one-element float32 device tensor."""
+    rows, cols = x.shape
+    if out is None:
+        out = torch.empty(1, dtype=torch.float32, device=x.device)
+    w, nb = _ws(lib().puro_amax_workspace_size(rows, cols), ws, x.device)
+    _check("puro_amax", lib().puro_amax(_ptr(x), rows, cols, _ld(x), _ptr(out), _ptr(w), nb, _stream()))
+    return out
+
+
+# --------------------------------------------------------------- quantise
+def quantize_fp8(x, fmt, mode=SCALE_TENSOR, rnd=SCALE_FP32, amax_in=None, want_q=True, want_qT=False,
+                 out=None, ws=None):
+    """Quantise a 2-D BF16 tensor; returns dict(q, scale, qT, scaleT) (absent
+    outputs are None). ``out`` may supply preallocated outputs."""
+    rows, cols = x.shape
+    dev = x.device
+    out = dict(out or {})
+    G = 128
+    if mode == SCALE_COL_128x1:
+        want_q, want_qT = False, True
+    q = out.get("q") if want_q else None
+    if want_q and q is None:
+        q = torch.empty(rows, cols, dtype=torch.uint8, device=dev)
+    qT = out.get("qT") if want_qT else None
+    if want_qT and qT is None:
+        qT = torch.empty(cols, rows, dtype=torch.uint8, device=dev)
+    scale = out.get("scale")
+    scaleT = out.get("scaleT")
+    if mode == SCALE_TENSOR:
+        scale = scale if scale is not None else torch.empty(1, dtype=torch.float32, device=dev)
+        scaleT = None
+    elif mode == SCALE_ROW_1x128:
+        scale = scale if scale is not None else torch.empty(rows, cols // G, dtype=torch.float32, device=dev)
+        if want_qT and scaleT is None:
+            scaleT = torch.empty(cols, rows // G, dtype=torch.float32, device=dev)
+    elif mode == SCALE_COL_128x1:
+        scale = None
+        scaleT = scaleT if scaleT is not None else torch.empty(cols, rows // G, dtype=torch.float32, device=dev)
+    elif mode == SCALE_BLOCK_128x128:
+        scale = scale if scale is not None else torch.empty(rows // G, cols // G, dtype=torch.float32, device=dev)
+        if want_qT and scaleT is None:
+            scaleT = torch.empty(cols // G, rows // G, dtype=torch.float32, device=dev)
+    if not want_qT:
+        scaleT = None
+    w, nb = _ws(lib().puro_quantize_workspace_size(rows, cols), ws, dev)
+    _check("puro_quantize_fp8", lib().puro_quantize_fp8(
+        _ptr(x), rows, cols, _ld(x), fmt, mode, rnd, _ptr(amax_in), _ptr(q), _ptr(scale), _ptr(qT),
+        _ptr(scaleT), _ptr(w), nb, _stream()))
+    return dict(q=q, scale=scale, qT=qT, scaleT=scaleT)
+
+
+# ------------------------------------------------------------------- GEMM
+def operand(data, fmt, mode, scale):
+    """Describe a reduction-contiguous FP8 operand [rows, K]."""
+    op = Operand(data.data_ptr(), _ld(data), fmt, mode, scale.data_ptr())
+    op._keep = (data, scale)
+    return op
+
+
+def fp8_gemm_workspace_size(M, N, K, out_dtype):
+    return lib().puro_fp8_gemm_workspace_size(M, N, K, out_dtype)
+
+
+def fp8_gemm(A, a_rows, B, b_rows, K, out_dtype=OUT_BF16, D=None, accumulate=False, ws=None):
+    """D[M, N] (+)= sum_k A[m, k] B[n, k] with M = a_rows, N = b_rows."""
+    M, N = a_rows, b_rows
+    dev = torch.device("cuda", torch.cuda.current_device())
+    if D is None:
+        dt = torch.bfloat16 if out_dtype == OUT_BF16 else torch.float32
+        D = torch.empty(M, N, dtype=dt, device=dev)
+    w, nb = _ws(fp8_gemm_workspace_size(M, N, K, out_dtype), ws, dev)
+    _check("puro_fp8_gemm", lib().puro_fp8_gemm(M, N, K, ctypes.byref(A), ctypes.byref(B), _ptr(D),
+                                                out_dtype, _ld(D), int(bool(accumulate)), _ptr(w), nb,
+                                                _stream()))
+    return D
+
+
+# ----------------------------------------------------------- linear layer
+@dataclass
+class LinearRecipe:
+    x_fmt: int = E4M3
+    w_fmt: int = E4M3
+    dy_fmt: int = E5M2
+    blockwise: int = 0
+    rnd: int = SCALE_FP32
+
+    def c(self):
+        return Recipe(self.x_fmt, self.w_fmt, self.dy_fmt, self.blockwise, self.rnd)
+
+
+def linear_saved(M, N, K, recipe, device):
+    """Allocate the saved-for-backward buffers of a linear layer."""
+    sizes = (_sz * 4)()
+    lib().puro_linear_saved_bytes(M, N, K, ctypes.byref(recipe.c()), ctypes.byref(sizes))
+    G = 128
+    xq_t = torch.empty(K, M, dtype=torch.uint8, device=device)
+    wq_t = torch.empty(K, N, dtype=torch.uint8, device=device)
+    if recipe.blockwise:
+        xs = torch.empty(K, M // G, dtype=torch.float32, device=device)
+        wsc = torch.empty(K // G, N // G, dtype=torch.float32, device=device)
+    else:
+        xs = torch.empty(1, dtype=torch.float32, device=device)
+        wsc = torch.empty(1, dtype=torch.float32, device=device)
+    assert [xq_t.numel(), xs.numel() * 4, wq_t.numel(), wsc.numel() * 4] == list(sizes)
+    return dict(xq_t=xq_t, x_scale=xs, wq_t=wq_t, w_scale=wsc)
+
+
+def _saved_struct(saved):
+    return Saved(saved["xq_t"].data_ptr(), saved["x_scale"].data_ptr(), saved["wq_t"].data_ptr(),
+                 saved["w_scale"].data_ptr())
+
+
+def linear_fwd_workspace_size(M, N, K, recipe):
+    return lib().puro_linear_fwd_workspace_size(M, N, K, ctypes.byref(recipe.c()))
+
+
+def linear_bwd_workspace_size(M, N, K, recipe):
+    return lib().puro_linear_bwd_workspace_size(M, N, K, ctypes.byref(recipe.c()))
+
+
+def linear_fwd(X, W, recipe, Y=None, saved=None, ws=None):
+    """Y = X W^T (FP8 Fprop); returns (Y, saved)."""
+    M, K = X.shape
+    N = W.shape[0]
+    dev = X.device
+    if Y is None:
+        Y = torch.empty(M, N, dtype=torch.bfloat16, device=dev)
+    if saved is None:
+        saved = linear_saved(M, N, K, recipe, dev)
+    w, nb = _ws(linear_fwd_workspace_size(M, N, K, recipe), ws, dev)
+    s = _saved_struct(saved)
+    _check("puro_linear_fwd", lib().puro_linear_fwd(_ptr(X), _ptr(W), M, N, K, ctypes.byref(recipe.c()),
+                                                    _ptr(Y), ctypes.byref(s), _ptr(w), nb, _stream()))
+    return Y, saved
+
+
+def linear_bwd(dY, saved, recipe, K, want_dx=True, want_dw=True, dX=None, dW=None, accumulate_dw=False,
+               ws=None):
+    """dX = dY W (BF16) and dW = dY^T X (FP32); returns (dX, dW)."""
+    M, N = dY.shape
+    dev = dY.device
+    if want_dx and dX is None:
+        dX = torch.empty(M, K, dtype=torch.bfloat16, device=dev)
+    if want_dw and dW is None:
+        dW = torch.zeros(N, K, dtype=torch.float32, device=dev)
+    w, nb = _ws(linear_bwd_workspace_size(M, N, K, recipe), ws, dev)
+    s = _saved_struct(saved)
+    _check("puro_linear_bwd", lib().puro_linear_bwd(
+        _ptr(dY), ctypes.byref(s), M, N, K, ctypes.byref(recipe.c()), _ptr(dX if want_dx else None),
+        _ptr(dW if want_dw else None), int(bool(accumulate_dw)), _ptr(w), nb, _stream()))
+    return (dX if want_dx else None), (dW if want_dw else None)

@@ -1,0 +1,155 @@
+"""Host-side checks of the C ABI (no GPU): the library loads, exports every
+function include/puro.h declares, and rejects invalid arguments with the
+documented status before launching anything."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "puro.h")
+LIB = os.path.join(ROOT, "paper_2608_27370_amd", "libpuro.so")
+
+OK, ERR_NULL, ERR_SHAPE, ERR_UNSUPPORTED, ERR_ALIGN, ERR_WORKSPACE = 0, 1, 2, 3, 4, 5
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(puro_[a-z0-9_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def puro():
+    if not os.path.exists(LIB):
+        from paper_2608_27370_amd import build
+        build.build()
+    from paper_2608_27370_amd import puro as p
+    return p
+
+
+def test_header_declares_the_path():
+    names = _declared()
+    for n in ("puro_amax", "puro_quantize_fp8", "puro_fp8_gemm", "puro_linear_fwd", "puro_linear_bwd"):
+        assert n in names
+
+
+def test_library_exports_every_declared_function(puro):
+    lib = ctypes.CDLL(puro.LIB_PATH)
+    missing = [n for n in _declared() if not hasattr(lib, n)]
+    assert not missing
+
+
+def test_binding_covers_every_declared_function(puro):
+    assert set(_declared()) == set(puro._SIGS)
+
+
+def test_status_strings(puro):
+    for code in range(7):
+        assert puro.status_string(code)
+    assert puro.status_string(0) == "ok"
+
+
+FAKE = 0x10000   # a 16-byte aligned non-NULL address; validation fails before any use
+
+
+def test_amax_validation(puro):
+    L = puro.lib()
+    assert L.puro_amax(None, 4, 16, 16, FAKE, FAKE, 1 << 20, None) == ERR_NULL
+    assert L.puro_amax(FAKE, 4, 16, 8, FAKE, FAKE, 1 << 20, None) == ERR_SHAPE      # ld < cols
+    assert L.puro_amax(FAKE, -1, 16, 16, FAKE, FAKE, 1 << 20, None) == ERR_SHAPE
+    assert L.puro_amax(FAKE, 4, 12, 16, FAKE, FAKE, 1 << 20, None) == ERR_ALIGN     # cols % 8
+    assert L.puro_amax(FAKE + 2, 4, 16, 16, FAKE, FAKE, 1 << 20, None) == ERR_ALIGN
+    assert L.puro_amax(FAKE, 4, 16, 16, None, FAKE, 1 << 20, None) == ERR_NULL
+    assert L.puro_amax(FAKE, 4096, 4096, 4096, FAKE, FAKE, 0, None) == ERR_WORKSPACE
+    assert L.puro_amax_workspace_size(0, 16) == 0
+    assert L.puro_amax_workspace_size(4096, 4096) > 0
+
+
+def test_quantize_validation(puro):
+    L = puro.lib()
+    q = lambda *a: L.puro_quantize_fp8(*a)
+    big = 1 << 20
+    # bad format / rounding / mode
+    assert q(FAKE, 128, 128, 128, 7, 0, 0, None, FAKE, FAKE, None, None, FAKE, big, None) == ERR_UNSUPPORTED
+    assert q(FAKE, 128, 128, 128, 0, 0, 5, None, FAKE, FAKE, None, None, FAKE, big, None) == ERR_UNSUPPORTED
+    assert q(FAKE, 128, 128, 128, 0, 9, 0, None, FAKE, FAKE, None, None, FAKE, big, None) == ERR_UNSUPPORTED
+    # grouped modes require power-of-two scales and no supplied amax
+    assert q(FAKE, 128, 128, 128, 0, 1, 0, None, FAKE, FAKE, None, None, None, 0, None) == ERR_UNSUPPORTED
+    assert q(FAKE, 128, 128, 128, 0, 3, 1, FAKE, FAKE, FAKE, None, None, None, 0, None) == ERR_UNSUPPORTED
+    # outputs missing
+    assert q(FAKE, 128, 128, 128, 0, 0, 0, None, None, FAKE, None, None, FAKE, big, None) == ERR_NULL
+    assert q(FAKE, 128, 128, 128, 0, 0, 0, None, FAKE, None, None, None, FAKE, big, None) == ERR_NULL
+    assert q(FAKE, 128, 128, 128, 0, 2, 1, None, None, None, None, None, None, 0, None) == ERR_NULL
+    # alignment of grouped dimensions and of the transposed copy
+    assert q(FAKE, 128, 136, 136, 0, 1, 1, None, FAKE, FAKE, None, None, None, 0, None) == ERR_ALIGN
+    assert q(FAKE, 120, 128, 128, 0, 2, 1, None, None, None, FAKE, FAKE, None, 0, None) == ERR_ALIGN
+    assert q(FAKE, 120, 128, 128, 0, 3, 1, None, FAKE, FAKE, None, None, None, 0, None) == ERR_ALIGN
+    assert q(FAKE, 24, 128, 128, 0, 0, 0, None, None, FAKE, FAKE, None, FAKE, big, None) == ERR_ALIGN
+    assert q(FAKE, 16, 24, 24, 0, 0, 0, None, FAKE, FAKE, None, None, FAKE, big, None) == ERR_ALIGN
+    # per-tensor without workspace for the amax pass
+    assert q(FAKE, 4096, 4096, 4096, 0, 0, 0, None, FAKE, FAKE, None, None, FAKE, 0, None) == ERR_WORKSPACE
+
+
+def test_gemm_validation(puro):
+    L = puro.lib()
+    Op = puro.Operand
+    good = Op(FAKE, 256, 0, 0, FAKE)
+    byref = ctypes.byref
+
+    def g(M, N, K, A, B, D=FAKE, dt=0, ldd=None, ws=FAKE, wsb=1 << 30):
+        return L.puro_fp8_gemm(M, N, K, byref(A), byref(B), D, dt, N if ldd is None else ldd, 0, ws, wsb, None)
+
+    assert g(-1, 16, 256, good, good) == ERR_SHAPE
+    assert g(16, 16, 512, good, good) == ERR_SHAPE                      # ld < K
+    assert g(16, 16, 250, Op(FAKE, 256, 0, 0, FAKE), good) == ERR_ALIGN  # K % 16
+    assert g(16, 16, 256, Op(FAKE, 264, 0, 0, FAKE), good) == ERR_ALIGN  # ld % 16
+    assert g(16, 16, 256, Op(FAKE, 256, 3, 0, FAKE), good) == ERR_UNSUPPORTED
+    assert g(16, 16, 256, Op(FAKE, 256, 0, 2, FAKE), good) == ERR_UNSUPPORTED  # column mode is not a GEMM operand
+    assert g(16, 16, 256, Op(None, 256, 0, 0, FAKE), good) == ERR_NULL
+    assert g(16, 16, 256, Op(FAKE, 256, 0, 0, None), good) == ERR_NULL
+    assert g(16, 16, 0, Op(FAKE, 0, 0, 0, None), good) == ERR_NULL       # scale is read even for K == 0
+    assert g(16, 16, 208, Op(FAKE, 208, 0, 1, FAKE), Op(FAKE, 208, 0, 0, FAKE)) == ERR_ALIGN  # grouped needs K % 128
+    assert g(16, 16, 256, good, good, dt=4) == ERR_UNSUPPORTED
+    assert g(16, 16, 256, good, good, ldd=8) == ERR_SHAPE
+    assert g(16, 18, 256, good, good, ldd=18) == ERR_ALIGN
+    assert g(16, 16, 256, good, good, D=None) == ERR_NULL
+    assert g(16, 16, 256, good, good, D=FAKE + 4) == ERR_ALIGN
+    # a split-K plan needs its workspace
+    need = L.puro_fp8_gemm_workspace_size(128, 128, 8192, 1)
+    assert need > 0
+    big = Op(FAKE, 8192, 0, 0, FAKE)
+    assert L.puro_fp8_gemm(128, 128, 8192, byref(big), byref(big), FAKE, 1, 128, 0, FAKE, need - 1, None) \
+        == ERR_WORKSPACE
+    assert L.puro_fp8_gemm(0, 128, 8192, byref(big), byref(big), FAKE, 1, 128, 0, None, 0, None) == OK
+
+
+def test_linear_validation(puro):
+    L = puro.lib()
+    rc = puro.LinearRecipe().c()
+    rb = puro.LinearRecipe(blockwise=1).c()
+    bad = puro.LinearRecipe(x_fmt=9).c()
+    s = puro.Saved(FAKE, FAKE, FAKE, FAKE)
+    byref = ctypes.byref
+    assert L.puro_linear_fwd(FAKE, FAKE, 256, 256, 256, byref(bad), FAKE, byref(s), FAKE, 1 << 30, None) \
+        == ERR_UNSUPPORTED
+    assert L.puro_linear_fwd(FAKE, FAKE, 250, 256, 256, byref(rc), FAKE, byref(s), FAKE, 1 << 30, None) \
+        == ERR_ALIGN
+    assert L.puro_linear_fwd(FAKE, FAKE, 256, 256, 144, byref(rb), FAKE, byref(s), FAKE, 1 << 30, None) \
+        == ERR_ALIGN                                                       # blockwise needs 128
+    assert L.puro_linear_fwd(None, FAKE, 256, 256, 256, byref(rc), FAKE, byref(s), FAKE, 1 << 30, None) \
+        == ERR_NULL
+    need = L.puro_linear_fwd_workspace_size(256, 256, 256, byref(rc))
+    assert need > 0
+    assert L.puro_linear_fwd(FAKE, FAKE, 256, 256, 256, byref(rc), FAKE, byref(s), FAKE, need - 1, None) \
+        == ERR_WORKSPACE
+    need = L.puro_linear_bwd_workspace_size(256, 256, 256, byref(rb))
+    assert L.puro_linear_bwd(FAKE, byref(s), 256, 256, 256, byref(rb), FAKE, FAKE, 0, FAKE, need - 1, None) \
+        == ERR_WORKSPACE
+    sizes = (ctypes.c_size_t * 4)()
+    total = L.puro_linear_saved_bytes(256, 512, 384, byref(rb), byref(sizes))
+    assert list(sizes) == [384 * 256, 384 * 2 * 4, 384 * 512, 3 * 4 * 4] and total == sum(sizes)
+    total = L.puro_linear_saved_bytes(256, 512, 384, byref(rc), byref(sizes))
+    assert list(sizes) == [384 * 256, 4, 384 * 512, 4]

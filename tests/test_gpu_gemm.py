@@ -1,0 +1,201 @@
+"""GPU parity of the scaled FP8 GEMM against the oracle's FP64 GEMM.
+
+Operands are quantised by the oracle from seeded BF16 data and uploaded, so
+these tests isolate the GEMM kernels. FP32 outputs must satisfy
+|d - ref| <= 1e-5 * sum_k |a_k b_k|; BF16 outputs must be the BF16 rounding
+of a value within that tolerance."""
+
+import numpy as np
+import pytest
+
+from oracle import bf16, fp8, gemm, quant
+from paper_2608_27370_amd import inputs
+
+import mfma_model
+from gpu_util import bf16_bits, check_bf16, check_fp32, host, to_dev
+
+pytestmark = pytest.mark.gpu
+
+E4, E5 = 0, 1
+OFMT = {E4: fp8.E4M3, E5: fp8.E5M2}
+MODE = {"tensor": 0, "row": 1, "block": 3}
+
+
+@pytest.fixture(scope="module")
+def P():
+    from paper_2608_27370_amd import puro
+    puro.lib()
+    return puro
+
+
+def _operand_tensor(seed, rows, K, fmt, std=1.0, kind="normal"):
+    x = inputs.case(seed, (rows, K), std=std, kind=kind)
+    q, _, s, _ = quant.quantize_tensor(x, OFMT[fmt])
+    return q, s
+
+
+def _operand_grouped(seed, rows, K, fmt, mode, std=1.0, kind="normal"):
+    x = inputs.case(seed, (rows, K), std=std, kind=kind)
+    if mode == "row":
+        return quant.quantize_rows_1x128(x, OFMT[fmt])
+    pad = (-rows) % 128                            # blocks over a ragged row count
+    xp = np.concatenate([x, np.zeros((pad, K), np.uint16)]) if pad else x
+    q, s, _, _ = quant.quantize_blocks_128x128(xp, OFMT[fmt])
+    return q[:rows], s
+
+
+def _run(P, a, fa, sa, am, b, fb, sb, bm, out, D0=None, ld_pad=0):
+    M, K = a.shape
+    N = b.shape[0]
+    if ld_pad:
+        a = np.concatenate([a, np.full((M, ld_pad), 0x3F, np.uint8)], axis=1)   # junk beyond K
+        b = np.concatenate([b, np.full((N, ld_pad), 0x5A, np.uint8)], axis=1)
+    da, db = to_dev(a), to_dev(b)
+    dsa, dsb = to_dev(np.atleast_1d(np.asarray(sa, np.float32))), to_dev(np.atleast_1d(np.asarray(sb, np.float32)))
+    A = P.operand(da[:, :K] if ld_pad else da, fa, MODE[am], dsa)
+    B = P.operand(db[:, :K] if ld_pad else db, fb, MODE[bm], dsb)
+    D = None if D0 is None else to_dev(D0)
+    return P.fp8_gemm(A, M, B, N, K, out, D=D, accumulate=D0 is not None)
+
+
+def _check(P, out, D, ref, den, what, op):
+    """op: the oracle GEMM arguments, for the instruction-truncation allowance."""
+    slack = mfma_model.truncation_loss_full(*op)
+    if out == P.OUT_FP32:
+        check_fp32(host(D), ref, den, what=what, slack=slack)
+    else:
+        check_bf16(bf16_bits(D), ref, den, what=what, slack=slack)
+
+
+SHAPES = [(300, 520, 384), (256, 256, 1536), (64, 32, 16), (1, 4, 16), (200, 136, 208), (513, 260, 1040),
+          (1024, 2048, 256)]
+
+
+@pytest.mark.parametrize("shape", SHAPES, ids=lambda s: "x".join(map(str, s)))
+@pytest.mark.parametrize("out", [0, 1], ids=["bf16", "fp32"])
+def test_gemm_tensor_scales(P, shape, out):
+    M, N, K = shape
+    a, sa = _operand_tensor(1, M, K, E4)
+    b, sb = _operand_tensor(2, N, K, E4, std=0.02)
+    D = _run(P, a, E4, sa, "tensor", b, E4, sb, "tensor", out)
+    op = (a, fp8.E4M3, sa, "tensor", b, fp8.E4M3, sb, "tensor")
+    ref, den = gemm.gemm(*op)
+    _check(P, out, D, ref, den, "tensor %s" % (shape,), op)
+
+
+@pytest.mark.parametrize("fa,fb", [(E5, E4), (E4, E5), (E5, E5)])
+def test_gemm_formats(P, fa, fb):
+    M, N, K = 384, 264, 640
+    a, sa = _operand_tensor(3, M, K, fa, std=1e-3)
+    b, sb = _operand_tensor(4, N, K, fb, kind="student_t")
+    for out in (0, 1):
+        D = _run(P, a, fa, sa, "tensor", b, fb, sb, "tensor", out)
+        op = (a, OFMT[fa], sa, "tensor", b, OFMT[fb], sb, "tensor")
+        ref, den = gemm.gemm(*op)
+        _check(P, out, D, ref, den, "formats %d %d" % (fa, fb), op)
+
+
+@pytest.mark.parametrize("shape", [(128, 128, 8192), (64, 2048, 4096), (256, 96, 2048)],
+                         ids=lambda s: "x".join(map(str, s)))
+@pytest.mark.parametrize("out", [0, 1], ids=["bf16", "fp32"])
+def test_gemm_split_k(P, shape, out):
+    M, N, K = shape
+    assert P.fp8_gemm_workspace_size(M, N, K, out) > 0          # the split path is taken
+    a, sa = _operand_tensor(5, M, K, E5, std=1e-3)
+    b, sb = _operand_tensor(6, N, K, E4)
+    D = _run(P, a, E5, sa, "tensor", b, E4, sb, "tensor", out)
+    op = (a, fp8.E5M2, sa, "tensor", b, fp8.E4M3, sb, "tensor")
+    ref, den = gemm.gemm(*op)
+    _check(P, out, D, ref, den, "split-k %s" % (shape,), op)
+
+
+@pytest.mark.parametrize("out", [0, 1], ids=["bf16", "fp32"])
+@pytest.mark.parametrize("shape", [(256, 384, 512), (96, 64, 4096)], ids=lambda s: "x".join(map(str, s)))
+def test_gemm_accumulate(P, out, shape):
+    M, N, K = shape
+    a, sa = _operand_tensor(7, M, K, E4)
+    b, sb = _operand_tensor(8, N, K, E4)
+    g = np.random.default_rng(3)
+    D0f = g.standard_normal((M, N)).astype(np.float32)
+    if out == P.OUT_FP32:
+        D0 = D0f
+        old = D0f.astype(np.float64)
+    else:
+        D0 = inputs.bf16_from_f64(D0f).view(np.int16)
+        old = bf16.to_f32(D0.view(np.uint16)).astype(np.float64)
+    import torch
+    D = _run(P, a, E4, sa, "tensor", b, E4, sb, "tensor", out, D0=D0)
+    if out == P.OUT_BF16:
+        D = D.view(torch.bfloat16) if D.dtype != torch.bfloat16 else D
+    op = (a, fp8.E4M3, sa, "tensor", b, fp8.E4M3, sb, "tensor")
+    ref, den = gemm.gemm(*op)
+    # the old value enters the FP32 sum exactly; its own rounding adds |old| * 2**-24
+    _check(P, out, D, ref + old, den + np.abs(old) * 2.0 ** -24 / 1e-5, "accumulate", op)
+
+
+@pytest.mark.parametrize("am,bm", [("row", "block"), ("row", "row"), ("tensor", "block"), ("row", "tensor")])
+@pytest.mark.parametrize("shape", [(256, 384, 512), (300, 260, 384), (128, 128, 128)],
+                         ids=lambda s: "x".join(map(str, s)))
+def test_gemm_grouped_scales(P, am, bm, shape):
+    M, N, K = shape
+    if am == "tensor":
+        a, sa = _operand_tensor(9, M, K, E4)
+    else:
+        a, sa = _operand_grouped(9, M, K, E4, am, kind="outliers")
+    if bm == "tensor":
+        b, sb = _operand_tensor(10, N, K, E4, std=0.02)
+    else:
+        b, sb = _operand_grouped(10, N, K, E4, bm, std=0.02)
+    for out in (0, 1):
+        D = _run(P, a, E4, sa, am, b, E4, sb, bm, out)
+        op = (a, fp8.E4M3, sa, am, b, fp8.E4M3, sb, bm)
+        ref, den = gemm.gemm(*op)
+        _check(P, out, D, ref, den, "grouped %s/%s %s" % (am, bm, shape), op)
+
+
+def test_gemm_grouped_split_k(P):
+    """Wgrad form (row scales on both operands) with a long reduction."""
+    M, N, K = 128, 256, 8192
+    a, sa = _operand_grouped(11, M, K, E5, "row", std=1e-3)
+    b, sb = _operand_grouped(12, N, K, E4, "row")
+    assert P.fp8_gemm_workspace_size(M, N, K, 1) > 0
+    D = _run(P, a, E5, sa, "row", b, E4, sb, "row", 1)
+    op = (a, fp8.E5M2, sa, "row", b, fp8.E4M3, sb, "row")
+    ref, den = gemm.gemm(*op)
+    check_fp32(host(D), ref, den, what="grouped split-k", slack=mfma_model.truncation_loss_full(*op))
+
+
+def test_gemm_padded_leading_dimension(P):
+    M, N, K = 200, 132, 256
+    a, sa = _operand_tensor(13, M, K, E4)
+    b, sb = _operand_tensor(14, N, K, E4)
+    D = _run(P, a, E4, sa, "tensor", b, E4, sb, "tensor", 1, ld_pad=32)
+    op = (a, fp8.E4M3, sa, "tensor", b, fp8.E4M3, sb, "tensor")
+    ref, den = gemm.gemm(*op)
+    check_fp32(host(D), ref, den, what="padded ld", slack=mfma_model.truncation_loss_full(*op))
+
+
+def test_gemm_empty_reduction(P):
+    import torch
+    a = np.zeros((64, 0), np.uint8)
+    b = np.zeros((32, 0), np.uint8)
+    da = torch.empty(64, 16, dtype=torch.uint8, device="cuda")[:, :0]
+    db = torch.empty(32, 16, dtype=torch.uint8, device="cuda")[:, :0]
+    s = to_dev(np.array([2.0], np.float32))
+    A = P.operand(da, E4, 0, s)
+    B = P.operand(db, E4, 0, s)
+    D = P.fp8_gemm(A, 64, B, 32, 0, P.OUT_FP32)
+    assert float(D.abs().max()) == 0.0
+    D0 = torch.full((64, 32), 3.0, dtype=torch.float32, device="cuda")
+    D = P.fp8_gemm(A, 64, B, 32, 0, P.OUT_FP32, D=D0, accumulate=True)
+    assert float((D - 3.0).abs().max()) == 0.0
+    del a, b
+
+
+def test_gemm_is_deterministic(P):
+    M, N, K = 128, 256, 8192      # split-K path
+    a, sa = _operand_tensor(15, M, K, E4)
+    b, sb = _operand_tensor(16, N, K, E4)
+    D1 = host(_run(P, a, E4, sa, "tensor", b, E4, sb, "tensor", 1))
+    D2 = host(_run(P, a, E4, sa, "tensor", b, E4, sb, "tensor", 1))
+    assert np.array_equal(D1.view(np.uint32), D2.view(np.uint32))
