@@ -57,6 +57,7 @@ struct Params {
     int M, N, K;
     int a_mode, b_mode;
     int ld_sa, ld_sb;          // scale row pitch (K/128) for grouped modes
+    uint32_t sa_bytes, sb_bytes;  // sizes of the scale arrays (grouped modes)
     int ksteps, ksteps_per_split, splits;
     int tiles_m, tiles_n;
     int accumulate;
@@ -65,10 +66,55 @@ struct Params {
 
 __device__ __forceinline__ uint32_t e8m0_of(float s) { return (__float_as_uint(s) >> 23) & 0xFFu; }
 
-__device__ __forceinline__ uint32_t f32_to_bf16(float f) {
-    const uint32_t u = __float_as_uint(f);
-    if ((u & 0x7FFFFFFFu) > 0x7F800000u) return (u >> 16) | 0x40u;  // quiet NaN
-    return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+typedef float v2f __attribute__((ext_vector_type(2)));
+typedef __bf16 v2bf __attribute__((ext_vector_type(2)));
+
+// Two FP32 values -> two BF16 (round to nearest even) in one word, low half
+// first: the conversion instruction (v_cvt_pk_bf16_f32).
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector((v2f){a, b}, v2bf));
+}
+__device__ __forceinline__ uint16_t to_bf16(float a) { return (uint16_t)pack_bf16x2(a, 0.0f); }
+
+typedef int v4i __attribute__((ext_vector_type(4)));
+
+// Raw buffer descriptor (base, num_records bytes; 32-bit data format); every
+// field is made wave-uniform so that it lives in SGPRs.
+__device__ __forceinline__ v4i make_rsrc(const void* base, uint32_t bytes) {
+    const uint64_t a = (uint64_t)base;
+    v4i r;
+    r.x = __builtin_amdgcn_readfirstlane((int)(uint32_t)a);
+    r.y = __builtin_amdgcn_readfirstlane((int)((a >> 32) & 0xFFFFu));
+    r.z = __builtin_amdgcn_readfirstlane((int)bytes);
+    r.w = (int)kRsrcWord3;
+    return r;
+}
+
+// LDS byte address of a __shared__ object (the value M0 takes for a DMA).
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+    return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) uint8_t*)p;
+}
+
+// Global -> LDS DMA of BYTES (16 or 4) per lane: lane l's data lands at
+// LDS address lds + BYTES * l; offsets at or beyond the descriptor's
+// num_records read as zero. Issued from inline assembly so that the
+// compiler, which cannot tell which LDS bytes a DMA writes, does not make
+// every later LDS read wait for it: the kernel waits explicitly
+// (s_waitcnt vmcnt(0) + barrier) before reading a stage. M0 is saved and
+// restored around the DMA (the compiler may keep a value there), and one wait
+// state separates the M0 write from the DMA that reads it.
+template <int BYTES>
+__device__ __forceinline__ void dma_to_lds(v4i rsrc, uint32_t lds, uint32_t voff) {
+    lds = (uint32_t)__builtin_amdgcn_readfirstlane((int)lds);   // wave-uniform by construction
+    uint32_t saved;
+    if constexpr (BYTES == 16)
+        asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\ts_nop 0\n\t"
+                     "buffer_load_dwordx4 %2, %3, 0 offen lds\n\ts_mov_b32 m0, %0"
+                     : "=&s"(saved) : "s"(lds), "v"(voff), "s"(rsrc) : "memory");
+    else
+        asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\ts_nop 0\n\t"
+                     "buffer_load_dword %2, %3, 0 offen lds\n\ts_mov_b32 m0, %0"
+                     : "=&s"(saved) : "s"(lds), "v"(voff), "s"(rsrc) : "memory");
 }
 
 template <int BM, int BN, int WM, int WN, int FA, int FB, int OUT, bool GROUPED, int GM>
@@ -82,6 +128,8 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_fp8_kernel(Params p) {
     static_assert(BM % (8 * NW) == 0 && BN % (8 * NW) == 0, "tile / wave mismatch");
 
     __shared__ __attribute__((aligned(1024))) uint8_t smem[2 * STAGE];
+    // grouped scales of the stage's rows (A then B), float, DMA'd like the operands
+    __shared__ __attribute__((aligned(16))) float ssc[GROUPED ? 2 * (BM + BN) : 1];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -105,10 +153,8 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_fp8_kernel(Params p) {
     const int kb1 = min(kb0 + p.ksteps_per_split, p.ksteps);
 
     const int valid_m = min(BM, p.M - m0), valid_n = min(BN, p.N - n0);
-    const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc(
-        (void*)(p.A + (int64_t)m0 * p.lda), 0, (int)(valid_m * p.lda), kRsrcWord3);
-    const __amdgpu_buffer_rsrc_t rb = __builtin_amdgcn_make_buffer_rsrc(
-        (void*)(p.B + (int64_t)n0 * p.ldb), 0, (int)(valid_n * p.ldb), kRsrcWord3);
+    const v4i ra = make_rsrc(p.A + (int64_t)m0 * p.lda, (uint32_t)(valid_m * p.lda));
+    const v4i rb = make_rsrc(p.B + (int64_t)n0 * p.ldb, (uint32_t)(valid_n * p.ldb));
 
     // per-lane source offsets of the DMA loads. Lane l of DMA load q fills
     // LDS row (wave * LOADS + q) * 8 + l / 8 at chunk position l % 8, so it
@@ -118,48 +164,42 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_fp8_kernel(Params p) {
     const uint32_t baseA = (uint32_t)((wave * A_LOADS * 8 + lrow) * p.lda) + kch;
     const uint32_t baseB = (uint32_t)((wave * B_LOADS * 8 + lrow) * p.ldb) + kch;
     const uint32_t stepA = (uint32_t)(8 * p.lda), stepB = (uint32_t)(8 * p.ldb);
+    const uint32_t smem_lds = lds_addr(smem);
+    const uint32_t ssc_lds = lds_addr(ssc);
+
+    // grouped scales: lane l of scale DMA t loads the scale of tile row
+    // t * 64 + l (A rows first, then B rows); rows past the matrix read zero
+    constexpr int SC_LOADS = (BM + BN) / 64;
+    v4i rsa{}, rsb{};
+    if constexpr (GROUPED) {
+        rsa = make_rsrc(p.sa, p.a_mode == kSTensor ? 0u : p.sa_bytes);
+        rsb = make_rsrc(p.sb, p.b_mode == kSTensor ? 0u : p.sb_bytes);
+    }
 
     auto load_stage = [&](int stage, int kb) {
         const int k0 = kb * kBK;
-        const bool kin = k0 + kch < p.K;
-        uint8_t* sA = smem + stage * STAGE;
-        uint8_t* sB = sA + A_BYTES;
+        // the k tail (K % 128 != 0) reads out of range on purpose: zeros
+        const uint32_t oob = (k0 + kch < p.K) ? 0u : kOOB;
+        const uint32_t sA = smem_lds + stage * STAGE + wave * A_LOADS * 1024;
+        const uint32_t sB = smem_lds + stage * STAGE + A_BYTES + wave * B_LOADS * 1024;
 #pragma unroll
-        for (int q = 0; q < A_LOADS; ++q) {
-            const uint32_t off = kin ? baseA + q * stepA + k0 : kOOB;
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_void_t*)(sA + (wave * A_LOADS + q) * 1024),
-                                                     16, off, 0, 0, 0);
-        }
+        for (int q = 0; q < A_LOADS; ++q)
+            dma_to_lds<16>(ra, sA + q * 1024, (baseA + q * stepA + k0) | oob);
 #pragma unroll
-        for (int q = 0; q < B_LOADS; ++q) {
-            const uint32_t off = kin ? baseB + q * stepB + k0 : kOOB;
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (lds_void_t*)(sB + (wave * B_LOADS + q) * 1024),
-                                                     16, off, 0, 0, 0);
-        }
-    };
-
-    // grouped scales: E8M0 of the lane's A row (per fragment i) and B row (per j)
-    int rowA[FM], rowB[FN];
-#pragma unroll
-    for (int i = 0; i < FM; ++i) rowA[i] = min(m0 + wm * WTM + i * 32 + (lane & 31), p.M - 1);
-#pragma unroll
-    for (int j = 0; j < FN; ++j) rowB[j] = min(n0 + wn * WTN + j * 32 + (lane & 31), p.N - 1);
-    uint32_t scA[FM], scB[FN];
-    auto load_scales = [&](int kb) {
-#pragma unroll
-        for (int i = 0; i < FM; ++i) {
-            if (p.a_mode == kSTensor) scA[i] = 127u;
-            else {
-                const int r = p.a_mode == kSRow ? rowA[i] : rowA[i] >> 7;
-                scA[i] = e8m0_of(p.sa[(int64_t)r * p.ld_sa + kb]);
-            }
-        }
-#pragma unroll
-        for (int j = 0; j < FN; ++j) {
-            if (p.b_mode == kSTensor) scB[j] = 127u;
-            else {
-                const int r = p.b_mode == kSRow ? rowB[j] : rowB[j] >> 7;
-                scB[j] = e8m0_of(p.sb[(int64_t)r * p.ld_sb + kb]);
+        for (int q = 0; q < B_LOADS; ++q)
+            dma_to_lds<16>(rb, sB + q * 1024, (baseB + q * stepB + k0) | oob);
+        if constexpr (GROUPED) {
+            for (int t = wave; t < SC_LOADS; t += NW) {
+                const int r = t * 64 + lane;                  // tile row, A rows then B rows
+                const bool is_a = r < BM;
+                const int row = is_a ? m0 + r : n0 + (r - BM);
+                const int mode = is_a ? p.a_mode : p.b_mode;
+                const int ld = is_a ? p.ld_sa : p.ld_sb;
+                const int srow = mode == kSBlock ? row >> 7 : row;
+                const uint32_t off = (uint32_t)(srow * ld + kb) * 4u;
+                const uint32_t dst = ssc_lds + (stage * (BM + BN) + t * 64) * 4;
+                if (t * 64 < BM) dma_to_lds<4>(rsa, dst, off);
+                else dma_to_lds<4>(rsb, dst, off);
             }
         }
     };
@@ -179,12 +219,20 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_fp8_kernel(Params p) {
     if (kb0 < kb1) load_stage(0, kb0);
     for (int kb = kb0; kb < kb1; ++kb) {
         const int stage = (kb - kb0) & 1;
-        if constexpr (GROUPED) load_scales(kb);
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         __syncthreads();
         if (kb + 1 < kb1) load_stage(stage ^ 1, kb + 1);
         const uint8_t* sA = smem + stage * STAGE;
         const uint8_t* sB = sA + A_BYTES;
+        uint32_t scA[FM], scB[FN];
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+            scA[i] = (GROUPED && p.a_mode != kSTensor)
+                         ? e8m0_of(ssc[stage * (BM + BN) + wm * WTM + i * 32 + fr]) : 127u;
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+            scB[j] = (GROUPED && p.b_mode != kSTensor)
+                         ? e8m0_of(ssc[stage * (BM + BN) + BM + wn * WTN + j * 32 + fr]) : 127u;
 #pragma unroll
         for (int kk = 0; kk < 2; ++kk) {
             v8i af[FM], bf[FN];
@@ -220,67 +268,92 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_fp8_kernel(Params p) {
         }
     }
 
-    // ---- epilogue: lane holds, for fragment (i, j), output row
-    // m = i*32 + (lane & 31) and columns n = j*32 + 8 g + 4 (lane >> 5) + {0..3}
+    // ---- epilogue. Lane l holds, for fragment (i, j), wave-tile row
+    // i*32 + (l & 31) and columns j*32 + 8g + 4(l >> 5) + {0..3}, g = 0..3.
+    // Written straight to memory that would scatter 16-byte pieces over 32
+    // rows per store; instead each wave stages its FP32 tile in its own part
+    // of the (now idle) stage buffers, 16-byte chunks XOR-swizzled by row so
+    // that both the writes and the row reads are free of bank conflicts, and
+    // then stores whole rows: consecutive lanes on consecutive 16-byte chunks
+    // (4 FP32 values), converted and scaled on the way out.
     float alpha = p.alpha;
     if (OUT != 2) {
         if (p.a_mode == kSTensor) alpha *= p.sa[0];
         if (p.b_mode == kSTensor) alpha *= p.sb[0];
     }
+    constexpr int ROWB = WTN * 4;                 // bytes of one staged wave-tile row (FP32)
+    constexpr int CPR = ROWB / 16;                // 16-byte chunks per row
+    constexpr int REGION = 2 * STAGE / NW;        // LDS bytes per wave
+    constexpr int RPP = (REGION / ROWB) < WTM ? (REGION / ROWB) : WTM;   // rows per pass
+    static_assert(RPP % 32 == 0 && WTM % RPP == 0 && (RPP * CPR) % 64 == 0, "epilogue tiling");
+    static_assert(CPR >= 16, "row swizzle needs 16 chunks per row");
+    uint8_t* ep = smem + wave * REGION;
+    const int mrow0 = m0 + wm * WTM;
+    const int ncol0 = n0 + wn * WTN;
+    float* const part = p.partial + (int64_t)ks * p.M * p.N;
+    __syncthreads();   // every wave is done with the last stage
 #pragma unroll
-    for (int i = 0; i < FM; ++i) {
-        const int m = m0 + wm * WTM + i * 32 + (lane & 31);
-        if (m >= p.M) continue;
+    for (int pass = 0; pass < WTM / RPP; ++pass) {
 #pragma unroll
-        for (int j = 0; j < FN; ++j) {
+        for (int ii = 0; ii < RPP / 32; ++ii) {
+            const int i = pass * (RPP / 32) + ii;
+            const int r = ii * 32 + (lane & 31);
 #pragma unroll
-            for (int g = 0; g < 4; ++g) {
-                const int n = n0 + wn * WTN + j * 32 + g * 8 + (lane >> 5) * 4;
-                if (n >= p.N) continue;
-                float v0 = acc[i][j][4 * g + 0], v1 = acc[i][j][4 * g + 1];
-                float v2 = acc[i][j][4 * g + 2], v3 = acc[i][j][4 * g + 3];
-                if constexpr (OUT == 2) {
-                    // split-K partial sums, dense [splits][M][N] FP32 (N % 4 == 0)
-                    float* dst = p.partial + ((int64_t)ks * p.M + m) * p.N + n;
-                    *reinterpret_cast<float4*>(dst) = make_float4(v0, v1, v2, v3);
+            for (int j = 0; j < FN; ++j)
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    const int chunk = j * 8 + g * 2 + (lane >> 5);
+                    float4 v = make_float4(acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2],
+                                           acc[i][j][4 * g + 3]);
+                    *reinterpret_cast<float4*>(ep + r * ROWB + ((chunk ^ (r & 15)) << 4)) = v;
+                }
+        }
+        __syncthreads();
+#pragma unroll
+        for (int it = 0; it < RPP * CPR / 64; ++it) {
+            const int q = it * 64 + lane;
+            const int r = q / CPR, c = q % CPR;
+            float4 v = *reinterpret_cast<const float4*>(ep + r * ROWB + ((c ^ (r & 15)) << 4));
+            const int m = mrow0 + pass * RPP + r;
+            const int n = ncol0 + c * 4;
+            if (m >= p.M || n >= p.N) continue;
+            if constexpr (OUT == 2) {
+                // split-K partial sums, dense [splits][M][N] FP32 (N % 4 == 0)
+                *reinterpret_cast<float4*>(part + (int64_t)m * p.N + n) = v;
+                continue;
+            }
+            v.x *= alpha; v.y *= alpha; v.z *= alpha; v.w *= alpha;
+            if (n + 3 < p.N) {
+                if constexpr (OUT == kOutF32) {
+                    float4* dst = reinterpret_cast<float4*>(reinterpret_cast<float*>(p.D) + (int64_t)m * p.ldd + n);
+                    if (p.accumulate) {
+                        const float4 o = *dst;
+                        v.x += o.x; v.y += o.y; v.z += o.z; v.w += o.w;
+                    }
+                    *dst = v;
                 } else {
-                    v0 *= alpha; v1 *= alpha; v2 *= alpha; v3 *= alpha;
-                    const bool full = n + 3 < p.N;
+                    uint2* dst = reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(p.D) + (int64_t)m * p.ldd + n);
+                    if (p.accumulate) {
+                        const uint2 o = *dst;
+                        v.x += bf16lo(o.x); v.y += bf16hi(o.x); v.z += bf16lo(o.y); v.w += bf16hi(o.y);
+                    }
+                    *dst = make_uint2(pack_bf16x2(v.x, v.y), pack_bf16x2(v.z, v.w));
+                }
+            } else {
+                // ragged right edge: element by element
+                const float vv[4] = {v.x, v.y, v.z, v.w};
+                for (int t = 0; t < 4 && n + t < p.N; ++t) {
                     if constexpr (OUT == kOutF32) {
-                        float* dst = reinterpret_cast<float*>(p.D) + (int64_t)m * p.ldd + n;
-                        if (full) {
-                            if (p.accumulate) {
-                                const float4 o = *reinterpret_cast<const float4*>(dst);
-                                v0 += o.x; v1 += o.y; v2 += o.z; v3 += o.w;
-                            }
-                            *reinterpret_cast<float4*>(dst) = make_float4(v0, v1, v2, v3);
-                        } else {
-                            const float vv[4] = {v0, v1, v2, v3};
-                            for (int t = 0; t < 4 && n + t < p.N; ++t)
-                                dst[t] = p.accumulate ? dst[t] + vv[t] : vv[t];
-                        }
+                        float* dst = reinterpret_cast<float*>(p.D) + (int64_t)m * p.ldd + n + t;
+                        *dst = p.accumulate ? *dst + vv[t] : vv[t];
                     } else {
-                        uint16_t* dst = reinterpret_cast<uint16_t*>(p.D) + (int64_t)m * p.ldd + n;
-                        if (full) {
-                            if (p.accumulate) {
-                                const uint2 o = *reinterpret_cast<const uint2*>(dst);
-                                v0 += bf16lo(o.x); v1 += bf16hi(o.x); v2 += bf16lo(o.y); v3 += bf16hi(o.y);
-                            }
-                            const uint2 w = make_uint2(f32_to_bf16(v0) | (f32_to_bf16(v1) << 16),
-                                                       f32_to_bf16(v2) | (f32_to_bf16(v3) << 16));
-                            *reinterpret_cast<uint2*>(dst) = w;
-                        } else {
-                            const float vv[4] = {v0, v1, v2, v3};
-                            for (int t = 0; t < 4 && n + t < p.N; ++t) {
-                                float v = vv[t];
-                                if (p.accumulate) v += __uint_as_float((uint32_t)dst[t] << 16);
-                                dst[t] = (uint16_t)f32_to_bf16(v);
-                            }
-                        }
+                        uint16_t* dst = reinterpret_cast<uint16_t*>(p.D) + (int64_t)m * p.ldd + n + t;
+                        *dst = to_bf16(p.accumulate ? vv[t] + __uint_as_float((uint32_t)*dst << 16) : vv[t]);
                     }
                 }
             }
         }
+        if (pass + 1 < WTM / RPP) __syncthreads();   // the next pass reuses the region
     }
 }
 
@@ -317,8 +390,7 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restr
             const uint2 o = *reinterpret_cast<const uint2*>(dst);
             s.x += bf16lo(o.x); s.y += bf16hi(o.x); s.z += bf16lo(o.y); s.w += bf16hi(o.y);
         }
-        *reinterpret_cast<uint2*>(dst) = make_uint2(f32_to_bf16(s.x) | (f32_to_bf16(s.y) << 16),
-                                                    f32_to_bf16(s.z) | (f32_to_bf16(s.w) << 16));
+        *reinterpret_cast<uint2*>(dst) = make_uint2(pack_bf16x2(s.x, s.y), pack_bf16x2(s.z, s.w));
     }
 }
 
@@ -396,6 +468,13 @@ void launch_gemm(const GemmProblem& g, void* ws, hipStream_t stream) {
     prm.M = (int)g.M; prm.N = (int)g.N; prm.K = (int)g.K;
     prm.a_mode = g.sa_mode; prm.b_mode = g.sb_mode;
     prm.ld_sa = (int)(g.K / kBK); prm.ld_sb = (int)(g.K / kBK);
+    auto scale_bytes = [&](int mode, int64_t rows) -> uint32_t {
+        if (mode == kSTensor) return 4u;
+        const int64_t srows = mode == kSRow ? rows : (rows + 127) / 128;
+        return (uint32_t)(srows * (g.K / kBK) * 4);
+    };
+    prm.sa_bytes = scale_bytes(g.sa_mode, g.M);
+    prm.sb_bytes = scale_bytes(g.sb_mode, g.N);
     prm.ksteps = (int)((g.K + kBK - 1) / kBK);
     prm.ksteps_per_split = pl.ksteps_per_split;
     prm.splits = pl.splits;
