@@ -42,7 +42,8 @@ typedef int v8i __attribute__((ext_vector_type(8)));
 typedef float v16f __attribute__((ext_vector_type(16)));
 typedef __attribute__((address_space(3))) void lds_void_t;
 
-constexpr int kBK = 128;                   // bytes of k per stage
+constexpr int kBK = 128;                   // k block of the grouped scales (and of split-K ranges)
+constexpr int kSL = 64;                    // bytes of k per pipeline slice
 constexpr uint32_t kRsrcWord3 = 0x00020000u;  // raw buffer, 32-bit data format
 constexpr uint32_t kOOB = 0x80000000u;     // offset that fails the range check
 
@@ -117,19 +118,27 @@ __device__ __forceinline__ void dma_to_lds(v4i rsrc, uint32_t lds, uint32_t voff
                      : "=&s"(saved) : "s"(lds), "v"(voff), "s"(rsrc) : "memory");
 }
 
-template <int BM, int BN, int WM, int WN, int FA, int FB, int OUT, bool GROUPED, int GM>
+template <int BM, int BN, int WM, int WN, int FA, int FB, int OUT, bool GROUPED, int GM, int NST>
 __global__ __launch_bounds__(WM * WN * 64) void gemm_fp8_kernel(Params p) {
     constexpr int NW = WM * WN;
     constexpr int WTM = BM / WM, WTN = BN / WN;
     constexpr int FM = WTM / 32, FN = WTN / 32;
-    constexpr int A_BYTES = BM * kBK, B_BYTES = BN * kBK;
-    constexpr int STAGE = A_BYTES + B_BYTES;
-    constexpr int A_LOADS = BM / 8 / NW, B_LOADS = BN / 8 / NW;   // 1 KB DMA loads per wave
-    static_assert(BM % (8 * NW) == 0 && BN % (8 * NW) == 0, "tile / wave mismatch");
+    constexpr int A_BYTES = BM * kSL, B_BYTES = BN * kSL;
+    constexpr int STAGE = A_BYTES + B_BYTES;        // one 64-byte k slice of both tiles
+    // 1 KB DMA loads (16 rows of 64 bytes) per wave and slice; when the row
+    // blocks do not divide evenly, the surplus loads repeat earlier blocks
+    // (the same bytes to the same place), so every wave issues the same
+    // number of loads and can wait on an exact count
+    constexpr int A_BLK = BM / 16, B_BLK = BN / 16;
+    constexpr int A_PER = (A_BLK + NW - 1) / NW, B_PER = (B_BLK + NW - 1) / NW;
+    constexpr int SC_BLK = (BM + BN) / 64;          // 64 scales per 4-byte DMA load
+    constexpr int LOADS = A_PER + B_PER + (GROUPED ? 1 : 0);
+    static_assert(BM % 16 == 0 && BN % 16 == 0 && (BM + BN) % 64 == 0, "tile shape");
+    static_assert(NST >= 3 && NST <= 4, "pipeline depth");
 
-    __shared__ __attribute__((aligned(1024))) uint8_t smem[2 * STAGE];
-    // grouped scales of the stage's rows (A then B), float, DMA'd like the operands
-    __shared__ __attribute__((aligned(16))) float ssc[GROUPED ? 2 * (BM + BN) : 1];
+    __shared__ __attribute__((aligned(1024))) uint8_t smem[NST * STAGE];
+    // grouped scales of a slice's rows (A then B), float, DMA'd like the operands
+    __shared__ __attribute__((aligned(16))) float ssc[GROUPED ? NST * (BM + BN) : 1];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -149,58 +158,66 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_fp8_kernel(Params p) {
     const int r2 = rem - group * GM * p.tiles_n;
     const int tm = first_m + r2 % gsz, tn = r2 / gsz;
     const int m0 = tm * BM, n0 = tn * BN;
-    const int kb0 = ks * p.ksteps_per_split;
-    const int kb1 = min(kb0 + p.ksteps_per_split, p.ksteps);
+    // k slices [s0, s1) of 64 bytes: this split's 128-wide k blocks, twice
+    const int s0 = 2 * ks * p.ksteps_per_split;
+    const int s1 = 2 * min((ks + 1) * p.ksteps_per_split, p.ksteps);
 
     const int valid_m = min(BM, p.M - m0), valid_n = min(BN, p.N - n0);
     const v4i ra = make_rsrc(p.A + (int64_t)m0 * p.lda, (uint32_t)(valid_m * p.lda));
     const v4i rb = make_rsrc(p.B + (int64_t)n0 * p.ldb, (uint32_t)(valid_n * p.ldb));
 
-    // per-lane source offsets of the DMA loads. Lane l of DMA load q fills
-    // LDS row (wave * LOADS + q) * 8 + l / 8 at chunk position l % 8, so it
-    // fetches source chunk (l % 8) ^ (row & 7) = (l % 8) ^ (l / 8).
-    const int lrow = lane >> 3;
-    const int kch = ((lane & 7) ^ lrow) * 16;
-    const uint32_t baseA = (uint32_t)((wave * A_LOADS * 8 + lrow) * p.lda) + kch;
-    const uint32_t baseB = (uint32_t)((wave * B_LOADS * 8 + lrow) * p.ldb) + kch;
-    const uint32_t stepA = (uint32_t)(8 * p.lda), stepB = (uint32_t)(8 * p.ldb);
+    // LDS layout of a slice: row r of a tile is 64 bytes (four 16-byte chunks)
+    // and its chunk c sits at position c ^ key(r), key(r) = ((r >> 1) & 3) ^
+    // ((r >> 3) & 1). Among 16 consecutive rows the rows sharing a 64-byte
+    // position in a 256-byte bank line get distinct keys, and so do the rows
+    // of 8 consecutive rows sharing a position in a 128-byte line: the 16 (or
+    // 8) lanes of a ds_read_b128 phase, reading consecutive rows at the same
+    // logical chunk, hit distinct banks with 64 (or 32) four-byte banks.
+    // Lane l of a DMA load fills row 16 * blk + l / 4 at position l % 4; since
+    // blocks are 16 rows, key(row) = ((l >> 3) & 3) ^ ((l >> 5) & 1) for every
+    // block, so each lane fetches one fixed chunk of its row.
+    const int dkey = ((lane >> 3) & 3) ^ ((lane >> 5) & 1);
+    const int kch = ((lane & 3) ^ dkey) * 16;
+    const uint32_t rowA = (uint32_t)((lane >> 2) * p.lda), rowB = (uint32_t)((lane >> 2) * p.ldb);
+    const uint32_t blkA = (uint32_t)(16 * p.lda), blkB = (uint32_t)(16 * p.ldb);
     const uint32_t smem_lds = lds_addr(smem);
     const uint32_t ssc_lds = lds_addr(ssc);
 
-    // grouped scales: lane l of scale DMA t loads the scale of tile row
-    // t * 64 + l (A rows first, then B rows); rows past the matrix read zero
-    constexpr int SC_LOADS = (BM + BN) / 64;
     v4i rsa{}, rsb{};
     if constexpr (GROUPED) {
         rsa = make_rsrc(p.sa, p.a_mode == kSTensor ? 0u : p.sa_bytes);
         rsb = make_rsrc(p.sb, p.b_mode == kSTensor ? 0u : p.sb_bytes);
     }
 
-    auto load_stage = [&](int stage, int kb) {
-        const int k0 = kb * kBK;
-        // the k tail (K % 128 != 0) reads out of range on purpose: zeros
-        const uint32_t oob = (k0 + kch < p.K) ? 0u : kOOB;
-        const uint32_t sA = smem_lds + stage * STAGE + wave * A_LOADS * 1024;
-        const uint32_t sB = smem_lds + stage * STAGE + A_BYTES + wave * B_LOADS * 1024;
+    // all LOADS DMA loads of slice `sl` into ring stage `st`
+    auto load_slice = [&](int st, int sl) {
+        const int k0 = sl * kSL;
+        // the k tail (K % 64 != 0) reads out of range on purpose: zeros
+        const uint32_t off = (k0 + kch < p.K) ? (uint32_t)(k0 + kch) : kOOB;
+        const uint32_t sbase = smem_lds + st * STAGE;
 #pragma unroll
-        for (int q = 0; q < A_LOADS; ++q)
-            dma_to_lds<16>(ra, sA + q * 1024, (baseA + q * stepA + k0) | oob);
+        for (int q = 0; q < A_PER; ++q) {
+            const int blk = (wave * A_PER + q) % A_BLK;
+            dma_to_lds<16>(ra, sbase + blk * 1024, rowA + blk * blkA + off);
+        }
 #pragma unroll
-        for (int q = 0; q < B_LOADS; ++q)
-            dma_to_lds<16>(rb, sB + q * 1024, (baseB + q * stepB + k0) | oob);
+        for (int q = 0; q < B_PER; ++q) {
+            const int blk = (wave * B_PER + q) % B_BLK;
+            dma_to_lds<16>(rb, sbase + A_BYTES + blk * 1024, rowB + blk * blkB + off);
+        }
         if constexpr (GROUPED) {
-            for (int t = wave; t < SC_LOADS; t += NW) {
-                const int r = t * 64 + lane;                  // tile row, A rows then B rows
-                const bool is_a = r < BM;
-                const int row = is_a ? m0 + r : n0 + (r - BM);
-                const int mode = is_a ? p.a_mode : p.b_mode;
-                const int ld = is_a ? p.ld_sa : p.ld_sb;
-                const int srow = mode == kSBlock ? row >> 7 : row;
-                const uint32_t off = (uint32_t)(srow * ld + kb) * 4u;
-                const uint32_t dst = ssc_lds + (stage * (BM + BN) + t * 64) * 4;
-                if (t * 64 < BM) dma_to_lds<4>(rsa, dst, off);
-                else dma_to_lds<4>(rsb, dst, off);
-            }
+            // lane l of scale load t brings the scale of tile row 64 t + l
+            // (A rows, then B rows) for the 128-wide k block of the slice
+            const int t = wave % SC_BLK;
+            const int r = t * 64 + lane;
+            const bool is_a = t * 64 < BM;
+            const int row = is_a ? m0 + r : n0 + (r - BM);
+            const int mode = is_a ? p.a_mode : p.b_mode;
+            const int ld = is_a ? p.ld_sa : p.ld_sb;
+            const int srow = mode == kSBlock ? row >> 7 : row;
+            const uint32_t soff = (uint32_t)(srow * ld + (sl >> 1)) * 4u;
+            const uint32_t dst = ssc_lds + (st * (BM + BN) + t * 64) * 4;
+            dma_to_lds<4>(is_a ? rsa : rsb, dst, soff);
         }
     };
 
@@ -212,60 +229,66 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_fp8_kernel(Params p) {
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
 
-    // LDS read addresses of the fragments (row within the stage, swizzle key)
-    const int fr = lane & 31;           // fragment row of this lane
-    const int khalf = (lane >> 5) * 2;  // first of this lane's two 16-byte chunks in a 64-byte slice
+    const int fr = lane & 31;                 // fragment row of this lane
+    const int c0 = (lane >> 5) * 2;           // this lane's two 16-byte chunks of a slice row
+    // key of the lane's fragment rows (fragments start at multiples of 32)
+    const int key = ((fr >> 1) & 3) ^ ((fr >> 3) & 1);
+    const int pos0 = (c0 ^ key) << 4, pos1 = ((c0 + 1) ^ key) << 4;
 
-    if (kb0 < kb1) load_stage(0, kb0);
-    for (int kb = kb0; kb < kb1; ++kb) {
-        const int stage = (kb - kb0) & 1;
-        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    // prologue: slices s0 .. s0 + NST - 2 in flight
+#pragma unroll
+    for (int t = 0; t < NST - 1; ++t)
+        if (s0 + t < s1) load_slice(t, s0 + t);
+
+    for (int sl = s0; sl < s1; ++sl) {
+        const int st = (sl - s0) % NST;
+        // this wave's loads of slice sl are done once at most `later` slices
+        // issued after it remain outstanding
+        const int later = min(s1 - 1 - sl, NST - 2);
+        if (later >= 2) asm volatile("s_waitcnt vmcnt(%0)" :: "n"(2 * LOADS) : "memory");
+        else if (later == 1) asm volatile("s_waitcnt vmcnt(%0)" :: "n"(LOADS) : "memory");
+        else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        // every wave's loads of slice sl have landed, and every wave is done
+        // with slice sl - 1, whose stage the next load reuses
         __syncthreads();
-        if (kb + 1 < kb1) load_stage(stage ^ 1, kb + 1);
-        const uint8_t* sA = smem + stage * STAGE;
+        const uint8_t* sA = smem + st * STAGE;
         const uint8_t* sB = sA + A_BYTES;
         uint32_t scA[FM], scB[FN];
 #pragma unroll
         for (int i = 0; i < FM; ++i)
             scA[i] = (GROUPED && p.a_mode != kSTensor)
-                         ? e8m0_of(ssc[stage * (BM + BN) + wm * WTM + i * 32 + fr]) : 127u;
+                         ? e8m0_of(ssc[st * (BM + BN) + wm * WTM + i * 32 + fr]) : 127u;
 #pragma unroll
         for (int j = 0; j < FN; ++j)
             scB[j] = (GROUPED && p.b_mode != kSTensor)
-                         ? e8m0_of(ssc[stage * (BM + BN) + BM + wn * WTN + j * 32 + fr]) : 127u;
+                         ? e8m0_of(ssc[st * (BM + BN) + BM + wn * WTN + j * 32 + fr]) : 127u;
+        v8i af[FM], bf[FN];
 #pragma unroll
-        for (int kk = 0; kk < 2; ++kk) {
-            v8i af[FM], bf[FN];
+        for (int i = 0; i < FM; ++i) {
+            const uint8_t* row = sA + (wm * WTM + i * 32 + fr) * kSL;
+            const uint4 lo = *reinterpret_cast<const uint4*>(row + pos0);
+            const uint4 hi = *reinterpret_cast<const uint4*>(row + pos1);
+            af[i] = v8i{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, (int)hi.x, (int)hi.y, (int)hi.z, (int)hi.w};
+        }
 #pragma unroll
-            for (int i = 0; i < FM; ++i) {
-                const int r = wm * WTM + i * 32 + fr;
-                const uint8_t* row = sA + r * kBK;
-                const int c0 = kk * 4 + khalf;
-                const uint4 lo = *reinterpret_cast<const uint4*>(row + ((c0 ^ (r & 7)) << 4));
-                const uint4 hi = *reinterpret_cast<const uint4*>(row + (((c0 + 1) ^ (r & 7)) << 4));
-                af[i] = v8i{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, (int)hi.x, (int)hi.y, (int)hi.z, (int)hi.w};
-            }
+        for (int j = 0; j < FN; ++j) {
+            const uint8_t* row = sB + (wn * WTN + j * 32 + fr) * kSL;
+            const uint4 lo = *reinterpret_cast<const uint4*>(row + pos0);
+            const uint4 hi = *reinterpret_cast<const uint4*>(row + pos1);
+            bf[j] = v8i{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, (int)hi.x, (int)hi.y, (int)hi.z, (int)hi.w};
+        }
+        if (sl + NST - 1 < s1) load_slice((st + NST - 1) % NST, sl + NST - 1);
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
 #pragma unroll
             for (int j = 0; j < FN; ++j) {
-                const int r = wn * WTN + j * 32 + fr;
-                const uint8_t* row = sB + r * kBK;
-                const int c0 = kk * 4 + khalf;
-                const uint4 lo = *reinterpret_cast<const uint4*>(row + ((c0 ^ (r & 7)) << 4));
-                const uint4 hi = *reinterpret_cast<const uint4*>(row + (((c0 + 1) ^ (r & 7)) << 4));
-                bf[j] = v8i{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, (int)hi.x, (int)hi.y, (int)hi.z, (int)hi.w};
+                if constexpr (GROUPED)
+                    acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
+                        bf[j], af[i], acc[i][j], FB, FA, 0, (int)scB[j], 0, (int)scA[i]);
+                else
+                    acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
+                        bf[j], af[i], acc[i][j], FB, FA, 0, 127, 0, 127);
             }
-#pragma unroll
-            for (int i = 0; i < FM; ++i)
-#pragma unroll
-                for (int j = 0; j < FN; ++j) {
-                    if constexpr (GROUPED)
-                        acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
-                            bf[j], af[i], acc[i][j], FB, FA, 0, (int)scB[j], 0, (int)scA[i]);
-                    else
-                        acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
-                            bf[j], af[i], acc[i][j], FB, FA, 0, 127, 0, 127);
-                }
-        }
     }
 
     // ---- epilogue. Lane l holds, for fragment (i, j), wave-tile row
@@ -283,10 +306,13 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_fp8_kernel(Params p) {
     }
     constexpr int ROWB = WTN * 4;                 // bytes of one staged wave-tile row (FP32)
     constexpr int CPR = ROWB / 16;                // 16-byte chunks per row
-    constexpr int REGION = 2 * STAGE / NW;        // LDS bytes per wave
-    constexpr int RPP = (REGION / ROWB) < WTM ? (REGION / ROWB) : WTM;   // rows per pass
-    static_assert(RPP % 32 == 0 && WTM % RPP == 0 && (RPP * CPR) % 64 == 0, "epilogue tiling");
-    static_assert(CPR >= 16, "row swizzle needs 16 chunks per row");
+    constexpr int REGION = NST * STAGE / NW;      // LDS bytes per wave
+    constexpr int RFIT = (REGION / ROWB) / 32 * 32;
+    constexpr int RPP = RFIT < WTM ? RFIT : WTM;  // rows per pass
+    // XOR key of the chunk swizzle: 16 distinct keys when rows have 16*k chunks, else 8
+    constexpr int SWZ = (CPR % 16 == 0) ? 15 : 7;
+    static_assert(RPP >= 32 && WTM % RPP == 0 && (RPP * CPR) % 64 == 0, "epilogue tiling");
+    static_assert(CPR % 8 == 0, "row swizzle needs 8k chunks per row");
     uint8_t* ep = smem + wave * REGION;
     const int mrow0 = m0 + wm * WTM;
     const int ncol0 = n0 + wn * WTN;
@@ -305,7 +331,7 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_fp8_kernel(Params p) {
                     const int chunk = j * 8 + g * 2 + (lane >> 5);
                     float4 v = make_float4(acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2],
                                            acc[i][j][4 * g + 3]);
-                    *reinterpret_cast<float4*>(ep + r * ROWB + ((chunk ^ (r & 15)) << 4)) = v;
+                    *reinterpret_cast<float4*>(ep + r * ROWB + ((chunk ^ (r & SWZ)) << 4)) = v;
                 }
         }
         __syncthreads();
@@ -313,7 +339,7 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_fp8_kernel(Params p) {
         for (int it = 0; it < RPP * CPR / 64; ++it) {
             const int q = it * 64 + lane;
             const int r = q / CPR, c = q % CPR;
-            float4 v = *reinterpret_cast<const float4*>(ep + r * ROWB + ((c ^ (r & 15)) << 4));
+            float4 v = *reinterpret_cast<const float4*>(ep + r * ROWB + ((c ^ (r & SWZ)) << 4));
             const int m = mrow0 + pass * RPP + r;
             const int n = ncol0 + c * 4;
             if (m >= p.M || n >= p.N) continue;
@@ -397,32 +423,47 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restr
 // ---- tile configurations and the plan for a problem ---------------------------
 
 struct Plan {
+    int cfg;             // index into kTiles
     int bm, bn;          // tile
     int splits;          // k slices
     int ksteps_per_split;
 };
 
+struct TileCfg {
+    int bm, bn;
+    float eff;           // relative MFMA efficiency of the configuration
+};
+// 256x256 and 256x192: 8 waves (2 per SIMD) in a 4x2 grid (wave tiles 64x128,
+// 64x96); 128x128: 4 waves in 2x2 (wave tiles 64x64) for small problems.
+constexpr TileCfg kTiles[] = {{256, 256, 1.0f}, {256, 192, 0.95f}, {128, 128, 0.35f}};
 constexpr int kCUs = 256;
 
+// Pick the tile shape and the k split with the smallest estimated time: MFMA
+// time of the waves of work units over the CUs, plus the traffic of split-K
+// partial sums (written, then read by the reduction) when splitting.
 Plan make_plan(int64_t M, int64_t N, int64_t K, int out) {
     const int ksteps = (int)((K + kBK - 1) / kBK);
-    Plan best{256, 256, 1, ksteps};
-    const int64_t big_tiles = ((M + 255) / 256) * ((N + 255) / 256);
-    if (big_tiles < kCUs / 2) {
-        const int64_t small_tiles = ((M + 127) / 128) * ((N + 127) / 128);
-        if (small_tiles > big_tiles) best = Plan{128, 128, 1, ksteps};
-    }
-    const int64_t tiles = ((M + best.bm - 1) / best.bm) * ((N + best.bn - 1) / best.bn);
-    if (tiles == 0) return best;
-    // split K when the grid covers well under the CUs and the k range is long
-    // enough; split-K needs N % 4 == 0 for the vector partials
-    if (tiles < kCUs / 2 && ksteps >= 8 && (N % 4) == 0) {
-        int s = (int)((kCUs + tiles - 1) / tiles);
-        if (s > ksteps / 4) s = ksteps / 4;
-        if (s > 16) s = 16;
-        if (s > 1) {
-            best.ksteps_per_split = (ksteps + s - 1) / s;
-            best.splits = (ksteps + best.ksteps_per_split - 1) / best.ksteps_per_split;
+    Plan best{0, 256, 256, 1, ksteps};
+    double best_cost = -1.0;
+    for (int c = 0; c < 3; ++c) {
+        const TileCfg t = kTiles[c];
+        const int64_t tiles = ((M + t.bm - 1) / t.bm) * ((N + t.bn - 1) / t.bn);
+        if (tiles == 0) return best;
+        const int max_s = (N % 4 == 0) ? (ksteps / 4 < 16 ? ksteps / 4 : 16) : 1;
+        for (int s = 1; s <= (max_s > 1 ? max_s : 1); ++s) {
+            const int kps = (ksteps + s - 1) / s;
+            const int splits = kps > 0 ? (ksteps + kps - 1) / kps : 1;
+            if (splits != s) continue;
+            const int64_t units = tiles * splits;
+            const int64_t waves = (units + kCUs - 1) / kCUs;
+            // cycles: one k-step of a tile is bm*bn*128*2 FLOP at 8192 FLOP/clk
+            double cost = (double)waves * t.bm * t.bn * (kps > 0 ? kps : 1) * 256.0 / 8192.0 / t.eff;
+            if (splits > 1)   // partials written and read back, mostly in the 256 MB MALL (~8 KB/clk)
+                cost += 2.0 * splits * (double)M * N * 4.0 / 8192.0;
+            if (best_cost < 0 || cost < best_cost) {
+                best_cost = cost;
+                best = Plan{c, t.bm, t.bn, splits, kps};
+            }
         }
     }
     (void)out;
@@ -432,23 +473,25 @@ Plan make_plan(int64_t M, int64_t N, int64_t K, int out) {
 template <int BM, int BN, int WM, int WN, int FA, int FB, int OUT>
 void launch_cfg(const Params& prm, bool grouped, int grid, hipStream_t stream) {
     constexpr int GM = 8;
+    constexpr int NST = 4;
     if (grouped)
-        gemm_fp8_kernel<BM, BN, WM, WN, FA, FB, OUT, true, GM><<<grid, WM * WN * 64, 0, stream>>>(prm);
+        gemm_fp8_kernel<BM, BN, WM, WN, FA, FB, OUT, true, GM, NST><<<grid, WM * WN * 64, 0, stream>>>(prm);
     else
-        gemm_fp8_kernel<BM, BN, WM, WN, FA, FB, OUT, false, GM><<<grid, WM * WN * 64, 0, stream>>>(prm);
+        gemm_fp8_kernel<BM, BN, WM, WN, FA, FB, OUT, false, GM, NST><<<grid, WM * WN * 64, 0, stream>>>(prm);
 }
 
-template <int BM, int BN, int FA, int FB>
+template <int BM, int BN, int WM, int WN, int FA, int FB>
 void launch_tile(const Params& prm, int out, bool grouped, int grid, hipStream_t stream) {
-    if (out == 2) launch_cfg<BM, BN, 2, 2, FA, FB, 2>(prm, grouped, grid, stream);
-    else if (out == kOutF32) launch_cfg<BM, BN, 2, 2, FA, FB, kOutF32>(prm, grouped, grid, stream);
-    else launch_cfg<BM, BN, 2, 2, FA, FB, kOutBF16>(prm, grouped, grid, stream);
+    if (out == 2) launch_cfg<BM, BN, WM, WN, FA, FB, 2>(prm, grouped, grid, stream);
+    else if (out == kOutF32) launch_cfg<BM, BN, WM, WN, FA, FB, kOutF32>(prm, grouped, grid, stream);
+    else launch_cfg<BM, BN, WM, WN, FA, FB, kOutBF16>(prm, grouped, grid, stream);
 }
 
 template <int FA, int FB>
 void launch_fmt(const Params& prm, const Plan& pl, int out, bool grouped, int grid, hipStream_t stream) {
-    if (pl.bm == 256) launch_tile<256, 256, FA, FB>(prm, out, grouped, grid, stream);
-    else launch_tile<128, 128, FA, FB>(prm, out, grouped, grid, stream);
+    if (pl.cfg == 0) launch_tile<256, 256, 4, 2, FA, FB>(prm, out, grouped, grid, stream);
+    else if (pl.cfg == 1) launch_tile<256, 192, 4, 2, FA, FB>(prm, out, grouped, grid, stream);
+    else launch_tile<128, 128, 2, 2, FA, FB>(prm, out, grouped, grid, stream);
 }
 
 }  // namespace
