@@ -14,6 +14,7 @@ timed on a slice of the same workload.
 """
 
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -35,6 +36,10 @@ def parse():
     ap.add_argument("--tokens", type=int, default=8192)
     ap.add_argument("--cpu-tokens", type=int, default=4096,
                     help="tokens of the workload the CPU oracle is timed on (0: skip)")
+    ap.add_argument("--only", choices=("step",) + CALLS + ("copy",),
+                    help="run just this call (or a whole step) warmup + steps times and print its average "
+                         "time, for profilers; 'copy' is a plain 256 MiB device copy that calibrates "
+                         "the HBM byte counters")
     return ap.parse_args()
 
 
@@ -56,6 +61,94 @@ def cpu_baseline(tokens):
             "seconds": round(dt, 2),
             "sample": "oracle linear fwd+bwd on the first %d of 8192 tokens (X[%d,1536], W[2048,1536], "
                       "dY[%d,2048]); FP64 GEMMs on %d OpenMP threads" % (tokens, tokens, tokens, threads)}
+
+
+CALLS = ("quantize_x", "quantize_w", "fprop", "quantize_dy", "dgrad", "wgrad")
+
+
+def calls(torch, puro, dev, M, N, K, X, W, dY, Y, dX, dW, saved):
+    """The step's calls one at a time, on buffers of their own, as
+    (key, label, fn, flops, algorithmic bytes, kernel launches) rows."""
+    xq = torch.empty(M, K, dtype=torch.uint8, device=dev)
+    wq = torch.empty(N, K, dtype=torch.uint8, device=dev)
+    dyq = torch.empty(M, N, dtype=torch.uint8, device=dev)
+    dyqT = torch.empty(N, M, dtype=torch.uint8, device=dev)
+    sx = torch.empty(1, dtype=torch.float32, device=dev)
+    sw = torch.empty(1, dtype=torch.float32, device=dev)
+    sdy = torch.empty(1, dtype=torch.float32, device=dev)
+    qws = torch.empty(max(1, puro.lib().puro_quantize_workspace_size(M, N)), dtype=torch.uint8, device=dev)
+    gws = torch.empty(max(1, max(puro.fp8_gemm_workspace_size(M, N, K, 0), puro.fp8_gemm_workspace_size(M, K, N, 0),
+                                 puro.fp8_gemm_workspace_size(N, K, M, 1))), dtype=torch.uint8, device=dev)
+    A_f = puro.operand(xq, puro.E4M3, puro.SCALE_TENSOR, sx)
+    B_f = puro.operand(wq, puro.E4M3, puro.SCALE_TENSOR, sw)
+    A_d = puro.operand(dyq, puro.E5M2, puro.SCALE_TENSOR, sdy)
+    B_d = puro.operand(saved["wq_t"], puro.E4M3, puro.SCALE_TENSOR, sw)
+    A_w = puro.operand(dyqT, puro.E5M2, puro.SCALE_TENSOR, sdy)
+    B_w = puro.operand(saved["xq_t"], puro.E4M3, puro.SCALE_TENSOR, sx)
+    # quantisation moves 2 B read + 1 B (q) + 1 B (qT) written per element
+    return [
+        ("quantize_x", "quantize X (amax + encode, q and qT)", lambda: puro.quantize_fp8(
+            X, puro.E4M3, out=dict(q=xq, scale=sx, qT=saved["xq_t"]), want_qT=True, ws=qws), None,
+         M * K * 4.0, 2),
+        ("quantize_w", "quantize W (amax + encode, q and qT)", lambda: puro.quantize_fp8(
+            W, puro.E4M3, out=dict(q=wq, scale=sw, qT=saved["wq_t"]), want_qT=True, ws=qws), None,
+         N * K * 4.0, 2),
+        ("fprop", "fprop GEMM %dx%dx%d" % (M, N, K),
+         lambda: puro.fp8_gemm(A_f, M, B_f, N, K, puro.OUT_BF16, D=Y, ws=gws), 2.0 * M * N * K, None,
+         1 + (puro.fp8_gemm_workspace_size(M, N, K, 0) > 0)),
+        ("quantize_dy", "quantize dY (amax + encode, q and qT)", lambda: puro.quantize_fp8(
+            dY, puro.E5M2, out=dict(q=dyq, scale=sdy, qT=dyqT), want_qT=True, ws=qws), None, M * N * 4.0, 2),
+        ("dgrad", "dgrad GEMM %dx%dx%d" % (M, K, N),
+         lambda: puro.fp8_gemm(A_d, M, B_d, K, N, puro.OUT_BF16, D=dX, ws=gws), 2.0 * M * N * K, None,
+         1 + (puro.fp8_gemm_workspace_size(M, K, N, 0) > 0)),
+        ("wgrad", "wgrad GEMM %dx%dx%d" % (N, K, M),
+         lambda: puro.fp8_gemm(A_w, N, B_w, K, M, puro.OUT_FP32, D=dW, ws=gws), 2.0 * M * N * K, None,
+         1 + (puro.fp8_gemm_workspace_size(N, K, M, 1) > 0)),
+    ]
+
+
+COPY_BYTES = 256 << 20
+TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "hbm_bytes_qkv.md")
+
+
+def profiled_traffic(call):
+    """HBM-side bytes per launch of `call` at the 8192-token workload, from the
+    committed rocprofv3 FETCH_SIZE / WRITE_SIZE summary (scaled by its copy
+    calibration); None when that summary is missing or any source it was
+    measured on has changed since."""
+    try:
+        text = open(TRAFFIC_PROFILE).read()
+        d = json.loads(text.split("```json", 1)[1].split("```", 1)[0])
+        for path, digest in d["sources"].items():
+            if hashlib.sha256(open(os.path.join(ROOT, path), "rb").read()).hexdigest() != digest:
+                return None
+        return d["calls"][call]["bytes"]
+    except (OSError, IndexError, KeyError, ValueError):
+        return None
+
+
+def run_only(args, torch, stream, step, make_calls):
+    """Profiling mode: one call (or the whole step) warmup + steps times."""
+    if args.only == "copy":
+        src = torch.empty(COPY_BYTES // 4, dtype=torch.float32, device=stream.device).fill_(1.0)
+        dst = torch.empty_like(src)
+        fn, label = (lambda: dst.copy_(src)), "plain device copy of %d bytes" % COPY_BYTES
+    elif args.only == "step":
+        fn, label = step, "linear fwd + bwd step"
+    else:
+        row = [r for r in make_calls() if r[0] == args.only][0]
+        fn, label = row[2], row[1]
+    for _ in range(args.warmup):
+        fn()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(args.steps):
+        fn()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    print(json.dumps({"only": args.only, "call": label, "launches": args.steps,
+                      "us_per_call": round(e0.elapsed_time(e1) / max(1, args.steps) * 1e3, 2)}))
 
 
 def main():
@@ -93,6 +186,9 @@ def main():
         puro.linear_bwd(dY, saved, rc, K, dX=dX, dW=dW, ws=wsb)
 
     stream = torch.cuda.current_stream()
+    if args.only:
+        run_only(args, torch, stream, step, lambda: calls(torch, puro, dev, M, N, K, X, W, dY, Y, dX, dW, saved))
+        return
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
@@ -108,47 +204,15 @@ def main():
     gemm_flops = 3 * 2.0 * M * N * K
     value = gemm_flops / (ms_per_step * 1e-3) / 1e12
 
-    # ---- per-kernel timing: the same calls one at a time, events around each
-    xq = torch.empty(M, K, dtype=torch.uint8, device=dev)
-    wq = torch.empty(N, K, dtype=torch.uint8, device=dev)
-    dyq = torch.empty(M, N, dtype=torch.uint8, device=dev)
-    dyqT = torch.empty(N, M, dtype=torch.uint8, device=dev)
-    sx = torch.empty(1, dtype=torch.float32, device=dev)
-    sw = torch.empty(1, dtype=torch.float32, device=dev)
-    sdy = torch.empty(1, dtype=torch.float32, device=dev)
-    qws = torch.empty(max(1, puro.lib().puro_quantize_workspace_size(M, N)), dtype=torch.uint8, device=dev)
-    gws = torch.empty(max(1, max(puro.fp8_gemm_workspace_size(M, N, K, 0), puro.fp8_gemm_workspace_size(M, K, N, 0),
-                                 puro.fp8_gemm_workspace_size(N, K, M, 1))), dtype=torch.uint8, device=dev)
-    A_f = puro.operand(xq, puro.E4M3, puro.SCALE_TENSOR, sx)
-    B_f = puro.operand(wq, puro.E4M3, puro.SCALE_TENSOR, sw)
-    A_d = puro.operand(dyq, puro.E5M2, puro.SCALE_TENSOR, sdy)
-    B_d = puro.operand(saved["wq_t"], puro.E4M3, puro.SCALE_TENSOR, sw)
-    A_w = puro.operand(dyqT, puro.E5M2, puro.SCALE_TENSOR, sdy)
-    B_w = puro.operand(saved["xq_t"], puro.E4M3, puro.SCALE_TENSOR, sx)
-    kernels = [
-        ("quantize X (amax + encode, q and qT)", lambda: puro.quantize_fp8(
-            X, puro.E4M3, out=dict(q=xq, scale=sx, qT=saved["xq_t"]), want_qT=True, ws=qws), None,
-         M * K * 4.0),
-        ("quantize W (amax + encode, q and qT)", lambda: puro.quantize_fp8(
-            W, puro.E4M3, out=dict(q=wq, scale=sw, qT=saved["wq_t"]), want_qT=True, ws=qws), None,
-         N * K * 4.0),
-        ("fprop GEMM 8192x2048x1536", lambda: puro.fp8_gemm(A_f, M, B_f, N, K, puro.OUT_BF16, D=Y, ws=gws),
-         2.0 * M * N * K, None),
-        ("quantize dY (amax + encode, q and qT)", lambda: puro.quantize_fp8(
-            dY, puro.E5M2, out=dict(q=dyq, scale=sdy, qT=dyqT), want_qT=True, ws=qws), None, M * N * 4.0),
-        ("dgrad GEMM 8192x1536x2048", lambda: puro.fp8_gemm(A_d, M, B_d, K, N, puro.OUT_BF16, D=dX, ws=gws),
-         2.0 * M * N * K, None),
-        ("wgrad GEMM 2048x1536x8192", lambda: puro.fp8_gemm(A_w, N, B_w, K, M, puro.OUT_FP32, D=dW, ws=gws),
-         2.0 * M * N * K, None),
-    ]
+    kernels = calls(torch, puro, dev, M, N, K, X, W, dY, Y, dX, dW, saved)
     reps = max(20, args.steps // 2)
-    for _, fn, _, _ in kernels:
+    for _, _, fn, _, _, _ in kernels:
         fn()
     torch.cuda.synchronize()
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in kernels]
     tot = [0.0] * len(kernels)
     for _ in range(reps):
-        for i, (_, fn, _, _) in enumerate(kernels):
+        for i, (_, _, fn, _, _, _) in enumerate(kernels):
             ev[i][0].record(stream)
             fn()
             ev[i][1].record(stream)
@@ -156,7 +220,7 @@ def main():
         for i in range(len(kernels)):
             tot[i] += ev[i][0].elapsed_time(ev[i][1])
     breakdown = []
-    for i, (name, _, flops, nbytes) in enumerate(kernels):
+    for i, (_, name, _, flops, nbytes, _) in enumerate(kernels):
         us = tot[i] / reps * 1e3
         row = {"call": name, "us": round(us, 2)}
         if flops:
@@ -166,9 +230,16 @@ def main():
         breakdown.append(row)
     gemm_rows = [r for r in breakdown if "tflops" in r]
     gemm_us = sum(r["us"] for r in gemm_rows)
-    dom = max(gemm_rows, key=lambda r: r["us"])
+    # dominant kernel: the slowest GEMM call that is a single kernel launch (a
+    # call that splits K adds a reduction launch and is not one kernel)
+    single = [r for r, k in zip(breakdown, kernels) if "tflops" in r and k[5] == 1]
+    dom = max(single, key=lambda r: r["us"])
+    dom_key = [k[0] for r, k in zip(breakdown, kernels) if r is dom][0]
+    traffic = profiled_traffic(dom_key) if M == 8192 else None
     roofline = {"bound": "mfma", "kernel": dom["call"], "achieved": dom["tflops"], "peak": FP8_PEAK_TFLOPS,
-                "unit": "TFLOP/s", "frac": round(dom["tflops"] / FP8_PEAK_TFLOPS, 4), "traffic": None}
+                "unit": "TFLOP/s", "frac": round(dom["tflops"] / FP8_PEAK_TFLOPS, 4), "traffic": traffic,
+                "traffic_unit": "bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
+                "algorithmic_flops_per_launch": 2.0 * M * N * K}
 
     out = {
         "metric": METRIC,
