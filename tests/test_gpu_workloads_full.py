@@ -1,0 +1,240 @@
+"""GPU parity at full size for the MLP, 28-layer blockwise and LM-head
+workloads (Qwen2-1.5B shapes), through puro_linear_fwd / puro_linear_bwd as
+the benchmark calls them.
+
+The oracle cannot quantise and multiply these tensors whole in seconds, so
+each check uses a subset that it computes exactly:
+
+* quantised bytes and scales are compared on sampled rows (and on sampled
+  rows of the transposed copies). Per-tensor codes of a row subset are the
+  oracle's codes for those rows under the whole tensor's amax. 1x128 groups
+  lie within rows and 128x1 groups within columns, so subsets by row or
+  column are exact. The small weight tensors are quantised whole;
+* GEMM outputs are checked on 16 entries in every 256x256 output tile. The
+  entries of a tile come from 4 random rows x 4 random columns of it, which
+  keeps the operand rows the oracle must quantise few. Where the reduction
+  length allows, every entry of the first and last tiles is checked too (the
+  last tile is the ragged corner of the 151936-wide LM head). Each entry is
+  a full-length FP64 dot product of the oracle.
+"""
+
+import numpy as np
+import pytest
+
+from oracle import bf16, gemm, quant
+from paper_2608_27370_amd import inputs
+
+import mfma_model
+from gpu_util import (assert_bytes_equal, assert_f32_bits_equal, bf16_bits, check_bf16, check_fp32, host,
+                      to_dev_bf16)
+
+pytestmark = pytest.mark.gpu
+
+E4, E5 = 0, 1
+ONAME = {E4: "e4m3", E5: "e5m2"}
+TILE = 256
+
+
+@pytest.fixture(scope="module")
+def P():
+    from paper_2608_27370_amd import puro
+    puro.lib()
+    return puro
+
+
+def sample_sparse(M, N, rng, rows_per_tile=4, cols_per_tile=4, per_tile=16, full=True):
+    """per_tile entries in every TILE x TILE block, drawn from rows_per_tile x
+    cols_per_tile random rows and columns of the block; with ``full`` also every
+    entry of the first and the last block."""
+    ms, ns = [], []
+    for t0 in range(0, M, TILE):
+        h = min(TILE, M - t0)
+        rows = t0 + rng.choice(h, min(rows_per_tile, h), replace=False)
+        for u0 in range(0, N, TILE):
+            w = min(TILE, N - u0)
+            cols = u0 + rng.choice(w, min(cols_per_tile, w), replace=False)
+            ms.append(rng.choice(rows, per_tile))
+            ns.append(rng.choice(cols, per_tile))
+    if full:
+        for t0, u0 in ((0, 0), ((M - 1) // TILE * TILE, (N - 1) // TILE * TILE)):
+            h, w = min(TILE, M - t0), min(TILE, N - u0)
+            mm, nn = np.meshgrid(np.arange(t0, t0 + h), np.arange(u0, u0 + w), indexing="ij")
+            ms.append(mm.ravel())
+            ns.append(nn.ravel())
+    return np.concatenate(ms).astype(np.int64), np.concatenate(ns).astype(np.int64)
+
+
+# ---- oracle operands for a subset of rows ------------------------------------------------
+# An operand is (codes, fmt, scale, mode, rows): ``codes`` holds the operand rows listed in the
+# sorted array ``rows`` (None: every row, as the block-scaled weights are kept whole).
+
+def full_amax(x_bits):
+    return quant.amax(bf16.to_f32(x_bits))
+
+
+def tensor_rows(x_bits, rows, fmt, a):
+    """Per-tensor operand rows of x (the GEMM reads x as stored)."""
+    q = quant.quantize_tensor(np.ascontiguousarray(x_bits[rows]), fmt, amax_in=a)[0]
+    return (q, fmt, quant.tensor_scale(a, fmt)[0], "tensor", rows)
+
+
+def tensor_cols(x_bits, cols, fmt, a):
+    """Per-tensor operand rows of x's transposed copy, i.e. columns of x."""
+    q = quant.quantize_tensor(np.ascontiguousarray(x_bits[:, cols].T), fmt, amax_in=a)[0]
+    return (q, fmt, quant.tensor_scale(a, fmt)[0], "tensor", cols)
+
+
+def group_rows(x_bits, rows, fmt):
+    """1x128 row-group operand rows (groups along x's rows)."""
+    q, s = quant.quantize_rows_1x128(np.ascontiguousarray(x_bits[rows]), fmt)
+    return (q, fmt, s, "row", rows)
+
+
+def group_cols(x_bits, cols, fmt):
+    """128x1 column-group operand rows of the transposed copy (columns of x)."""
+    q, s = quant.quantize_cols_128x1(np.ascontiguousarray(x_bits[:, cols]), fmt)
+    return (q, fmt, s, "row", cols)
+
+
+def check_entries(D, out, ms, ns, A, B, what):
+    am = ms if A[4] is None else np.searchsorted(A[4], ms)
+    bn = ns if B[4] is None else np.searchsorted(B[4], ns)
+    op = A[:4] + B[:4]
+    K = A[0].shape[1]
+    ref, den = gemm.gemm_entries(am, bn, *op)
+    slack = mfma_model.truncation_loss(am, bn, *op, chunk=max(16, (1 << 24) // max(K, 1)))
+    if out == "fp32":
+        check_fp32(host(D)[ms, ns], ref, den, what=what, slack=slack)
+    else:
+        check_bf16(bf16_bits(D)[ms, ns], ref, den, what=what, slack=slack)
+
+
+def uniq(a):
+    return np.unique(np.asarray(a, dtype=np.int64))
+
+
+def run_tensor_layer(P, X, W, dY, dyf, what, full_limit=9000):
+    """Per-tensor linear fwd + bwd on the GPU, checked against the oracle on
+    samples. X [M, K], W [N, K], dY [M, N] BF16 bits."""
+    M, K = X.shape
+    N = W.shape[0]
+    print("%s: GPU fwd + bwd M=%d N=%d K=%d" % (what, M, N, K), flush=True)
+    rc = P.LinearRecipe(E4, E4, dyf, 0, P.SCALE_FP32)
+    X_, W_, dY_ = to_dev_bf16(X), to_dev_bf16(W), to_dev_bf16(dY)
+    Y, saved = P.linear_fwd(X_, W_, rc)
+    dX, dW = P.linear_bwd(dY_, saved, rc, K)
+    # dY's bytes are internal to the backward call: the same quantiser call, made on its own
+    dq = P.quantize_fp8(dY_, dyf, want_qT=True)
+    del X_, W_, dY_
+    g = np.random.default_rng(7)
+    ax, aw, ady = full_amax(X), full_amax(W), full_amax(dY)
+    fy = ONAME[dyf]
+
+    # scales
+    assert_f32_bits_equal(host(saved["x_scale"]), np.array([quant.tensor_scale(ax, "e4m3")[0]]), what + " x scale")
+    assert_f32_bits_equal(host(saved["w_scale"]), np.array([quant.tensor_scale(aw, "e4m3")[0]]), what + " w scale")
+    assert_f32_bits_equal(host(dq["scale"]), np.array([quant.tensor_scale(ady, fy)[0]]), what + " dY scale")
+    # quantised bytes on sampled rows of every stored copy
+    kr = uniq(g.choice(K, 64, replace=False))
+    assert_bytes_equal(host(saved["xq_t"])[kr], tensor_cols(X, kr, "e4m3", ax)[0], what + " xq_t rows")
+    assert_bytes_equal(host(saved["wq_t"])[kr], tensor_cols(W, kr, "e4m3", aw)[0], what + " wq_t rows")
+    mr = uniq(g.choice(M, 64, replace=False))
+    assert_bytes_equal(host(dq["q"])[mr], tensor_rows(dY, mr, fy, ady)[0], what + " dYq rows")
+    nr = uniq(g.choice(N, 64, replace=False))
+    assert_bytes_equal(host(dq["qT"])[nr], tensor_cols(dY, nr, fy, ady)[0], what + " dYqT rows")
+
+    print("%s: quantised bytes and scales match; checking GEMM samples" % what, flush=True)
+    # Fprop Y [M, N] = Xq Wq^T
+    ms, ns = sample_sparse(M, N, g, full=K <= full_limit)
+    check_entries(Y, "bf16", ms, ns, tensor_rows(X, uniq(ms), "e4m3", ax), tensor_rows(W, uniq(ns), "e4m3", aw),
+                  what + " Y")
+    # Dgrad dX [M, K] = dYq (WqT)^T, reduction over N
+    ms, ks = sample_sparse(M, K, g, full=N <= full_limit)
+    check_entries(dX, "bf16", ms, ks, tensor_rows(dY, uniq(ms), fy, ady), tensor_cols(W, uniq(ks), "e4m3", aw),
+                  what + " dX")
+    # Wgrad dW [N, K] = dYqT (XqT)^T, reduction over M
+    ns, ks = sample_sparse(N, K, g, full=M <= full_limit)
+    check_entries(dW, "fp32", ns, ks, tensor_cols(dY, uniq(ns), fy, ady), tensor_cols(X, uniq(ks), "e4m3", ax),
+                  what + " dW")
+
+
+@pytest.fixture(scope="module")
+def mlp():
+    return inputs.mlp()
+
+
+def test_mlp_gate_up_8192x17920x1536(P, mlp):
+    """Fused gate/up projection: X [8192,1536] N(0,1) with 1% outlier channels
+    x20, W [17920,1536] N(0,0.02^2), dY [8192,17920] N(0,1e-6); per-tensor,
+    X/W E4M3, dY E5M2."""
+    run_tensor_layer(P, mlp["X"], mlp["W_gu"], mlp["dY_gu"], E5, "gate_up")
+
+
+def test_mlp_down_8192x1536x8960(P, mlp):
+    """Down projection: H [8192,8960] N(0,1) with 1% outlier channels x20,
+    W [1536,8960] N(0,0.02^2), dY [8192,1536] N(0,1e-6)."""
+    run_tensor_layer(P, mlp["H"], mlp["W_dn"], mlp["dY_dn"], E5, "down")
+
+
+@pytest.mark.timeout(1200)
+def test_lm_head_8192x151936x1536(P):
+    """LM head: X [8192,1536] Student-t(3), W [151936,1536] N(0,0.02^2),
+    dY = softmax(X W^T) - onehot(targets) computed on the host in FP32 and
+    rounded to BF16; per-tensor, X/W E4M3, dY E5M2. The output width 151936
+    is not a multiple of the tile, so the last tile column is ragged."""
+    print("lm_head: generating inputs on the host", flush=True)
+    d = inputs.lm_head()
+    run_tensor_layer(P, d["X"], d["W"], d["dY"], E5, "lm_head")
+
+
+@pytest.mark.parametrize("layer,j", [(0, 0), (0, 1), (0, 2), (0, 3), (27, 3)],
+                         ids=["l0-qkv", "l0-o", "l0-gate_up", "l0-down", "l27-down"])
+def test_layer_blockwise_m16384(P, layer, j):
+    """One linear of the 28-layer step at M = 16384: 1x128 groups for X and dY
+    (row groups for Fprop/Dgrad, column groups stored transposed for Wgrad),
+    128x128 blocks for W, power-of-two scales, E4M3 throughout."""
+    d = inputs.layer_linear(layer, j)
+    X, W, dY = d["X"], d["W"], d["dY"]
+    M, K = X.shape
+    N = W.shape[0]
+    what = "layer %d %s" % (layer, d["name"])
+    rc = P.LinearRecipe(E4, E4, E4, 1, P.SCALE_FP32)
+    X_, W_, dY_ = to_dev_bf16(X), to_dev_bf16(W), to_dev_bf16(dY)
+    Y, saved = P.linear_fwd(X_, W_, rc)
+    dX, dW = P.linear_bwd(dY_, saved, rc, K)
+    # dY's bytes are internal to the backward call: the same quantiser call
+    # (row groups and, from the same read, column groups), made on its own
+    dq = P.quantize_fp8(dY_, E4, mode=P.SCALE_ROW_1x128, rnd=P.SCALE_POW2, want_qT=True)
+    del X_, W_, dY_
+    g = np.random.default_rng(11)
+
+    # W blocks, whole
+    wq, ws, wqT, wsT = quant.quantize_blocks_128x128(W, "e4m3")
+    assert_bytes_equal(host(saved["wq_t"]), wqT, what + " wq_t")
+    assert_f32_bits_equal(host(saved["w_scale"]), wsT, what + " w scales (transposed)")
+    # X column groups (saved for Wgrad) and dY row/column groups on sampled rows
+    kr = uniq(g.choice(K, 32, replace=False))
+    q, s = quant.quantize_cols_128x1(np.ascontiguousarray(X[:, kr]), "e4m3")
+    assert_bytes_equal(host(saved["xq_t"])[kr], q, what + " xq_t rows")
+    assert_f32_bits_equal(host(saved["x_scale"])[kr], s, what + " x column-group scales")
+    mr = uniq(g.choice(M, 32, replace=False))
+    q, s = quant.quantize_rows_1x128(np.ascontiguousarray(dY[mr]), "e4m3")
+    assert_bytes_equal(host(dq["q"])[mr], q, what + " dYq rows")
+    assert_f32_bits_equal(host(dq["scale"])[mr], s, what + " dY row-group scales")
+    nr = uniq(g.choice(N, 32, replace=False))
+    q, s = quant.quantize_cols_128x1(np.ascontiguousarray(dY[:, nr]), "e4m3")
+    assert_bytes_equal(host(dq["qT"])[nr], q, what + " dYqT rows")
+    assert_f32_bits_equal(host(dq["scaleT"])[nr], s, what + " dY column-group scales")
+
+    Wb = (wq, "e4m3", ws, "block", None)
+    WbT = (wqT, "e4m3", wsT, "block", None)
+    # Fprop Y [M, N] = Xq(1x128) Wq(128x128)^T
+    ms, ns = sample_sparse(M, N, g, full=False)
+    check_entries(Y, "bf16", ms, ns, group_rows(X, uniq(ms), "e4m3"), Wb, what + " Y")
+    # Dgrad dX [M, K] = dYq(1x128) WqT(128x128)^T
+    ms, ks = sample_sparse(M, K, g, full=False)
+    check_entries(dX, "bf16", ms, ks, group_rows(dY, uniq(ms), "e4m3"), WbT, what + " dX")
+    # Wgrad dW [N, K] = dYqT(128x1) XqT(128x1)^T
+    ns, ks = sample_sparse(N, K, g, full=False)
+    check_entries(dW, "fp32", ns, ks, group_cols(dY, uniq(ns), "e4m3"), group_cols(X, uniq(ks), "e4m3"),
+                  what + " dW")
