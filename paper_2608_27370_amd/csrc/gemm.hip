@@ -8,27 +8,35 @@
 // Design (CDNA4):
 //  * Both operands reduction-contiguous ("TN"); Dgrad and Wgrad are posed
 //    this way by feeding the transposed FP8 copies the quantiser writes.
-//  * Workgroup tile BM x BN, k-step 128 bytes (one 128-wide scale group).
-//    Operand tiles are staged global -> LDS with buffer_load ... lds
-//    (16 bytes per lane, no VGRP staging), double-buffered: the loads for
-//    k-step t+1 are in flight while k-step t is multiplied.
-//  * LDS rows are 128 bytes; the 16-byte chunk c of row r is stored at
-//    position c ^ (r & 7), so the eight lanes of a ds_read_b128 phase hit
-//    eight different 16-byte bank groups (conflict-free); the XOR is applied
-//    on the global side because the DMA writes lane l at base + 16 l.
-//  * v_mfma_scale_f32_32x32x64_f8f6f4: 32x32 outputs per 64-long k slice.
+//  * Four waves per workgroup, one per SIMD, in a 2x2 grid; workgroup tiles
+//    up to 256x256 (wave tiles up to 128x128, accumulators in AGPRs).
+//  * Operand tiles move global -> LDS by buffer_load ... lds (16 bytes per
+//    lane, no VGPR staging) in k slices of SL = 128 bytes: one 1 KB DMA load
+//    covers 8 rows x 128 bytes, whole cache lines. A ring of NST slices
+//    keeps the next ones in flight while one is multiplied.
+//  * Within a slice the wave works in 64-byte k steps; the fragments of
+//    the next step are read from LDS into a second register set while the
+//    MFMAs of the current one run, and the DMA loads are spread between
+//    the MFMAs too. The loop body has no branches and waits on constant
+//    counts; one barrier per slice.
+//  * LDS rows are XOR-swizzled in 16-byte chunks (conflict-free reads; the
+//    swizzle is applied on the global side because the DMA writes lane l at
+//    base + 16 l).
+//  * v_mfma_scale_f32_32x32x64_f8f6f4: 32x32 outputs per 64-long k step.
 //    Grouped scales become the instruction's E8M0 operands (exact powers of
 //    two, applied inside the MFMA); per-tensor scales multiply the FP32
 //    result once in the epilogue. The instruction is issued with the B tile
 //    as its first operand, so each lane's accumulators hold four consecutive
-//    output columns of one row, stored as one 8-byte (BF16) or 16-byte
-//    (FP32) vector.
+//    output columns of one row.
 //  * Out-of-range rows and the k tail are zero-filled by the buffer
 //    descriptor's range check (num_records) rather than by branches.
 //  * Tiles are remapped so the eight XCDs (workgroups are dealt round-robin
 //    to them) each own a contiguous range of tiles, grouped by row panels to
 //    share operand panels in that XCD's L2.
-//  * Small grids split K into slices whose FP32 partial sums a second kernel
+//  * The epilogue stages each wave's FP32 tile in the idle ring and stores
+//    whole rows; interior tiles take a branch-free path that issues all LDS
+//    reads of a pass before its stores.
+//  * Small grids split K into ranges whose FP32 partial sums a second kernel
 //    adds in a fixed order (deterministic).
 
 #include "device_common.h"
@@ -43,7 +51,6 @@ typedef float v16f __attribute__((ext_vector_type(16)));
 typedef __attribute__((address_space(3))) void lds_void_t;
 
 constexpr int kBK = 128;                   // k block of the grouped scales (and of split-K ranges)
-constexpr int kSL = 64;                    // bytes of k per pipeline slice
 constexpr uint32_t kRsrcWord3 = 0x00020000u;  // raw buffer, 32-bit data format
 constexpr uint32_t kOOB = 0x80000000u;     // offset that fails the range check
 
@@ -118,23 +125,28 @@ __device__ __forceinline__ void dma_to_lds(v4i rsrc, uint32_t lds, uint32_t voff
                      : "=&s"(saved) : "s"(lds), "v"(voff), "s"(rsrc) : "memory");
 }
 
-template <int BM, int BN, int WM, int WN, int FA, int FB, int OUT, bool GROUPED, int GM, int NST>
+template <int BM, int BN, int WM, int WN, int FA, int FB, int OUT, bool GROUPED, int GM, int SL, int NST>
 __global__ __launch_bounds__(WM * WN * 64) void gemm_fp8_kernel(Params p) {
     constexpr int NW = WM * WN;
     constexpr int WTM = BM / WM, WTN = BN / WN;
     constexpr int FM = WTM / 32, FN = WTN / 32;
-    constexpr int A_BYTES = BM * kSL, B_BYTES = BN * kSL;
-    constexpr int STAGE = A_BYTES + B_BYTES;        // one 64-byte k slice of both tiles
-    // 1 KB DMA loads (16 rows of 64 bytes) per wave and slice; when the row
+    constexpr int KH = SL / 64;                     // 64-byte MFMA k steps per slice
+    constexpr int A_BYTES = BM * SL, B_BYTES = BN * SL;
+    constexpr int STAGE = A_BYTES + B_BYTES;        // one SL-byte k slice of both tiles
+    // 1 KB DMA loads (RPL rows of SL bytes) per wave and slice; when the row
     // blocks do not divide evenly, the surplus loads repeat earlier blocks
     // (the same bytes to the same place), so every wave issues the same
     // number of loads and can wait on an exact count
-    constexpr int A_BLK = BM / 16, B_BLK = BN / 16;
+    constexpr int RPL = 1024 / SL;                  // rows per DMA load
+    constexpr int CPR = SL / 16;                    // 16-byte chunks per LDS row
+    constexpr int A_BLK = BM / RPL, B_BLK = BN / RPL;
     constexpr int A_PER = (A_BLK + NW - 1) / NW, B_PER = (B_BLK + NW - 1) / NW;
     constexpr int SC_BLK = (BM + BN) / 64;          // 64 scales per 4-byte DMA load
-    constexpr int LOADS = A_PER + B_PER + (GROUPED ? 1 : 0);
-    static_assert(BM % 16 == 0 && BN % 16 == 0 && (BM + BN) % 64 == 0, "tile shape");
-    static_assert(NST >= 3 && NST <= 4, "pipeline depth");
+    constexpr int SC_PER = GROUPED ? (SC_BLK + NW - 1) / NW : 0;
+    constexpr int LOADS = A_PER + B_PER + SC_PER;
+    static_assert(SL == 64 || SL == 128, "slice width");
+    static_assert(BM % 32 == 0 && BN % 32 == 0 && (BM + BN) % 64 == 0, "tile shape");
+    static_assert(NST >= 2 && (NST - 1) * LOADS <= 63, "pipeline depth");
 
     __shared__ __attribute__((aligned(1024))) uint8_t smem[NST * STAGE];
     // grouped scales of a slice's rows (A then B), float, DMA'd like the operands
@@ -158,28 +170,42 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_fp8_kernel(Params p) {
     const int r2 = rem - group * GM * p.tiles_n;
     const int tm = first_m + r2 % gsz, tn = r2 / gsz;
     const int m0 = tm * BM, n0 = tn * BN;
-    // k slices [s0, s1) of 64 bytes: this split's 128-wide k blocks, twice
-    const int s0 = 2 * ks * p.ksteps_per_split;
-    const int s1 = 2 * min((ks + 1) * p.ksteps_per_split, p.ksteps);
+    // per-tensor scales, applied to the FP32 sums in the epilogue (loaded
+    // here so that their latency hides behind the main loop)
+    float alpha = p.alpha;
+    if (OUT != 2) {
+        if (p.a_mode == kSTensor) alpha *= p.sa[0];
+        if (p.b_mode == kSTensor) alpha *= p.sb[0];
+    }
+    // k slices [s0, s1) of SL bytes: this split's 128-wide k blocks
+    constexpr int SPB = kBK / SL;                   // slices per 128-wide k block
+    const int s0 = SPB * ks * p.ksteps_per_split;
+    const int s1 = SPB * min((ks + 1) * p.ksteps_per_split, p.ksteps);
 
     const int valid_m = min(BM, p.M - m0), valid_n = min(BN, p.N - n0);
     const v4i ra = make_rsrc(p.A + (int64_t)m0 * p.lda, (uint32_t)(valid_m * p.lda));
     const v4i rb = make_rsrc(p.B + (int64_t)n0 * p.ldb, (uint32_t)(valid_n * p.ldb));
 
-    // LDS layout of a slice: row r of a tile is 64 bytes (four 16-byte chunks)
-    // and its chunk c sits at position c ^ key(r), key(r) = ((r >> 1) & 3) ^
-    // ((r >> 3) & 1). Among 16 consecutive rows the rows sharing a 64-byte
-    // position in a 256-byte bank line get distinct keys, and so do the rows
-    // of 8 consecutive rows sharing a position in a 128-byte line: the 16 (or
-    // 8) lanes of a ds_read_b128 phase, reading consecutive rows at the same
-    // logical chunk, hit distinct banks with 64 (or 32) four-byte banks.
-    // Lane l of a DMA load fills row 16 * blk + l / 4 at position l % 4; since
-    // blocks are 16 rows, key(row) = ((l >> 3) & 3) ^ ((l >> 5) & 1) for every
-    // block, so each lane fetches one fixed chunk of its row.
-    const int dkey = ((lane >> 3) & 3) ^ ((lane >> 5) & 1);
-    const int kch = ((lane & 3) ^ dkey) * 16;
-    const uint32_t rowA = (uint32_t)((lane >> 2) * p.lda), rowB = (uint32_t)((lane >> 2) * p.ldb);
-    const uint32_t blkA = (uint32_t)(16 * p.lda), blkB = (uint32_t)(16 * p.ldb);
+    // LDS layout of a slice: row r of a tile is SL bytes (CPR 16-byte chunks)
+    // and its logical chunk c sits at position c ^ key(r). The 16 (or 8)
+    // lanes of a ds_read_b128 phase read 16 (8) consecutive rows at the same
+    // logical chunk; the keys make them hit distinct banks with 64 (32)
+    // four-byte banks:
+    //  * SL = 64, key(r) = ((r >> 1) & 3) ^ ((r >> 3) & 1): of 16 consecutive
+    //    rows, those sharing a 64-byte position in a 256-byte bank line get
+    //    distinct keys, and so do those of 8 rows in a 128-byte line;
+    //  * SL = 128, key(r) = (r & 7) ^ ((r >> 3) & 1): of 16 consecutive rows
+    //    the 8 even (odd) ones, which share the lower (upper) half of a
+    //    256-byte bank line, get distinct keys, and 8 consecutive rows in a
+    //    128-byte line get the keys 0..7.
+    // Lane l of a DMA load fills row RPL * blk + l / CPR at position l % CPR,
+    // so it fetches the logical chunk (l % CPR) ^ key(row) of that row.
+    auto row_key = [](int r) { return SL == 64 ? ((r >> 1) & 3) ^ ((r >> 3) & 1) : (r & 7) ^ ((r >> 3) & 1); };
+    // logical k byte a lane fetches in a load of an even / odd row block
+    const int kch0 = ((lane % CPR) ^ row_key(lane / CPR)) * 16;
+    const int kch1 = ((lane % CPR) ^ row_key(RPL + lane / CPR)) * 16;
+    const uint32_t rowA = (uint32_t)((lane / CPR) * p.lda), rowB = (uint32_t)((lane / CPR) * p.ldb);
+    const uint32_t blkA = (uint32_t)(RPL * p.lda), blkB = (uint32_t)(RPL * p.ldb);
     const uint32_t smem_lds = lds_addr(smem);
     const uint32_t ssc_lds = lds_addr(ssc);
 
@@ -189,33 +215,33 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_fp8_kernel(Params p) {
         rsb = make_rsrc(p.sb, p.b_mode == kSTensor ? 0u : p.sb_bytes);
     }
 
-    // all LOADS DMA loads of slice `sl` into ring stage `st`
-    auto load_slice = [&](int st, int sl) {
-        const int k0 = sl * kSL;
-        // the k tail (K % 64 != 0) reads out of range on purpose: zeros
-        const uint32_t off = (k0 + kch < p.K) ? (uint32_t)(k0 + kch) : kOOB;
+    // DMA load q (0 <= q < LOADS) of this wave for slice `sl` into ring
+    // stage `st`. With `valid` false the load still issues (so that every
+    // wave always has the same number in flight and waits on constant
+    // counts) but reads out of range: no memory traffic, zeros into a stage
+    // no later slice uses.
+    auto dma_one = [&](int st, int sl, int q, bool valid) __attribute__((always_inline)) {
+        const int k0 = sl * SL;
         const uint32_t sbase = smem_lds + st * STAGE;
-#pragma unroll
-        for (int q = 0; q < A_PER; ++q) {
-            const int blk = (wave * A_PER + q) % A_BLK;
-            dma_to_lds<16>(ra, sbase + blk * 1024, rowA + blk * blkA + off);
-        }
-#pragma unroll
-        for (int q = 0; q < B_PER; ++q) {
-            const int blk = (wave * B_PER + q) % B_BLK;
-            dma_to_lds<16>(rb, sbase + A_BYTES + blk * 1024, rowB + blk * blkB + off);
-        }
-        if constexpr (GROUPED) {
+        if (q < A_PER + B_PER) {
+            const bool is_a = q < A_PER;
+            const int blk = is_a ? (wave * A_PER + q) % A_BLK : (wave * B_PER + (q - A_PER)) % B_BLK;
+            const int kch = (blk & 1) ? kch1 : kch0;
+            // the k tail (K % SL != 0) also reads out of range on purpose: zeros
+            const uint32_t off = (valid && k0 + kch < p.K) ? (uint32_t)(k0 + kch) : kOOB;
+            if (is_a) dma_to_lds<16>(ra, sbase + blk * 1024, rowA + blk * blkA + off);
+            else dma_to_lds<16>(rb, sbase + A_BYTES + blk * 1024, rowB + blk * blkB + off);
+        } else if constexpr (GROUPED) {
             // lane l of scale load t brings the scale of tile row 64 t + l
             // (A rows, then B rows) for the 128-wide k block of the slice
-            const int t = wave % SC_BLK;
+            const int t = (wave * SC_PER + (q - A_PER - B_PER)) % SC_BLK;
             const int r = t * 64 + lane;
             const bool is_a = t * 64 < BM;
             const int row = is_a ? m0 + r : n0 + (r - BM);
             const int mode = is_a ? p.a_mode : p.b_mode;
             const int ld = is_a ? p.ld_sa : p.ld_sb;
             const int srow = mode == kSBlock ? row >> 7 : row;
-            const uint32_t soff = (uint32_t)(srow * ld + (sl >> 1)) * 4u;
+            const uint32_t soff = valid ? (uint32_t)(srow * ld + sl / SPB) * 4u : kOOB;
             const uint32_t dst = ssc_lds + (st * (BM + BN) + t * 64) * 4;
             dma_to_lds<4>(is_a ? rsa : rsb, dst, soff);
         }
@@ -230,66 +256,115 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_fp8_kernel(Params p) {
             for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
 
     const int fr = lane & 31;                 // fragment row of this lane
-    const int c0 = (lane >> 5) * 2;           // this lane's two 16-byte chunks of a slice row
+    const int c0 = (lane >> 5) * 2;           // first of this lane's two chunks in a 64-byte k step
     // key of the lane's fragment rows (fragments start at multiples of 32)
-    const int key = ((fr >> 1) & 3) ^ ((fr >> 3) & 1);
-    const int pos0 = (c0 ^ key) << 4, pos1 = ((c0 + 1) ^ key) << 4;
+    const int key = row_key(fr);
 
-    // prologue: slices s0 .. s0 + NST - 2 in flight
-#pragma unroll
-    for (int t = 0; t < NST - 1; ++t)
-        if (s0 + t < s1) load_slice(t, s0 + t);
+    // The operand fragments of one 64-byte k step as this wave holds them:
+    // for each 32-row fragment (A fragments first) 32 bytes of k per lane,
+    // bytes 32 (l >> 5) .. + 31 of the step in row l & 31, from two 16-byte
+    // LDS reads; and the E8M0 scale of each fragment row.
+    struct Frags {
+        v8i f[FM + FN];
+        uint32_t sc[FM + FN];
+    };
+    // read piece t of k step h of the slice in stage st: t < FM + FN are
+    // the operand fragments, the rest the scales
+    constexpr int NPIECE = (FM + FN) * (GROUPED ? 2 : 1);
+    auto read_piece = [&](Frags& f, int st, int h, int t) __attribute__((always_inline)) {
+        if (t < FM + FN) {
+            const uint8_t* row = t < FM ? smem + st * STAGE + (wm * WTM + t * 32 + fr) * SL
+                                        : smem + st * STAGE + A_BYTES + (wn * WTN + (t - FM) * 32 + fr) * SL;
+            const int cc = 4 * h + c0;
+            const v4i lo = *reinterpret_cast<const v4i*>(row + ((cc ^ key) << 4));
+            const v4i hi = *reinterpret_cast<const v4i*>(row + (((cc + 1) ^ key) << 4));
+            f.f[t] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+        } else {
+            const int fi = t - (FM + FN);
+            const int r = fi < FM ? wm * WTM + fi * 32 + fr : BM + wn * WTN + (fi - FM) * 32 + fr;
+            const bool scaled = fi < FM ? p.a_mode != kSTensor : p.b_mode != kSTensor;
+            f.sc[fi] = scaled ? e8m0_of(ssc[st * (BM + BN) + r]) : 127u;
+        }
+    };
+    auto mfma_one = [&](const Frags& f, int t) __attribute__((always_inline)) {
+        const int i = t / FN, j = t % FN;
+        if constexpr (GROUPED)
+            acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
+                f.f[FM + j], f.f[i], acc[i][j], FB, FA, 0, (int)f.sc[FM + j], 0, (int)f.sc[i]);
+        else
+            acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
+                f.f[FM + j], f.f[i], acc[i][j], FB, FA, 0, 127, 0, 127);
+    };
 
-    for (int sl = s0; sl < s1; ++sl) {
+    // One pipeline step: the MFMAs of k step h of slice sl (fragments in
+    // `cur`, read during the previous step) with the LDS reads of the next
+    // k step (into `nxt`) and, in a slice's last k step, the DMA loads of
+    // slice sl + NST interleaved between them, so that LDS and memory
+    // latency hide behind the MFMAs.
+    // Before the reads of the next slice (in its last k step) a wave waits
+    // until at most NST - 2 slices of its DMA loads remain in flight (every
+    // wave always has NST - 1 in flight then, so its loads of slice sl + 1
+    // have landed) and until its reads of slice sl are complete
+    // (lgkmcnt(0)). After the barrier every wave is at that point: slice
+    // sl + 1 is in LDS and the stage of slice sl is free for the DMA of slice
+    // sl + NST. The loop body has no branches: reads past the last slice
+    // fetch stale LDS data that is never used, and DMA loads past it read
+    // nothing.
+    constexpr int NMFMA = FM * FN;
+    auto step = [&](int sl, int h, Frags& cur, Frags& nxt) __attribute__((always_inline)) {
+        const bool last = h == KH - 1;
+        if (last) {
+            asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)" :: "n"((NST - 2) * LOADS) : "memory");
+            __syncthreads();
+        }
         const int st = (sl - s0) % NST;
-        // this wave's loads of slice sl are done once at most `later` slices
-        // issued after it remain outstanding
-        const int later = min(s1 - 1 - sl, NST - 2);
-        if (later >= 2) asm volatile("s_waitcnt vmcnt(%0)" :: "n"(2 * LOADS) : "memory");
-        else if (later == 1) asm volatile("s_waitcnt vmcnt(%0)" :: "n"(LOADS) : "memory");
-        else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-        // every wave's loads of slice sl have landed, and every wave is done
-        // with slice sl - 1, whose stage the next load reuses
-        __syncthreads();
-        const uint8_t* sA = smem + st * STAGE;
-        const uint8_t* sB = sA + A_BYTES;
-        uint32_t scA[FM], scB[FN];
+        const int rst = last ? (sl + 1 - s0) % NST : st;   // stage and k step read into nxt
+        const int rh = last ? 0 : h + 1;
+        const bool refill = sl + NST < s1;
+        // read piece u goes after MFMA u * NMFMA / NPIECE, DMA load q after
+        // MFMA q * NMFMA / LOADS (constant loop bounds, so that everything
+        // unrolls and the fragments stay in registers)
 #pragma unroll
-        for (int i = 0; i < FM; ++i)
-            scA[i] = (GROUPED && p.a_mode != kSTensor)
-                         ? e8m0_of(ssc[st * (BM + BN) + wm * WTM + i * 32 + fr]) : 127u;
+        for (int t = 0; t < NMFMA; ++t) {
+            mfma_one(cur, t);
 #pragma unroll
-        for (int j = 0; j < FN; ++j)
-            scB[j] = (GROUPED && p.b_mode != kSTensor)
-                         ? e8m0_of(ssc[st * (BM + BN) + BM + wn * WTN + j * 32 + fr]) : 127u;
-        v8i af[FM], bf[FN];
+            for (int u = 0; u < NPIECE; ++u)
+                if (u * NMFMA / NPIECE == t) read_piece(nxt, rst, rh, u);
+            if (last) {
 #pragma unroll
-        for (int i = 0; i < FM; ++i) {
-            const uint8_t* row = sA + (wm * WTM + i * 32 + fr) * kSL;
-            const uint4 lo = *reinterpret_cast<const uint4*>(row + pos0);
-            const uint4 hi = *reinterpret_cast<const uint4*>(row + pos1);
-            af[i] = v8i{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, (int)hi.x, (int)hi.y, (int)hi.z, (int)hi.w};
-        }
-#pragma unroll
-        for (int j = 0; j < FN; ++j) {
-            const uint8_t* row = sB + (wn * WTN + j * 32 + fr) * kSL;
-            const uint4 lo = *reinterpret_cast<const uint4*>(row + pos0);
-            const uint4 hi = *reinterpret_cast<const uint4*>(row + pos1);
-            bf[j] = v8i{(int)lo.x, (int)lo.y, (int)lo.z, (int)lo.w, (int)hi.x, (int)hi.y, (int)hi.z, (int)hi.w};
-        }
-        if (sl + NST - 1 < s1) load_slice((st + NST - 1) % NST, sl + NST - 1);
-#pragma unroll
-        for (int i = 0; i < FM; ++i)
-#pragma unroll
-            for (int j = 0; j < FN; ++j) {
-                if constexpr (GROUPED)
-                    acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
-                        bf[j], af[i], acc[i][j], FB, FA, 0, (int)scB[j], 0, (int)scA[i]);
-                else
-                    acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
-                        bf[j], af[i], acc[i][j], FB, FA, 0, 127, 0, 127);
+                for (int q = 0; q < LOADS; ++q)
+                    if (q * NMFMA / LOADS == t) dma_one(st, sl + NST, q, refill);
             }
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    };
+
+    // prologue: slices s0 .. s0 + NST - 1 in flight, then k step 0 of slice s0 read
+#pragma unroll
+    for (int t = 0; t < NST; ++t)
+#pragma unroll
+        for (int q = 0; q < LOADS; ++q) dma_one(t, s0 + t, q, s0 + t < s1);
+    Frags F0, F1;
+    asm volatile("s_waitcnt vmcnt(%0)" :: "n"((NST - 1) * LOADS) : "memory");
+    __syncthreads();
+#pragma unroll
+    for (int t = 0; t < NPIECE; ++t) read_piece(F0, 0, 0, t);
+    if constexpr (KH == 2) {
+        for (int sl = s0; sl < s1; ++sl) {
+            step(sl, 0, F0, F1);
+            step(sl, 1, F1, F0);
+        }
+    } else {
+        int sl = s0;
+        for (; sl + 1 < s1; sl += 2) {
+            step(sl, 0, F0, F1);
+            step(sl + 1, 0, F1, F0);
+        }
+        if (sl < s1) step(sl, 0, F0, F1);
     }
+    // the loads issued for slices past the end write zeros into the ring,
+    // which the epilogue reuses: let them land first
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 
     // ---- epilogue. Lane l holds, for fragment (i, j), wave-tile row
     // i*32 + (l & 31) and columns j*32 + 8g + 4(l >> 5) + {0..3}, g = 0..3.
@@ -299,24 +374,24 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_fp8_kernel(Params p) {
     // that both the writes and the row reads are free of bank conflicts, and
     // then stores whole rows: consecutive lanes on consecutive 16-byte chunks
     // (4 FP32 values), converted and scaled on the way out.
-    float alpha = p.alpha;
-    if (OUT != 2) {
-        if (p.a_mode == kSTensor) alpha *= p.sa[0];
-        if (p.b_mode == kSTensor) alpha *= p.sb[0];
-    }
     constexpr int ROWB = WTN * 4;                 // bytes of one staged wave-tile row (FP32)
-    constexpr int CPR = ROWB / 16;                // 16-byte chunks per row
+    constexpr int ECPR = ROWB / 16;               // 16-byte chunks per staged row
     constexpr int REGION = NST * STAGE / NW;      // LDS bytes per wave
-    constexpr int RFIT = (REGION / ROWB) / 32 * 32;
-    constexpr int RPP = RFIT < WTM ? RFIT : WTM;  // rows per pass
+    constexpr int RFIT = REGION / ROWB;          // rows that fit in the region
+    // rows per pass: WTM halved until it fits
+    constexpr int RPP = WTM <= RFIT ? WTM : (WTM / 2 <= RFIT ? WTM / 2 : WTM / 4);
     // XOR key of the chunk swizzle: 16 distinct keys when rows have 16*k chunks, else 8
-    constexpr int SWZ = (CPR % 16 == 0) ? 15 : 7;
-    static_assert(RPP >= 32 && WTM % RPP == 0 && (RPP * CPR) % 64 == 0, "epilogue tiling");
-    static_assert(CPR % 8 == 0, "row swizzle needs 8k chunks per row");
+    constexpr int SWZ = (ECPR % 16 == 0) ? 15 : 7;
+    static_assert(RPP >= 32 && WTM % RPP == 0 && (RPP * ECPR) % 64 == 0, "epilogue tiling");
+    static_assert(ECPR % 8 == 0, "row swizzle needs 8k chunks per row");
     uint8_t* ep = smem + wave * REGION;
     const int mrow0 = m0 + wm * WTM;
     const int ncol0 = n0 + wn * WTN;
     float* const part = p.partial + (int64_t)ks * p.M * p.N;
+    // a tile inside the matrix whose sums overwrite the output stores whole
+    // 4-column vectors everywhere: a branch-free path that issues all of a
+    // pass's LDS reads before its stores
+    const bool fast = m0 + BM <= p.M && n0 + BN <= p.N && (OUT == 2 || !p.accumulate);
     __syncthreads();   // every wave is done with the last stage
 #pragma unroll
     for (int pass = 0; pass < WTM / RPP; ++pass) {
@@ -334,11 +409,43 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_fp8_kernel(Params p) {
                     *reinterpret_cast<float4*>(ep + r * ROWB + ((chunk ^ (r & SWZ)) << 4)) = v;
                 }
         }
-        __syncthreads();
+        // the region belongs to this wave alone: once its own writes are
+        // done other lanes of the wave may read them (and the next pass
+        // writes only after this pass's reads have returned their data)
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+        constexpr int IT = RPP * ECPR / 64;
+        if (fast) {
+            float4 v[IT];
 #pragma unroll
-        for (int it = 0; it < RPP * CPR / 64; ++it) {
+            for (int it = 0; it < IT; ++it) {
+                const int q = it * 64 + lane;
+                const int r = q / ECPR, c = q % ECPR;
+                v[it] = *reinterpret_cast<const float4*>(ep + r * ROWB + ((c ^ (r & SWZ)) << 4));
+            }
+#pragma unroll
+            for (int it = 0; it < IT; ++it) {
+                const int q = it * 64 + lane;
+                const int r = q / ECPR, c = q % ECPR;
+                const int64_t m = mrow0 + pass * RPP + r;
+                const int n = ncol0 + c * 4;
+                float4 w = v[it];
+                if constexpr (OUT == 2) {
+                    *reinterpret_cast<float4*>(part + m * p.N + n) = w;
+                } else {
+                    w.x *= alpha; w.y *= alpha; w.z *= alpha; w.w *= alpha;
+                    if constexpr (OUT == kOutF32)
+                        *reinterpret_cast<float4*>(reinterpret_cast<float*>(p.D) + m * p.ldd + n) = w;
+                    else
+                        *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(p.D) + m * p.ldd + n) =
+                            make_uint2(pack_bf16x2(w.x, w.y), pack_bf16x2(w.z, w.w));
+                }
+            }
+            continue;
+        }
+#pragma unroll
+        for (int it = 0; it < IT; ++it) {
             const int q = it * 64 + lane;
-            const int r = q / CPR, c = q % CPR;
+            const int r = q / ECPR, c = q % ECPR;
             float4 v = *reinterpret_cast<const float4*>(ep + r * ROWB + ((c ^ (r & SWZ)) << 4));
             const int m = mrow0 + pass * RPP + r;
             const int n = ncol0 + c * 4;
@@ -368,7 +475,9 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_fp8_kernel(Params p) {
             } else {
                 // ragged right edge: element by element
                 const float vv[4] = {v.x, v.y, v.z, v.w};
-                for (int t = 0; t < 4 && n + t < p.N; ++t) {
+#pragma unroll
+                for (int t = 0; t < 4; ++t) {
+                    if (n + t >= p.N) continue;
                     if constexpr (OUT == kOutF32) {
                         float* dst = reinterpret_cast<float*>(p.D) + (int64_t)m * p.ldd + n + t;
                         *dst = p.accumulate ? *dst + vv[t] : vv[t];
@@ -379,7 +488,6 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_fp8_kernel(Params p) {
                 }
             }
         }
-        if (pass + 1 < WTM / RPP) __syncthreads();   // the next pass reuses the region
     }
 }
 
@@ -422,30 +530,39 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restr
 
 // ---- tile configurations and the plan for a problem ---------------------------
 
-struct Plan {
-    int cfg;             // index into kTiles
-    int bm, bn;          // tile
-    int splits;          // k slices
-    int ksteps_per_split;
-};
-
 struct TileCfg {
-    int bm, bn;
+    int bm, bn;          // workgroup tile
+    int wm, wn;          // wave grid (wave tile bm/wm x bn/wn)
+    int sl, nst;         // k bytes per pipeline slice, ring stages
     float eff;           // relative MFMA efficiency of the configuration
 };
-// 256x256 and 256x192: 8 waves (2 per SIMD) in a 4x2 grid (wave tiles 64x128,
-// 64x96); 128x128: 4 waves in 2x2 (wave tiles 64x64) for small problems.
-constexpr TileCfg kTiles[] = {{256, 256, 1.0f}, {256, 192, 0.95f}, {128, 128, 0.35f}};
+// Four waves (one per SIMD) in a 2x2 grid. The large wave tiles need the
+// least LDS traffic per MFMA (128x128: 16 MFMAs per 16 KB of fragment reads);
+// the smaller ones give more tiles to fill the 256 CUs on narrow problems.
+#define PURO_TILE_LIST(X)                         \
+    X(0, 256, 256, 2, 2, 128, 2, 1.0f)            \
+    X(1, 256, 192, 2, 2, 128, 2, 0.95f)           \
+    X(2, 256, 128, 2, 2, 128, 3, 0.85f)           \
+    X(3, 128, 128, 2, 2, 128, 2, 0.6f)
+#define PURO_TILE_ROW(i, bm, bn, wm, wn, sl, nst, eff) {bm, bn, wm, wn, sl, nst, eff},
+constexpr TileCfg kTiles[] = {PURO_TILE_LIST(PURO_TILE_ROW)};
+constexpr int kNumTiles = sizeof(kTiles) / sizeof(kTiles[0]);
 constexpr int kCUs = 256;
+
+struct Plan {
+    int cfg;             // index into kTiles
+    int splits;          // k ranges (split-K)
+    int ksteps_per_split;
+};
 
 // Pick the tile shape and the k split with the smallest estimated time: MFMA
 // time of the waves of work units over the CUs, plus the traffic of split-K
 // partial sums (written, then read by the reduction) when splitting.
 Plan make_plan(int64_t M, int64_t N, int64_t K, int out) {
     const int ksteps = (int)((K + kBK - 1) / kBK);
-    Plan best{0, 256, 256, 1, ksteps};
+    Plan best{0, 1, ksteps};
     double best_cost = -1.0;
-    for (int c = 0; c < 3; ++c) {
+    for (int c = 0; c < kNumTiles; ++c) {
         const TileCfg t = kTiles[c];
         const int64_t tiles = ((M + t.bm - 1) / t.bm) * ((N + t.bn - 1) / t.bn);
         if (tiles == 0) return best;
@@ -462,7 +579,7 @@ Plan make_plan(int64_t M, int64_t N, int64_t K, int out) {
                 cost += 2.0 * splits * (double)M * N * 4.0 / 8192.0;
             if (best_cost < 0 || cost < best_cost) {
                 best_cost = cost;
-                best = Plan{c, t.bm, t.bn, splits, kps};
+                best = Plan{c, splits, kps};
             }
         }
     }
@@ -470,40 +587,38 @@ Plan make_plan(int64_t M, int64_t N, int64_t K, int out) {
     return best;
 }
 
-template <int BM, int BN, int WM, int WN, int FA, int FB, int OUT>
+template <int BM, int BN, int WM, int WN, int SL, int NST, int FA, int FB, int OUT>
 void launch_cfg(const Params& prm, bool grouped, int grid, hipStream_t stream) {
     constexpr int GM = 8;
-    constexpr int NST = 4;
     if (grouped)
-        gemm_fp8_kernel<BM, BN, WM, WN, FA, FB, OUT, true, GM, NST><<<grid, WM * WN * 64, 0, stream>>>(prm);
+        gemm_fp8_kernel<BM, BN, WM, WN, FA, FB, OUT, true, GM, SL, NST><<<grid, WM * WN * 64, 0, stream>>>(prm);
     else
-        gemm_fp8_kernel<BM, BN, WM, WN, FA, FB, OUT, false, GM, NST><<<grid, WM * WN * 64, 0, stream>>>(prm);
+        gemm_fp8_kernel<BM, BN, WM, WN, FA, FB, OUT, false, GM, SL, NST><<<grid, WM * WN * 64, 0, stream>>>(prm);
 }
 
-template <int BM, int BN, int WM, int WN, int FA, int FB>
+template <int BM, int BN, int WM, int WN, int SL, int NST, int FA, int FB>
 void launch_tile(const Params& prm, int out, bool grouped, int grid, hipStream_t stream) {
-    if (out == 2) launch_cfg<BM, BN, WM, WN, FA, FB, 2>(prm, grouped, grid, stream);
-    else if (out == kOutF32) launch_cfg<BM, BN, WM, WN, FA, FB, kOutF32>(prm, grouped, grid, stream);
-    else launch_cfg<BM, BN, WM, WN, FA, FB, kOutBF16>(prm, grouped, grid, stream);
+    if (out == 2) launch_cfg<BM, BN, WM, WN, SL, NST, FA, FB, 2>(prm, grouped, grid, stream);
+    else if (out == kOutF32) launch_cfg<BM, BN, WM, WN, SL, NST, FA, FB, kOutF32>(prm, grouped, grid, stream);
+    else launch_cfg<BM, BN, WM, WN, SL, NST, FA, FB, kOutBF16>(prm, grouped, grid, stream);
 }
 
 template <int FA, int FB>
-void launch_fmt(const Params& prm, const Plan& pl, int out, bool grouped, int grid, hipStream_t stream) {
-    if (pl.cfg == 0) launch_tile<256, 256, 4, 2, FA, FB>(prm, out, grouped, grid, stream);
-    else if (pl.cfg == 1) launch_tile<256, 192, 4, 2, FA, FB>(prm, out, grouped, grid, stream);
-    else launch_tile<128, 128, 2, 2, FA, FB>(prm, out, grouped, grid, stream);
+void launch_fmt(const Params& prm, int cfg, int out, bool grouped, int grid, hipStream_t stream) {
+#define PURO_TILE_CASE(i, bm, bn, wm, wn, sl, nst, eff) \
+    case i: launch_tile<bm, bn, wm, wn, sl, nst, FA, FB>(prm, out, grouped, grid, stream); break;
+    switch (cfg) { PURO_TILE_LIST(PURO_TILE_CASE) }
+#undef PURO_TILE_CASE
 }
 
-}  // namespace
-
-size_t gemm_workspace_bytes(int64_t M, int64_t N, int64_t K, int out) {
-    const Plan pl = make_plan(M, N, K, out);
+size_t plan_workspace_bytes(int64_t M, int64_t N, const Plan& pl) {
     if (pl.splits <= 1) return 0;
     return (size_t)pl.splits * (size_t)M * (size_t)N * sizeof(float);
 }
 
-void launch_gemm(const GemmProblem& g, void* ws, hipStream_t stream) {
-    const Plan pl = make_plan(g.M, g.N, g.K, g.out);
+// Enqueue the GEMM of `g` with plan `pl`; `ws` holds plan_workspace_bytes.
+void run_plan(const GemmProblem& g, const Plan& pl, void* ws, hipStream_t stream) {
+    const TileCfg t = kTiles[pl.cfg];
     Params prm{};
     prm.A = g.A; prm.B = g.B; prm.sa = g.sa; prm.sb = g.sb;
     prm.D = g.D; prm.partial = reinterpret_cast<float*>(ws);
@@ -521,17 +636,17 @@ void launch_gemm(const GemmProblem& g, void* ws, hipStream_t stream) {
     prm.ksteps = (int)((g.K + kBK - 1) / kBK);
     prm.ksteps_per_split = pl.ksteps_per_split;
     prm.splits = pl.splits;
-    prm.tiles_m = (int)((g.M + pl.bm - 1) / pl.bm);
-    prm.tiles_n = (int)((g.N + pl.bn - 1) / pl.bn);
+    prm.tiles_m = (int)((g.M + t.bm - 1) / t.bm);
+    prm.tiles_n = (int)((g.N + t.bn - 1) / t.bn);
     prm.accumulate = g.accumulate;
     prm.alpha = 1.0f;
     const bool grouped = g.sa_mode != kSTensor || g.sb_mode != kSTensor;
     const int out = pl.splits > 1 ? 2 : g.out;
     const int grid = prm.tiles_m * prm.tiles_n * pl.splits;
-    if (g.fa == kE4M3 && g.fb == kE4M3) launch_fmt<kE4M3, kE4M3>(prm, pl, out, grouped, grid, stream);
-    else if (g.fa == kE5M2 && g.fb == kE4M3) launch_fmt<kE5M2, kE4M3>(prm, pl, out, grouped, grid, stream);
-    else if (g.fa == kE4M3 && g.fb == kE5M2) launch_fmt<kE4M3, kE5M2>(prm, pl, out, grouped, grid, stream);
-    else launch_fmt<kE5M2, kE5M2>(prm, pl, out, grouped, grid, stream);
+    if (g.fa == kE4M3 && g.fb == kE4M3) launch_fmt<kE4M3, kE4M3>(prm, pl.cfg, out, grouped, grid, stream);
+    else if (g.fa == kE5M2 && g.fb == kE4M3) launch_fmt<kE5M2, kE4M3>(prm, pl.cfg, out, grouped, grid, stream);
+    else if (g.fa == kE4M3 && g.fb == kE5M2) launch_fmt<kE4M3, kE5M2>(prm, pl.cfg, out, grouped, grid, stream);
+    else launch_fmt<kE5M2, kE5M2>(prm, pl.cfg, out, grouped, grid, stream);
     if (pl.splits > 1) {
         const int64_t n = g.M * (g.N / 4);
         const int blocks = (int)((n + 255) / 256);
@@ -544,6 +659,16 @@ void launch_gemm(const GemmProblem& g, void* ws, hipStream_t stream) {
                 prm.partial, pl.splits, prm.M, prm.N, g.sa, g.sb, g.sa_mode == kSTensor,
                 g.sb_mode == kSTensor, g.D, g.ldd, g.accumulate);
     }
+}
+
+}  // namespace
+
+size_t gemm_workspace_bytes(int64_t M, int64_t N, int64_t K, int out) {
+    return plan_workspace_bytes(M, N, make_plan(M, N, K, out));
+}
+
+void launch_gemm(const GemmProblem& g, void* ws, hipStream_t stream) {
+    run_plan(g, make_plan(g.M, g.N, g.K, g.out), ws, stream);
 }
 
 }  // namespace puro
