@@ -82,7 +82,8 @@ puro_status puro_amax(const uint16_t* x, int64_t rows, int64_t cols, int64_t ld,
 
 // --------------------------------------------------------------- quantise
 size_t puro_quantize_workspace_size(int64_t rows, int64_t cols) {
-    return amax_ws(rows, cols);
+    if (rows < 0 || cols < 0) return 0;
+    return quant_tensor_ws_bytes(rows, cols);
 }
 
 puro_status puro_quantize_fp8(const uint16_t* x, int64_t rows, int64_t cols, int64_t ld,
@@ -96,7 +97,8 @@ puro_status puro_quantize_fp8(const uint16_t* x, int64_t rows, int64_t cols, int
     QuantArgs a{};
     a.x = x; a.rows = rows; a.cols = cols; a.ld = ld;
     a.q = q; a.scale = scale; a.qT = qT; a.scaleT = scaleT;
-    a.amax_in = amax_in;
+    a.amax = amax_in;
+    a.supplied = amax_in != nullptr;
     a.pow2 = rnd == PURO_SCALE_POW2;
     // outputs of an empty tensor are never written (torch hands out NULL for them)
     const bool empty = rows == 0 || cols == 0;
@@ -131,15 +133,12 @@ puro_status puro_quantize_fp8(const uint16_t* x, int64_t rows, int64_t cols, int
         return PURO_ERR_UNSUPPORTED;
     }
     if (qmode == kQTensor && !amax_in) {
-        const int P = amax_num_partials(rows, cols);
-        if (P > 0 && !ws) return PURO_ERR_NULL;
-        if (ws_bytes < (size_t)P * sizeof(uint32_t)) return PURO_ERR_WORKSPACE;
-        a.partial = reinterpret_cast<const uint32_t*>(ws);
-        a.npartial = P;
-        if (P > 0) launch_amax_partials(x, rows, cols, ld, reinterpret_cast<uint32_t*>(ws), P, stream);
+        if (!ws) return PURO_ERR_NULL;
+        if (ws_bytes < quant_tensor_ws_bytes(rows, cols)) return PURO_ERR_WORKSPACE;
+        launch_quantize_tensor(fmt, a, ws, stream);
+        return launched();
     }
-    // an empty tensor has no groups; its per-tensor scale (amax 0) is 1 and is
-    // written by the single block the launcher uses for it
+    // an empty tensor has no groups
     if ((rows == 0 || cols == 0) && qmode != kQTensor) return PURO_OK;
     launch_quantize(fmt, qmode, a, stream);
     return launched();
@@ -230,8 +229,8 @@ FwdLayout fwd_layout(int64_t M, int64_t N, int64_t K, const puro_linear_recipe* 
         l.xs_row = c.take((size_t)M * (K / kGroup) * sizeof(float));
         l.w_blk = c.take((size_t)(N / kGroup) * (K / kGroup) * sizeof(float));
     } else {
-        l.part_x = c.take(amax_ws(M, K));
-        l.part_w = c.take(amax_ws(N, K));
+        l.part_x = c.take(quant_tensor_ws_bytes(M, K));
+        l.part_w = c.take(quant_tensor_ws_bytes(N, K));
     }
     l.gemm = c.take(gemm_workspace_bytes(M, N, K, kOutBF16));
     l.total = c.used;
@@ -252,7 +251,7 @@ BwdLayout bwd_layout(int64_t M, int64_t N, int64_t K, const puro_linear_recipe* 
         l.dy_scale_t = c.take((size_t)N * (M / kGroup) * sizeof(float));
     } else {
         l.dy_scale = c.take(sizeof(float));
-        l.part = c.take(amax_ws(M, N));
+        l.part = c.take(quant_tensor_ws_bytes(M, N));
     }
     const size_t g1 = gemm_workspace_bytes(M, K, N, kOutBF16);
     const size_t g2 = gemm_workspace_bytes(N, K, M, kOutF32);
@@ -305,12 +304,22 @@ puro_status puro_linear_fwd(const uint16_t* X, const uint16_t* W, int64_t M, int
     uint8_t* wq = w8 + l.wq;
     puro_fp8_operand A{}, B{};
     if (!r->blockwise) {
-        st = puro_quantize_fp8(X, M, K, K, r->x_fmt, PURO_SCALE_TENSOR, r->rnd, nullptr, xq, saved->x_scale,
-                               saved->xq_t, nullptr, w8 + l.part_x, amax_ws(M, K), stream);
-        if (st != PURO_OK) return st;
-        st = puro_quantize_fp8(W, N, K, K, r->w_fmt, PURO_SCALE_TENSOR, r->rnd, nullptr, wq, saved->w_scale,
-                               saved->wq_t, nullptr, w8 + l.part_w, amax_ws(N, K), stream);
-        if (st != PURO_OK) return st;
+        // X and W with their own amax each: q (Fprop) and qT (kept for Wgrad
+        // and Dgrad), in one amax launch and one quantise launch for both
+        QuantArgs ax{}, aw{};
+        ax.x = X; ax.rows = M; ax.cols = K; ax.ld = K;
+        ax.q = xq; ax.scale = saved->x_scale; ax.qT = saved->xq_t;
+        ax.pow2 = r->rnd == PURO_SCALE_POW2;
+        aw = ax;
+        aw.x = W; aw.rows = N;
+        aw.q = wq; aw.scale = saved->w_scale; aw.qT = saved->wq_t;
+        if (r->x_fmt == r->w_fmt) {
+            launch_quantize_tensor_pair(r->x_fmt, ax, w8 + l.part_x, aw, w8 + l.part_w, stream);
+        } else {
+            launch_quantize_tensor(r->x_fmt, ax, w8 + l.part_x, stream);
+            launch_quantize_tensor(r->w_fmt, aw, w8 + l.part_w, stream);
+        }
+        if ((st = launched()) != PURO_OK) return st;
         A = puro_fp8_operand{xq, K, r->x_fmt, PURO_SCALE_TENSOR, saved->x_scale};
         B = puro_fp8_operand{wq, K, r->w_fmt, PURO_SCALE_TENSOR, saved->w_scale};
     } else {
@@ -355,7 +364,7 @@ puro_status puro_linear_bwd(const uint16_t* dY, const puro_linear_saved* saved, 
     puro_fp8_operand dA{}, dB{}, wA{}, wB{};
     if (!r->blockwise) {
         st = puro_quantize_fp8(dY, M, N, N, r->dy_fmt, PURO_SCALE_TENSOR, r->rnd, nullptr, dyq, dys, dyq_t,
-                               nullptr, w8 + l.part, amax_ws(M, N), stream);
+                               nullptr, w8 + l.part, quant_tensor_ws_bytes(M, N), stream);
         if (st != PURO_OK) return st;
         dA = puro_fp8_operand{dyq, N, r->dy_fmt, PURO_SCALE_TENSOR, dys};
         dB = puro_fp8_operand{saved->wq_t, N, r->w_fmt, PURO_SCALE_TENSOR, saved->w_scale};

@@ -534,20 +534,24 @@ struct TileCfg {
     int bm, bn;          // workgroup tile
     int wm, wn;          // wave grid (wave tile bm/wm x bn/wn)
     int sl, nst;         // k bytes per pipeline slice, ring stages
-    float eff;           // relative MFMA efficiency of the configuration
+    float fixed_us;      // time model: per wave of work units ...
+    float slice_us;      // ... plus per k slice of a unit (MI355X, all CUs busy)
 };
 // Four waves (one per SIMD) in a 2x2 grid. The large wave tiles need the
 // least LDS traffic per MFMA (128x128: 16 MFMAs per 16 KB of fragment reads);
-// the smaller ones give more tiles to fill the 256 CUs on narrow problems.
-#define PURO_TILE_LIST(X)                         \
-    X(0, 256, 256, 2, 2, 128, 2, 1.0f)            \
-    X(1, 256, 192, 2, 2, 128, 2, 0.95f)           \
-    X(2, 256, 128, 2, 2, 128, 3, 0.85f)           \
-    X(3, 128, 128, 2, 2, 128, 2, 0.6f)
-#define PURO_TILE_ROW(i, bm, bn, wm, wn, sl, nst, eff) {bm, bn, wm, wn, sl, nst, eff},
+// the 128x128 tiles give more work units on narrow problems, with a deep ring
+// (one workgroup per CU) or a short one (two per CU). The time constants are
+// least-squares fits to measured kernel times on the Qwen2-1.5B layer shapes.
+#define PURO_TILE_LIST(X)                              \
+    X(0, 256, 256, 2, 2, 128, 2, 6.9f, 1.40f)          \
+    X(1, 256, 192, 2, 2, 128, 2, 5.5f, 1.19f)          \
+    X(2, 128, 128, 2, 2, 128, 4, 2.8f, 0.50f)          \
+    X(3, 128, 128, 2, 2, 128, 2, 3.5f, 0.765f)
+#define PURO_TILE_ROW(i, bm, bn, wm, wn, sl, nst, f, s) {bm, bn, wm, wn, sl, nst, f, s},
 constexpr TileCfg kTiles[] = {PURO_TILE_LIST(PURO_TILE_ROW)};
 constexpr int kNumTiles = sizeof(kTiles) / sizeof(kTiles[0]);
 constexpr int kCUs = 256;
+constexpr int kLdsBytes = 160 * 1024;
 
 struct Plan {
     int cfg;             // index into kTiles
@@ -555,10 +559,18 @@ struct Plan {
     int ksteps_per_split;
 };
 
-// Pick the tile shape and the k split with the smallest estimated time: MFMA
-// time of the waves of work units over the CUs, plus the traffic of split-K
-// partial sums (written, then read by the reduction) when splitting.
-Plan make_plan(int64_t M, int64_t N, int64_t K, int out) {
+// Workgroups of a configuration that fit on one CU (by LDS).
+int per_cu(const TileCfg& t, bool grouped) {
+    const int lds = (t.bm + t.bn) * t.sl * t.nst + (grouped ? (t.bm + t.bn) * 4 * t.nst : 0);
+    const int n = kLdsBytes / lds;
+    return n < 1 ? 1 : n;
+}
+
+// Pick the tile configuration and k split with the smallest modelled time:
+// waves of work units over the CUs, each a fixed cost plus a cost per k
+// slice (lower when part of the GPU idles and the clock rises; higher with
+// block scales), plus the split-K partial sums written and read back.
+Plan make_plan(int64_t M, int64_t N, int64_t K, bool grouped) {
     const int ksteps = (int)((K + kBK - 1) / kBK);
     Plan best{0, 1, ksteps};
     double best_cost = -1.0;
@@ -566,24 +578,24 @@ Plan make_plan(int64_t M, int64_t N, int64_t K, int out) {
         const TileCfg t = kTiles[c];
         const int64_t tiles = ((M + t.bm - 1) / t.bm) * ((N + t.bn - 1) / t.bn);
         if (tiles == 0) return best;
+        const int64_t slots = (int64_t)kCUs * per_cu(t, grouped);
         const int max_s = (N % 4 == 0) ? (ksteps / 4 < 16 ? ksteps / 4 : 16) : 1;
         for (int s = 1; s <= (max_s > 1 ? max_s : 1); ++s) {
             const int kps = (ksteps + s - 1) / s;
             const int splits = kps > 0 ? (ksteps + kps - 1) / kps : 1;
             if (splits != s) continue;
             const int64_t units = tiles * splits;
-            const int64_t waves = (units + kCUs - 1) / kCUs;
-            // cycles: one k-step of a tile is bm*bn*128*2 FLOP at 8192 FLOP/clk
-            double cost = (double)waves * t.bm * t.bn * (kps > 0 ? kps : 1) * 256.0 / 8192.0 / t.eff;
-            if (splits > 1)   // partials written and read back, mostly in the 256 MB MALL (~8 KB/clk)
-                cost += 2.0 * splits * (double)M * N * 4.0 / 8192.0;
+            const int64_t waves = (units + slots - 1) / slots;
+            const double busy = units < slots ? (double)units / slots : 1.0;
+            double cost = (double)waves * (t.fixed_us + t.slice_us * (kps > 0 ? kps : 1) * (1.0 - 0.146 * (1.0 - busy)));
+            if (grouped) cost *= 1.5;
+            if (splits > 1) cost += 0.294e-6 * splits * (double)M * N * 4.0;
             if (best_cost < 0 || cost < best_cost) {
                 best_cost = cost;
                 best = Plan{c, splits, kps};
             }
         }
     }
-    (void)out;
     return best;
 }
 
@@ -605,7 +617,7 @@ void launch_tile(const Params& prm, int out, bool grouped, int grid, hipStream_t
 
 template <int FA, int FB>
 void launch_fmt(const Params& prm, int cfg, int out, bool grouped, int grid, hipStream_t stream) {
-#define PURO_TILE_CASE(i, bm, bn, wm, wn, sl, nst, eff) \
+#define PURO_TILE_CASE(i, bm, bn, wm, wn, sl, nst, f, s) \
     case i: launch_tile<bm, bn, wm, wn, sl, nst, FA, FB>(prm, out, grouped, grid, stream); break;
     switch (cfg) { PURO_TILE_LIST(PURO_TILE_CASE) }
 #undef PURO_TILE_CASE
@@ -664,11 +676,16 @@ void run_plan(const GemmProblem& g, const Plan& pl, void* ws, hipStream_t stream
 }  // namespace
 
 size_t gemm_workspace_bytes(int64_t M, int64_t N, int64_t K, int out) {
-    return plan_workspace_bytes(M, N, make_plan(M, N, K, out));
+    // enough for the plan with or without block scales
+    (void)out;
+    const size_t a = plan_workspace_bytes(M, N, make_plan(M, N, K, false));
+    const size_t b = plan_workspace_bytes(M, N, make_plan(M, N, K, true));
+    return a > b ? a : b;
 }
 
 void launch_gemm(const GemmProblem& g, void* ws, hipStream_t stream) {
-    run_plan(g, make_plan(g.M, g.N, g.K, g.out), ws, stream);
+    const bool grouped = g.sa_mode != kSTensor || g.sb_mode != kSTensor;
+    run_plan(g, make_plan(g.M, g.N, g.K, grouped), ws, stream);
 }
 
 }  // namespace puro

@@ -9,6 +9,15 @@ namespace puro {
 
 // ---- amax / quantisation (quant.hip) ----------------------------------------
 
+// One tensor of an amax pass: P blocks over its rows write partial[0..P).
+struct AmaxJob {
+    const uint16_t* x;
+    int64_t rows, ld;
+    uint32_t* partial;
+    uint32_t cpr;    // 8-value chunks per row
+    int P;
+};
+
 // Number of per-block partial maxima the amax pass writes for a tensor.
 int amax_num_partials(int64_t rows, int64_t cols);
 
@@ -27,13 +36,26 @@ struct QuantArgs {
     float* scale;
     uint8_t* qT;
     float* scaleT;
-    // per-tensor mode: the amax source (amax_in, or the partial maxima) and the rule
+    // per-tensor mode: the amax as a device scalar, or (amax NULL) the
+    // partial maxima to reduce; supplied: the caller gave the amax (values
+    // beyond it saturate) rather than it being computed from x
+    const float* amax;
     const uint32_t* partial;
     int npartial;
-    const float* amax_in;
+    int supplied;
     int pow2;
 };
 
+// Workspace of a per-tensor quantisation that computes its own amax.
+size_t quant_tensor_ws_bytes(int64_t rows, int64_t cols);
+// Per-tensor quantisation with the tensor's own amax: the partial maxima
+// pass, then the quantise pass (which reduces them, or reads the amax a
+// one-block reduction wrote). ws holds quant_tensor_ws_bytes.
+void launch_quantize_tensor(int fmt, QuantArgs a, void* ws, hipStream_t stream);
+// The same for two tensors of one format, with one amax launch and one
+// quantise launch for both (each tensor with its own workspace).
+void launch_quantize_tensor_pair(int fmt, QuantArgs a0, void* ws0, QuantArgs a1, void* ws1,
+                                 hipStream_t stream);
 void launch_quantize(int fmt, int mode, const QuantArgs& a, hipStream_t stream);
 
 // ---- GEMM (gemm.hip) ----------------------------------------------------------

@@ -11,9 +11,12 @@
 // per requested copy. Each thread owns an 8x8 sub-block of a 128x128 tile, so
 // a transposed copy is produced by an in-register 8x8 byte transpose and
 // stored as 8-byte runs of the transposed rows, without an LDS round trip.
-// Per-tensor scaling needs the whole tensor's amax first: a first pass writes
-// per-block partial maxima (no atomics, no zero-initialised state), and every
-// block of the quantise pass reduces them before encoding.
+// Per-tensor scaling needs the whole tensor's amax before any encoding: a
+// first pass writes per-block partial maxima (no atomics, no zero-initialised
+// state); the quantise pass reduces them in every block (few partials) or
+// reads the amax a one-block reduction kernel wrote (many partials).
+
+#include <algorithm>
 
 #include "device_common.h"
 #include "kernels.h"
@@ -24,6 +27,9 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kTile = 128;
+// Above this many partial maxima a one-block kernel reduces them once,
+// rather than every block of the quantise pass reading them all.
+constexpr int kMaxInlinePartials = 2048;
 
 __device__ __forceinline__ uint32_t wave_max(uint32_t v) {
 #pragma unroll
@@ -42,22 +48,28 @@ __device__ __forceinline__ uint32_t block_max(uint32_t v, uint32_t* red) {
 }
 
 // ---------------------------------------------------------------- amax ---
+// Partial maxima of one or two tensors in one launch: blocks [0, j0.P) cover
+// the rows of the first tensor in P contiguous ranges, the rest the second.
 template <bool DENSE>
-__global__ __launch_bounds__(kThreads) void amax_partial_kernel(const uint16_t* __restrict__ x,
-                                                                int64_t rows, uint32_t cpr,
-                                                                int64_t ld,
-                                                                uint32_t* __restrict__ partial) {
+__global__ __launch_bounds__(kThreads) void amax_partial_kernel(AmaxJob j0, AmaxJob j1) {
     __shared__ uint32_t red[4];
-    const int P = gridDim.x;
-    const int64_t r0 = rows * blockIdx.x / P, r1 = rows * (blockIdx.x + 1) / P;
+    const bool second = (int)blockIdx.x >= j0.P;
+    const uint16_t* x = second ? j1.x : j0.x;
+    const int64_t rows = second ? j1.rows : j0.rows;
+    const int64_t ld = second ? j1.ld : j0.ld;
+    const uint32_t cpr = second ? j1.cpr : j0.cpr;
+    uint32_t* partial = second ? j1.partial : j0.partial;
+    const int P = second ? j1.P : j0.P;
+    const int bid = second ? (int)blockIdx.x - j0.P : (int)blockIdx.x;
+    const int64_t r0 = rows * bid / P, r1 = rows * (bid + 1) / P;
     const uint32_t n = (uint32_t)((r1 - r0) * cpr);
     uint32_t m = 0;
-    constexpr int U = 4;
-    for (uint32_t j0 = threadIdx.x; j0 < n; j0 += kThreads * U) {
+    constexpr int U = 8;
+    for (uint32_t j0i = threadIdx.x; j0i < n; j0i += kThreads * U) {
         uint4 v[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            const uint32_t j = j0 + u * kThreads;
+            const uint32_t j = j0i + u * kThreads;
             v[u] = make_uint4(0, 0, 0, 0);
             if (j < n) {
                 const uint16_t* p;
@@ -77,7 +89,7 @@ __global__ __launch_bounds__(kThreads) void amax_partial_kernel(const uint16_t* 
         }
     }
     m = block_max(m, red);
-    if (threadIdx.x == 0) partial[blockIdx.x] = m;
+    if (threadIdx.x == 0) partial[bid] = m;
 }
 
 __global__ __launch_bounds__(kThreads) void amax_finalize_kernel(const uint32_t* __restrict__ partial,
@@ -97,15 +109,17 @@ struct Tile {
     bool col_ok;
 };
 
-__device__ __forceinline__ Tile tile_coords(int64_t cols) {
+// The thread's 8x8 block in tile (bx, by) (tile column, tile row).
+__device__ __forceinline__ Tile tile_coords(int64_t cols, int64_t bx, int64_t by) {
     Tile t;
     t.cc = threadIdx.x & 15;
     t.rg = threadIdx.x >> 4;
-    t.row0 = (int64_t)blockIdx.y * kTile + t.rg * 8;
-    t.col = (int64_t)blockIdx.x * kTile + t.cc * 8;
+    t.row0 = by * kTile + t.rg * 8;
+    t.col = bx * kTile + t.cc * 8;
     t.col_ok = t.col < cols;
     return t;
 }
+__device__ __forceinline__ Tile tile_coords(int64_t cols) { return tile_coords(cols, blockIdx.x, blockIdx.y); }
 
 __device__ __forceinline__ void load_8x8(const QuantArgs& a, const Tile& t, uint32_t w[8][4]) {
 #pragma unroll
@@ -161,26 +175,11 @@ __device__ __forceinline__ uint32_t elem_mag(const uint32_t w[8][4], int i, int 
     return ((j & 1) ? (word >> 16) : word) & 0x7FFFu;
 }
 
-// Per-tensor quantisation: scale from amax_in or from the partial maxima.
+// Scale of a per-tensor quantisation and the encoding of the thread's 8x8
+// block. `saturate`: the amax was supplied and values beyond it saturate.
 template <int FMT>
-__global__ __launch_bounds__(kThreads) void quant_tensor_kernel(QuantArgs a) {
-    __shared__ uint32_t red[4];
-    const Tile t = tile_coords(a.cols);
-    uint32_t w[8][4];
-    load_8x8(a, t, w);
-
-    float amax;
-    bool safe;
-    if (a.amax_in) {
-        amax = *a.amax_in;
-        safe = true;   // values beyond a supplied amax saturate
-    } else {
-        uint32_t m = 0;
-        for (int i = threadIdx.x; i < a.npartial; i += kThreads) m = max(m, a.partial[i]);
-        m = block_max(m, red);
-        amax = __uint_as_float(m << 16);
-        safe = false;
-    }
+__device__ __forceinline__ void encode_tensor_block(const QuantArgs& a, const Tile& t, const uint32_t w[8][4],
+                                                    float amax, bool saturate, bool first_tile) {
     float s, r;
     constexpr float fm = Fp8Traits<FMT>::kMax;
     if (a.pow2) {
@@ -206,8 +205,8 @@ __global__ __launch_bounds__(kThreads) void quant_tensor_kernel(QuantArgs a) {
         s = amax / fm;
         r = fm / amax;
     }
-    safe = safe || !(fabsf(amax) <= 3.4028235e38f) || !(fabsf(r) <= 3.4028235e38f);
-    if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0 && a.scale) a.scale[0] = s;
+    const bool safe = saturate || !(fabsf(amax) <= 3.4028235e38f) || !(fabsf(r) <= 3.4028235e38f);
+    if (first_tile && threadIdx.x == 0 && a.scale) a.scale[0] = s;
 
     uint2 c[8];
     if (safe) {
@@ -219,6 +218,32 @@ __global__ __launch_bounds__(kThreads) void quant_tensor_kernel(QuantArgs a) {
     }
     if (a.q) store_rows(a, t, c);
     if (a.qT) store_transposed(a, t, c);
+}
+
+// Per-tensor quantisation of one or two tensors in one launch (1-D grid:
+// the first tensor's tiles, then the second's). The amax comes from a
+// device scalar, or is reduced from the partial maxima of the amax pass.
+template <int FMT>
+__global__ __launch_bounds__(kThreads) void quant_tensor_kernel(QuantArgs a0, QuantArgs a1, int tiles0,
+                                                                int gx0, int gx1) {
+    __shared__ uint32_t red[4];
+    const bool second = (int)blockIdx.x >= tiles0;
+    const QuantArgs a = second ? a1 : a0;
+    const int tile = second ? (int)blockIdx.x - tiles0 : (int)blockIdx.x;
+    const int gx = second ? gx1 : gx0;
+    const Tile t = tile_coords(a.cols, tile % gx, tile / gx);
+    uint32_t w[8][4];
+    load_8x8(a, t, w);
+    float amax;
+    if (a.amax) {
+        amax = *a.amax;
+    } else {
+        uint32_t m = 0;
+        for (int i = threadIdx.x; i < a.npartial; i += kThreads) m = max(m, a.partial[i]);
+        m = block_max(m, red);
+        amax = __uint_as_float(m << 16);
+    }
+    encode_tensor_block<FMT>(a, t, w, amax, a.supplied != 0, tile == 0);
 }
 
 // 1x128 row groups (q, scale) and/or 128x1 column groups (qT, scaleT).
@@ -355,7 +380,8 @@ void launch_quantize_fmt(int mode, const QuantArgs& a, hipStream_t stream) {
     const dim3 grid((unsigned)(gx > 0 ? gx : 1), (unsigned)(gy > 0 ? gy : 1));
     switch (mode) {
     case kQTensor:
-        quant_tensor_kernel<FMT><<<grid, kThreads, 0, stream>>>(a);
+        quant_tensor_kernel<FMT><<<(unsigned)(grid.x * grid.y), kThreads, 0, stream>>>(a, a, (int)(grid.x * grid.y),
+                                                                                      (int)grid.x, 1);
         break;
     case kQRow:
         if (a.qT) quant_groups_kernel<FMT, true, true><<<grid, kThreads, 0, stream>>>(a);
@@ -375,20 +401,18 @@ void launch_quantize_fmt(int mode, const QuantArgs& a, hipStream_t stream) {
 int amax_num_partials(int64_t rows, int64_t cols) {
     if (rows <= 0 || cols <= 0) return 0;
     const int64_t chunks = rows * (cols / 8);
-    int64_t P = chunks / (kThreads * 16);   // ~16 vector loads per thread
+    int64_t P = chunks / (kThreads * 8);    // ~8 vector loads per thread
     if (P < 1) P = 1;
-    if (P > 1024) P = 1024;
+    if (P > 4096) P = 4096;
     if (P > rows) P = rows;                 // whole rows per block
     return (int)P;
 }
 
 void launch_amax_partials(const uint16_t* x, int64_t rows, int64_t cols, int64_t ld,
                           uint32_t* partial, int P, hipStream_t stream) {
-    const uint32_t cpr = (uint32_t)(cols / 8);
-    if (ld == cols)
-        amax_partial_kernel<true><<<P, kThreads, 0, stream>>>(x, rows, cpr, ld, partial);
-    else
-        amax_partial_kernel<false><<<P, kThreads, 0, stream>>>(x, rows, cpr, ld, partial);
+    const AmaxJob j{x, rows, ld, partial, (uint32_t)(cols / 8), P};
+    if (ld == cols) amax_partial_kernel<true><<<P, kThreads, 0, stream>>>(j, j);
+    else amax_partial_kernel<false><<<P, kThreads, 0, stream>>>(j, j);
 }
 
 void launch_amax_finalize(const uint32_t* partial, int P, float* amax, hipStream_t stream) {
@@ -398,6 +422,67 @@ void launch_amax_finalize(const uint32_t* partial, int P, float* amax, hipStream
 void launch_quantize(int fmt, int mode, const QuantArgs& a, hipStream_t stream) {
     if (fmt == kE4M3) launch_quantize_fmt<kE4M3>(mode, a, stream);
     else launch_quantize_fmt<kE5M2>(mode, a, stream);
+}
+
+// Workspace: the partial maxima, then the amax scalar.
+size_t quant_tensor_ws_bytes(int64_t rows, int64_t cols) {
+    return ((size_t)amax_num_partials(rows, cols) * sizeof(uint32_t) + 255) / 256 * 256 + sizeof(float);
+}
+
+namespace {
+
+// Amax source of a per-tensor quantisation whose partial maxima are in ws:
+// reduced by every quantise block (few partials) or once by a one-block
+// kernel into the amax slot of ws.
+void amax_source(QuantArgs& a, int P, void* ws, hipStream_t stream) {
+    uint32_t* partial = reinterpret_cast<uint32_t*>(ws);
+    a.supplied = 0;
+    if (P > kMaxInlinePartials) {
+        float* amax = reinterpret_cast<float*>(reinterpret_cast<uint8_t*>(ws) + ((size_t)P * 4 + 255) / 256 * 256);
+        launch_amax_finalize(partial, P, amax, stream);
+        a.amax = amax;
+    } else {
+        // an empty tensor (P = 0) reduces to amax 0: scale 1
+        a.amax = nullptr;
+        a.partial = partial;
+        a.npartial = P;
+    }
+}
+
+int64_t tiles_x(int64_t cols) { const int64_t g = (cols + kTile - 1) / kTile; return g > 0 ? g : 1; }
+int64_t tiles_y(int64_t rows) { const int64_t g = (rows + kTile - 1) / kTile; return g > 0 ? g : 1; }
+
+}  // namespace
+
+void launch_quantize_tensor(int fmt, QuantArgs a, void* ws, hipStream_t stream) {
+    const int P = amax_num_partials(a.rows, a.cols);
+    if (P > 0) launch_amax_partials(a.x, a.rows, a.cols, a.ld, reinterpret_cast<uint32_t*>(ws), P, stream);
+    amax_source(a, P, ws, stream);
+    launch_quantize(fmt, kQTensor, a, stream);
+}
+
+void launch_quantize_tensor_pair(int fmt, QuantArgs a0, void* ws0, QuantArgs a1, void* ws1,
+                                 hipStream_t stream) {
+    const int P0 = amax_num_partials(a0.rows, a0.cols), P1 = amax_num_partials(a1.rows, a1.cols);
+    const bool dense = a0.ld == a0.cols && a1.ld == a1.cols;
+    if (P0 == 0 || P1 == 0 || P0 + P1 > (int64_t)INT32_MAX) {
+        launch_quantize_tensor(fmt, a0, ws0, stream);
+        launch_quantize_tensor(fmt, a1, ws1, stream);
+        return;
+    }
+    const AmaxJob j0{a0.x, a0.rows, a0.ld, reinterpret_cast<uint32_t*>(ws0), (uint32_t)(a0.cols / 8), P0};
+    const AmaxJob j1{a1.x, a1.rows, a1.ld, reinterpret_cast<uint32_t*>(ws1), (uint32_t)(a1.cols / 8), P1};
+    if (dense) amax_partial_kernel<true><<<P0 + P1, kThreads, 0, stream>>>(j0, j1);
+    else amax_partial_kernel<false><<<P0 + P1, kThreads, 0, stream>>>(j0, j1);
+    amax_source(a0, P0, ws0, stream);
+    amax_source(a1, P1, ws1, stream);
+    const int64_t gx0 = tiles_x(a0.cols), gx1 = tiles_x(a1.cols);
+    const int64_t t0 = gx0 * tiles_y(a0.rows), t1 = gx1 * tiles_y(a1.rows);
+    const unsigned grid = (unsigned)(t0 + t1);
+    if (fmt == kE4M3)
+        quant_tensor_kernel<kE4M3><<<grid, kThreads, 0, stream>>>(a0, a1, (int)t0, (int)gx0, (int)gx1);
+    else
+        quant_tensor_kernel<kE5M2><<<grid, kThreads, 0, stream>>>(a0, a1, (int)t0, (int)gx0, (int)gx1);
 }
 
 }  // namespace puro
