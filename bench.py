@@ -8,9 +8,9 @@ puro_linear_bwd). Inputs are seeded synthetic tensors resident in HBM before
 the timed region.
 
 Prints one JSON line: the metric (TFLOP/s of fwd + dgrad + wgrad GEMM work per
-step time), a roofline entry for the dominant kernel (its average launch time
-from HIP events around each launch in a second timed loop), and the CPU oracle
-timed on a slice of the same workload.
+step time), a per-call breakdown and a roofline entry for the dominant kernel
+(each call timed with HIP events on its stream around back-to-back launches),
+and the CPU oracle timed on a sample of the same workload.
 """
 
 import argparse
@@ -34,8 +34,9 @@ def parse():
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--tokens", type=int, default=8192)
-    ap.add_argument("--cpu-tokens", type=int, default=4096,
+    ap.add_argument("--cpu-tokens", type=int, default=8192,
                     help="tokens of the workload the CPU oracle is timed on (0: skip)")
+    ap.add_argument("--cpu-reps", type=int, default=4, help="repetitions of the CPU oracle sample")
     ap.add_argument("--only", choices=("step",) + CALLS + ("copy",),
                     help="run just this call (or a whole step) warmup + steps times and print its average "
                          "time, for profilers; 'copy' is a plain 256 MiB device copy that calibrates "
@@ -43,24 +44,25 @@ def parse():
     return ap.parse_args()
 
 
-def cpu_baseline(tokens):
+def cpu_baseline(tokens, reps):
     """The oracle (test infrastructure, unmodified) on the first `tokens`
-    tokens of the same workload: quantisation of X, W, dY and the three FP64
-    GEMMs; reported as TFLOP/s of the sampled GEMM work."""
+    tokens of the same workload, `reps` times over: quantisation of X, W, dY
+    and the three FP64 GEMMs; reported as TFLOP/s of the sampled GEMM work."""
     from oracle import linear
     from paper_2608_27370_amd import inputs
     d = inputs.qkv(M=tokens)
     rc = linear.recipe("tensor")
     t0 = time.perf_counter()
-    _, _, saved = linear.linear_fwd(d["X"], d["W"], rc)
-    linear.linear_bwd(d["dY"], saved, rc)
+    for _ in range(reps):
+        _, _, saved = linear.linear_fwd(d["X"], d["W"], rc)
+        linear.linear_bwd(d["dY"], saved, rc)
     dt = time.perf_counter() - t0
-    flops = 3 * 2.0 * tokens * inputs.QKV_OUT * inputs.HIDDEN
+    flops = reps * 3 * 2.0 * tokens * inputs.QKV_OUT * inputs.HIDDEN
     threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
     return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
             "seconds": round(dt, 2),
-            "sample": "oracle linear fwd+bwd on the first %d of 8192 tokens (X[%d,1536], W[2048,1536], "
-                      "dY[%d,2048]); FP64 GEMMs on %d OpenMP threads" % (tokens, tokens, tokens, threads)}
+            "sample": "oracle linear fwd+bwd on %d of the 8192 tokens (X[%d,1536], W[2048,1536], dY[%d,2048]), "
+                      "%d times; FP64 GEMMs on %d OpenMP threads" % (tokens, tokens, tokens, reps, threads)}
 
 
 CALLS = ("quantize_x", "quantize_w", "fprop", "quantize_dy", "dgrad", "wgrad")
@@ -95,15 +97,15 @@ def calls(torch, puro, dev, M, N, K, X, W, dY, Y, dX, dW, saved):
          N * K * 4.0, 2),
         ("fprop", "fprop GEMM %dx%dx%d" % (M, N, K),
          lambda: puro.fp8_gemm(A_f, M, B_f, N, K, puro.OUT_BF16, D=Y, ws=gws), 2.0 * M * N * K, None,
-         1 + (puro.fp8_gemm_workspace_size(M, N, K, 0) > 0)),
+         puro.fp8_gemm_plan(M, N, K)["launches"]),
         ("quantize_dy", "quantize dY (amax + encode, q and qT)", lambda: puro.quantize_fp8(
             dY, puro.E5M2, out=dict(q=dyq, scale=sdy, qT=dyqT), want_qT=True, ws=qws), None, M * N * 4.0, 2),
         ("dgrad", "dgrad GEMM %dx%dx%d" % (M, K, N),
          lambda: puro.fp8_gemm(A_d, M, B_d, K, N, puro.OUT_BF16, D=dX, ws=gws), 2.0 * M * N * K, None,
-         1 + (puro.fp8_gemm_workspace_size(M, K, N, 0) > 0)),
+         puro.fp8_gemm_plan(M, K, N)["launches"]),
         ("wgrad", "wgrad GEMM %dx%dx%d" % (N, K, M),
          lambda: puro.fp8_gemm(A_w, N, B_w, K, M, puro.OUT_FP32, D=dW, ws=gws), 2.0 * M * N * K, None,
-         1 + (puro.fp8_gemm_workspace_size(N, K, M, 1) > 0)),
+         puro.fp8_gemm_plan(N, K, M)["launches"]),
     ]
 
 
@@ -204,25 +206,23 @@ def main():
     gemm_flops = 3 * 2.0 * M * N * K
     value = gemm_flops / (ms_per_step * 1e-3) / 1e12
 
+    # each call on its own, timed over back-to-back launches between two
+    # events on the stream they run on (so that host launch latency hides
+    # behind the queue, as in the step)
     kernels = calls(torch, puro, dev, M, N, K, X, W, dY, Y, dX, dW, saved)
     reps = max(20, args.steps // 2)
-    for _, _, fn, _, _, _ in kernels:
-        fn()
-    torch.cuda.synchronize()
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in kernels]
-    tot = [0.0] * len(kernels)
-    for _ in range(reps):
-        for i, (_, _, fn, _, _, _) in enumerate(kernels):
-            ev[i][0].record(stream)
-            fn()
-            ev[i][1].record(stream)
-        torch.cuda.synchronize()
-        for i in range(len(kernels)):
-            tot[i] += ev[i][0].elapsed_time(ev[i][1])
     breakdown = []
-    for i, (_, name, _, flops, nbytes, _) in enumerate(kernels):
-        us = tot[i] / reps * 1e3
-        row = {"call": name, "us": round(us, 2)}
+    for _, name, fn, flops, nbytes, launches in kernels:
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(reps):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) / reps * 1e3
+        row = {"call": name, "us": round(us, 2), "launches": launches}
         if flops:
             row["tflops"] = round(flops / (us * 1e-6) / 1e12, 1)
         if nbytes:
@@ -230,16 +230,21 @@ def main():
         breakdown.append(row)
     gemm_rows = [r for r in breakdown if "tflops" in r]
     gemm_us = sum(r["us"] for r in gemm_rows)
-    # dominant kernel: the slowest GEMM call that is a single kernel launch (a
-    # call that splits K adds a reduction launch and is not one kernel)
-    single = [r for r, k in zip(breakdown, kernels) if "tflops" in r and k[5] == 1]
-    dom = max(single, key=lambda r: r["us"])
-    dom_key = [k[0] for r, k in zip(breakdown, kernels) if r is dom][0]
-    traffic = profiled_traffic(dom_key) if M == 8192 else None
-    roofline = {"bound": "mfma", "kernel": dom["call"], "achieved": dom["tflops"], "peak": FP8_PEAK_TFLOPS,
-                "unit": "TFLOP/s", "frac": round(dom["tflops"] / FP8_PEAK_TFLOPS, 4), "traffic": traffic,
-                "traffic_unit": "bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
-                "algorithmic_flops_per_launch": 2.0 * M * N * K}
+    # dominant kernel: the slowest call that is a single kernel launch
+    single = [(r, k) for r, k in zip(breakdown, kernels) if k[5] == 1]
+    dom, dom_k = max(single, key=lambda rk: rk[0]["us"])
+    traffic = profiled_traffic(dom_k[0]) if M == 8192 else None
+    if "tflops" in dom:
+        roofline = {"bound": "mfma", "kernel": dom["call"], "achieved": dom["tflops"], "peak": FP8_PEAK_TFLOPS,
+                    "unit": "TFLOP/s", "frac": round(dom["tflops"] / FP8_PEAK_TFLOPS, 4),
+                    "algorithmic_flops_per_launch": dom_k[3]}
+    else:
+        roofline = {"bound": "hbm", "kernel": dom["call"], "achieved": dom["gbs_algorithmic"], "peak": HBM_PEAK_GBS,
+                    "unit": "GB/s", "frac": round(dom["gbs_algorithmic"] / HBM_PEAK_GBS, 4),
+                    "algorithmic_bytes_per_launch": dom_k[4]}
+    roofline["us_per_launch"] = dom["us"]
+    roofline["traffic"] = traffic
+    roofline["traffic_unit"] = "HBM-side bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)"
 
     out = {
         "metric": METRIC,
@@ -263,7 +268,7 @@ def main():
         "wall_s_timed": round(wall, 3),
     }
     if args.cpu_tokens > 0:
-        out["cpu_baseline"] = cpu_baseline(args.cpu_tokens)
+        out["cpu_baseline"] = cpu_baseline(args.cpu_tokens, args.cpu_reps)
     print(json.dumps(out))
 
 

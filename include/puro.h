@@ -148,6 +148,17 @@ typedef struct {
 } puro_fp8_operand;
 
 size_t puro_fp8_gemm_workspace_size(int64_t M, int64_t N, int64_t K, puro_out_dtype d_type);
+/* The execution plan puro_fp8_gemm chooses for this problem (host-side query;
+ * enqueues nothing): the workgroup tile (tile_m x tile_n outputs), the depth
+ * of its LDS ring (stages), the number of k ranges (splits > 1: FP32 partial
+ * sums in ws plus a fixed-order reduction kernel) and the kernel launches
+ * that makes. a_mode / b_mode are the operands' scale modes (the plan differs
+ * with block scales). Outputs may be NULL. PURO_ERR_SHAPE for negative sizes,
+ * PURO_ERR_UNSUPPORTED for a mode the GEMM does not take. For tests and
+ * benchmarks that need to know which kernel configuration runs. */
+puro_status puro_fp8_gemm_plan(int64_t M, int64_t N, int64_t K, puro_scale_mode a_mode,
+                               puro_scale_mode b_mode, int* tile_m, int* tile_n, int* stages,
+                               int* splits, int* launches);
 puro_status puro_fp8_gemm(int64_t M, int64_t N, int64_t K,
                           const puro_fp8_operand* A, const puro_fp8_operand* B,
                           void* D, puro_out_dtype d_type, int64_t ldd, int accumulate,

@@ -150,6 +150,24 @@ size_t puro_fp8_gemm_workspace_size(int64_t M, int64_t N, int64_t K, puro_out_dt
     return gemm_workspace_bytes(M, N, K, d_type == PURO_OUT_FP32 ? kOutF32 : kOutBF16);
 }
 
+puro_status puro_fp8_gemm_plan(int64_t M, int64_t N, int64_t K, puro_scale_mode a_mode,
+                               puro_scale_mode b_mode, int* tile_m, int* tile_n, int* stages, int* splits,
+                               int* launches) {
+    if (M < 0 || N < 0 || K < 0) return PURO_ERR_SHAPE;
+    auto ok = [](puro_scale_mode m) {
+        return m == PURO_SCALE_TENSOR || m == PURO_SCALE_ROW_1x128 || m == PURO_SCALE_BLOCK_128x128;
+    };
+    if (!ok(a_mode) || !ok(b_mode)) return PURO_ERR_UNSUPPORTED;
+    int tm = 0, tn = 0, ns = 0, s = 1;
+    gemm_plan(M, N, K, a_mode != PURO_SCALE_TENSOR || b_mode != PURO_SCALE_TENSOR, &tm, &tn, &ns, &s);
+    if (tile_m) *tile_m = tm;
+    if (tile_n) *tile_n = tn;
+    if (stages) *stages = ns;
+    if (splits) *splits = s;
+    if (launches) *launches = (M > 0 && N > 0) ? 1 + (s > 1) : 0;
+    return PURO_OK;
+}
+
 static puro_status check_operand(const puro_fp8_operand* o, int64_t rows, int64_t K, int* smode) {
     if (!o) return PURO_ERR_NULL;
     // the scale is read whenever the operand has rows (also for K == 0, where

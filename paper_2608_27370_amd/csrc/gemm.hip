@@ -683,6 +683,15 @@ size_t gemm_workspace_bytes(int64_t M, int64_t N, int64_t K, int out) {
     return a > b ? a : b;
 }
 
+void gemm_plan(int64_t M, int64_t N, int64_t K, bool grouped, int* tile_m, int* tile_n, int* stages,
+               int* splits) {
+    const Plan p = make_plan(M, N, K, grouped);
+    *tile_m = kTiles[p.cfg].bm;
+    *tile_n = kTiles[p.cfg].bn;
+    *stages = kTiles[p.cfg].nst;
+    *splits = p.splits;
+}
+
 void launch_gemm(const GemmProblem& g, void* ws, hipStream_t stream) {
     const bool grouped = g.sa_mode != kSTensor || g.sb_mode != kSTensor;
     run_plan(g, make_plan(g.M, g.N, g.K, grouped), ws, stream);

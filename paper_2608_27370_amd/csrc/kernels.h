@@ -81,6 +81,9 @@ struct GemmProblem {
 
 // Workspace the GEMM needs for split-K partial sums (0 when it runs unsplit).
 size_t gemm_workspace_bytes(int64_t M, int64_t N, int64_t K, int out);
+// The plan launch_gemm takes: tile, ring depth, k ranges.
+void gemm_plan(int64_t M, int64_t N, int64_t K, bool grouped, int* tile_m, int* tile_n, int* stages,
+               int* splits);
 // Enqueue the GEMM; `ws` must hold gemm_workspace_bytes(...) bytes.
 void launch_gemm(const GemmProblem& p, void* ws, hipStream_t stream);
 

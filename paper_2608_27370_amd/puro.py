@@ -56,6 +56,8 @@ _SIGS = {
     "puro_quantize_workspace_size": (_sz, [_i64, _i64]),
     "puro_quantize_fp8": (_i, [_p, _i64, _i64, _i64, _i, _i, _i, _p, _p, _p, _p, _p, _p, _sz, _p]),
     "puro_fp8_gemm_workspace_size": (_sz, [_i64, _i64, _i64, _i]),
+    "puro_fp8_gemm_plan": (_i, [_i64, _i64, _i64, _i, _i, ctypes.POINTER(_i), ctypes.POINTER(_i),
+                                ctypes.POINTER(_i), ctypes.POINTER(_i), ctypes.POINTER(_i)]),
     "puro_fp8_gemm": (_i, [_i64, _i64, _i64, ctypes.POINTER(Operand), ctypes.POINTER(Operand),
                            _p, _i, _i64, _i, _p, _sz, _p]),
     "puro_linear_saved_bytes": (_sz, [_i64, _i64, _i64, ctypes.POINTER(Recipe), ctypes.POINTER(_sz * 4)]),
@@ -183,6 +185,13 @@ def operand(data, fmt, mode, scale):
 
 def fp8_gemm_workspace_size(M, N, K, out_dtype):
     return lib().puro_fp8_gemm_workspace_size(M, N, K, out_dtype)
+
+
+def fp8_gemm_plan(M, N, K, a_mode=SCALE_TENSOR, b_mode=SCALE_TENSOR):
+    """The plan puro_fp8_gemm takes: dict(tile_m, tile_n, stages, splits, launches)."""
+    v = [_i() for _ in range(5)]
+    _check("puro_fp8_gemm_plan", lib().puro_fp8_gemm_plan(M, N, K, a_mode, b_mode, *[ctypes.byref(x) for x in v]))
+    return dict(zip(("tile_m", "tile_n", "stages", "splits", "launches"), (x.value for x in v)))
 
 
 def fp8_gemm(A, a_rows, B, b_rows, K, out_dtype=OUT_BF16, D=None, accumulate=False, ws=None):

@@ -153,3 +153,28 @@ def test_linear_validation(puro):
     assert list(sizes) == [384 * 256, 384 * 2 * 4, 384 * 512, 3 * 4 * 4] and total == sum(sizes)
     total = L.puro_linear_saved_bytes(256, 512, 384, byref(rc), byref(sizes))
     assert list(sizes) == [384 * 256, 4, 384 * 512, 4]
+
+
+# Shapes on which the GEMM planner takes each of its kernel configurations
+# (tile, ring depth) and the split-K path; tests/test_gpu_gemm.py runs them.
+PLAN_SHAPES = {(256, 256, 2): (3072, 4096, 256), (256, 192, 2): (3072, 3072, 256),
+               (128, 128, 4): (256, 256, 256), (128, 128, 2): (1536, 3072, 256)}
+SPLIT_SHAPE = (256, 256, 1024)
+
+
+@pytest.mark.parametrize("modes", [(0, 0), (1, 3)], ids=["tensor", "row-block"])
+def test_gemm_plan_covers_every_configuration(puro, modes):
+    for cfg, shape in PLAN_SHAPES.items():
+        p = puro.fp8_gemm_plan(*shape, *modes)
+        assert (p["tile_m"], p["tile_n"], p["stages"]) == cfg, (shape, p)
+        assert p["splits"] == 1 and p["launches"] == 1
+    p = puro.fp8_gemm_plan(*SPLIT_SHAPE, *modes)
+    assert p["splits"] > 1 and p["launches"] == 2
+
+
+def test_gemm_plan_validation(puro):
+    L = puro.lib()
+    assert L.puro_fp8_gemm_plan(-1, 16, 16, 0, 0, None, None, None, None, None) == ERR_SHAPE
+    assert L.puro_fp8_gemm_plan(16, 16, 16, 2, 0, None, None, None, None, None) == ERR_UNSUPPORTED  # 128x1
+    assert L.puro_fp8_gemm_plan(16, 16, 16, 0, 0, None, None, None, None, None) == OK
+    assert puro.fp8_gemm_plan(0, 16, 16)["launches"] == 0

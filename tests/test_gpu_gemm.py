@@ -199,3 +199,37 @@ def test_gemm_is_deterministic(P):
     D1 = host(_run(P, a, E4, sa, "tensor", b, E4, sb, "tensor", 1))
     D2 = host(_run(P, a, E4, sa, "tensor", b, E4, sb, "tensor", 1))
     assert np.array_equal(D1.view(np.uint32), D2.view(np.uint32))
+
+
+# One shape per kernel configuration of the planner (tile, ring depth) and one
+# that takes the split-K path; tests/test_abi.py checks that the planner maps
+# them so. Outputs are compared on stratified samples plus the whole first and
+# last 256x256 tiles.
+PLAN_CASES = [(3072, 4096, 256), (3072, 3072, 256), (256, 256, 256), (1536, 3072, 256), (256, 256, 1024)]
+
+
+@pytest.mark.parametrize("shape", PLAN_CASES, ids=lambda s: "x".join(map(str, s)))
+@pytest.mark.parametrize("scales", ["tensor", "row-block"])
+def test_gemm_every_configuration(P, shape, scales):
+    from gpu_util import sample_entries
+    M, N, K = shape
+    if scales == "tensor":
+        a, sa = _operand_tensor(21, M, K, E5, std=1e-3)
+        b, sb = _operand_tensor(22, N, K, E4, std=0.02)
+        am, bm = "tensor", "tensor"
+    else:
+        a, sa = _operand_grouped(21, M, K, E5, "row", std=1e-3)
+        b, sb = _operand_grouped(22, N, K, E4, "block", std=0.02)
+        am, bm = "row", "block"
+    plan = P.fp8_gemm_plan(M, N, K, MODE[am], MODE[bm])
+    op = (a, fp8.E5M2, sa, am, b, fp8.E4M3, sb, bm)
+    ms, ns = sample_entries(M, N, np.random.default_rng(M + N + K))
+    ref, den = gemm.gemm_entries(ms, ns, *op)
+    slack = mfma_model.truncation_loss(ms, ns, *op)
+    for out in (0, 1):
+        D = _run(P, a, E5, sa, am, b, E4, sb, bm, out)
+        what = "%s %s plan %s out %d" % (scales, shape, plan, out)
+        if out == 1:
+            check_fp32(host(D)[ms, ns], ref, den, what=what, slack=slack)
+        else:
+            check_bf16(bf16_bits(D)[ms, ns], ref, den, what=what, slack=slack)
