@@ -37,6 +37,9 @@ def parse():
     ap.add_argument("--cpu-tokens", type=int, default=8192,
                     help="tokens of the workload the CPU oracle is timed on (0: skip)")
     ap.add_argument("--cpu-reps", type=int, default=4, help="repetitions of the CPU oracle sample")
+    ap.add_argument("--graph", action="store_true",
+                    help="replay the step captured in a HIP graph instead of launching its kernels one by one "
+                         "(measured no faster: the launches are not host-bound)")
     ap.add_argument("--only", choices=("step",) + CALLS + ("copy",),
                     help="run just this call (or a whole step) warmup + steps times and print its average "
                          "time, for profilers; 'copy' is a plain 256 MiB device copy that calibrates "
@@ -194,11 +197,28 @@ def main():
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
+    run = step
+    if args.graph:
+        # the step's launches captured once in a HIP graph and replayed: the
+        # same kernels on the same buffers, without per-launch host overhead
+        side = torch.cuda.Stream()
+        side.wait_stream(stream)
+        with torch.cuda.stream(side):
+            step()
+        stream.wait_stream(side)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            step()
+        run = graph.replay
+        for _ in range(args.warmup):
+            run()
+        torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     t0 = time.perf_counter()
     e0.record(stream)
     for _ in range(args.steps):
-        step()
+        run()
     e1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
@@ -260,7 +280,8 @@ def main():
         "dtype": "fp8",
         "data": "synthetic",
         "config": {"workload": "qkv_projection_fwd_dgrad_wgrad", "M": M, "K": K, "N": N,
-                   "recipe": "per-tensor scales, X/W E4M3, dY E5M2, BF16 Y/dX, FP32 dW"},
+                   "recipe": "per-tensor scales, X/W E4M3, dY E5M2, BF16 Y/dX, FP32 dW",
+                   "launch": "hip_graph" if args.graph else "eager"},
         "pct_fp8_peak": round(100 * value / FP8_PEAK_TFLOPS, 2),
         "gemm_only_tflops": round(gemm_flops / (gemm_us * 1e-6) / 1e12, 1),
         "breakdown": breakdown,
