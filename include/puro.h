@@ -181,8 +181,14 @@ typedef struct {
 /* What the forward pass keeps for the backward pass (caller-allocated):
  * the quantised input, transposed for Wgrad (Section 3.2 keeps the quantised
  * input for Wgrad), and the quantised weight, transposed for Dgrad.
- *   xq_t    [K, M] FP8;  x_scale: per-tensor [1], blockwise [K, M/128]
- *   wq_t    [K, N] FP8;  w_scale: per-tensor [1], blockwise [K/128, N/128]  */
+ *   xq_t    [K, M] FP8;  x_scale: per-tensor [1], blockwise [M/128, K]
+ *   wq_t    [K, N] FP8;  w_scale: per-tensor [1], blockwise [N/128, K/128]
+ * Blockwise scales are stored k-block-major (the group index along the
+ * reduction dimension of the GEMM that reads them outermost): x_scale[b][k]
+ * is the scale of xq_t row k, m in [128 b, 128 b + 128); w_scale[b][c] that
+ * of the block of wq_t rows [128 c, 128 c + 128) and columns [128 b, ...).
+ * The Wgrad and Dgrad GEMMs then read a k block's scales as one contiguous
+ * run. (puro_quantize_fp8 and puro_fp8_gemm use the row-major layouts.)  */
 typedef struct {
     uint8_t* xq_t;
     float* x_scale;

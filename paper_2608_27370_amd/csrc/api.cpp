@@ -86,10 +86,16 @@ size_t puro_quantize_workspace_size(int64_t rows, int64_t cols) {
     return quant_tensor_ws_bytes(rows, cols);
 }
 
-puro_status puro_quantize_fp8(const uint16_t* x, int64_t rows, int64_t cols, int64_t ld,
-                              puro_fp8_format fmt, puro_scale_mode mode, puro_scale_rounding rnd,
-                              const float* amax_in, uint8_t* q, float* scale, uint8_t* qT,
-                              float* scaleT, void* ws, size_t ws_bytes, hipStream_t stream) {
+}  // extern "C"
+
+namespace {
+
+// puro_quantize_fp8 with a choice of grouped-scale layout (kmajor: k-block-
+// major, as the linear layer keeps its scales for the GEMM).
+puro_status quantize_impl(const uint16_t* x, int64_t rows, int64_t cols, int64_t ld, puro_fp8_format fmt,
+                          puro_scale_mode mode, puro_scale_rounding rnd, const float* amax_in, uint8_t* q,
+                          float* scale, uint8_t* qT, float* scaleT, void* ws, size_t ws_bytes, int kmajor,
+                          hipStream_t stream) {
     puro_status st = check_bf16_matrix(x, rows, cols, ld);
     if (st != PURO_OK) return st;
     if (!fmt_ok(fmt) || (rnd != PURO_SCALE_FP32 && rnd != PURO_SCALE_POW2)) return PURO_ERR_UNSUPPORTED;
@@ -100,6 +106,7 @@ puro_status puro_quantize_fp8(const uint16_t* x, int64_t rows, int64_t cols, int
     a.amax = amax_in;
     a.supplied = amax_in != nullptr;
     a.pow2 = rnd == PURO_SCALE_POW2;
+    a.kmajor = kmajor;
     // outputs of an empty tensor are never written (torch hands out NULL for them)
     const bool empty = rows == 0 || cols == 0;
     int qmode;
@@ -142,6 +149,18 @@ puro_status puro_quantize_fp8(const uint16_t* x, int64_t rows, int64_t cols, int
     if ((rows == 0 || cols == 0) && qmode != kQTensor) return PURO_OK;
     launch_quantize(fmt, qmode, a, stream);
     return launched();
+}
+
+}  // namespace
+
+extern "C" {
+
+puro_status puro_quantize_fp8(const uint16_t* x, int64_t rows, int64_t cols, int64_t ld,
+                              puro_fp8_format fmt, puro_scale_mode mode, puro_scale_rounding rnd,
+                              const float* amax_in, uint8_t* q, float* scale, uint8_t* qT,
+                              float* scaleT, void* ws, size_t ws_bytes, hipStream_t stream) {
+    return quantize_impl(x, rows, cols, ld, fmt, mode, rnd, amax_in, q, scale, qT, scaleT, ws, ws_bytes, 0,
+                         stream);
 }
 
 // ------------------------------------------------------------------- GEMM
@@ -188,9 +207,14 @@ static puro_status check_operand(const puro_fp8_operand* o, int64_t rows, int64_
     return PURO_OK;
 }
 
-puro_status puro_fp8_gemm(int64_t M, int64_t N, int64_t K, const puro_fp8_operand* A,
-                          const puro_fp8_operand* B, void* D, puro_out_dtype d_type, int64_t ldd,
-                          int accumulate, void* ws, size_t ws_bytes, hipStream_t stream) {
+}  // extern "C"
+
+namespace {
+
+// puro_fp8_gemm with a choice of grouped-scale layout per operand.
+puro_status gemm_impl(int64_t M, int64_t N, int64_t K, const puro_fp8_operand* A, const puro_fp8_operand* B,
+                      void* D, puro_out_dtype d_type, int64_t ldd, int accumulate, void* ws, size_t ws_bytes,
+                      int a_kmajor, int b_kmajor, hipStream_t stream) {
     if (M < 0 || N < 0 || K < 0) return PURO_ERR_SHAPE;
     if (M > INT32_MAX / 2 || N > INT32_MAX / 2 || K > INT32_MAX / 2) return PURO_ERR_SHAPE;
     int sa = 0, sb = 0;
@@ -213,8 +237,19 @@ puro_status puro_fp8_gemm(int64_t M, int64_t N, int64_t K, const puro_fp8_operan
     g.A = A->data; g.lda = A->ld; g.fa = A->fmt; g.sa_mode = sa; g.sa = A->scale;
     g.B = B->data; g.ldb = B->ld; g.fb = B->fmt; g.sb_mode = sb; g.sb = B->scale;
     g.D = D; g.ldd = ldd; g.out = out; g.accumulate = accumulate != 0;
+    g.sa_kmajor = a_kmajor; g.sb_kmajor = b_kmajor;
     launch_gemm(g, ws, stream);
     return launched();
+}
+
+}  // namespace
+
+extern "C" {
+
+puro_status puro_fp8_gemm(int64_t M, int64_t N, int64_t K, const puro_fp8_operand* A,
+                          const puro_fp8_operand* B, void* D, puro_out_dtype d_type, int64_t ldd,
+                          int accumulate, void* ws, size_t ws_bytes, hipStream_t stream) {
+    return gemm_impl(M, N, K, A, B, D, d_type, ldd, accumulate, ws, ws_bytes, 0, 0, stream);
 }
 
 // ----------------------------------------------------------- linear layer
@@ -345,17 +380,19 @@ puro_status puro_linear_fwd(const uint16_t* X, const uint16_t* W, int64_t M, int
         // column-grouped transposed copy kept for Wgrad.
         float* xs_row = reinterpret_cast<float*>(w8 + l.xs_row);
         float* w_blk = reinterpret_cast<float*>(w8 + l.w_blk);
-        st = puro_quantize_fp8(X, M, K, K, r->x_fmt, PURO_SCALE_ROW_1x128, PURO_SCALE_POW2, nullptr, xq,
-                               xs_row, saved->xq_t, saved->x_scale, nullptr, 0, stream);
+        st = quantize_impl(X, M, K, K, r->x_fmt, PURO_SCALE_ROW_1x128, PURO_SCALE_POW2, nullptr, xq, xs_row,
+                           saved->xq_t, saved->x_scale, nullptr, 0, 1, stream);
         if (st != PURO_OK) return st;
         // W: 128x128 blocks, plus the transposed copy (same blocks) kept for Dgrad.
-        st = puro_quantize_fp8(W, N, K, K, r->w_fmt, PURO_SCALE_BLOCK_128x128, PURO_SCALE_POW2, nullptr, wq,
-                               w_blk, saved->wq_t, saved->w_scale, nullptr, 0, stream);
+        st = quantize_impl(W, N, K, K, r->w_fmt, PURO_SCALE_BLOCK_128x128, PURO_SCALE_POW2, nullptr, wq, w_blk,
+                           saved->wq_t, saved->w_scale, nullptr, 0, 1, stream);
         if (st != PURO_OK) return st;
         A = puro_fp8_operand{xq, K, r->x_fmt, PURO_SCALE_ROW_1x128, xs_row};
         B = puro_fp8_operand{wq, K, r->w_fmt, PURO_SCALE_BLOCK_128x128, w_blk};
     }
-    return puro_fp8_gemm(M, N, K, &A, &B, Y, PURO_OUT_BF16, N, 0, w8 + l.gemm, ws_bytes - l.gemm, stream);
+    // blockwise scales are kept k-block-major: the GEMM loads a slice's scales as contiguous runs
+    const int km = r->blockwise ? 1 : 0;
+    return gemm_impl(M, N, K, &A, &B, Y, PURO_OUT_BF16, N, 0, w8 + l.gemm, ws_bytes - l.gemm, km, km, stream);
 }
 
 puro_status puro_linear_bwd(const uint16_t* dY, const puro_linear_saved* saved, int64_t M, int64_t N,
@@ -389,20 +426,21 @@ puro_status puro_linear_bwd(const uint16_t* dY, const puro_linear_saved* saved, 
         wA = puro_fp8_operand{dyq_t, M, r->dy_fmt, PURO_SCALE_TENSOR, dys};
         wB = puro_fp8_operand{saved->xq_t, M, r->x_fmt, PURO_SCALE_TENSOR, saved->x_scale};
     } else {
-        st = puro_quantize_fp8(dY, M, N, N, r->dy_fmt, PURO_SCALE_ROW_1x128, PURO_SCALE_POW2, nullptr, dyq,
-                               dys, dyq_t, dys_t, nullptr, 0, stream);
+        st = quantize_impl(dY, M, N, N, r->dy_fmt, PURO_SCALE_ROW_1x128, PURO_SCALE_POW2, nullptr, dyq, dys,
+                           dyq_t, dys_t, nullptr, 0, 1, stream);
         if (st != PURO_OK) return st;
         dA = puro_fp8_operand{dyq, N, r->dy_fmt, PURO_SCALE_ROW_1x128, dys};
         dB = puro_fp8_operand{saved->wq_t, N, r->w_fmt, PURO_SCALE_BLOCK_128x128, saved->w_scale};
         wA = puro_fp8_operand{dyq_t, M, r->dy_fmt, PURO_SCALE_ROW_1x128, dys_t};
         wB = puro_fp8_operand{saved->xq_t, M, r->x_fmt, PURO_SCALE_ROW_1x128, saved->x_scale};
     }
+    const int km = r->blockwise ? 1 : 0;
     if (dX) {
-        st = puro_fp8_gemm(M, K, N, &dA, &dB, dX, PURO_OUT_BF16, K, 0, gws, gws_bytes, stream);
+        st = gemm_impl(M, K, N, &dA, &dB, dX, PURO_OUT_BF16, K, 0, gws, gws_bytes, km, km, stream);
         if (st != PURO_OK) return st;
     }
     if (dW) {
-        st = puro_fp8_gemm(N, K, M, &wA, &wB, dW, PURO_OUT_FP32, K, accumulate_dW, gws, gws_bytes, stream);
+        st = gemm_impl(N, K, M, &wA, &wB, dW, PURO_OUT_FP32, K, accumulate_dW, gws, gws_bytes, km, km, stream);
         if (st != PURO_OK) return st;
     }
     return PURO_OK;

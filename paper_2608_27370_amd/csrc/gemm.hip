@@ -64,7 +64,8 @@ struct Params {
     int64_t lda, ldb, ldd;
     int M, N, K;
     int a_mode, b_mode;
-    int ld_sa, ld_sb;          // scale row pitch (K/128) for grouped modes
+    int a_kmajor, b_kmajor;    // grouped scales k-block-major rather than row-major
+    int ld_sa, ld_sb;          // scale pitch: K/128 (row-major) or the row (block) count (k-major)
     uint32_t sa_bytes, sb_bytes;  // sizes of the scale arrays (grouped modes)
     int ksteps, ksteps_per_split, splits;
     int tiles_m, tiles_n;
@@ -232,16 +233,29 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_fp8_kernel(Params p) {
             if (is_a) dma_to_lds<16>(ra, sbase + blk * 1024, rowA + blk * blkA + off);
             else dma_to_lds<16>(rb, sbase + A_BYTES + blk * 1024, rowB + blk * blkB + off);
         } else if constexpr (GROUPED) {
-            // lane l of scale load t brings the scale of tile row 64 t + l
-            // (A rows, then B rows) for the 128-wide k block of the slice
+            // scale load t brings entries 64 t .. 64 t + 63 of the slice's
+            // scale vector: BM entries for A, then BN for B. A row-scaled
+            // operand has one entry per tile row, a block-scaled one one per
+            // 128-row block (entries past that are unused). With k-major
+            // scales a load reads consecutive floats.
             const int t = (wave * SC_PER + (q - A_PER - B_PER)) % SC_BLK;
-            const int r = t * 64 + lane;
             const bool is_a = t * 64 < BM;
-            const int row = is_a ? m0 + r : n0 + (r - BM);
+            const int r = t * 64 + lane - (is_a ? 0 : BM);
             const int mode = is_a ? p.a_mode : p.b_mode;
+            const bool km = is_a ? p.a_kmajor : p.b_kmajor;
             const int ld = is_a ? p.ld_sa : p.ld_sb;
-            const int srow = mode == kSBlock ? row >> 7 : row;
-            const uint32_t soff = valid ? (uint32_t)(srow * ld + sl / SPB) * 4u : kOOB;
+            const int row0 = is_a ? m0 : n0;
+            const int kb = sl / SPB;
+            int idx = -1;
+            if (mode == kSBlock) {
+                const int blocks = ((is_a ? p.M : p.N) + 127) >> 7;
+                const int b = (row0 >> 7) + r;
+                if (r < ((is_a ? BM : BN) + 127) / 128 && b < blocks) idx = km ? kb * ld + b : b * ld + kb;
+            } else if (mode == kSRow) {
+                const int row = row0 + r;
+                if (row < (is_a ? p.M : p.N)) idx = km ? kb * ld + row : row * ld + kb;
+            }
+            const uint32_t soff = (valid && idx >= 0) ? (uint32_t)idx * 4u : kOOB;
             const uint32_t dst = ssc_lds + (st * (BM + BN) + t * 64) * 4;
             dma_to_lds<4>(is_a ? rsa : rsb, dst, soff);
         }
@@ -281,9 +295,11 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_fp8_kernel(Params p) {
             f.f[t] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
         } else {
             const int fi = t - (FM + FN);
-            const int r = fi < FM ? wm * WTM + fi * 32 + fr : BM + wn * WTN + (fi - FM) * 32 + fr;
-            const bool scaled = fi < FM ? p.a_mode != kSTensor : p.b_mode != kSTensor;
-            f.sc[fi] = scaled ? e8m0_of(ssc[st * (BM + BN) + r]) : 127u;
+            const bool is_a = fi < FM;
+            const int r = is_a ? wm * WTM + fi * 32 + fr : wn * WTN + (fi - FM) * 32 + fr;   // tile row
+            const int mode = is_a ? p.a_mode : p.b_mode;
+            const int idx = (is_a ? 0 : BM) + (mode == kSBlock ? r >> 7 : r);
+            f.sc[fi] = mode != kSTensor ? e8m0_of(ssc[st * (BM + BN) + idx]) : 127u;
         }
     };
     auto mfma_one = [&](const Frags& f, int t) __attribute__((always_inline)) {
@@ -637,7 +653,13 @@ void run_plan(const GemmProblem& g, const Plan& pl, void* ws, hipStream_t stream
     prm.lda = g.lda; prm.ldb = g.ldb; prm.ldd = g.ldd;
     prm.M = (int)g.M; prm.N = (int)g.N; prm.K = (int)g.K;
     prm.a_mode = g.sa_mode; prm.b_mode = g.sb_mode;
-    prm.ld_sa = (int)(g.K / kBK); prm.ld_sb = (int)(g.K / kBK);
+    prm.a_kmajor = g.sa_kmajor; prm.b_kmajor = g.sb_kmajor;
+    auto scale_ld = [&](int mode, bool km, int64_t rows) -> int {
+        if (!km) return (int)(g.K / kBK);
+        return (int)(mode == kSBlock ? (rows + 127) / 128 : rows);
+    };
+    prm.ld_sa = scale_ld(g.sa_mode, g.sa_kmajor, g.M);
+    prm.ld_sb = scale_ld(g.sb_mode, g.sb_kmajor, g.N);
     auto scale_bytes = [&](int mode, int64_t rows) -> uint32_t {
         if (mode == kSTensor) return 4u;
         const int64_t srows = mode == kSRow ? rows : (rows + 127) / 128;

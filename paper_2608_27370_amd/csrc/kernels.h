@@ -44,6 +44,9 @@ struct QuantArgs {
     int npartial;
     int supplied;
     int pow2;
+    // grouped modes: scale arrays k-block-major (the group index along the
+    // quantised copy's columns outermost) instead of row-major
+    int kmajor;
 };
 
 // Workspace of a per-tensor quantisation that computes its own amax.
@@ -77,6 +80,9 @@ struct GemmProblem {
     int64_t ldd;
     int out;
     int accumulate;
+    // grouped scales stored k-block-major ([K/128][rows] or [K/128][rows/128])
+    // instead of row-major ([rows][K/128] or [rows/128][K/128])
+    int sa_kmajor, sb_kmajor;
 };
 
 // Workspace the GEMM needs for split-K partial sums (0 when it runs unsplit).

@@ -280,7 +280,7 @@ __global__ __launch_bounds__(kThreads) void quant_groups_kernel(QuantArgs a) {
 #pragma unroll
             for (int i = 0; i < 8; ++i) {
                 const int64_t r = t.row0 + i;
-                if (r < a.rows) a.scale[r * ng + blockIdx.x] = srow[i];
+                if (r < a.rows) a.scale[a.kmajor ? (int64_t)blockIdx.x * a.rows + r : r * ng + blockIdx.x] = srow[i];
             }
         }
     }
@@ -334,7 +334,8 @@ __global__ __launch_bounds__(kThreads) void quant_groups_kernel(QuantArgs a) {
         if (t.rg == 0 && t.col_ok) {
             const int64_t ng = a.rows / kTile;
 #pragma unroll
-            for (int j = 0; j < 8; ++j) a.scaleT[(t.col + j) * ng + blockIdx.y] = scol[j];
+            for (int j = 0; j < 8; ++j)
+                a.scaleT[a.kmajor ? (int64_t)blockIdx.y * a.cols + t.col + j : (t.col + j) * ng + blockIdx.y] = scol[j];
         }
     }
 }
@@ -368,8 +369,10 @@ __global__ __launch_bounds__(kThreads) void quant_block_kernel(QuantArgs a) {
     store_rows(a, t, c);
     if (a.qT) store_transposed(a, t, c);
     if (threadIdx.x == 0) {
-        a.scale[(int64_t)blockIdx.y * (a.cols / kTile) + blockIdx.x] = s;
-        if (a.scaleT) a.scaleT[(int64_t)blockIdx.x * (a.rows / kTile) + blockIdx.y] = s;
+        // block (by, bx) of q; scaleT holds the transposed copy's blocks
+        const int64_t by = blockIdx.y, bx = blockIdx.x, nby = a.rows / kTile, nbx = a.cols / kTile;
+        a.scale[a.kmajor ? bx * nby + by : by * nbx + bx] = s;
+        if (a.scaleT) a.scaleT[a.kmajor ? by * nbx + bx : bx * nby + by] = s;
     }
 }
 

@@ -229,8 +229,9 @@ def linear_saved(M, N, K, recipe, device):
     xq_t = torch.empty(K, M, dtype=torch.uint8, device=device)
     wq_t = torch.empty(K, N, dtype=torch.uint8, device=device)
     if recipe.blockwise:
-        xs = torch.empty(K, M // G, dtype=torch.float32, device=device)
-        wsc = torch.empty(K // G, N // G, dtype=torch.float32, device=device)
+        # k-block-major scale layouts (include/puro.h)
+        xs = torch.empty(M // G, K, dtype=torch.float32, device=device)
+        wsc = torch.empty(N // G, K // G, dtype=torch.float32, device=device)
     else:
         xs = torch.empty(1, dtype=torch.float32, device=device)
         wsc = torch.empty(1, dtype=torch.float32, device=device)

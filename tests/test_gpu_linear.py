@@ -58,8 +58,9 @@ def test_linear_fwd_bwd(P, case):
     assert_bytes_equal(host(saved["xq_t"]), osaved["xq_t"], "saved xq_t")
     assert_bytes_equal(host(saved["wq_t"]), osaved["wq_t"], "saved wq_t")
     if blockwise:
-        assert_f32_bits_equal(host(saved["x_scale"]), osaved["x_scale_t"], "saved x scales")
-        assert_f32_bits_equal(host(saved["w_scale"]), osaved["w_scale_t"], "saved w scales")
+        # the saved blockwise scales are k-block-major: transposed views of the oracle's
+        assert_f32_bits_equal(host(saved["x_scale"]).T, osaved["x_scale_t"], "saved x scales")
+        assert_f32_bits_equal(host(saved["w_scale"]).T, osaved["w_scale_t"], "saved w scales")
     else:
         assert_f32_bits_equal(host(saved["x_scale"]), np.array([osaved["x_scale"]]), "x scale")
         assert_f32_bits_equal(host(saved["w_scale"]), np.array([osaved["w_scale"]]), "w scale")

@@ -211,12 +211,12 @@ def test_layer_blockwise_m16384(P, layer, j):
     # W blocks, whole
     wq, ws, wqT, wsT = quant.quantize_blocks_128x128(W, "e4m3")
     assert_bytes_equal(host(saved["wq_t"]), wqT, what + " wq_t")
-    assert_f32_bits_equal(host(saved["w_scale"]), wsT, what + " w scales (transposed)")
+    assert_f32_bits_equal(host(saved["w_scale"]).T, wsT, what + " w scales (transposed, k-block-major)")
     # X column groups (saved for Wgrad) and dY row/column groups on sampled rows
     kr = uniq(g.choice(K, 32, replace=False))
     q, s = quant.quantize_cols_128x1(np.ascontiguousarray(X[:, kr]), "e4m3")
     assert_bytes_equal(host(saved["xq_t"])[kr], q, what + " xq_t rows")
-    assert_f32_bits_equal(host(saved["x_scale"])[kr], s, what + " x column-group scales")
+    assert_f32_bits_equal(host(saved["x_scale"])[:, kr].T, s, what + " x column-group scales")
     mr = uniq(g.choice(M, 32, replace=False))
     q, s = quant.quantize_rows_1x128(np.ascontiguousarray(dY[mr]), "e4m3")
     assert_bytes_equal(host(dq["q"])[mr], q, what + " dYq rows")
