@@ -211,10 +211,43 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_fp8_kernel(Params p) {
     const uint32_t ssc_lds = lds_addr(ssc);
 
     v4i rsa{}, rsb{};
+    // Scale load j of this wave brings entries 64 t .. 64 t + 63 (t = its
+    // chunk) of a slice's scale vector: BM entries for A, then BN for B. A
+    // row-scaled operand has one entry per tile row, a block-scaled one one
+    // per 128-row block (entries past that are unused). The element lane l
+    // loads for k block kb is sc_base[j] + kb * sc_kstride[j] (row-major
+    // scales: stride 1; k-major: the array's row pitch), or nothing when
+    // sc_base[j] < 0; all of it is fixed before the main loop.
+    int sc_base[SC_PER > 0 ? SC_PER : 1], sc_kstride[SC_PER > 0 ? SC_PER : 1];
+    bool sc_is_a[SC_PER > 0 ? SC_PER : 1];
     if constexpr (GROUPED) {
         rsa = make_rsrc(p.sa, p.a_mode == kSTensor ? 0u : p.sa_bytes);
         rsb = make_rsrc(p.sb, p.b_mode == kSTensor ? 0u : p.sb_bytes);
+#pragma unroll
+        for (int j = 0; j < SC_PER; ++j) {
+            const int t = (wave * SC_PER + j) % SC_BLK;
+            const bool is_a = t * 64 < BM;
+            const int r = t * 64 + lane - (is_a ? 0 : BM);
+            const int mode = is_a ? p.a_mode : p.b_mode;
+            const bool km = is_a ? p.a_kmajor : p.b_kmajor;
+            const int ld = is_a ? p.ld_sa : p.ld_sb;
+            const int row0 = is_a ? m0 : n0;
+            const int rows = is_a ? p.M : p.N;
+            int unit = -1;   // row (row scales) or 128-row block (block scales) of this lane's entry
+            if (mode == kSBlock) {
+                // the 128-row blocks the tile's rows touch: from row0's to (row0 + BM - 1)'s
+                const int b = (row0 >> 7) + r;
+                const int last = (row0 + (is_a ? BM : BN) - 1) >> 7;
+                if (b <= last && b < (rows + 127) >> 7) unit = b;
+            } else if (mode == kSRow) {
+                if (row0 + r < rows) unit = row0 + r;
+            }
+            sc_is_a[j] = is_a;
+            sc_base[j] = unit < 0 ? -1 : (km ? unit : unit * ld);
+            sc_kstride[j] = km ? ld : 1;
+        }
     }
+    (void)sc_base; (void)sc_kstride; (void)sc_is_a;
 
     // DMA load q (0 <= q < LOADS) of this wave for slice `sl` into ring
     // stage `st`. With `valid` false the load still issues (so that every
@@ -233,31 +266,12 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_fp8_kernel(Params p) {
             if (is_a) dma_to_lds<16>(ra, sbase + blk * 1024, rowA + blk * blkA + off);
             else dma_to_lds<16>(rb, sbase + A_BYTES + blk * 1024, rowB + blk * blkB + off);
         } else if constexpr (GROUPED) {
-            // scale load t brings entries 64 t .. 64 t + 63 of the slice's
-            // scale vector: BM entries for A, then BN for B. A row-scaled
-            // operand has one entry per tile row, a block-scaled one one per
-            // 128-row block (entries past that are unused). With k-major
-            // scales a load reads consecutive floats.
-            const int t = (wave * SC_PER + (q - A_PER - B_PER)) % SC_BLK;
-            const bool is_a = t * 64 < BM;
-            const int r = t * 64 + lane - (is_a ? 0 : BM);
-            const int mode = is_a ? p.a_mode : p.b_mode;
-            const bool km = is_a ? p.a_kmajor : p.b_kmajor;
-            const int ld = is_a ? p.ld_sa : p.ld_sb;
-            const int row0 = is_a ? m0 : n0;
+            const int j = q - A_PER - B_PER;
+            const int t = (wave * SC_PER + j) % SC_BLK;
             const int kb = sl / SPB;
-            int idx = -1;
-            if (mode == kSBlock) {
-                const int blocks = ((is_a ? p.M : p.N) + 127) >> 7;
-                const int b = (row0 >> 7) + r;
-                if (r < ((is_a ? BM : BN) + 127) / 128 && b < blocks) idx = km ? kb * ld + b : b * ld + kb;
-            } else if (mode == kSRow) {
-                const int row = row0 + r;
-                if (row < (is_a ? p.M : p.N)) idx = km ? kb * ld + row : row * ld + kb;
-            }
-            const uint32_t soff = (valid && idx >= 0) ? (uint32_t)idx * 4u : kOOB;
+            const uint32_t soff = (valid && sc_base[j] >= 0) ? (uint32_t)(sc_base[j] + kb * sc_kstride[j]) * 4u : kOOB;
             const uint32_t dst = ssc_lds + (st * (BM + BN) + t * 64) * 4;
-            dma_to_lds<4>(is_a ? rsa : rsb, dst, soff);
+            dma_to_lds<4>(sc_is_a[j] ? rsa : rsb, dst, soff);
         }
     };
 
@@ -282,6 +296,21 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_fp8_kernel(Params p) {
         v8i f[FM + FN];
         uint32_t sc[FM + FN];
     };
+    // the LDS entry of each fragment row's scale within a stage's scale
+    // vector (block scales: the row's 128-row block counted from the block
+    // of the tile's first row, which need not start a block when the tile
+    // is 192 rows), and whether the operand has grouped scales at all
+    int sc_off[FM + FN];
+    bool sc_on[FM + FN];
+#pragma unroll
+    for (int fi = 0; fi < FM + FN; ++fi) {
+        const bool is_a = fi < FM;
+        const int r = is_a ? wm * WTM + fi * 32 + fr : wn * WTN + (fi - FM) * 32 + fr;   // tile row
+        const int row0 = is_a ? m0 : n0;
+        const int mode = is_a ? p.a_mode : p.b_mode;
+        sc_off[fi] = (is_a ? 0 : BM) + (mode == kSBlock ? ((row0 + r) >> 7) - (row0 >> 7) : r);
+        sc_on[fi] = mode != kSTensor;
+    }
     // read piece t of k step h of the slice in stage st: t < FM + FN are
     // the operand fragments, the rest the scales
     constexpr int NPIECE = (FM + FN) * (GROUPED ? 2 : 1);
@@ -295,11 +324,8 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_fp8_kernel(Params p) {
             f.f[t] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
         } else {
             const int fi = t - (FM + FN);
-            const bool is_a = fi < FM;
-            const int r = is_a ? wm * WTM + fi * 32 + fr : wn * WTN + (fi - FM) * 32 + fr;   // tile row
-            const int mode = is_a ? p.a_mode : p.b_mode;
-            const int idx = (is_a ? 0 : BM) + (mode == kSBlock ? r >> 7 : r);
-            f.sc[fi] = mode != kSTensor ? e8m0_of(ssc[st * (BM + BN) + idx]) : 127u;
+            const uint32_t e = e8m0_of(ssc[st * (BM + BN) + sc_off[fi]]);
+            f.sc[fi] = sc_on[fi] ? e : 127u;
         }
     };
     auto mfma_one = [&](const Frags& f, int t) __attribute__((always_inline)) {
@@ -559,10 +585,10 @@ struct TileCfg {
 // (one workgroup per CU) or a short one (two per CU). The time constants are
 // least-squares fits to measured kernel times on the Qwen2-1.5B layer shapes.
 #define PURO_TILE_LIST(X)                              \
-    X(0, 256, 256, 2, 2, 128, 2, 6.9f, 1.40f)          \
-    X(1, 256, 192, 2, 2, 128, 2, 5.5f, 1.19f)          \
-    X(2, 128, 128, 2, 2, 128, 4, 2.8f, 0.50f)          \
-    X(3, 128, 128, 2, 2, 128, 2, 3.5f, 0.765f)
+    X(0, 256, 256, 2, 2, 128, 2, 7.86f, 1.322f)        \
+    X(1, 256, 192, 2, 2, 128, 2, 6.37f, 1.120f)        \
+    X(2, 128, 128, 2, 2, 128, 4, 3.03f, 0.537f)        \
+    X(3, 128, 128, 2, 2, 128, 2, 4.37f, 0.803f)
 #define PURO_TILE_ROW(i, bm, bn, wm, wn, sl, nst, f, s) {bm, bn, wm, wn, sl, nst, f, s},
 constexpr TileCfg kTiles[] = {PURO_TILE_LIST(PURO_TILE_ROW)};
 constexpr int kNumTiles = sizeof(kTiles) / sizeof(kTiles[0]);
@@ -603,9 +629,9 @@ Plan make_plan(int64_t M, int64_t N, int64_t K, bool grouped) {
             const int64_t units = tiles * splits;
             const int64_t waves = (units + slots - 1) / slots;
             const double busy = units < slots ? (double)units / slots : 1.0;
-            double cost = (double)waves * (t.fixed_us + t.slice_us * (kps > 0 ? kps : 1) * (1.0 - 0.146 * (1.0 - busy)));
-            if (grouped) cost *= 1.5;
-            if (splits > 1) cost += 0.294e-6 * splits * (double)M * N * 4.0;
+            double cost = (double)waves * (t.fixed_us + t.slice_us * (kps > 0 ? kps : 1) * (1.0 - 0.332 * (1.0 - busy)));
+            if (grouped) cost *= 1.14;
+            if (splits > 1) cost += 0.289e-6 * splits * (double)M * N * 4.0;
             if (best_cost < 0 || cost < best_cost) {
                 best_cost = cost;
                 best = Plan{c, splits, kps};

@@ -233,3 +233,32 @@ def test_gemm_every_configuration(P, shape, scales):
             check_fp32(host(D)[ms, ns], ref, den, what=what, slack=slack)
         else:
             check_bf16(bf16_bits(D)[ms, ns], ref, den, what=what, slack=slack)
+
+
+@pytest.mark.parametrize("shape", [(3072, 3072, 256), (6144, 1344, 256)], ids=lambda s: "x".join(map(str, s)))
+def test_gemm_block_scales_change_between_blocks(P, shape):
+    """Block-scaled B whose 128-row blocks all get different power-of-two
+    scales (rows of block b scaled by 2^(b mod 7)), on shapes planned with
+    192-wide tiles whose rows straddle block boundaries."""
+    from gpu_util import sample_entries
+    M, N, K = shape
+    a, sa = _operand_grouped(23, M, K, E4, "row")
+    x = inputs.case(24, (N, K), std=0.02)
+    mult = np.repeat(2.0 ** (np.arange((N + 127) // 128) % 7), 128)[:N]
+    xb = bf16.from_f64_rne(bf16.to_f32(x).astype(np.float64) * mult[:, None])
+    pad = (-N) % 128                               # blocks over a ragged row count
+    xp = np.concatenate([xb, np.zeros((pad, K), np.uint16)]) if pad else xb
+    b, sb, _, _ = quant.quantize_blocks_128x128(xp, fp8.E4M3)
+    b = b[:N]
+    assert len(np.unique(sb[:, 0])) > 1
+    op = (a, fp8.E4M3, sa, "row", b, fp8.E4M3, sb, "block")
+    ms, ns = sample_entries(M, N, np.random.default_rng(5))
+    ref, den = gemm.gemm_entries(ms, ns, *op)
+    slack = mfma_model.truncation_loss(ms, ns, *op)
+    for out in (0, 1):
+        D = _run(P, a, E4, sa, "row", b, E4, sb, "block", out)
+        what = "block-scale boundaries %s plan %s out %d" % (shape, P.fp8_gemm_plan(M, N, K, 1, 3), out)
+        if out == 1:
+            check_fp32(host(D)[ms, ns], ref, den, what=what, slack=slack)
+        else:
+            check_bf16(bf16_bits(D)[ms, ns], ref, den, what=what, slack=slack)
