@@ -25,9 +25,14 @@ E4M3 = "e4m3"
 E5M2 = "e5m2"
 
 
-def recipe(mode="tensor", x_fmt=E4M3, w_fmt=E4M3, dy_fmt=E5M2):
+def recipe(mode="tensor", x_fmt=E4M3, w_fmt=E4M3, dy_fmt=E5M2, rule=None):
+    """``rule``: the scale rule ("fp32", "pow2" or "pow2_floor"); by default
+    "fp32" for one scale per tensor and "pow2" for block scales."""
     assert mode in ("tensor", "block")
-    return dict(mode=mode, x_fmt=x_fmt, w_fmt=w_fmt, dy_fmt=dy_fmt)
+    if rule is None:
+        rule = "fp32" if mode == "tensor" else "pow2"
+    assert rule in (("fp32", "pow2", "pow2_floor") if mode == "tensor" else ("pow2", "pow2_floor"))
+    return dict(mode=mode, x_fmt=x_fmt, w_fmt=w_fmt, dy_fmt=dy_fmt, rule=rule)
 
 
 def fwd_operands(X, W, rc):
@@ -38,15 +43,15 @@ def fwd_operands(X, W, rc):
     what the backward pass reuses plus the forward's quantised bytes.
     """
     if rc["mode"] == "tensor":
-        xq, xqT, sx, ax = quant.quantize_tensor(X, rc["x_fmt"])
-        wq, wqT, sw, aw = quant.quantize_tensor(W, rc["w_fmt"])
+        xq, xqT, sx, ax = quant.quantize_tensor(X, rc["x_fmt"], rule=rc["rule"])
+        wq, wqT, sw, aw = quant.quantize_tensor(W, rc["w_fmt"], rule=rc["rule"])
         fprop = (xq, rc["x_fmt"], sx, "tensor", wq, rc["w_fmt"], sw, "tensor")
         saved = dict(xq=xq, xq_t=xqT, x_scale=sx, x_amax=ax,
                      wq=wq, wq_t=wqT, w_scale=sw, w_amax=aw)
     else:
-        xq, sx = quant.quantize_rows_1x128(X, rc["x_fmt"])
-        xqT, sxT = quant.quantize_cols_128x1(X, rc["x_fmt"])
-        wq, sw, wqT, swT = quant.quantize_blocks_128x128(W, rc["w_fmt"])
+        xq, sx = quant.quantize_rows_1x128(X, rc["x_fmt"], rc["rule"])
+        xqT, sxT = quant.quantize_cols_128x1(X, rc["x_fmt"], rc["rule"])
+        wq, sw, wqT, swT = quant.quantize_blocks_128x128(W, rc["w_fmt"], rc["rule"])
         fprop = (xq, rc["x_fmt"], sx, "row", wq, rc["w_fmt"], sw, "block")
         saved = dict(xq=xq, x_scale=sx, xq_t=xqT, x_scale_t=sxT,
                      wq=wq, w_scale=sw, wq_t=wqT, w_scale_t=swT)
@@ -59,15 +64,15 @@ def bwd_operands(dY, saved, rc):
     Returns (dgrad, wgrad, dq): GEMM argument tuples and dY's quantised bytes.
     """
     if rc["mode"] == "tensor":
-        dyq, dyqT, sdy, ady = quant.quantize_tensor(dY, rc["dy_fmt"])
+        dyq, dyqT, sdy, ady = quant.quantize_tensor(dY, rc["dy_fmt"], rule=rc["rule"])
         dgrad = (dyq, rc["dy_fmt"], sdy, "tensor",
                  saved["wq_t"], rc["w_fmt"], saved["w_scale"], "tensor")
         wgrad = (dyqT, rc["dy_fmt"], sdy, "tensor",
                  saved["xq_t"], rc["x_fmt"], saved["x_scale"], "tensor")
         dq = dict(dyq=dyq, dyq_t=dyqT, dy_scale=sdy, dy_amax=ady)
     else:
-        dyq, sdy = quant.quantize_rows_1x128(dY, rc["dy_fmt"])
-        dyqT, sdyT = quant.quantize_cols_128x1(dY, rc["dy_fmt"])
+        dyq, sdy = quant.quantize_rows_1x128(dY, rc["dy_fmt"], rc["rule"])
+        dyqT, sdyT = quant.quantize_cols_128x1(dY, rc["dy_fmt"], rc["rule"])
         dgrad = (dyq, rc["dy_fmt"], sdy, "row",
                  saved["wq_t"], rc["w_fmt"], saved["w_scale_t"], "block")
         wgrad = (dyqT, rc["dy_fmt"], sdyT, "row",

@@ -175,3 +175,65 @@ def test_zero_tensor_and_zero_groups():
     assert q[1, 130] == 0x78                           # 0.5 * 2**9 = 256 = 2**8: exponent field 15
     q, _, s, a = quant.quantize_tensor(np.zeros((3, 16), np.uint16), fp8.E5M2)
     assert s == 1.0 and a == 0.0 and not q.any()
+
+
+# ---- the OCP-MX (floor) power-of-two rule, kept for comparison -------------
+
+@pytest.mark.parametrize("fmt", ["e4m3", "e5m2"])
+def test_pow2_floor_exponent_closed_forms(fmt):
+    fm = fp8.fmax(fmt)
+    em = quant.emax(fmt)
+    assert fm == 1.75 * 2.0 ** em                          # 448 = 1.75 * 2^8, 57344 = 1.75 * 2^15
+    for j in range(-20, 20):
+        assert quant.pow2_floor_exponent(2.0 ** (em + j), fmt) == j
+        assert quant.pow2_floor_exponent(fm * 2.0 ** j, fmt) == j
+        # significand above 1.75: the floor rule stays at j, the ceil rule moves to j + 1
+        a = fm * 2.0 ** j * (1 + 2.0 ** -7)
+        assert quant.pow2_floor_exponent(a, fmt) == j and quant.pow2_exponent(a, fmt) == j + 1
+        assert quant.pow2_floor_exponent(2.0 ** (em + j + 1) * (1 - 2.0 ** -8), fmt) == j
+    assert quant.pow2_floor_exponent(0.0, fmt) == 0
+    assert quant.pow2_floor_exponent(np.inf, fmt) == 127
+    assert quant.pow2_floor_exponent(np.nan, fmt) is None
+    assert quant.pow2_floor_exponent(1e-38, fmt) == -127
+    assert quant.pow2_floor_exponent(3e38, fmt) == 127 - em           # 3e38 = 1.76 * 2^127
+
+
+@pytest.mark.parametrize("fmt", ["e4m3", "e5m2"])
+def test_pow2_floor_matches_log2_on_every_bf16_magnitude(fmt):
+    """Brute force over all positive finite BF16 patterns: the floor rule is
+    floor(log2 a) - emax, with log2 from the math library (exact here: a
+    BF16 value that is not a power of two is at least 2^-8 of an octave away
+    from one)."""
+    em = quant.emax(fmt)
+    bits = np.arange(1, 0x7F80, dtype=np.uint16)
+    vals = bf16.to_f32(bits).astype(np.float64)
+    got = np.array([quant.pow2_floor_exponent(v, fmt) for v in vals])
+    want = np.clip(np.floor(np.log2(vals)).astype(int) - em, -127, 127)
+    assert np.array_equal(got, want)
+    # and it is the ceil rule's exponent, or one less exactly when the
+    # significand exceeds FMAX's 1.75 (outside the clamp)
+    ceil = np.array([quant.pow2_exponent(v, fmt) for v in vals])
+    sig = vals / 2.0 ** np.floor(np.log2(vals))
+    inside = (want > -127) & (want < 127) & (ceil > -127) & (ceil < 127)
+    assert np.array_equal((ceil - got)[inside], (sig > 1.75)[inside].astype(int))
+
+
+@pytest.mark.parametrize("fmt", ["e4m3", "e5m2"])
+def test_pow2_floor_saturates_only_above_fmax_significand(fmt):
+    fm = fp8.fmax(fmt)
+    rng = np.random.default_rng(9)
+    for top in (1.5, 1.75, 1.875):
+        x = rng.uniform(-1, 1, (4, 128))
+        x[:, 7] = top                                  # the block's amax, significand `top`
+        xb = bf16.from_f64_rne(x * 2.0 ** 3)
+        q, s = quant.quantize_rows_1x128(xb, fmt, "pow2_floor")
+        d = fp8.decode(q, fmt).astype(np.float64) * s.repeat(128, axis=1)
+        amax_code = q[:, 7]
+        if top > 1.75:
+            # the top value is clipped to FMAX * s, below the amax
+            assert np.all(fp8.decode(amax_code, fmt) == fm)
+            assert np.all(d[:, 7] < bf16.to_f32(xb[:, 7]))
+        else:
+            # nothing saturates: the ceil rule gives the same scales and bytes
+            q2, s2 = quant.quantize_rows_1x128(xb, fmt, "pow2")
+            assert np.array_equal(q, q2) and np.array_equal(s, s2)
