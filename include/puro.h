@@ -70,7 +70,10 @@ typedef enum {
  * exponent-only E8M0 representation of MXFP8). */
 typedef enum {
     PURO_SCALE_FP32 = 0, /* s = amax / FMAX in binary32 (per-tensor mode only) */
-    PURO_SCALE_POW2 = 1  /* s = 2^e, the smallest power of two that avoids saturation */
+    PURO_SCALE_POW2 = 1, /* s = 2^e, the smallest power of two that avoids saturation */
+    PURO_SCALE_POW2_FLOOR = 2 /* s = 2^(floor(log2 amax) - emax), the OCP-MX rule (emax 8 for
+                                 E4M3, 15 for E5M2): the largest values of a group whose amax
+                                 has a significand above 1.75 saturate. For comparison. */
 } puro_scale_rounding;
 
 typedef enum { PURO_OUT_BF16 = 0, PURO_OUT_FP32 = 1 } puro_out_dtype;
@@ -95,7 +98,7 @@ puro_status puro_amax(const uint16_t* x, int64_t rows, int64_t cols, int64_t ld,
  * reduction dimension, weights in 128x128 blocks, or one scale per tensor.
  *
  *  mode TENSOR: q [rows, cols] and/or qT [cols, rows] (the same codes,
- *      transposed); scale[0] = s. rnd FP32 or POW2. If amax_in is not NULL
+ *      transposed); scale[0] = s. rnd FP32, POW2 or POW2_FLOOR. If amax_in is not NULL
  *      the device scalar *amax_in is used instead of the tensor's own amax
  *      (values beyond it saturate).
  *  mode ROW_1x128: q [rows, cols], scale [rows, cols/128]. If qT is not NULL
@@ -106,7 +109,7 @@ puro_status puro_amax(const uint16_t* x, int64_t rows, int64_t cols, int64_t ld,
  *  mode BLOCK_128x128: q [rows, cols] with scale [rows/128, cols/128], and
  *      if qT is not NULL also qT [cols, rows] with scaleT [cols/128, rows/128]
  *      (the same codes and scales, transposed).
- *  Grouped modes require rnd == POW2 and amax_in == NULL.
+ *  Grouped modes require rnd == POW2 or POW2_FLOOR, and amax_in == NULL.
  *
  * Requirements: cols % 16 == 0 and ld % 8 == 0 with x 16-byte aligned;
  * rows % 16 == 0 when qT is written; the grouped dimension(s) % 128 == 0.
@@ -171,7 +174,7 @@ puro_status puro_fp8_gemm(int64_t M, int64_t N, int64_t K,
  * Recipe: blockwise = 0 -> one scale per tensor (rule `rnd`); blockwise = 1
  * -> X and dY in 1x128 groups along each GEMM's reduction dimension (row
  * groups for Fprop and Dgrad, column groups for Wgrad), W in 128x128 blocks,
- * power-of-two scales (`rnd` ignored). */
+ * power-of-two scales (rule POW2_FLOOR if rnd says so, else POW2). */
 typedef struct {
     puro_fp8_format x_fmt, w_fmt, dy_fmt;
     int blockwise;

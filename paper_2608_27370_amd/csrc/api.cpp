@@ -98,14 +98,16 @@ puro_status quantize_impl(const uint16_t* x, int64_t rows, int64_t cols, int64_t
                           hipStream_t stream) {
     puro_status st = check_bf16_matrix(x, rows, cols, ld);
     if (st != PURO_OK) return st;
-    if (!fmt_ok(fmt) || (rnd != PURO_SCALE_FP32 && rnd != PURO_SCALE_POW2)) return PURO_ERR_UNSUPPORTED;
+    if (!fmt_ok(fmt) || (rnd != PURO_SCALE_FP32 && rnd != PURO_SCALE_POW2 && rnd != PURO_SCALE_POW2_FLOOR))
+        return PURO_ERR_UNSUPPORTED;
+    const bool pow2 = rnd == PURO_SCALE_POW2 || rnd == PURO_SCALE_POW2_FLOOR;
     if ((cols % 16) != 0) return PURO_ERR_ALIGN;
     QuantArgs a{};
     a.x = x; a.rows = rows; a.cols = cols; a.ld = ld;
     a.q = q; a.scale = scale; a.qT = qT; a.scaleT = scaleT;
     a.amax = amax_in;
     a.supplied = amax_in != nullptr;
-    a.pow2 = rnd == PURO_SCALE_POW2;
+    a.pow2 = rnd == PURO_SCALE_POW2 ? 1 : (rnd == PURO_SCALE_POW2_FLOOR ? 2 : 0);
     a.kmajor = kmajor;
     // outputs of an empty tensor are never written (torch hands out NULL for them)
     const bool empty = rows == 0 || cols == 0;
@@ -119,20 +121,20 @@ puro_status quantize_impl(const uint16_t* x, int64_t rows, int64_t cols, int64_t
         break;
     case PURO_SCALE_ROW_1x128:
         if (!empty && (!q || !scale || (qT && !scaleT))) return PURO_ERR_NULL;
-        if (rnd != PURO_SCALE_POW2 || amax_in) return PURO_ERR_UNSUPPORTED;
+        if (!pow2 || amax_in) return PURO_ERR_UNSUPPORTED;
         if ((cols % kGroup) != 0 || (qT && (rows % kGroup) != 0)) return PURO_ERR_ALIGN;
         qmode = kQRow;
         break;
     case PURO_SCALE_COL_128x1:
         if (!empty && (!qT || !scaleT)) return PURO_ERR_NULL;
-        if (rnd != PURO_SCALE_POW2 || amax_in) return PURO_ERR_UNSUPPORTED;
+        if (!pow2 || amax_in) return PURO_ERR_UNSUPPORTED;
         if ((rows % kGroup) != 0) return PURO_ERR_ALIGN;
         a.q = nullptr; a.scale = nullptr;
         qmode = kQCol;
         break;
     case PURO_SCALE_BLOCK_128x128:
         if (!empty && (!q || !scale || (qT && !scaleT))) return PURO_ERR_NULL;
-        if (rnd != PURO_SCALE_POW2 || amax_in) return PURO_ERR_UNSUPPORTED;
+        if (!pow2 || amax_in) return PURO_ERR_UNSUPPORTED;
         if ((rows % kGroup) != 0 || (cols % kGroup) != 0) return PURO_ERR_ALIGN;
         qmode = kQBlock;
         break;
@@ -255,10 +257,15 @@ puro_status puro_fp8_gemm(int64_t M, int64_t N, int64_t K, const puro_fp8_operan
 // ----------------------------------------------------------- linear layer
 namespace {
 
+// The power-of-two rule of a blockwise recipe.
+puro_scale_rounding block_rule(const puro_linear_recipe* r) {
+    return r->rnd == PURO_SCALE_POW2_FLOOR ? PURO_SCALE_POW2_FLOOR : PURO_SCALE_POW2;
+}
+
 bool recipe_ok(const puro_linear_recipe* r) {
     return r && fmt_ok(r->x_fmt) && fmt_ok(r->w_fmt) && fmt_ok(r->dy_fmt) &&
            (r->blockwise == 0 || r->blockwise == 1) &&
-           (r->rnd == PURO_SCALE_FP32 || r->rnd == PURO_SCALE_POW2);
+           (r->rnd == PURO_SCALE_FP32 || r->rnd == PURO_SCALE_POW2 || r->rnd == PURO_SCALE_POW2_FLOOR);
 }
 
 puro_status check_linear_dims(int64_t M, int64_t N, int64_t K, const puro_linear_recipe* r) {
@@ -362,7 +369,7 @@ puro_status puro_linear_fwd(const uint16_t* X, const uint16_t* W, int64_t M, int
         QuantArgs ax{}, aw{};
         ax.x = X; ax.rows = M; ax.cols = K; ax.ld = K;
         ax.q = xq; ax.scale = saved->x_scale; ax.qT = saved->xq_t;
-        ax.pow2 = r->rnd == PURO_SCALE_POW2;
+        ax.pow2 = r->rnd == PURO_SCALE_POW2 ? 1 : (r->rnd == PURO_SCALE_POW2_FLOOR ? 2 : 0);
         aw = ax;
         aw.x = W; aw.rows = N;
         aw.q = wq; aw.scale = saved->w_scale; aw.qT = saved->wq_t;
@@ -380,11 +387,11 @@ puro_status puro_linear_fwd(const uint16_t* X, const uint16_t* W, int64_t M, int
         // column-grouped transposed copy kept for Wgrad.
         float* xs_row = reinterpret_cast<float*>(w8 + l.xs_row);
         float* w_blk = reinterpret_cast<float*>(w8 + l.w_blk);
-        st = quantize_impl(X, M, K, K, r->x_fmt, PURO_SCALE_ROW_1x128, PURO_SCALE_POW2, nullptr, xq, xs_row,
+        st = quantize_impl(X, M, K, K, r->x_fmt, PURO_SCALE_ROW_1x128, block_rule(r), nullptr, xq, xs_row,
                            saved->xq_t, saved->x_scale, nullptr, 0, 1, stream);
         if (st != PURO_OK) return st;
         // W: 128x128 blocks, plus the transposed copy (same blocks) kept for Dgrad.
-        st = quantize_impl(W, N, K, K, r->w_fmt, PURO_SCALE_BLOCK_128x128, PURO_SCALE_POW2, nullptr, wq, w_blk,
+        st = quantize_impl(W, N, K, K, r->w_fmt, PURO_SCALE_BLOCK_128x128, block_rule(r), nullptr, wq, w_blk,
                            saved->wq_t, saved->w_scale, nullptr, 0, 1, stream);
         if (st != PURO_OK) return st;
         A = puro_fp8_operand{xq, K, r->x_fmt, PURO_SCALE_ROW_1x128, xs_row};
@@ -426,7 +433,7 @@ puro_status puro_linear_bwd(const uint16_t* dY, const puro_linear_saved* saved, 
         wA = puro_fp8_operand{dyq_t, M, r->dy_fmt, PURO_SCALE_TENSOR, dys};
         wB = puro_fp8_operand{saved->xq_t, M, r->x_fmt, PURO_SCALE_TENSOR, saved->x_scale};
     } else {
-        st = quantize_impl(dY, M, N, N, r->dy_fmt, PURO_SCALE_ROW_1x128, PURO_SCALE_POW2, nullptr, dyq, dys,
+        st = quantize_impl(dY, M, N, N, r->dy_fmt, PURO_SCALE_ROW_1x128, block_rule(r), nullptr, dyq, dys,
                            dyq_t, dys_t, nullptr, 0, 1, stream);
         if (st != PURO_OK) return st;
         dA = puro_fp8_operand{dyq, N, r->dy_fmt, PURO_SCALE_ROW_1x128, dys};

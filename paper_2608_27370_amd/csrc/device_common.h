@@ -97,20 +97,27 @@ __device__ __forceinline__ uint32_t absmax_bits8(const uint32_t w[4]) {
     return m;
 }
 
-// Power-of-two scale exponent: the smallest e with amax <= FMAX * 2^e,
-// clamped to [-127, 127]; amax given as its BF16 magnitude pattern (finite,
-// non-NaN). amax = 0 -> 0. Writing amax = f * 2^E with f in [1, 2):
-// e = E - Emax, plus one when f > 1.75 (FMAX = 1.75 * 2^Emax).
+// Power-of-two scale exponent; amax given as its BF16 magnitude pattern
+// (finite, non-NaN), amax = 0 -> 0, clamped to [-127, 127]. Writing
+// amax = f * 2^E with f in [1, 2) and FMAX = 1.75 * 2^Emax:
+//  * default rule, the smallest e with amax <= FMAX * 2^e: e = E - Emax,
+//    plus one when f > 1.75;
+//  * OCP-MX rule (floor): e = E - Emax, floor(log2 amax) - Emax; values of
+//    a group whose amax has f > 1.75 may then saturate.
 template <int FMT>
-__device__ __forceinline__ int pow2_exponent_bf16(uint32_t mag) {
+__device__ __forceinline__ int pow2_exponent_bf16(uint32_t mag, bool floor_rule = false) {
     if (mag == 0) return 0;
     if (mag >= 0x7F80u) return 127;                 // infinity
     uint32_t bits = mag << 16;
     int ef = (int)(bits >> 23);
     if (ef == 0) return -127;                        // subnormal: far below the clamp
-    int e = ef - 127 - Fp8Traits<FMT>::kEmax + ((bits & 0x7FFFFFu) > 0x600000u ? 1 : 0);
+    int e = ef - 127 - Fp8Traits<FMT>::kEmax + (!floor_rule && (bits & 0x7FFFFFu) > 0x600000u ? 1 : 0);
     return e < -127 ? -127 : (e > 127 ? 127 : e);
 }
+
+// Under the floor rule, whether a group with this amax (BF16 magnitude
+// pattern) can hold values beyond FMAX after scaling (significand > 1.75).
+__device__ __forceinline__ bool floor_rule_saturates(uint32_t mag) { return (mag & 0x7Fu) > 0x60u; }
 
 // 2^e as binary32 for e in [-127, 127] (2^-127 is subnormal).
 __device__ __forceinline__ float exp2i(int e) {

@@ -193,8 +193,11 @@ __device__ __forceinline__ void encode_tensor_block(const QuantArgs& a, const Ti
             else if (bits >= 0x7F800000u) e = 127;
             else if ((bits >> 23) == 0) e = -127;
             else {
-                e = (int)(bits >> 23) - 127 - Fp8Traits<FMT>::kEmax + ((bits & 0x7FFFFFu) > 0x600000u ? 1 : 0);
+                const bool above = (bits & 0x7FFFFFu) > 0x600000u;   // significand > 1.75
+                e = (int)(bits >> 23) - 127 - Fp8Traits<FMT>::kEmax + (a.pow2 != 2 && above ? 1 : 0);
                 e = e < -127 ? -127 : (e > 127 ? 127 : e);
+                // the floor rule (pow2 == 2) saturates the top values of such a tensor
+                saturate = saturate || (a.pow2 == 2 && above);
             }
             s = exp2i(e);
             r = exp2i(-e);
@@ -253,6 +256,7 @@ __global__ __launch_bounds__(kThreads) void quant_groups_kernel(QuantArgs a) {
     const Tile t = tile_coords(a.cols);
     uint32_t w[8][4];
     load_8x8(a, t, w);
+    const bool floor_rule = a.pow2 == 2;
 
     if constexpr (ROWS) {
         uint2 c[8];
@@ -263,9 +267,10 @@ __global__ __launch_bounds__(kThreads) void quant_groups_kernel(QuantArgs a) {
 #pragma unroll
             for (int o = 8; o >= 1; o >>= 1) m = max(m, (uint32_t)__shfl_xor((int)m, o, 16));
             if (m <= 0x7F7Fu) {                      // finite group
-                const int e = pow2_exponent_bf16<FMT>(m);
+                const int e = pow2_exponent_bf16<FMT>(m, floor_rule);
                 srow[i] = exp2i(e);
-                c[i] = encode8<FMT, false>(w[i], exp2i(-e));
+                if (floor_rule && floor_rule_saturates(m)) c[i] = encode8<FMT, true>(w[i], exp2i(-e));
+                else c[i] = encode8<FMT, false>(w[i], exp2i(-e));
             } else if (m == 0x7F80u) {               // an infinity: largest scale, saturate
                 srow[i] = exp2i(127);
                 c[i] = encode8<FMT, true>(w[i], exp2i(-127));
@@ -310,9 +315,10 @@ __global__ __launch_bounds__(kThreads) void quant_groups_kernel(QuantArgs a) {
             const int k = t.cc * 8 + j;
             const uint32_t m = max(max(colmax[0][k], colmax[1][k]), max(colmax[2][k], colmax[3][k]));
             if (m <= 0x7F7Fu) {
-                const int e = pow2_exponent_bf16<FMT>(m);
+                const int e = pow2_exponent_bf16<FMT>(m, floor_rule);
                 scol[j] = exp2i(e);
                 rcol[j] = exp2i(-e);
+                if (floor_rule && floor_rule_saturates(m)) finite = false;   // take the saturating path
             } else if (m == 0x7F80u) {
                 scol[j] = exp2i(127);
                 rcol[j] = exp2i(-127);
@@ -353,12 +359,18 @@ __global__ __launch_bounds__(kThreads) void quant_block_kernel(QuantArgs a) {
     m = block_max(m, red);
     float s;
     uint2 c[8];
+    const bool floor_rule = a.pow2 == 2;
     if (m <= 0x7F7Fu) {
-        const int e = pow2_exponent_bf16<FMT>(m);
+        const int e = pow2_exponent_bf16<FMT>(m, floor_rule);
         s = exp2i(e);
         const float r = exp2i(-e);
+        if (floor_rule && floor_rule_saturates(m)) {
 #pragma unroll
-        for (int i = 0; i < 8; ++i) c[i] = encode8<FMT, false>(w[i], r);
+            for (int i = 0; i < 8; ++i) c[i] = encode8<FMT, true>(w[i], r);
+        } else {
+#pragma unroll
+            for (int i = 0; i < 8; ++i) c[i] = encode8<FMT, false>(w[i], r);
+        }
     } else {
         const bool inf = m == 0x7F80u;
         s = inf ? exp2i(127) : __uint_as_float(0x7FC00000u);

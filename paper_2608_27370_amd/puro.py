@@ -20,7 +20,7 @@ LIB_PATH = os.path.join(_HERE, "libpuro.so")
 
 E4M3, E5M2 = 0, 1
 SCALE_TENSOR, SCALE_ROW_1x128, SCALE_COL_128x1, SCALE_BLOCK_128x128 = 0, 1, 2, 3
-SCALE_FP32, SCALE_POW2 = 0, 1
+SCALE_FP32, SCALE_POW2, SCALE_POW2_FLOOR = 0, 1, 2
 OUT_BF16, OUT_FP32 = 0, 1
 
 FMAX = {E4M3: 448.0, E5M2: 57344.0}

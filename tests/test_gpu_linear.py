@@ -32,25 +32,29 @@ def P():
 
 
 CASES = [
-    # (M, N, K, blockwise, dy_fmt)
-    (256, 384, 512, 0, E5),
-    (304, 400, 160, 0, E5),
-    (512, 256, 1024, 0, E4),
-    (256, 384, 512, 1, E4),
-    (384, 256, 128, 1, E4),
-    (256, 512, 384, 1, E5),
+    # (M, N, K, blockwise, dy_fmt, rounding: 0 FP32 / 1 POW2 / 2 POW2_FLOOR)
+    (256, 384, 512, 0, E5, 0),
+    (304, 400, 160, 0, E5, 0),
+    (512, 256, 1024, 0, E4, 0),
+    (256, 384, 512, 0, E5, 2),
+    (256, 384, 512, 1, E4, 1),
+    (384, 256, 128, 1, E4, 1),
+    (256, 512, 384, 1, E5, 1),
+    (256, 384, 512, 1, E4, 2),
 ]
+RULE = {0: "fp32", 1: "pow2", 2: "pow2_floor"}
 
 
-@pytest.mark.parametrize("case", CASES, ids=lambda c: "M%d_N%d_K%d_%s_%s" % (
-    c[0], c[1], c[2], "block" if c[3] else "tensor", ONAME[c[4]]))
+@pytest.mark.parametrize("case", CASES, ids=lambda c: "M%d_N%d_K%d_%s_%s_%s" % (
+    c[0], c[1], c[2], "block" if c[3] else "tensor", ONAME[c[4]], RULE[c[5]]))
 def test_linear_fwd_bwd(P, case):
-    M, N, K, blockwise, dyf = case
+    M, N, K, blockwise, dyf, rnd = case
     X = inputs.case(40, (M, K), kind="outliers")
     W = inputs.case(41, (N, K), std=0.02)
     dY = inputs.case(42, (M, N), std=1e-3)
-    rc = P.LinearRecipe(E4, E4, dyf, blockwise, P.SCALE_FP32)
-    orc = linear.recipe("block" if blockwise else "tensor", dy_fmt=ONAME[dyf])
+    rc = P.LinearRecipe(E4, E4, dyf, blockwise, rnd)
+    orc = linear.recipe("block" if blockwise else "tensor", dy_fmt=ONAME[dyf],
+                        rule=None if (rnd == 0 and blockwise) else RULE[rnd])
 
     Y, saved = P.linear_fwd(to_dev_bf16(X), to_dev_bf16(W), rc)
     fprop, osaved = linear.fwd_operands(X, W, orc)

@@ -13,6 +13,7 @@ pytestmark = pytest.mark.gpu
 
 E4, E5 = 0, 1
 OFMT = {E4: fp8.E4M3, E5: fp8.E5M2}
+RULE = {0: "fp32", 1: "pow2", 2: "pow2_floor"}      # puro_scale_rounding -> oracle rule
 
 
 @pytest.fixture(scope="module")
@@ -49,28 +50,27 @@ def test_amax_strided_and_specials(P):
 
 
 @pytest.mark.parametrize("fmt", [E4, E5])
-@pytest.mark.parametrize("rnd", [0, 1])
+@pytest.mark.parametrize("rnd", [0, 1, 2])
 @pytest.mark.parametrize("shape", [(304, 400), (16, 16), (128, 1536), (1040, 2064)])
 def test_quantize_tensor(P, fmt, rnd, shape):
     x = inputs.case(12, shape, kind="outliers")
     r = P.quantize_fp8(to_dev_bf16(x), fmt, P.SCALE_TENSOR, rnd, want_q=True, want_qT=True)
-    q, qT, s, _ = quant.quantize_tensor(x, OFMT[fmt], rule="pow2" if rnd else "fp32")
+    q, qT, s, _ = quant.quantize_tensor(x, OFMT[fmt], rule=RULE[rnd])
     assert_f32_bits_equal(host(r["scale"]), np.array([s]), "scale")
     assert_bytes_equal(host(r["q"]), q, "q")
     assert_bytes_equal(host(r["qT"]), qT, "qT")
 
 
 @pytest.mark.parametrize("fmt", [E4, E5])
-@pytest.mark.parametrize("rnd", [0, 1])
-@pytest.mark.parametrize("amax_in", [448.0, 1.0, 3.0, 57344.0, 1e-30, 2e-36, 3.0e38, 0.0])
+@pytest.mark.parametrize("rnd", [0, 1, 2])
+@pytest.mark.parametrize("amax_in", [448.0, 1.0, 3.0, 57344.0, 1e-30, 2e-36, 3.0e38, 0.0, 15.0])
 def test_quantize_every_bf16_pattern_with_supplied_amax(P, fmt, rnd, amax_in):
     """All 65536 BF16 patterns (NaN, Inf, subnormals included) through the
     saturating path: exercises the whole codec on the device."""
     x = np.arange(65536, dtype=np.uint32).astype(np.uint16).reshape(256, 256)
     a = to_dev(np.array([amax_in], np.float32))
     r = P.quantize_fp8(to_dev_bf16(x), fmt, P.SCALE_TENSOR, rnd, amax_in=a, want_q=True, want_qT=True)
-    q, qT, s, _ = quant.quantize_tensor(x, OFMT[fmt], amax_in=np.float32(amax_in),
-                                        rule="pow2" if rnd else "fp32")
+    q, qT, s, _ = quant.quantize_tensor(x, OFMT[fmt], amax_in=np.float32(amax_in), rule=RULE[rnd])
     assert_f32_bits_equal(host(r["scale"]), np.array([s]), "scale")
     assert_bytes_equal(host(r["q"]), q, "q")
     assert_bytes_equal(host(r["qT"]), qT, "qT")
@@ -82,9 +82,9 @@ def test_quantize_tensor_nonfinite(P, fmt):
     for special in (0x7F80, 0xFF80, 0x7FC0):
         y = x.copy()
         y[5, 7] = special
-        for rnd in (0, 1):
+        for rnd in (0, 1, 2):
             r = P.quantize_fp8(to_dev_bf16(y), fmt, P.SCALE_TENSOR, rnd, want_q=True, want_qT=True)
-            q, qT, s, _ = quant.quantize_tensor(y, OFMT[fmt], rule="pow2" if rnd else "fp32")
+            q, qT, s, _ = quant.quantize_tensor(y, OFMT[fmt], rule=RULE[rnd])
             assert_f32_bits_equal(host(r["scale"]), np.array([s]), "scale %#x" % special)
             assert_bytes_equal(host(r["q"]), q, "q %#x" % special)
             assert_bytes_equal(host(r["qT"]), qT, "qT %#x" % special)
@@ -106,34 +106,39 @@ def _groups_case(shape, seed, kind, specials):
     return x
 
 
+@pytest.mark.parametrize("rnd", [1, 2], ids=["pow2", "pow2_floor"])
 @pytest.mark.parametrize("fmt", [E4, E5])
 @pytest.mark.parametrize("shape,kind,specials", [((256, 384), "normal", False), ((128, 128), "student_t", False),
                                                  ((384, 1024), "outliers", False), ((256, 384), "normal", True)])
-def test_quantize_rows_and_columns(P, fmt, shape, kind, specials):
+def test_quantize_rows_and_columns(P, fmt, shape, kind, specials, rnd):
     x = _groups_case(shape, 14, kind, specials)
     d = to_dev_bf16(x)
-    q, s = quant.quantize_rows_1x128(x, OFMT[fmt])
-    qT, sT = quant.quantize_cols_128x1(x, OFMT[fmt])
-    r = P.quantize_fp8(d, fmt, P.SCALE_ROW_1x128, P.SCALE_POW2, want_q=True, want_qT=True)
+    q, s = quant.quantize_rows_1x128(x, OFMT[fmt], RULE[rnd])
+    qT, sT = quant.quantize_cols_128x1(x, OFMT[fmt], RULE[rnd])
+    if rnd == 2:
+        # groups whose amax significand exceeds 1.75 saturate under the floor rule
+        assert (q & 0x7F == (0x7E if fmt == E4 else 0x7B)).any()
+    r = P.quantize_fp8(d, fmt, P.SCALE_ROW_1x128, rnd, want_q=True, want_qT=True)
     assert_bytes_equal(host(r["q"]), q, "row q")
     assert_f32_bits_equal(host(r["scale"]), s, "row scale")
     assert_bytes_equal(host(r["qT"]), qT, "col qT (dual)")
     assert_f32_bits_equal(host(r["scaleT"]), sT, "col scaleT (dual)")
-    r = P.quantize_fp8(d, fmt, P.SCALE_ROW_1x128, P.SCALE_POW2, want_q=True, want_qT=False)
+    r = P.quantize_fp8(d, fmt, P.SCALE_ROW_1x128, rnd, want_q=True, want_qT=False)
     assert_bytes_equal(host(r["q"]), q, "row q only")
     assert_f32_bits_equal(host(r["scale"]), s, "row scale only")
-    r = P.quantize_fp8(d, fmt, P.SCALE_COL_128x1, P.SCALE_POW2)
+    r = P.quantize_fp8(d, fmt, P.SCALE_COL_128x1, rnd)
     assert_bytes_equal(host(r["qT"]), qT, "col qT")
     assert_f32_bits_equal(host(r["scaleT"]), sT, "col scaleT")
 
 
+@pytest.mark.parametrize("rnd", [1, 2], ids=["pow2", "pow2_floor"])
 @pytest.mark.parametrize("fmt", [E4, E5])
 @pytest.mark.parametrize("shape,kind,specials", [((256, 384), "normal", False), ((128, 128), "student_t", False),
                                                  ((512, 256), "outliers", False), ((256, 384), "normal", True)])
-def test_quantize_blocks(P, fmt, shape, kind, specials):
+def test_quantize_blocks(P, fmt, shape, kind, specials, rnd):
     x = _groups_case(shape, 15, kind, specials)
-    q, s, qT, sT = quant.quantize_blocks_128x128(x, OFMT[fmt])
-    r = P.quantize_fp8(to_dev_bf16(x), fmt, P.SCALE_BLOCK_128x128, P.SCALE_POW2, want_q=True, want_qT=True)
+    q, s, qT, sT = quant.quantize_blocks_128x128(x, OFMT[fmt], RULE[rnd])
+    r = P.quantize_fp8(to_dev_bf16(x), fmt, P.SCALE_BLOCK_128x128, rnd, want_q=True, want_qT=True)
     assert_bytes_equal(host(r["q"]), q, "block q")
     assert_f32_bits_equal(host(r["scale"]), s, "block scale")
     assert_bytes_equal(host(r["qT"]), qT, "block qT")
