@@ -40,6 +40,10 @@ def parse():
     ap.add_argument("--graph", action="store_true",
                     help="replay the step captured in a HIP graph instead of launching its kernels one by one "
                          "(measured no faster: the launches are not host-bound)")
+    ap.add_argument("--suite", action="store_true",
+                    help="instead of the headline step, time every workload (the five Qwen2-1.5B-shaped ones "
+                         "and the paper's own 1.7B shapes under both power-of-two scale rules) next to the "
+                         "same GEMMs in BF16, and report the FP8 errors of the two rules; one JSON line each")
     ap.add_argument("--only", choices=("step",) + CALLS + ("copy",),
                     help="run just this call (or a whole step) warmup + steps times and print its average "
                          "time, for profilers; 'copy' is a plain 256 MiB device copy that calibrates "
@@ -156,6 +160,199 @@ def run_only(args, torch, stream, step, make_calls):
                       "us_per_call": round(e0.elapsed_time(e1) / max(1, args.steps) * 1e3, 2)}))
 
 
+class Suite:
+    """Workloads for the comparison mode: device-drawn seeded inputs with the
+    distributions of the parity inputs, each FP8 pass timed next to the same
+    three GEMMs in BF16 (hipBLASLt through torch.mm)."""
+
+    def __init__(self, torch, puro):
+        self.torch, self.puro = torch, puro
+        self.dev = torch.device("cuda", 0)
+        self.stream = torch.cuda.current_stream()
+        self.gen = torch.Generator(device=self.dev)
+        self.gen.manual_seed(0)
+        self.e0 = torch.cuda.Event(enable_timing=True)
+        self.e1 = torch.cuda.Event(enable_timing=True)
+
+    def normal(self, shape, std=1.0):
+        t = self.torch
+        return (t.randn(shape, generator=self.gen, device=self.dev) * std).to(t.bfloat16)
+
+    def outliers(self, shape):
+        """N(0,1) with 1% of the columns (input channels) scaled by 20."""
+        t = self.torch
+        x = t.randn(shape, generator=self.gen, device=self.dev)
+        cols = t.randperm(shape[1], generator=self.gen, device=self.dev)[:max(1, shape[1] // 100)]
+        x[:, cols] *= 20.0
+        return x.to(t.bfloat16)
+
+    def student_t3(self, shape):
+        """Student-t with 3 degrees of freedom: z / sqrt(chi2_3 / 3)."""
+        t = self.torch
+        z = t.randn(shape, generator=self.gen, device=self.dev)
+        c = sum(t.randn(shape, generator=self.gen, device=self.dev) ** 2 for _ in range(3))
+        return (z / t.sqrt(c / 3.0)).to(t.bfloat16)
+
+    def time_us(self, fn, reps):
+        for _ in range(2):
+            fn()
+        self.torch.cuda.synchronize()
+        self.e0.record(self.stream)
+        for _ in range(reps):
+            fn()
+        self.e1.record(self.stream)
+        self.torch.cuda.synchronize()
+        return self.e0.elapsed_time(self.e1) / reps * 1e3
+
+    def fp8_layers(self, layers, recipe):
+        """Forward of every linear in order, then backward in reverse order,
+        as a training step runs them. layers: list of (X, W, dY)."""
+        t, P = self.torch, self.puro
+        state, wsf, wsb = [], 1, 1
+        for X, W, dY in layers:
+            M, K = X.shape
+            N = W.shape[0]
+            wsf = max(wsf, P.linear_fwd_workspace_size(M, N, K, recipe))
+            wsb = max(wsb, P.linear_bwd_workspace_size(M, N, K, recipe))
+        wsf = t.empty(wsf, dtype=t.uint8, device=self.dev)
+        wsb = t.empty(wsb, dtype=t.uint8, device=self.dev)
+        outs = {}
+        for X, W, dY in layers:
+            M, K = X.shape
+            N = W.shape[0]
+            key = (M, N, K)
+            if key not in outs:   # outputs of equal shapes share buffers (overwritten)
+                outs[key] = (t.empty(M, N, dtype=t.bfloat16, device=self.dev),
+                             t.empty(M, K, dtype=t.bfloat16, device=self.dev),
+                             t.empty(N, K, dtype=t.float32, device=self.dev))
+            state.append((X, W, dY, K, P.linear_saved(M, N, K, recipe, self.dev)) + outs[key])
+
+        def run():
+            for X, W, dY, K, saved, Y, dX, dW in state:
+                P.linear_fwd(X, W, recipe, Y=Y, saved=saved, ws=wsf)
+            for X, W, dY, K, saved, Y, dX, dW in reversed(state):
+                P.linear_bwd(dY, saved, recipe, K, dX=dX, dW=dW, ws=wsb)
+        return run, state
+
+    def bf16_layers(self, layers):
+        """The same GEMMs in BF16: Y = X W^T, dX = dY W, dW = dY^T X."""
+        t = self.torch
+        outs, state = {}, []
+        for X, W, dY in layers:
+            M, K = X.shape
+            N = W.shape[0]
+            key = (M, N, K)
+            if key not in outs:
+                outs[key] = (t.empty(M, N, dtype=t.bfloat16, device=self.dev),
+                             t.empty(M, K, dtype=t.bfloat16, device=self.dev),
+                             t.empty(N, K, dtype=t.bfloat16, device=self.dev))
+            state.append((X, W, dY) + outs[key])
+
+        def run():
+            for X, W, dY, Y, dX, dW in state:
+                t.mm(X, W.t(), out=Y)
+            for X, W, dY, Y, dX, dW in reversed(state):
+                t.mm(dY, W, out=dX)
+                t.mm(dY.t(), X, out=dW)
+        return run
+
+    def compare(self, name, layers, recipe, reps, extra=None):
+        flops = sum(3 * 2.0 * X.shape[0] * X.shape[1] * W.shape[0] for X, W, _ in layers)
+        fp8, _ = self.fp8_layers(layers, recipe)
+        us8 = self.time_us(fp8, reps)
+        us16 = self.time_us(self.bf16_layers(layers), reps)
+        row = {"workload": name, "gemms": [list(X.shape) + [W.shape[0]] for X, W, _ in layers[:4]],
+               "linears": len(layers), "fp8_us": round(us8, 1), "bf16_us": round(us16, 1),
+               "fp8_tflops": round(flops / us8 / 1e6, 1), "bf16_tflops": round(flops / us16 / 1e6, 1),
+               "fp8_over_bf16": round(us16 / us8, 3)}
+        row.update(extra or {})
+        print(json.dumps(row), flush=True)
+        return row
+
+    def errors(self, X, W, dY, recipe):
+        """Relative Frobenius errors of the FP8 Y, dX, dW (and, for scale,
+        of the BF16 GEMMs) against FP32 products of the same BF16 inputs, and
+        the relative RMS error of X after quantisation and dequantisation in
+        1x128 groups."""
+        t, P = self.torch, self.puro
+        run, state = self.fp8_layers([(X, W, dY)], recipe)
+        run()
+        _, _, _, _, saved, Y, dX, dW = state[0]
+        Xf, Wf, dYf = X.float(), W.float(), dY.float()
+        ref = (t.mm(Xf, Wf.t()), t.mm(dYf, Wf), t.mm(dYf.t(), Xf))
+        bf = (t.mm(X, W.t()), t.mm(dY, W), t.mm(dY.t(), X))
+
+        def rel(a, b):
+            return float(t.linalg.vector_norm(a.float() - b) / t.linalg.vector_norm(b))
+        q = P.quantize_fp8(X, P.E4M3, mode=P.SCALE_ROW_1x128, rnd=recipe.rnd)
+        table = t.arange(256, dtype=t.uint8).view(t.float8_e4m3fn).float().to(self.dev)
+        xd = table[q["q"].long()] * q["scale"].repeat_interleave(128, dim=1)
+        out = {"rel_err_" + k: round(rel(a, b), 6) for k, a, b in zip(("Y", "dX", "dW"), (Y, dX, dW), ref)}
+        out.update({"bf16_rel_err_" + k: round(rel(a, b), 6) for k, a, b in zip(("Y", "dX", "dW"), bf, ref)})
+        out["x_rel_rms_1x128"] = round(rel(xd, Xf), 6)
+        return out
+
+
+def run_suite(args):
+    import torch
+    from paper_2608_27370_amd import inputs, puro
+
+    puro.lib()
+    torch.cuda.set_device(0)
+    S = Suite(torch, puro)
+    reps = max(3, min(args.steps, 20))
+    E4, E5 = puro.E4M3, puro.E5M2
+    tensor = puro.LinearRecipe(E4, E4, E5, 0, puro.SCALE_FP32)
+    H, Q, F, V = inputs.HIDDEN, inputs.QKV_OUT, inputs.MLP, inputs.VOCAB
+
+    # single FP8 linear forward, 256 x 1536 x 1536
+    X, W = S.normal((256, H)), S.normal((H, H), 0.02)
+    y = torch.empty(256, H, dtype=torch.bfloat16, device=S.dev)
+    sv = puro.linear_saved(256, H, H, tensor, S.dev)
+    us8 = S.time_us(lambda: puro.linear_fwd(X, W, tensor, Y=y, saved=sv), 200)
+    us16 = S.time_us(lambda: torch.mm(X, W.t(), out=y), 200)
+    f = 2.0 * 256 * H * H
+    print(json.dumps({"workload": "single_fwd_256x1536x1536", "fp8_us": round(us8, 2), "bf16_us": round(us16, 2),
+                      "fp8_tflops": round(f / us8 / 1e6, 2), "bf16_tflops": round(f / us16 / 1e6, 2),
+                      "fp8_over_bf16": round(us16 / us8, 3)}), flush=True)
+    # QKV projection, M 8192
+    S.compare("qkv_m8192", [(S.normal((8192, H)), S.normal((Q, H), 0.02), S.normal((8192, Q), 1e-3))], tensor, reps)
+    # MLP: gate/up then down, outlier-channel activations
+    S.compare("mlp_m8192", [(S.outliers((8192, H)), S.normal((2 * F, H), 0.02), S.normal((8192, 2 * F), 1e-3)),
+                            (S.outliers((8192, F)), S.normal((H, F), 0.02), S.normal((8192, H), 1e-3))],
+              tensor, reps)
+    # LM head: Student-t(3) hidden states, dY = softmax(X W^T) - onehot(target)
+    X, W = S.student_t3((8192, H)), S.normal((V, H), 0.02)
+    tgt = torch.randint(0, V, (8192,), generator=S.gen, device=S.dev)
+    dY = torch.empty(8192, V, dtype=torch.bfloat16, device=S.dev)
+    Wf = W.float()
+    for r0 in range(0, 8192, 1024):
+        p = torch.softmax(torch.mm(X[r0:r0 + 1024].float(), Wf.t()), dim=1)
+        p[torch.arange(p.shape[0], device=S.dev), tgt[r0:r0 + 1024]] -= 1.0
+        dY[r0:r0 + 1024] = p.to(torch.bfloat16)
+    del Wf, p
+    S.compare("lm_head_m8192", [(X, W, dY)], tensor, reps)
+    del X, W, dY
+    torch.cuda.empty_cache()
+    # 28 layers x (qkv, o, gate/up, down) at M 16384, blockwise E4M3 (one
+    # weight set per layer; activations and gradients shared per linear kind)
+    block = puro.LinearRecipe(E4, E4, E4, 1, puro.SCALE_POW2)
+    acts = [(S.normal((16384, K)), S.normal((16384, N), 1e-3)) for _, N, K in inputs.LAYER_LINEARS]
+    layers = [(acts[j][0], S.normal((N, K), 0.02), acts[j][1])
+              for _ in range(inputs.LAYERS) for j, (_, N, K) in enumerate(inputs.LAYER_LINEARS)]
+    S.compare("layers28_blockwise_m16384", layers, block, max(2, reps // 4))
+    del layers, acts
+    torch.cuda.empty_cache()
+    # the paper's 1.7B shapes at M 8192, blockwise E4M3, both scale rules
+    paper = [(S.outliers((8192, K)), S.normal((N, K), 0.02), S.normal((8192, N), 1e-3))
+             for _, N, K in inputs.PAPER_LINEARS]
+    for rnd, rule in ((puro.SCALE_POW2, "ceil"), (puro.SCALE_POW2_FLOOR, "floor_ocp_mx")):
+        rc = puro.LinearRecipe(E4, E4, E4, 1, rnd)
+        for (name, _, _), lin in zip(inputs.PAPER_LINEARS, paper):
+            S.compare("paper_%s_m8192_%s" % (name, rule), [lin], rc, reps, S.errors(*lin, rc))
+        S.compare("paper_layer_m8192_%s" % rule, paper, rc, reps)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -164,6 +361,9 @@ def main():
               "supported" % args.gpus, file=sys.stderr)
         sys.exit(2)
 
+    if args.suite:
+        run_suite(args)
+        return
     import torch
     from paper_2608_27370_amd import inputs, puro
 

@@ -25,6 +25,11 @@ Workloads (M tokens, K input features, N output features):
 * ``lm_head``     -- M 8192, K 1536, N 151936: X ~ Student-t(3), W ~
   N(0, 0.02^2), targets uniform over the vocabulary, dY = softmax(X W^T) -
   onehot(target) per row (no 1/M factor); ``SeedSequence([0, 5, t])``.
+* ``paper_linear`` -- the paper's 1.7B ladder model (d 2048, 16 query and 8
+  key/value heads of 128, d_ff 6144) at M 8192: qkv 4096x2048, o 2048x2048,
+  fused gate/up 12288x2048, down 2048x6144; X ~ N(0,1) with 1% outlier
+  channels scaled by 20, W ~ N(0, 0.02^2), dY ~ N(0, (1e-3)^2);
+  ``SeedSequence([0, 6, j, t])``.
 """
 
 import numpy as np
@@ -37,6 +42,10 @@ LAYERS = 28
 
 LAYER_LINEARS = (("qkv", QKV_OUT, HIDDEN), ("o", HIDDEN, HIDDEN),
                  ("gate_up", 2 * MLP, HIDDEN), ("down", HIDDEN, MLP))
+# the paper's 1.7B model: (name, N out, K in)
+PAPER_D, PAPER_QKV, PAPER_FF = 2048, 4096, 6144
+PAPER_LINEARS = (("qkv", PAPER_QKV, PAPER_D), ("o", PAPER_D, PAPER_D),
+                 ("gate_up", 2 * PAPER_FF, PAPER_D), ("down", PAPER_D, PAPER_FF))
 
 
 def bf16_from_f64(x):
@@ -104,6 +113,14 @@ def layer_linear(layer, j, M=16384):
                 X=normal(rng(0, 4, layer, j, 0), (M, K)),
                 W=normal(rng(0, 4, layer, j, 1), (N, K), 0.02),
                 dY=normal(rng(0, 4, layer, j, 2), (M, N), 1e-3))
+
+
+def paper_linear(j, M=8192):
+    name, N, K = PAPER_LINEARS[j]
+    return dict(name=name,
+                X=with_outlier_columns(rng(0, 6, j, 0), (M, K)),
+                W=normal(rng(0, 6, j, 1), (N, K), 0.02),
+                dY=normal(rng(0, 6, j, 2), (M, N), 1e-3))
 
 
 def lm_head_xw(M=8192, V=VOCAB):

@@ -84,15 +84,15 @@ def tensor_cols(x_bits, cols, fmt, a):
     return (q, fmt, quant.tensor_scale(a, fmt)[0], "tensor", cols)
 
 
-def group_rows(x_bits, rows, fmt):
+def group_rows(x_bits, rows, fmt, rule="pow2"):
     """1x128 row-group operand rows (groups along x's rows)."""
-    q, s = quant.quantize_rows_1x128(np.ascontiguousarray(x_bits[rows]), fmt)
+    q, s = quant.quantize_rows_1x128(np.ascontiguousarray(x_bits[rows]), fmt, rule)
     return (q, fmt, s, "row", rows)
 
 
-def group_cols(x_bits, cols, fmt):
+def group_cols(x_bits, cols, fmt, rule="pow2"):
     """128x1 column-group operand rows of the transposed copy (columns of x)."""
-    q, s = quant.quantize_cols_128x1(np.ascontiguousarray(x_bits[:, cols]), fmt)
+    q, s = quant.quantize_cols_128x1(np.ascontiguousarray(x_bits[:, cols]), fmt, rule)
     return (q, fmt, s, "row", cols)
 
 
@@ -187,42 +187,38 @@ def test_lm_head_8192x151936x1536(P):
     run_tensor_layer(P, d["X"], d["W"], d["dY"], E5, "lm_head")
 
 
-@pytest.mark.parametrize("layer,j", [(0, 0), (0, 1), (0, 2), (0, 3), (27, 3)],
-                         ids=["l0-qkv", "l0-o", "l0-gate_up", "l0-down", "l27-down"])
-def test_layer_blockwise_m16384(P, layer, j):
-    """One linear of the 28-layer step at M = 16384: 1x128 groups for X and dY
-    (row groups for Fprop/Dgrad, column groups stored transposed for Wgrad),
-    128x128 blocks for W, power-of-two scales, E4M3 throughout."""
-    d = inputs.layer_linear(layer, j)
-    X, W, dY = d["X"], d["W"], d["dY"]
+def run_block_layer(P, X, W, dY, what, rule="pow2"):
+    """Blockwise linear fwd + bwd (E4M3 throughout, power-of-two `rule`) on
+    the GPU, checked against the oracle: W's blocks whole, X's column groups
+    and dY's row and column groups on sampled rows, GEMM outputs on samples."""
     M, K = X.shape
     N = W.shape[0]
-    what = "layer %d %s" % (layer, d["name"])
-    rc = P.LinearRecipe(E4, E4, E4, 1, P.SCALE_FP32)
+    rnd = P.SCALE_POW2 if rule == "pow2" else P.SCALE_POW2_FLOOR
+    rc = P.LinearRecipe(E4, E4, E4, 1, rnd)
     X_, W_, dY_ = to_dev_bf16(X), to_dev_bf16(W), to_dev_bf16(dY)
     Y, saved = P.linear_fwd(X_, W_, rc)
     dX, dW = P.linear_bwd(dY_, saved, rc, K)
     # dY's bytes are internal to the backward call: the same quantiser call
     # (row groups and, from the same read, column groups), made on its own
-    dq = P.quantize_fp8(dY_, E4, mode=P.SCALE_ROW_1x128, rnd=P.SCALE_POW2, want_qT=True)
+    dq = P.quantize_fp8(dY_, E4, mode=P.SCALE_ROW_1x128, rnd=rnd, want_qT=True)
     del X_, W_, dY_
     g = np.random.default_rng(11)
 
     # W blocks, whole
-    wq, ws, wqT, wsT = quant.quantize_blocks_128x128(W, "e4m3")
+    wq, ws, wqT, wsT = quant.quantize_blocks_128x128(W, "e4m3", rule)
     assert_bytes_equal(host(saved["wq_t"]), wqT, what + " wq_t")
     assert_f32_bits_equal(host(saved["w_scale"]).T, wsT, what + " w scales (transposed, k-block-major)")
     # X column groups (saved for Wgrad) and dY row/column groups on sampled rows
     kr = uniq(g.choice(K, 32, replace=False))
-    q, s = quant.quantize_cols_128x1(np.ascontiguousarray(X[:, kr]), "e4m3")
+    q, s = quant.quantize_cols_128x1(np.ascontiguousarray(X[:, kr]), "e4m3", rule)
     assert_bytes_equal(host(saved["xq_t"])[kr], q, what + " xq_t rows")
     assert_f32_bits_equal(host(saved["x_scale"])[:, kr].T, s, what + " x column-group scales")
     mr = uniq(g.choice(M, 32, replace=False))
-    q, s = quant.quantize_rows_1x128(np.ascontiguousarray(dY[mr]), "e4m3")
+    q, s = quant.quantize_rows_1x128(np.ascontiguousarray(dY[mr]), "e4m3", rule)
     assert_bytes_equal(host(dq["q"])[mr], q, what + " dYq rows")
     assert_f32_bits_equal(host(dq["scale"])[mr], s, what + " dY row-group scales")
     nr = uniq(g.choice(N, 32, replace=False))
-    q, s = quant.quantize_cols_128x1(np.ascontiguousarray(dY[:, nr]), "e4m3")
+    q, s = quant.quantize_cols_128x1(np.ascontiguousarray(dY[:, nr]), "e4m3", rule)
     assert_bytes_equal(host(dq["qT"])[nr], q, what + " dYqT rows")
     assert_f32_bits_equal(host(dq["scaleT"])[nr], s, what + " dY column-group scales")
 
@@ -230,11 +226,31 @@ def test_layer_blockwise_m16384(P, layer, j):
     WbT = (wqT, "e4m3", wsT, "block", None)
     # Fprop Y [M, N] = Xq(1x128) Wq(128x128)^T
     ms, ns = sample_sparse(M, N, g, full=False)
-    check_entries(Y, "bf16", ms, ns, group_rows(X, uniq(ms), "e4m3"), Wb, what + " Y")
+    check_entries(Y, "bf16", ms, ns, group_rows(X, uniq(ms), "e4m3", rule), Wb, what + " Y")
     # Dgrad dX [M, K] = dYq(1x128) WqT(128x128)^T
     ms, ks = sample_sparse(M, K, g, full=False)
-    check_entries(dX, "bf16", ms, ks, group_rows(dY, uniq(ms), "e4m3"), WbT, what + " dX")
+    check_entries(dX, "bf16", ms, ks, group_rows(dY, uniq(ms), "e4m3", rule), WbT, what + " dX")
     # Wgrad dW [N, K] = dYqT(128x1) XqT(128x1)^T
     ns, ks = sample_sparse(N, K, g, full=False)
-    check_entries(dW, "fp32", ns, ks, group_cols(dY, uniq(ns), "e4m3"), group_cols(X, uniq(ks), "e4m3"),
-                  what + " dW")
+    check_entries(dW, "fp32", ns, ks, group_cols(dY, uniq(ns), "e4m3", rule),
+                  group_cols(X, uniq(ks), "e4m3", rule), what + " dW")
+
+
+@pytest.mark.parametrize("layer,j", [(0, 0), (0, 1), (0, 2), (0, 3), (27, 3)],
+                         ids=["l0-qkv", "l0-o", "l0-gate_up", "l0-down", "l27-down"])
+def test_layer_blockwise_m16384(P, layer, j):
+    """One linear of the 28-layer step at M = 16384: 1x128 groups for X and dY
+    (row groups for Fprop/Dgrad, column groups stored transposed for Wgrad),
+    128x128 blocks for W, power-of-two scales, E4M3 throughout."""
+    d = inputs.layer_linear(layer, j)
+    run_block_layer(P, d["X"], d["W"], d["dY"], "layer %d %s" % (layer, d["name"]))
+
+
+@pytest.mark.parametrize("rule", ["pow2", "pow2_floor"])
+@pytest.mark.parametrize("j", [0, 1, 2, 3], ids=["qkv", "o", "gate_up", "down"])
+def test_paper_layer_blockwise_m8192(P, j, rule):
+    """The paper's own recipe at its 1.7B model's shapes (d 2048, QKV 4096,
+    O 2048, fused gate/up 12288, down K 6144; M 8192): blockwise E4M3 for X,
+    W and dY, with the default or the OCP-MX (floor) power-of-two rule."""
+    d = inputs.paper_linear(j)
+    run_block_layer(P, d["X"], d["W"], d["dY"], "paper %s %s" % (d["name"], rule), rule)
