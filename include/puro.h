@@ -112,7 +112,8 @@ puro_status puro_amax(const uint16_t* x, int64_t rows, int64_t cols, int64_t ld,
  *  Grouped modes require rnd == POW2 or POW2_FLOOR, and amax_in == NULL.
  *
  * Requirements: cols % 16 == 0 and ld % 8 == 0 with x 16-byte aligned;
- * rows % 16 == 0 when qT is written; the grouped dimension(s) % 128 == 0.
+ * ld < 2^23 (else PURO_ERR_SHAPE); rows % 16 == 0 when qT is written; the
+ * grouped dimension(s) % 128 == 0.
  * Outputs are dense (row pitch = their column count). ws:
  * puro_quantize_workspace_size(rows, cols) bytes (used in TENSOR mode). */
 size_t puro_quantize_workspace_size(int64_t rows, int64_t cols);

@@ -102,6 +102,8 @@ puro_status quantize_impl(const uint16_t* x, int64_t rows, int64_t cols, int64_t
         return PURO_ERR_UNSUPPORTED;
     const bool pow2 = rnd == PURO_SCALE_POW2 || rnd == PURO_SCALE_POW2_FLOOR;
     if ((cols % 16) != 0) return PURO_ERR_ALIGN;
+    // a 128-row tile spans less than 2^31 bytes (32-bit buffer offsets)
+    if (ld >= ((int64_t)1 << 23)) return PURO_ERR_SHAPE;
     QuantArgs a{};
     a.x = x; a.rows = rows; a.cols = cols; a.ld = ld;
     a.q = q; a.scale = scale; a.qT = qT; a.scaleT = scaleT;

@@ -8,13 +8,16 @@
 //
 // These passes are bound by HBM bandwidth: every element is read once as BF16
 // (16-byte vector loads, coalesced along rows) and written as one FP8 byte
-// per requested copy. Each thread owns an 8x8 sub-block of a 128x128 tile, so
-// a transposed copy is produced by an in-register 8x8 byte transpose and
-// stored as 8-byte runs of the transposed rows, without an LDS round trip.
+// per requested copy. Each thread owns an 8x8 sub-block of a 128x128 tile.
+// A transposed copy starts as an in-register 8x8 byte transpose; the
+// transposed blocks meet in LDS, from where the block stores whole 128-byte
+// runs of the transposed rows (16 bytes per lane).
 // Per-tensor scaling needs the whole tensor's amax before any encoding: a
 // first pass writes per-block partial maxima (no atomics, no zero-initialised
 // state); the quantise pass reduces them in every block (few partials) or
 // reads the amax a one-block reduction kernel wrote (many partials).
+// Loads go through buffer descriptors whose range check supplies the zeros
+// outside a tensor, so they carry no branches and never wait on each other.
 
 #include <algorithm>
 
@@ -27,6 +30,7 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kTile = 128;
+typedef int v4i __attribute__((ext_vector_type(4)));
 // Above this many partial maxima a one-block kernel reduces them once,
 // rather than every block of the quantise pass reading them all.
 constexpr int kMaxInlinePartials = 2048;
@@ -121,12 +125,27 @@ __device__ __forceinline__ Tile tile_coords(int64_t cols, int64_t bx, int64_t by
 }
 __device__ __forceinline__ Tile tile_coords(int64_t cols) { return tile_coords(cols, blockIdx.x, blockIdx.y); }
 
+// Buffer descriptor over `bytes` bytes from `base` (32-bit raw data): loads
+// at offsets at or beyond `bytes` return zeros and touch no memory.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, (int)bytes, 0x00020000);
+}
+constexpr uint32_t kOOB = 0x80000000u;   // an offset beyond every descriptor's range (ld < 2^23)
+
+// The thread's 8x8 block, zeros outside the tensor, by buffer loads over the
+// tile's rows: positions outside the tensor read as zeros through the
+// descriptor's range check, so the loads carry no branches and issue back to
+// back (and independent loads issued before them are not waited for).
 __device__ __forceinline__ void load_8x8(const QuantArgs& a, const Tile& t, uint32_t w[8][4]) {
+    const int64_t tr0 = t.row0 - t.rg * 8;                        // the tile's first row
+    const int64_t vr = a.cols == 0 ? 0 : max((int64_t)0, min((int64_t)kTile, a.rows - tr0));
+    // rows tr0 .. tr0 + vr - 1: the last one ends at column cols
+    const uint32_t bytes = vr == 0 ? 0u : (uint32_t)(((vr - 1) * a.ld + a.cols) * 2);
+    const __amdgpu_buffer_rsrc_t rs = buffer_rsrc(vr == 0 ? a.x : a.x + tr0 * a.ld, bytes);
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-        uint4 v = make_uint4(0, 0, 0, 0);
-        const int64_t r = t.row0 + i;
-        if (t.col_ok && r < a.rows) v = *reinterpret_cast<const uint4*>(a.x + r * a.ld + t.col);
+        const uint32_t off = t.col_ok ? (uint32_t)(((t.rg * 8 + i) * a.ld + t.col) * 2) : kOOB;
+        const v4i v = __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0);
         w[i][0] = v.x; w[i][1] = v.y; w[i][2] = v.z; w[i][3] = v.w;
     }
 }
@@ -140,14 +159,44 @@ __device__ __forceinline__ void store_rows(const QuantArgs& a, const Tile& t, co
     }
 }
 
-// qT [cols, rows]: column j of the thread's block becomes 8 bytes of row col+j.
-__device__ __forceinline__ void store_transposed(const QuantArgs& a, const Tile& t, const uint2 c[8]) {
-    if (!t.col_ok || t.row0 >= a.rows) return;
+// qT [cols, rows] of the tile whose first element is (row0, col0), from the
+// codes c of every thread's 8x8 block. Column j of a thread's block becomes
+// 8 bytes of LDS row col + j (LDS row r = qT row col0 + r, 128 bytes = the
+// tile's rows); then each lane stores 16 bytes, eight lanes one whole
+// 128-byte run of a qT row. The 16-byte chunk h of LDS row r sits at
+// position h ^ ((r >> 3) & 7): the 8-byte writes of a wave (rows 8 apart
+// across lanes) then spread over the banks, and a wave's 16-byte reads of 8
+// consecutive rows cover all 64 banks four times (the minimum). rows % 16 ==
+// 0, so a 16-byte run never crosses the end of a qT row. Ends with a barrier,
+// after which the LDS buffer may be reused. qT not 16-byte aligned: 8-byte
+// stores straight from registers.
+__device__ __forceinline__ void store_transposed(const QuantArgs& a, const Tile& t, int64_t row0, int64_t col0,
+                                                 const uint2 c[8], uint8_t* lds) {
     uint2 ct[8];
     transpose8x8(c, ct);
+    if ((reinterpret_cast<uintptr_t>(a.qT) & 15) != 0) {
+        if (!t.col_ok || t.row0 >= a.rows) return;
 #pragma unroll
-    for (int j = 0; j < 8; ++j)
-        *reinterpret_cast<uint2*>(a.qT + (t.col + j) * a.rows + t.row0) = ct[j];
+        for (int j = 0; j < 8; ++j)
+            *reinterpret_cast<uint2*>(a.qT + (t.col + j) * a.rows + t.row0) = ct[j];
+        return;
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        const int r = t.cc * 8 + j;
+        const int pos = (((t.rg >> 1) ^ (r >> 3 & 7)) << 4) + ((t.rg & 1) << 3);
+        *reinterpret_cast<uint2*>(lds + r * kTile + pos) = ct[j];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < kTile * kTile / 16 / kThreads; ++i) {
+        const int q = i * kThreads + threadIdx.x;
+        const int r = q >> 3, h = q & 7;
+        const uint4 v = *reinterpret_cast<const uint4*>(lds + r * kTile + ((h ^ (r >> 3 & 7)) << 4));
+        const int64_t col = col0 + r, row = row0 + h * 16;
+        if (col < a.cols && row < a.rows) *reinterpret_cast<uint4*>(a.qT + col * a.rows + row) = v;
+    }
+    __syncthreads();
 }
 
 // Encode with one multiplier per column of the 8x8 block (column-grouped scales).
@@ -175,12 +224,19 @@ __device__ __forceinline__ uint32_t elem_mag(const uint32_t w[8][4], int i, int 
     return ((j & 1) ? (word >> 16) : word) & 0x7FFFu;
 }
 
-// Scale of a per-tensor quantisation and the encoding of the thread's 8x8
-// block. `saturate`: the amax was supplied and values beyond it saturate.
-template <int FMT>
-__device__ __forceinline__ void encode_tensor_block(const QuantArgs& a, const Tile& t, const uint32_t w[8][4],
-                                                    float amax, bool saturate, bool first_tile) {
+// Scale of a per-tensor quantisation: s (stored) and the multiplier r, and
+// whether encoding must take the saturating path (the amax was supplied and
+// values beyond it saturate, the floor rule clips the top values, or the
+// amax or r is not finite).
+struct TensorScale {
     float s, r;
+    bool safe;
+};
+
+template <int FMT>
+__device__ __forceinline__ TensorScale tensor_scale(const QuantArgs& a, float amax) {
+    float s, r;
+    bool saturate = a.supplied != 0;
     constexpr float fm = Fp8Traits<FMT>::kMax;
     if (a.pow2) {
         if (amax != amax) {
@@ -208,51 +264,82 @@ __device__ __forceinline__ void encode_tensor_block(const QuantArgs& a, const Ti
         s = amax / fm;
         r = fm / amax;
     }
-    const bool safe = saturate || !(fabsf(amax) <= 3.4028235e38f) || !(fabsf(r) <= 3.4028235e38f);
-    if (first_tile && threadIdx.x == 0 && a.scale) a.scale[0] = s;
+    return {s, r, saturate || !(fabsf(amax) <= 3.4028235e38f) || !(fabsf(r) <= 3.4028235e38f)};
+}
 
-    uint2 c[8];
-    if (safe) {
+// Partial maxima of a tensor's amax pass as this thread reads them (its
+// share of at most kMaxInlinePartials), issued before the tile loads so
+// that they return first and the reduction overlaps the tile's arrival.
+struct PartialShare {
+    uint32_t v[kMaxInlinePartials / kThreads];
+};
+
+// Buffer loads: entries past the partials (all of them when the amax is a
+// device scalar) read as zeros, which leave the maximum unchanged.
+__device__ __forceinline__ PartialShare load_partials(const QuantArgs& a, bool active = true) {
+    PartialShare p;
+    const __amdgpu_buffer_rsrc_t rs = buffer_rsrc(a.partial, (!active || a.amax) ? 0u : (uint32_t)a.npartial * 4u);
 #pragma unroll
-        for (int i = 0; i < 8; ++i) c[i] = encode8<FMT, true>(w[i], r);
-    } else {
+    for (int u = 0; u < kMaxInlinePartials / kThreads; ++u)
+        p.v[u] = (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(rs, (u * kThreads + threadIdx.x) * 4u, 0, 0);
+    return p;
+}
+
+// The tensor's amax: the supplied or finalised device scalar, or the block's
+// reduction of the partial maxima (every thread gets it).
+__device__ __forceinline__ float tensor_amax(const QuantArgs& a, const PartialShare& p, uint32_t* red) {
+    if (a.amax) return *a.amax;
+    uint32_t m = 0;
 #pragma unroll
-        for (int i = 0; i < 8; ++i) c[i] = encode8<FMT, false>(w[i], r);
-    }
-    if (a.q) store_rows(a, t, c);
-    if (a.qT) store_transposed(a, t, c);
+    for (int u = 0; u < kMaxInlinePartials / kThreads; ++u) m = max(m, p.v[u]);
+    m = block_max(m, red);
+    return __uint_as_float(m << 16);
 }
 
 // Per-tensor quantisation of one or two tensors in one launch (1-D grid:
-// the first tensor's tiles, then the second's). The amax comes from a
-// device scalar, or is reduced from the partial maxima of the amax pass.
+// the first tensor's tiles, then the second's). Each block loads the partial
+// maxima of both tensors and its tile's BF16 values before reducing any of
+// them, so that the amax reduction overlaps the arrival of the tile.
 template <int FMT>
 __global__ __launch_bounds__(kThreads) void quant_tensor_kernel(QuantArgs a0, QuantArgs a1, int tiles0,
                                                                 int gx0, int gx1) {
     __shared__ uint32_t red[4];
+    __shared__ __attribute__((aligned(16))) uint8_t tq[kTile * kTile];
+    const bool two = (int)gridDim.x > tiles0;   // a second tensor follows the first one's tiles
     const bool second = (int)blockIdx.x >= tiles0;
-    const QuantArgs a = second ? a1 : a0;
+    const QuantArgs& a = second ? a1 : a0;
     const int tile = second ? (int)blockIdx.x - tiles0 : (int)blockIdx.x;
     const int gx = second ? gx1 : gx0;
     const Tile t = tile_coords(a.cols, tile % gx, tile / gx);
+    const PartialShare p0 = load_partials(a0);
+    const PartialShare p1 = load_partials(a1, two);
     uint32_t w[8][4];
     load_8x8(a, t, w);
-    float amax;
-    if (a.amax) {
-        amax = *a.amax;
-    } else {
-        uint32_t m = 0;
-        for (int i = threadIdx.x; i < a.npartial; i += kThreads) m = max(m, a.partial[i]);
-        m = block_max(m, red);
-        amax = __uint_as_float(m << 16);
+    // the scales (every block derives the same values; block 0 stores them)
+    const TensorScale sc0 = tensor_scale<FMT>(a0, tensor_amax(a0, p0, red));
+    const TensorScale sc1 = two ? tensor_scale<FMT>(a1, tensor_amax(a1, p1, red)) : sc0;
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+        if (a0.scale) a0.scale[0] = sc0.s;
+        if (two && a1.scale) a1.scale[0] = sc1.s;
     }
-    encode_tensor_block<FMT>(a, t, w, amax, a.supplied != 0, tile == 0);
+    const TensorScale sc = second ? sc1 : sc0;
+    uint2 c[8];
+    if (sc.safe) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) c[i] = encode8<FMT, true>(w[i], sc.r);
+    } else {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) c[i] = encode8<FMT, false>(w[i], sc.r);
+    }
+    if (a.q) store_rows(a, t, c);
+    if (a.qT) store_transposed(a, t, (int64_t)(tile / gx) * kTile, (int64_t)(tile % gx) * kTile, c, tq);
 }
 
 // 1x128 row groups (q, scale) and/or 128x1 column groups (qT, scaleT).
 template <int FMT, bool ROWS, bool COLS>
 __global__ __launch_bounds__(kThreads) void quant_groups_kernel(QuantArgs a) {
     __shared__ uint32_t colmax[4][kTile];
+    __shared__ __attribute__((aligned(16))) uint8_t tq[COLS ? kTile * kTile : 16];
     const Tile t = tile_coords(a.cols);
     uint32_t w[8][4];
     load_8x8(a, t, w);
@@ -336,7 +423,7 @@ __global__ __launch_bounds__(kThreads) void quant_groups_kernel(QuantArgs a) {
 #pragma unroll
             for (int i = 0; i < 8; ++i) c[i] = encode8_cols<FMT, true>(w[i], rcol);
         }
-        store_transposed(a, t, c);
+        store_transposed(a, t, (int64_t)blockIdx.y * kTile, (int64_t)blockIdx.x * kTile, c, tq);
         if (t.rg == 0 && t.col_ok) {
             const int64_t ng = a.rows / kTile;
 #pragma unroll
@@ -350,6 +437,7 @@ __global__ __launch_bounds__(kThreads) void quant_groups_kernel(QuantArgs a) {
 template <int FMT>
 __global__ __launch_bounds__(kThreads) void quant_block_kernel(QuantArgs a) {
     __shared__ uint32_t red[4];
+    __shared__ __attribute__((aligned(16))) uint8_t tq[kTile * kTile];
     const Tile t = tile_coords(a.cols);
     uint32_t w[8][4];
     load_8x8(a, t, w);
@@ -379,7 +467,7 @@ __global__ __launch_bounds__(kThreads) void quant_block_kernel(QuantArgs a) {
         for (int i = 0; i < 8; ++i) c[i] = encode8<FMT, true>(w[i], r);
     }
     store_rows(a, t, c);
-    if (a.qT) store_transposed(a, t, c);
+    if (a.qT) store_transposed(a, t, (int64_t)blockIdx.y * kTile, (int64_t)blockIdx.x * kTile, c, tq);
     if (threadIdx.x == 0) {
         // block (by, bx) of q; scaleT holds the transposed copy's blocks
         const int64_t by = blockIdx.y, bx = blockIdx.x, nby = a.rows / kTile, nbx = a.cols / kTile;
@@ -395,8 +483,7 @@ void launch_quantize_fmt(int mode, const QuantArgs& a, hipStream_t stream) {
     const dim3 grid((unsigned)(gx > 0 ? gx : 1), (unsigned)(gy > 0 ? gy : 1));
     switch (mode) {
     case kQTensor:
-        quant_tensor_kernel<FMT><<<(unsigned)(grid.x * grid.y), kThreads, 0, stream>>>(a, a, (int)(grid.x * grid.y),
-                                                                                      (int)grid.x, 1);
+        quant_tensor_kernel<FMT><<<grid.x * grid.y, kThreads, 0, stream>>>(a, a, (int)(grid.x * grid.y), (int)grid.x, 1);
         break;
     case kQRow:
         if (a.qT) quant_groups_kernel<FMT, true, true><<<grid, kThreads, 0, stream>>>(a);

@@ -89,6 +89,8 @@ def test_quantize_validation(puro):
     assert q(FAKE, 120, 128, 128, 0, 3, 1, None, FAKE, FAKE, None, None, None, 0, None) == ERR_ALIGN
     assert q(FAKE, 24, 128, 128, 0, 0, 0, None, None, FAKE, FAKE, None, FAKE, big, None) == ERR_ALIGN
     assert q(FAKE, 16, 24, 24, 0, 0, 0, None, FAKE, FAKE, None, None, FAKE, big, None) == ERR_ALIGN
+    # a row pitch whose 128-row tiles exceed 32-bit buffer offsets
+    assert q(FAKE, 16, 128, 1 << 23, 0, 0, 0, None, FAKE, FAKE, None, None, FAKE, big, None) == ERR_SHAPE
     # per-tensor without workspace for the amax pass
     assert q(FAKE, 4096, 4096, 4096, 0, 0, 0, None, FAKE, FAKE, None, None, FAKE, 0, None) == ERR_WORKSPACE
 
