@@ -13,11 +13,13 @@ Training", and Appendix C, "FP8 implementation pipeline"):
                 for tiny inputs;
 * ``linear`` -- the linear layer's forward and backward composed from the
                 above;
-* ``bf16``   -- BF16 bit helpers used to state expected outputs.
+* ``bf16``   -- BF16 bit helpers used to state expected outputs;
+* ``swiglu`` -- the MLP's SwiGLU, whose BF16 output the down projection
+                quantises (the fused SwiGLU + quantise operation).
 
 It is test infrastructure: only ``tests/``, ``__graft_entry__.smoke()`` and
 the ``cpu_baseline`` leg of ``bench.py`` may import it. It shares no code with
 the HIP library and never imports it.
 """
 
-from . import bf16, fp8, quant, gemm, linear  # noqa: F401
+from . import bf16, fp8, quant, gemm, linear, swiglu  # noqa: F401

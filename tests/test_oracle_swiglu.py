@@ -1,0 +1,123 @@
+"""Pins of the SwiGLU oracle (oracle/swiglu.py) and of the band check used by
+the fused SwiGLU + quantise parity tests (tests/swiglu_check.py).
+
+silu(g) = g / (1 + e^-g) is pinned by the identity silu(g) - silu(-g) = g, by
+the library routine scipy.special.expit (silu(g) = g * expit(g)), and by its
+limits; the gate/up split and the linearity in u by constructed inputs; the
+band by values exactly on and next to BF16 rounding boundaries; the check by
+oracle-made results with one planted mistake each.
+"""
+
+import numpy as np
+import pytest
+from scipy.special import expit
+
+from oracle import bf16, quant, swiglu
+from tests import swiglu_check
+
+
+def bits(x):
+    return bf16.from_f64_rne(np.asarray(x, dtype=np.float64))
+
+
+def test_silu_identity_and_library():
+    g = np.linspace(-30, 30, 6001)
+    s = swiglu.silu_f64(g)
+    assert np.all(np.abs(s - swiglu.silu_f64(-g) - g) <= 1e-13 * np.maximum(1, np.abs(g)))
+    np.testing.assert_allclose(s, g * expit(g), rtol=1e-15, atol=1e-300)
+
+
+def test_silu_limits():
+    assert swiglu.silu_f64(0.0) == 0.0
+    assert swiglu.silu_f64(40.0) == 40.0          # e^-40 vanishes against 1 in float64
+    v = swiglu.silu_f64(np.array([-1000.0, -745.0]))
+    assert np.all(v == 0) and not np.isnan(v).any()
+    # the minimum of silu is at g ~ -1.278 with value ~ -0.2785
+    g = np.linspace(-3, 0, 300001)
+    assert abs(swiglu.silu_f64(g).min() + 0.27846454) < 1e-7
+
+
+def test_gate_up_split_and_linearity():
+    rng = np.random.default_rng(1)
+    C = 32
+    g = rng.standard_normal((4, C))
+    ones = np.ones((4, C))
+    h = swiglu.swiglu_f64(np.concatenate([bits(g), bits(ones)], axis=1), C)
+    np.testing.assert_array_equal(h, swiglu.silu_f64(bf16.to_f32(bits(g)).astype(np.float64)))
+    u = rng.standard_normal((4, C))
+    gu = np.concatenate([bits(g), bits(u)], axis=1)
+    gu2 = np.concatenate([bits(g), bits(2.0 * bf16.to_f32(bits(u)))], axis=1)
+    np.testing.assert_array_equal(swiglu.swiglu_f64(gu2, C), 2.0 * swiglu.swiglu_f64(gu, C))
+    # columns past 2C (a wider row pitch) are ignored
+    wide = np.concatenate([gu, bits(np.full((4, 16), 7.0))], axis=1)
+    np.testing.assert_array_equal(swiglu.swiglu_f64(wide, C), swiglu.swiglu_f64(gu, C))
+
+
+def test_band_exact_and_boundary_values():
+    # silu(40) = 40 exactly in float64, so H = 40 * u exactly
+    C = 4
+    u = np.array([[1.0, 1.5, 1.0 + 2.0 ** -5, -3.0]])
+    gu = np.concatenate([bits(np.full((1, C), 40.0)), bits(u)], axis=1)
+    mid, lo, hi = swiglu.swiglu_bf16_band(gu, C)
+    assert swiglu.unique_mask(lo, hi).all()
+    np.testing.assert_array_equal(bf16.to_f32(mid), 40.0 * u)
+    # silu(48) = 48, and 48 * (1 + 2^-7) = 48.375 lies exactly halfway between
+    # the BF16 neighbours 48.25 and 48.5 (spacing 0.25 at 32..64): both are
+    # accepted, and mid is the even one
+    u = np.array([[1.0 + 2.0 ** -7]])
+    gu = np.concatenate([bits([[48.0]]), bits(u)], axis=1)
+    assert bf16.to_f32(bits(u))[0, 0] == u[0, 0]
+    mid, lo, hi = swiglu.swiglu_bf16_band(gu, 1)
+    assert not swiglu.unique_mask(lo, hi)[0, 0]
+    assert (bf16.to_f32(lo)[0, 0], bf16.to_f32(hi)[0, 0]) == (48.25, 48.5)
+    assert bf16.to_f32(mid)[0, 0] == 48.5          # 48.5 = 1.1000010b * 2^5 has the even last bit
+    # signed zeros: silu(+0) * u keeps the sign of u; the band holds only zero
+    gu = np.concatenate([bits([[0.0, 0.0]]), bits([[2.0, -2.0]])], axis=1)
+    mid, lo, hi = swiglu.swiglu_bf16_band(gu, 2)
+    assert swiglu.unique_mask(lo, hi).all()
+    assert list(mid[0]) == [0x0000, 0x8000]
+    # where e^-g overflows binary32, zero is accepted
+    gu = np.concatenate([bits([[-100.0]]), bits([[1.0]])], axis=1)
+    mid, lo, hi = swiglu.swiglu_bf16_band(gu, 1)
+    assert bf16.to_f32(lo)[0, 0] <= 0.0 <= bf16.to_f32(hi)[0, 0]
+
+
+@pytest.mark.parametrize("axis,rule", [(None, "fp32"), (None, "pow2"), (1, "pow2"), (0, "pow2"), (1, "pow2_floor")])
+def test_band_check_accepts_oracle_and_rejects_mistakes(axis, rule):
+    rng = np.random.default_rng(2)
+    R, C = 256, 256
+    gu = bits(rng.standard_normal((R, 2 * C)))
+    mid, lo, hi = swiglu.swiglu_bf16_band(gu, C)
+    un = swiglu.unique_mask(lo, hi)
+    fmt = "e4m3"
+    if axis is None:
+        q, _, s, _ = quant.quantize_tensor(mid, fmt, rule=rule)
+    elif axis == 1:
+        q, s = quant.quantize_rows_1x128(mid, fmt, rule)
+    else:
+        qT, s = quant.quantize_cols_128x1(mid, fmt, rule)
+        q = qT.T
+    swiglu_check.check(q, s, mid, lo, hi, un, fmt, rule, axis, "oracle")
+    # a wrong code where H is unique
+    i = tuple(np.argwhere(un & (q != 0))[0])
+    q2 = q.copy()
+    q2[i] ^= 0x01
+    with pytest.raises(AssertionError):
+        swiglu_check.check(q2, s, mid, lo, hi, un, fmt, rule, axis, "planted code")
+    # a wrong scale
+    s2 = np.array(s, dtype=np.float32).reshape(-1).copy()
+    s2[0] *= 2
+    with pytest.raises(AssertionError):
+        swiglu_check.check(q, s2, mid, lo, hi, un, fmt, rule, axis, "planted scale")
+    # H taken without the up half (u = 1) must be caught
+    gu1 = np.concatenate([gu[:, :C], bits(np.ones((R, C)))], axis=1)
+    m1, _, _ = swiglu.swiglu_bf16_band(gu1, C)
+    if axis is None:
+        q1, _, s1, _ = quant.quantize_tensor(m1, fmt, rule=rule)
+    elif axis == 1:
+        q1, s1 = quant.quantize_rows_1x128(m1, fmt, rule)
+    else:
+        q1T, s1 = quant.quantize_cols_128x1(m1, fmt, rule)
+        q1 = q1T.T
+    with pytest.raises(AssertionError):
+        swiglu_check.check(q1, s1, mid, lo, hi, un, fmt, rule, axis, "planted operand")
