@@ -44,10 +44,11 @@ def parse():
                     help="instead of the headline step, time every workload (the five Qwen2-1.5B-shaped ones "
                          "and the paper's own 1.7B shapes under both power-of-two scale rules) next to the "
                          "same GEMMs in BF16, and report the FP8 errors of the two rules; one JSON line each")
-    ap.add_argument("--only", choices=("step",) + CALLS + ("copy",),
+    ap.add_argument("--only", choices=("step",) + CALLS + ("copy",) + SWIGLU_CALLS,
                     help="run just this call (or a whole step) warmup + steps times and print its average "
                          "time, for profilers; 'copy' is a plain 256 MiB device copy that calibrates "
-                         "the HBM byte counters")
+                         "the HBM byte counters; swiglu_* are the fused SwiGLU + quantise calls of the "
+                         "8192-token MLP")
     return ap.parse_args()
 
 
@@ -73,6 +74,45 @@ def cpu_baseline(tokens, reps):
 
 
 CALLS = ("quantize_x", "quantize_w", "fprop", "quantize_dy", "dgrad", "wgrad")
+SWIGLU_CALLS = ("swiglu_tensor", "swiglu_groups")
+
+
+def swiglu_workload(torch, puro, M=8192):
+    """The fused SwiGLU + quantise of the 8192-token MLP: H [M, 8960] from
+    a device-drawn gate/up output [M, 17920] ~ N(0, 1.7^2) (the spread of the
+    MLP's gate/up GEMM output), E4M3, per-tensor (q and qT) and 1x128 +
+    128x1 power-of-two groups. Returns {name: (fused call, unfused call,
+    algorithmic bytes)}; unfused is torch's BF16 silu and multiply, then
+    puro_quantize_fp8 of the BF16 H. Algorithmic bytes: gate and up read
+    once (4 B per H element) and one byte per element for each of q and qT."""
+    from paper_2608_27370_amd import inputs
+    F = inputs.MLP
+    dev = torch.device("cuda", 0)
+    g = torch.Generator(device=dev)
+    g.manual_seed(0)
+    gu = (torch.randn(M, 2 * F, generator=g, device=dev) * 1.7).to(torch.bfloat16)
+    E4 = puro.E4M3
+    outs = {"q": torch.empty(M, F, dtype=torch.uint8, device=dev), "qT": torch.empty(F, M, dtype=torch.uint8, device=dev)}
+    ts = dict(outs, scale=torch.empty(1, dtype=torch.float32, device=dev))
+    gs = dict(outs, scale=torch.empty(M, F // 128, dtype=torch.float32, device=dev),
+              scaleT=torch.empty(F, M // 128, dtype=torch.float32, device=dev))
+    ws = torch.empty(max(1, puro.lib().puro_swiglu_quantize_workspace_size(M, F)), dtype=torch.uint8, device=dev)
+    Hbuf = torch.empty(M, F, dtype=torch.bfloat16, device=dev)
+
+    def unfused(mode, rnd, out):
+        def fn():
+            torch.mul(torch.nn.functional.silu(gu[:, :F]), gu[:, F:], out=Hbuf)
+            puro.quantize_fp8(Hbuf, E4, mode=mode, rnd=rnd, want_qT=True, out=out, ws=ws)
+        return fn
+    nbytes = M * F * 6.0
+    return {
+        "swiglu_tensor": (lambda: puro.swiglu_quantize_fp8(gu, F, E4, puro.SCALE_TENSOR, puro.SCALE_FP32,
+                                                           want_qT=True, out=ts, ws=ws),
+                          unfused(puro.SCALE_TENSOR, puro.SCALE_FP32, ts), nbytes),
+        "swiglu_groups": (lambda: puro.swiglu_quantize_fp8(gu, F, E4, puro.SCALE_ROW_1x128, puro.SCALE_POW2,
+                                                           want_qT=True, out=gs, ws=ws),
+                          unfused(puro.SCALE_ROW_1x128, puro.SCALE_POW2, gs), nbytes),
+    }
 
 
 def calls(torch, puro, dev, M, N, K, X, W, dY, Y, dX, dW, saved):
@@ -138,7 +178,10 @@ def profiled_traffic(call):
 
 def run_only(args, torch, stream, step, make_calls):
     """Profiling mode: one call (or the whole step) warmup + steps times."""
-    if args.only == "copy":
+    if args.only in SWIGLU_CALLS:
+        from paper_2608_27370_amd import puro
+        fn, label = swiglu_workload(torch, puro)[args.only][0], "fused SwiGLU + quantise (%s)" % args.only
+    elif args.only == "copy":
         src = torch.empty(COPY_BYTES // 4, dtype=torch.float32, device=stream.device).fill_(1.0)
         dst = torch.empty_like(src)
         fn, label = (lambda: dst.copy_(src)), "plain device copy of %d bytes" % COPY_BYTES
@@ -351,6 +394,15 @@ def run_suite(args):
         for (name, _, _), lin in zip(inputs.PAPER_LINEARS, paper):
             S.compare("paper_%s_m8192_%s" % (name, rule), [lin], rc, reps, S.errors(*lin, rc))
         S.compare("paper_layer_m8192_%s" % rule, paper, rc, reps)
+    del paper
+    torch.cuda.empty_cache()
+    # the MLP's SwiGLU fused with the down projection's input quantisation
+    for name, (fused, unfused, nbytes) in swiglu_workload(torch, puro).items():
+        us_f, us_u = S.time_us(fused, 50), S.time_us(unfused, 50)
+        print(json.dumps({"workload": "mlp_%s_m8192" % name, "fused_us": round(us_f, 2), "unfused_us": round(us_u, 2),
+                          "fused_over_unfused": round(us_u / us_f, 3), "algorithmic_bytes": nbytes,
+                          "fused_gbs": round(nbytes / us_f / 1e3, 1),
+                          "fused_frac_hbm": round(nbytes / us_f / 1e3 / HBM_PEAK_GBS, 4)}), flush=True)
 
 
 def main():

@@ -123,6 +123,36 @@ puro_status puro_quantize_fp8(const uint16_t* x, int64_t rows, int64_t cols, int
                               uint8_t* qT, float* scaleT, void* ws, size_t ws_bytes,
                               hipStream_t stream);
 
+/* ------------------------------------------------- SwiGLU + quantise ---
+ * The MLP of the paper's model (the Qwen3-1.7B architecture, Section 2)
+ * computes down(silu(gate(x)) * up(x)); the hidden flow stays BF16 and the
+ * down projection quantises its input right before its GEMM (Section 3.2,
+ * Appendix C precision flow). This call fuses the two: from the fused
+ * gate/up output gu [rows, 2 cols] (gate = columns [0, cols), up = columns
+ * [cols, 2 cols), row pitch ld elements) it forms H = silu(gate) * up with
+ * silu(g) = g / (1 + e^-g) in binary32, rounds H to BF16 (nearest even) and
+ * quantises that H exactly as puro_quantize_fp8 would quantise a BF16 tensor
+ * holding it, without writing H. The BF16 value of H can differ in its last
+ * bit from another binary32 evaluation of exp; the codes and scales are
+ * those of the H this call forms.
+ *
+ * Modes: TENSOR (q and/or qT; scale[0]; rnd FP32, POW2 or POW2_FLOOR; the
+ * tensor's amax comes from a first pass over gu), ROW_1x128 (q, scale and
+ * optionally the 128x1 column-grouped qT, scaleT) and COL_128x1 (qT,
+ * scaleT), with the layouts of puro_quantize_fp8. BLOCK_128x128 returns
+ * PURO_ERR_UNSUPPORTED (weights, not activations, take 128x128 blocks).
+ *
+ * Requirements: those of puro_quantize_fp8 with the BF16 matrix being gu
+ * [rows, 2 cols] (ld >= 2 cols, ld % 8 == 0, ld < 2^23, gu 16-byte aligned)
+ * and cols % 16 == 0. ws: puro_swiglu_quantize_workspace_size(rows, cols)
+ * bytes (used in TENSOR mode). All pointers are device memory owned by the
+ * caller; nothing is allocated or synchronised. */
+size_t puro_swiglu_quantize_workspace_size(int64_t rows, int64_t cols);
+puro_status puro_swiglu_quantize_fp8(const uint16_t* gu, int64_t rows, int64_t cols, int64_t ld,
+                                     puro_fp8_format fmt, puro_scale_mode mode, puro_scale_rounding rnd,
+                                     uint8_t* q, float* scale, uint8_t* qT, float* scaleT, void* ws,
+                                     size_t ws_bytes, hipStream_t stream);
+
 /* ---------------------------------------------------------------- GEMM ---
  * D[m, n] = sum_k A[m, k] * B[n, k] with FP32 accumulation (Section 3.2:
  * the Fprop, Dgrad and Wgrad GEMMs of a linear layer run on FP8 operands).

@@ -19,8 +19,9 @@ Readings where the paper is silent (each restated in the design notes):
   H is not unique in its last BF16 bit: any BF16 value that an evaluation
   with relative error at most EPS = 2**-20 (plus 2**-148 absolute, for
   results in binary32's subnormal range) could round to is accepted; where
-  e^-g overflows binary32 (g < -88), zero is accepted as well (the exact H
-  is then below TINY * max(1, |u|), TINY = 2**-120). Where exactly one BF16
+  1 / (1 + e^-g) leaves binary32's normal range or e^-g overflows (g < -87),
+  zero is accepted as well (the exact H is then below TINY * max(1, |u|),
+  TINY = 2**-118). Where exactly one BF16
   value is accepted (almost everywhere) H is that value, rounded once from
   the float64 evaluation; the quantisation of every accepted H is the
   quantisers' (``oracle.quant``).
@@ -34,15 +35,16 @@ import numpy as np
 from . import bf16
 
 EPS = 2.0 ** -20
-TINY = 2.0 ** -120
+TINY = 2.0 ** -118
 
 
 def split(gu_bits, cols):
     """Gate and up halves of gu [R, 2*cols] as float64 (exact from BF16)."""
     gu = np.asarray(gu_bits, dtype=np.uint16)
     assert gu.ndim == 2 and gu.shape[1] >= 2 * cols
-    g = bf16.to_f32(gu[:, :cols]).astype(np.float64)
-    u = bf16.to_f32(gu[:, cols:2 * cols]).astype(np.float64)
+    with np.errstate(invalid="ignore"):
+        g = bf16.to_f32(gu[:, :cols]).astype(np.float64)
+        u = bf16.to_f32(gu[:, cols:2 * cols]).astype(np.float64)
     return g, u
 
 
@@ -71,7 +73,8 @@ def swiglu_bf16_band(gu_bits, cols):
     g, u = split(gu_bits, cols)
     with np.errstate(over="ignore", invalid="ignore"):
         t = silu_f64(g) * u
-        d = EPS * np.abs(t) + 2.0 ** -148 + np.where(g < -88.0, TINY * np.maximum(1.0, np.abs(u)), 0.0)
+        d = EPS * np.abs(t) + 2.0 ** -148 + np.where(g < -87.0, TINY * np.maximum(1.0, np.abs(u)), 0.0)
+        d = np.where(np.isfinite(t), d, 0.0)        # infinities are exact
         mid = bf16.from_f64_rne(t)
         lo = bf16.from_f64_rne(t - d)
         hi = bf16.from_f64_rne(t + d)

@@ -92,12 +92,16 @@ namespace {
 
 // puro_quantize_fp8 with a choice of grouped-scale layout (kmajor: k-block-
 // major, as the linear layer keeps its scales for the GEMM).
+// swiglu: x is a fused gate/up output [rows, 2 cols] and the values
+// quantised are H = BF16(silu(gate) * up) [rows, cols].
 puro_status quantize_impl(const uint16_t* x, int64_t rows, int64_t cols, int64_t ld, puro_fp8_format fmt,
                           puro_scale_mode mode, puro_scale_rounding rnd, const float* amax_in, uint8_t* q,
                           float* scale, uint8_t* qT, float* scaleT, void* ws, size_t ws_bytes, int kmajor,
-                          hipStream_t stream) {
-    puro_status st = check_bf16_matrix(x, rows, cols, ld);
+                          hipStream_t stream, bool swiglu = false) {
+    if (cols < 0) return PURO_ERR_SHAPE;
+    puro_status st = check_bf16_matrix(x, rows, swiglu ? 2 * cols : cols, ld);
     if (st != PURO_OK) return st;
+    if (swiglu && (amax_in || mode == PURO_SCALE_BLOCK_128x128)) return PURO_ERR_UNSUPPORTED;
     if (!fmt_ok(fmt) || (rnd != PURO_SCALE_FP32 && rnd != PURO_SCALE_POW2 && rnd != PURO_SCALE_POW2_FLOOR))
         return PURO_ERR_UNSUPPORTED;
     const bool pow2 = rnd == PURO_SCALE_POW2 || rnd == PURO_SCALE_POW2_FLOOR;
@@ -146,12 +150,12 @@ puro_status quantize_impl(const uint16_t* x, int64_t rows, int64_t cols, int64_t
     if (qmode == kQTensor && !amax_in) {
         if (!ws) return PURO_ERR_NULL;
         if (ws_bytes < quant_tensor_ws_bytes(rows, cols)) return PURO_ERR_WORKSPACE;
-        launch_quantize_tensor(fmt, a, ws, stream);
+        launch_quantize_tensor(fmt, a, ws, stream, swiglu);
         return launched();
     }
     // an empty tensor has no groups
     if ((rows == 0 || cols == 0) && qmode != kQTensor) return PURO_OK;
-    launch_quantize(fmt, qmode, a, stream);
+    launch_quantize(fmt, qmode, a, stream, swiglu);
     return launched();
 }
 
@@ -165,6 +169,20 @@ puro_status puro_quantize_fp8(const uint16_t* x, int64_t rows, int64_t cols, int
                               float* scaleT, void* ws, size_t ws_bytes, hipStream_t stream) {
     return quantize_impl(x, rows, cols, ld, fmt, mode, rnd, amax_in, q, scale, qT, scaleT, ws, ws_bytes, 0,
                          stream);
+}
+
+// ---------------------------------------------------- SwiGLU + quantise
+size_t puro_swiglu_quantize_workspace_size(int64_t rows, int64_t cols) {
+    if (rows < 0 || cols < 0) return 0;
+    return quant_tensor_ws_bytes(rows, cols);
+}
+
+puro_status puro_swiglu_quantize_fp8(const uint16_t* gu, int64_t rows, int64_t cols, int64_t ld,
+                                     puro_fp8_format fmt, puro_scale_mode mode, puro_scale_rounding rnd,
+                                     uint8_t* q, float* scale, uint8_t* qT, float* scaleT, void* ws,
+                                     size_t ws_bytes, hipStream_t stream) {
+    return quantize_impl(gu, rows, cols, ld, fmt, mode, rnd, nullptr, q, scale, qT, scaleT, ws, ws_bytes, 0,
+                         stream, true);
 }
 
 // ------------------------------------------------------------------- GEMM

@@ -25,6 +25,49 @@ template <> struct Fp8Traits<kE5M2> {
 __device__ __forceinline__ float bf16lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
 
+typedef float v2f __attribute__((ext_vector_type(2)));
+typedef __bf16 v2bf __attribute__((ext_vector_type(2)));
+
+// Two binary32 values -> two BF16 (round to nearest even) in one word, low
+// half first: the conversion instruction (v_cvt_pk_bf16_f32).
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector((v2f){a, b}, v2bf));
+}
+__device__ __forceinline__ uint16_t to_bf16(float a) { return (uint16_t)pack_bf16x2(a, 0.0f); }
+
+// e^x in binary32 within about 2 ulp: 2^(x log2 e) by the exp2 instruction,
+// with the rounding error of the product x log2 e (exact from an FMA, plus
+// the low part of log2 e) applied as a first-order factor, so that the error
+// does not grow with |x|. Overflows to infinity above x = 88.72 and gives 0
+// below -103; e^(+inf) = inf, e^(-inf) = 0, NaN stays NaN.
+__device__ __forceinline__ float exp_f32(float x) {
+    constexpr float kL2eHi = 1.44269502162933349609375f;      // log2 e rounded to binary32
+    constexpr float kL2eLo = 1.925962989e-8f;                 // log2 e - kL2eHi
+    constexpr float kLn2 = 0.693147180559945309f;
+    const float t = x * kL2eHi;
+    // the correction only where it matters and stays finite (the result is
+    // exactly 0 or infinity beyond)
+    const float err = fabsf(x) < 100.0f ? fmaf(x, kL2eHi, -t) + x * kL2eLo : 0.0f;   // x log2 e - t
+    return __builtin_amdgcn_exp2f(t) * (1.0f + err * kLn2);
+}
+
+// SwiGLU of one gate/up pair in binary32: silu(g) * u with silu(g) = g / (1 + e^-g),
+// the quotient as g times the reciprocal instruction's 1 / (1 + e^-g) (about
+// 1 ulp); altogether within about 5 ulp of the exact value. For g below about
+// -87.3 the reciprocal falls below binary32's normal range and may flush, and
+// for g < -88.72 e^-g overflows: silu(g) is then -0.
+__device__ __forceinline__ float swiglu1(float g, float u) {
+    return g * __builtin_amdgcn_rcpf(1.0f + exp_f32(-g)) * u;
+}
+
+// Eight SwiGLU values, BF16 (round to nearest even), from four words of gate
+// values and four words of up values (two BF16 values per word, low first).
+__device__ __forceinline__ void swiglu8(const uint32_t g[4], const uint32_t u[4], uint32_t h[4]) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+        h[i] = pack_bf16x2(swiglu1(bf16lo(g[i]), bf16lo(u[i])), swiglu1(bf16hi(g[i]), bf16hi(u[i])));
+}
+
 // Hardware conversion of two binary32 values to two FP8 codes (RNE), written
 // into byte pair HI (false: bytes 0-1, true: bytes 2-3) of `old`. In range it
 // rounds exactly like the encoding this library defines; it does not

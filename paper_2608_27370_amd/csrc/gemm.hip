@@ -75,15 +75,6 @@ struct Params {
 
 __device__ __forceinline__ uint32_t e8m0_of(float s) { return (__float_as_uint(s) >> 23) & 0xFFu; }
 
-typedef float v2f __attribute__((ext_vector_type(2)));
-typedef __bf16 v2bf __attribute__((ext_vector_type(2)));
-
-// Two FP32 values -> two BF16 (round to nearest even) in one word, low half
-// first: the conversion instruction (v_cvt_pk_bf16_f32).
-__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
-    return __builtin_bit_cast(uint32_t, __builtin_convertvector((v2f){a, b}, v2bf));
-}
-__device__ __forceinline__ uint16_t to_bf16(float a) { return (uint16_t)pack_bf16x2(a, 0.0f); }
 
 typedef int v4i __attribute__((ext_vector_type(4)));
 

@@ -21,9 +21,11 @@ struct AmaxJob {
 // Number of per-block partial maxima the amax pass writes for a tensor.
 int amax_num_partials(int64_t rows, int64_t cols);
 
-// Per-block maxima of the BF16 magnitude patterns of x into partial[0..P).
+// Per-block maxima of the BF16 magnitude patterns of x into partial[0..P);
+// swiglu: of H = BF16(silu(gate) * up) where x is [rows, 2 cols] (gate =
+// columns [0, cols), up = columns [cols, 2 cols)).
 void launch_amax_partials(const uint16_t* x, int64_t rows, int64_t cols, int64_t ld,
-                          uint32_t* partial, int P, hipStream_t stream);
+                          uint32_t* partial, int P, hipStream_t stream, bool swiglu = false);
 // amax = max of partial[0..P) as a float (0 when P == 0).
 void launch_amax_finalize(const uint32_t* partial, int P, float* amax, hipStream_t stream);
 
@@ -54,12 +56,15 @@ size_t quant_tensor_ws_bytes(int64_t rows, int64_t cols);
 // Per-tensor quantisation with the tensor's own amax: the partial maxima
 // pass, then the quantise pass (which reduces them, or reads the amax a
 // one-block reduction wrote). ws holds quant_tensor_ws_bytes.
-void launch_quantize_tensor(int fmt, QuantArgs a, void* ws, hipStream_t stream);
+// swiglu: the values are H = BF16(silu(gate) * up) of a.x [rows, 2 cols].
+void launch_quantize_tensor(int fmt, QuantArgs a, void* ws, hipStream_t stream, bool swiglu = false);
 // The same for two tensors of one format, with one amax launch and one
 // quantise launch for both (each tensor with its own workspace).
 void launch_quantize_tensor_pair(int fmt, QuantArgs a0, void* ws0, QuantArgs a1, void* ws1,
                                  hipStream_t stream);
-void launch_quantize(int fmt, int mode, const QuantArgs& a, hipStream_t stream);
+// Grouped modes, or per-tensor with a.amax set; swiglu as above (not in
+// 128x128 block mode).
+void launch_quantize(int fmt, int mode, const QuantArgs& a, hipStream_t stream, bool swiglu = false);
 
 // ---- GEMM (gemm.hip) ----------------------------------------------------------
 

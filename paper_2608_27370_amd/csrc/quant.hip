@@ -52,9 +52,15 @@ __device__ __forceinline__ uint32_t block_max(uint32_t v, uint32_t* red) {
 }
 
 // ---------------------------------------------------------------- amax ---
+// Sources of the values a pass reads: the BF16 tensor itself, or the SwiGLU
+// of a fused gate/up output [rows, 2 cols] (gate = columns [0, cols), up =
+// columns [cols, 2 cols)), rounded to BF16 as the tensor H = silu(gate) * up
+// would hold it.
+enum : int { kSrcBf16 = 0, kSrcSwiglu = 1 };
+
 // Partial maxima of one or two tensors in one launch: blocks [0, j0.P) cover
 // the rows of the first tensor in P contiguous ranges, the rest the second.
-template <bool DENSE>
+template <bool DENSE, int SRC>
 __global__ __launch_bounds__(kThreads) void amax_partial_kernel(AmaxJob j0, AmaxJob j1) {
     __shared__ uint32_t red[4];
     const bool second = (int)blockIdx.x >= j0.P;
@@ -70,11 +76,11 @@ __global__ __launch_bounds__(kThreads) void amax_partial_kernel(AmaxJob j0, Amax
     uint32_t m = 0;
     constexpr int U = 8;
     for (uint32_t j0i = threadIdx.x; j0i < n; j0i += kThreads * U) {
-        uint4 v[U];
+        uint4 v[U], vu[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const uint32_t j = j0i + u * kThreads;
-            v[u] = make_uint4(0, 0, 0, 0);
+            v[u] = vu[u] = make_uint4(0, 0, 0, 0);
             if (j < n) {
                 const uint16_t* p;
                 if constexpr (DENSE) {
@@ -84,11 +90,18 @@ __global__ __launch_bounds__(kThreads) void amax_partial_kernel(AmaxJob j0, Amax
                     p = x + (r0 + rr) * ld + (int64_t)cc * 8;
                 }
                 v[u] = *reinterpret_cast<const uint4*>(p);
+                // the up value of the same position, cols (= 8 cpr) further on
+                if constexpr (SRC == kSrcSwiglu) vu[u] = *reinterpret_cast<const uint4*>(p + 8 * cpr);
             }
         }
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            const uint32_t w[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
+            uint32_t w[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
+            if constexpr (SRC == kSrcSwiglu) {
+                const uint32_t wu[4] = {vu[u].x, vu[u].y, vu[u].z, vu[u].w};
+                const uint32_t wg[4] = {w[0], w[1], w[2], w[3]};
+                swiglu8(wg, wu, w);
+            }
             m = max(m, absmax_bits8(w));
         }
     }
@@ -135,18 +148,35 @@ constexpr uint32_t kOOB = 0x80000000u;   // an offset beyond every descriptor's 
 // The thread's 8x8 block, zeros outside the tensor, by buffer loads over the
 // tile's rows: positions outside the tensor read as zeros through the
 // descriptor's range check, so the loads carry no branches and issue back to
-// back (and independent loads issued before them are not waited for).
+// back (and independent loads issued before them are not waited for). With
+// the SwiGLU source each value is computed from the gate and up values at the
+// same position of the two halves of a row (zeros outside give silu(0) * 0 = 0).
+template <int SRC>
 __device__ __forceinline__ void load_8x8(const QuantArgs& a, const Tile& t, uint32_t w[8][4]) {
     const int64_t tr0 = t.row0 - t.rg * 8;                        // the tile's first row
     const int64_t vr = a.cols == 0 ? 0 : max((int64_t)0, min((int64_t)kTile, a.rows - tr0));
-    // rows tr0 .. tr0 + vr - 1: the last one ends at column cols
-    const uint32_t bytes = vr == 0 ? 0u : (uint32_t)(((vr - 1) * a.ld + a.cols) * 2);
+    // rows tr0 .. tr0 + vr - 1: the last one ends at column cols (2 cols with the SwiGLU source)
+    const int64_t width = SRC == kSrcSwiglu ? 2 * a.cols : a.cols;
+    const uint32_t bytes = vr == 0 ? 0u : (uint32_t)(((vr - 1) * a.ld + width) * 2);
     const __amdgpu_buffer_rsrc_t rs = buffer_rsrc(vr == 0 ? a.x : a.x + tr0 * a.ld, bytes);
+    uint32_t wu[8][4];
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
         const uint32_t off = t.col_ok ? (uint32_t)(((t.rg * 8 + i) * a.ld + t.col) * 2) : kOOB;
         const v4i v = __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0);
         w[i][0] = v.x; w[i][1] = v.y; w[i][2] = v.z; w[i][3] = v.w;
+        if constexpr (SRC == kSrcSwiglu) {
+            const uint32_t offu = t.col_ok ? off + (uint32_t)(a.cols * 2) : kOOB;
+            const v4i vu = __builtin_amdgcn_raw_buffer_load_b128(rs, offu, 0, 0);
+            wu[i][0] = vu.x; wu[i][1] = vu.y; wu[i][2] = vu.z; wu[i][3] = vu.w;
+        }
+    }
+    if constexpr (SRC == kSrcSwiglu) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const uint32_t g[4] = {w[i][0], w[i][1], w[i][2], w[i][3]};
+            swiglu8(g, wu[i], w[i]);
+        }
     }
 }
 
@@ -300,7 +330,7 @@ __device__ __forceinline__ float tensor_amax(const QuantArgs& a, const PartialSh
 // the first tensor's tiles, then the second's). Each block loads the partial
 // maxima of both tensors and its tile's BF16 values before reducing any of
 // them, so that the amax reduction overlaps the arrival of the tile.
-template <int FMT>
+template <int FMT, int SRC>
 __global__ __launch_bounds__(kThreads) void quant_tensor_kernel(QuantArgs a0, QuantArgs a1, int tiles0,
                                                                 int gx0, int gx1) {
     __shared__ uint32_t red[4];
@@ -314,7 +344,7 @@ __global__ __launch_bounds__(kThreads) void quant_tensor_kernel(QuantArgs a0, Qu
     const PartialShare p0 = load_partials(a0);
     const PartialShare p1 = load_partials(a1, two);
     uint32_t w[8][4];
-    load_8x8(a, t, w);
+    load_8x8<SRC>(a, t, w);
     // the scales (every block derives the same values; block 0 stores them)
     const TensorScale sc0 = tensor_scale<FMT>(a0, tensor_amax(a0, p0, red));
     const TensorScale sc1 = two ? tensor_scale<FMT>(a1, tensor_amax(a1, p1, red)) : sc0;
@@ -336,13 +366,13 @@ __global__ __launch_bounds__(kThreads) void quant_tensor_kernel(QuantArgs a0, Qu
 }
 
 // 1x128 row groups (q, scale) and/or 128x1 column groups (qT, scaleT).
-template <int FMT, bool ROWS, bool COLS>
+template <int FMT, bool ROWS, bool COLS, int SRC>
 __global__ __launch_bounds__(kThreads) void quant_groups_kernel(QuantArgs a) {
     __shared__ uint32_t colmax[4][kTile];
     __shared__ __attribute__((aligned(16))) uint8_t tq[COLS ? kTile * kTile : 16];
     const Tile t = tile_coords(a.cols);
     uint32_t w[8][4];
-    load_8x8(a, t, w);
+    load_8x8<SRC>(a, t, w);
     const bool floor_rule = a.pow2 == 2;
 
     if constexpr (ROWS) {
@@ -440,7 +470,7 @@ __global__ __launch_bounds__(kThreads) void quant_block_kernel(QuantArgs a) {
     __shared__ __attribute__((aligned(16))) uint8_t tq[kTile * kTile];
     const Tile t = tile_coords(a.cols);
     uint32_t w[8][4];
-    load_8x8(a, t, w);
+    load_8x8<kSrcBf16>(a, t, w);
     uint32_t m = 0;
 #pragma unroll
     for (int i = 0; i < 8; ++i) m = max(m, absmax_bits8(w[i]));
@@ -476,24 +506,25 @@ __global__ __launch_bounds__(kThreads) void quant_block_kernel(QuantArgs a) {
     }
 }
 
-template <int FMT>
+template <int FMT, int SRC>
 void launch_quantize_fmt(int mode, const QuantArgs& a, hipStream_t stream) {
     // at least one block, so that an empty tensor still gets its scale written
     const int64_t gx = (a.cols + kTile - 1) / kTile, gy = (a.rows + kTile - 1) / kTile;
     const dim3 grid((unsigned)(gx > 0 ? gx : 1), (unsigned)(gy > 0 ? gy : 1));
     switch (mode) {
     case kQTensor:
-        quant_tensor_kernel<FMT><<<grid.x * grid.y, kThreads, 0, stream>>>(a, a, (int)(grid.x * grid.y), (int)grid.x, 1);
+        quant_tensor_kernel<FMT, SRC><<<grid.x * grid.y, kThreads, 0, stream>>>(a, a, (int)(grid.x * grid.y),
+                                                                              (int)grid.x, 1);
         break;
     case kQRow:
-        if (a.qT) quant_groups_kernel<FMT, true, true><<<grid, kThreads, 0, stream>>>(a);
-        else quant_groups_kernel<FMT, true, false><<<grid, kThreads, 0, stream>>>(a);
+        if (a.qT) quant_groups_kernel<FMT, true, true, SRC><<<grid, kThreads, 0, stream>>>(a);
+        else quant_groups_kernel<FMT, true, false, SRC><<<grid, kThreads, 0, stream>>>(a);
         break;
     case kQCol:
-        quant_groups_kernel<FMT, false, true><<<grid, kThreads, 0, stream>>>(a);
+        quant_groups_kernel<FMT, false, true, SRC><<<grid, kThreads, 0, stream>>>(a);
         break;
     case kQBlock:
-        quant_block_kernel<FMT><<<grid, kThreads, 0, stream>>>(a);
+        if constexpr (SRC == kSrcBf16) quant_block_kernel<FMT><<<grid, kThreads, 0, stream>>>(a);
         break;
     }
 }
@@ -511,19 +542,25 @@ int amax_num_partials(int64_t rows, int64_t cols) {
 }
 
 void launch_amax_partials(const uint16_t* x, int64_t rows, int64_t cols, int64_t ld,
-                          uint32_t* partial, int P, hipStream_t stream) {
+                          uint32_t* partial, int P, hipStream_t stream, bool swiglu) {
     const AmaxJob j{x, rows, ld, partial, (uint32_t)(cols / 8), P};
-    if (ld == cols) amax_partial_kernel<true><<<P, kThreads, 0, stream>>>(j, j);
-    else amax_partial_kernel<false><<<P, kThreads, 0, stream>>>(j, j);
+    if (swiglu) amax_partial_kernel<false, kSrcSwiglu><<<P, kThreads, 0, stream>>>(j, j);
+    else if (ld == cols) amax_partial_kernel<true, kSrcBf16><<<P, kThreads, 0, stream>>>(j, j);
+    else amax_partial_kernel<false, kSrcBf16><<<P, kThreads, 0, stream>>>(j, j);
 }
 
 void launch_amax_finalize(const uint32_t* partial, int P, float* amax, hipStream_t stream) {
     amax_finalize_kernel<<<1, kThreads, 0, stream>>>(partial, P, amax);
 }
 
-void launch_quantize(int fmt, int mode, const QuantArgs& a, hipStream_t stream) {
-    if (fmt == kE4M3) launch_quantize_fmt<kE4M3>(mode, a, stream);
-    else launch_quantize_fmt<kE5M2>(mode, a, stream);
+void launch_quantize(int fmt, int mode, const QuantArgs& a, hipStream_t stream, bool swiglu) {
+    if (swiglu) {
+        if (fmt == kE4M3) launch_quantize_fmt<kE4M3, kSrcSwiglu>(mode, a, stream);
+        else launch_quantize_fmt<kE5M2, kSrcSwiglu>(mode, a, stream);
+    } else {
+        if (fmt == kE4M3) launch_quantize_fmt<kE4M3, kSrcBf16>(mode, a, stream);
+        else launch_quantize_fmt<kE5M2, kSrcBf16>(mode, a, stream);
+    }
 }
 
 // Workspace: the partial maxima, then the amax scalar.
@@ -556,11 +593,11 @@ int64_t tiles_y(int64_t rows) { const int64_t g = (rows + kTile - 1) / kTile; re
 
 }  // namespace
 
-void launch_quantize_tensor(int fmt, QuantArgs a, void* ws, hipStream_t stream) {
+void launch_quantize_tensor(int fmt, QuantArgs a, void* ws, hipStream_t stream, bool swiglu) {
     const int P = amax_num_partials(a.rows, a.cols);
-    if (P > 0) launch_amax_partials(a.x, a.rows, a.cols, a.ld, reinterpret_cast<uint32_t*>(ws), P, stream);
+    if (P > 0) launch_amax_partials(a.x, a.rows, a.cols, a.ld, reinterpret_cast<uint32_t*>(ws), P, stream, swiglu);
     amax_source(a, P, ws, stream);
-    launch_quantize(fmt, kQTensor, a, stream);
+    launch_quantize(fmt, kQTensor, a, stream, swiglu);
 }
 
 void launch_quantize_tensor_pair(int fmt, QuantArgs a0, void* ws0, QuantArgs a1, void* ws1,
@@ -574,17 +611,17 @@ void launch_quantize_tensor_pair(int fmt, QuantArgs a0, void* ws0, QuantArgs a1,
     }
     const AmaxJob j0{a0.x, a0.rows, a0.ld, reinterpret_cast<uint32_t*>(ws0), (uint32_t)(a0.cols / 8), P0};
     const AmaxJob j1{a1.x, a1.rows, a1.ld, reinterpret_cast<uint32_t*>(ws1), (uint32_t)(a1.cols / 8), P1};
-    if (dense) amax_partial_kernel<true><<<P0 + P1, kThreads, 0, stream>>>(j0, j1);
-    else amax_partial_kernel<false><<<P0 + P1, kThreads, 0, stream>>>(j0, j1);
+    if (dense) amax_partial_kernel<true, kSrcBf16><<<P0 + P1, kThreads, 0, stream>>>(j0, j1);
+    else amax_partial_kernel<false, kSrcBf16><<<P0 + P1, kThreads, 0, stream>>>(j0, j1);
     amax_source(a0, P0, ws0, stream);
     amax_source(a1, P1, ws1, stream);
     const int64_t gx0 = tiles_x(a0.cols), gx1 = tiles_x(a1.cols);
     const int64_t t0 = gx0 * tiles_y(a0.rows), t1 = gx1 * tiles_y(a1.rows);
     const unsigned grid = (unsigned)(t0 + t1);
     if (fmt == kE4M3)
-        quant_tensor_kernel<kE4M3><<<grid, kThreads, 0, stream>>>(a0, a1, (int)t0, (int)gx0, (int)gx1);
+        quant_tensor_kernel<kE4M3, kSrcBf16><<<grid, kThreads, 0, stream>>>(a0, a1, (int)t0, (int)gx0, (int)gx1);
     else
-        quant_tensor_kernel<kE5M2><<<grid, kThreads, 0, stream>>>(a0, a1, (int)t0, (int)gx0, (int)gx1);
+        quant_tensor_kernel<kE5M2, kSrcBf16><<<grid, kThreads, 0, stream>>>(a0, a1, (int)t0, (int)gx0, (int)gx1);
 }
 
 }  // namespace puro

@@ -107,6 +107,14 @@ def mlp(M=8192):
                 dY_dn=normal(rng(0, 3, 5), (M, HIDDEN), 1e-3))
 
 
+def mlp_gate_up(M=8192):
+    """A stand-in for the fused gate/up GEMM output [M, 2 * MLP] that the
+    SwiGLU consumes: normal with the spread that X W_gu^T has for the MLP
+    inputs above (rows of 1536 N(0,1) values, 1% of them x20, against
+    N(0, 0.02^2) weights: variance 0.02^2 * (1521 + 15 * 400) ~ 1.7^2)."""
+    return normal(rng(0, 3, 6), (M, 2 * MLP), 1.7)
+
+
 def layer_linear(layer, j, M=16384):
     name, N, K = LAYER_LINEARS[j]
     return dict(name=name,

@@ -55,6 +55,8 @@ _SIGS = {
     "puro_amax": (_i, [_p, _i64, _i64, _i64, _p, _p, _sz, _p]),
     "puro_quantize_workspace_size": (_sz, [_i64, _i64]),
     "puro_quantize_fp8": (_i, [_p, _i64, _i64, _i64, _i, _i, _i, _p, _p, _p, _p, _p, _p, _sz, _p]),
+    "puro_swiglu_quantize_workspace_size": (_sz, [_i64, _i64]),
+    "puro_swiglu_quantize_fp8": (_i, [_p, _i64, _i64, _i64, _i, _i, _i, _p, _p, _p, _p, _p, _sz, _p]),
     "puro_fp8_gemm_workspace_size": (_sz, [_i64, _i64, _i64, _i]),
     "puro_fp8_gemm_plan": (_i, [_i64, _i64, _i64, _i, _i, ctypes.POINTER(_i), ctypes.POINTER(_i),
                                 ctypes.POINTER(_i), ctypes.POINTER(_i), ctypes.POINTER(_i)]),
@@ -172,6 +174,45 @@ def quantize_fp8(x, fmt, mode=SCALE_TENSOR, rnd=SCALE_FP32, amax_in=None, want_q
     _check("puro_quantize_fp8", lib().puro_quantize_fp8(
         _ptr(x), rows, cols, _ld(x), fmt, mode, rnd, _ptr(amax_in), _ptr(q), _ptr(scale), _ptr(qT),
         _ptr(scaleT), _ptr(w), nb, _stream()))
+    return dict(q=q, scale=scale, qT=qT, scaleT=scaleT)
+
+
+# ----------------------------------------------------- SwiGLU + quantise
+def swiglu_quantize_fp8(gu, cols, fmt, mode=SCALE_TENSOR, rnd=SCALE_FP32, want_q=True, want_qT=False,
+                        out=None, ws=None):
+    """Quantise H = BF16(silu(gate) * up) of a fused gate/up output gu
+    [rows, 2 cols] (gate = gu[:, :cols], up = gu[:, cols:2 cols]) without
+    writing H; returns dict(q, scale, qT, scaleT) as quantize_fp8 does."""
+    rows = gu.shape[0]
+    assert gu.shape[1] >= 2 * cols
+    dev = gu.device
+    out = dict(out or {})
+    G = 128
+    if mode == SCALE_COL_128x1:
+        want_q, want_qT = False, True
+    q = out.get("q") if want_q else None
+    if want_q and q is None:
+        q = torch.empty(rows, cols, dtype=torch.uint8, device=dev)
+    qT = out.get("qT") if want_qT else None
+    if want_qT and qT is None:
+        qT = torch.empty(cols, rows, dtype=torch.uint8, device=dev)
+    scale, scaleT = out.get("scale"), out.get("scaleT")
+    if mode == SCALE_TENSOR:
+        scale = scale if scale is not None else torch.empty(1, dtype=torch.float32, device=dev)
+        scaleT = None
+    elif mode == SCALE_ROW_1x128:
+        scale = scale if scale is not None else torch.empty(rows, cols // G, dtype=torch.float32, device=dev)
+        if want_qT and scaleT is None:
+            scaleT = torch.empty(cols, rows // G, dtype=torch.float32, device=dev)
+    elif mode == SCALE_COL_128x1:
+        scale = None
+        scaleT = scaleT if scaleT is not None else torch.empty(cols, rows // G, dtype=torch.float32, device=dev)
+    if not want_qT:
+        scaleT = None
+    w, nb = _ws(lib().puro_swiglu_quantize_workspace_size(rows, cols), ws, dev)
+    _check("puro_swiglu_quantize_fp8", lib().puro_swiglu_quantize_fp8(
+        _ptr(gu), rows, cols, _ld(gu), fmt, mode, rnd, _ptr(q), _ptr(scale), _ptr(qT), _ptr(scaleT),
+        _ptr(w), nb, _stream()))
     return dict(q=q, scale=scale, qT=qT, scaleT=scaleT)
 
 

@@ -180,3 +180,24 @@ def test_gemm_plan_validation(puro):
     assert L.puro_fp8_gemm_plan(16, 16, 16, 2, 0, None, None, None, None, None) == ERR_UNSUPPORTED  # 128x1
     assert L.puro_fp8_gemm_plan(16, 16, 16, 0, 0, None, None, None, None, None) == OK
     assert puro.fp8_gemm_plan(0, 16, 16)["launches"] == 0
+
+
+def test_swiglu_quantize_validation(puro):
+    L = puro.lib()
+    f = L.puro_swiglu_quantize_fp8
+    big = 1 << 20
+    # gu NULL, and a row pitch shorter than the two halves
+    assert f(None, 16, 128, 256, 0, 0, 0, FAKE, FAKE, None, None, FAKE, big, None) == ERR_NULL
+    assert f(FAKE, 16, 128, 200, 0, 0, 0, FAKE, FAKE, None, None, FAKE, big, None) == ERR_SHAPE
+    assert f(FAKE, 16, -1, 256, 0, 0, 0, FAKE, FAKE, None, None, FAKE, big, None) == ERR_SHAPE
+    # cols % 16, misaligned gu
+    assert f(FAKE, 16, 24, 48, 0, 0, 0, FAKE, FAKE, None, None, FAKE, big, None) == ERR_ALIGN
+    assert f(FAKE + 8, 16, 128, 256, 0, 0, 0, FAKE, FAKE, None, None, FAKE, big, None) == ERR_ALIGN
+    # 128x128 blocks are for weights, not for this activation
+    assert f(FAKE, 128, 128, 256, 0, 3, 1, FAKE, FAKE, None, None, None, 0, None) == ERR_UNSUPPORTED
+    # grouped modes need a power-of-two rule; 1x128 groups need cols % 128
+    assert f(FAKE, 128, 128, 256, 0, 1, 0, FAKE, FAKE, None, None, None, 0, None) == ERR_UNSUPPORTED
+    assert f(FAKE, 128, 144, 288, 0, 1, 1, FAKE, FAKE, None, None, None, 0, None) == ERR_ALIGN
+    # per-tensor without workspace for the amax pass
+    assert f(FAKE, 4096, 4096, 8192, 0, 0, 0, FAKE, FAKE, None, None, FAKE, 0, None) == ERR_WORKSPACE
+    assert L.puro_swiglu_quantize_workspace_size(4096, 4096) == L.puro_quantize_workspace_size(4096, 4096)
