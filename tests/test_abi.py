@@ -160,8 +160,8 @@ def test_linear_validation(puro):
 # Shapes on which the GEMM planner takes each of its kernel configurations
 # (tile, ring depth) and the split-K path; tests/test_gpu_gemm.py runs them.
 PLAN_SHAPES = {(256, 256, 2): (3072, 4096, 256), (256, 192, 2): (3072, 3072, 256),
-               (128, 128, 4): (256, 256, 256), (128, 128, 2): (1536, 3072, 256)}
-SPLIT_SHAPE = (256, 256, 1024)
+               (128, 128, 4): (1024, 1024, 2048), (128, 128, 2): (1536, 3072, 256)}
+SPLIT_SHAPES = [(256, 256, 1024), (768, 768, 4096)]   # split-K with the 2- and the 4-deep 128x128 tiles
 
 
 @pytest.mark.parametrize("modes", [(0, 0), (1, 3)], ids=["tensor", "row-block"])
@@ -170,8 +170,9 @@ def test_gemm_plan_covers_every_configuration(puro, modes):
         p = puro.fp8_gemm_plan(*shape, *modes)
         assert (p["tile_m"], p["tile_n"], p["stages"]) == cfg, (shape, p)
         assert p["splits"] == 1 and p["launches"] == 1
-    p = puro.fp8_gemm_plan(*SPLIT_SHAPE, *modes)
-    assert p["splits"] > 1 and p["launches"] == 2
+    for shape, stages in zip(SPLIT_SHAPES, (2, 4)):
+        p = puro.fp8_gemm_plan(*shape, *modes)
+        assert p["splits"] > 1 and p["launches"] == 2 and p["stages"] == stages, (shape, p)
 
 
 def test_gemm_plan_validation(puro):

@@ -201,11 +201,13 @@ def test_gemm_is_deterministic(P):
     assert np.array_equal(D1.view(np.uint32), D2.view(np.uint32))
 
 
-# One shape per kernel configuration of the planner (tile, ring depth) and one
-# that takes the split-K path; tests/test_abi.py checks that the planner maps
+# One shape per kernel configuration of the planner (tile, ring depth) and two
+# that take the split-K path (with the 2- and the 4-deep 128x128 tiles, the
+# latter with producer waves); tests/test_abi.py checks that the planner maps
 # them so. Outputs are compared on stratified samples plus the whole first and
 # last 256x256 tiles.
-PLAN_CASES = [(3072, 4096, 256), (3072, 3072, 256), (256, 256, 256), (1536, 3072, 256), (256, 256, 1024)]
+PLAN_CASES = [(3072, 4096, 256), (3072, 3072, 256), (1024, 1024, 2048), (1536, 3072, 256), (256, 256, 1024),
+              (768, 768, 4096)]
 
 
 @pytest.mark.parametrize("shape", PLAN_CASES, ids=lambda s: "x".join(map(str, s)))
