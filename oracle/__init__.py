@@ -15,11 +15,14 @@ Training", and Appendix C, "FP8 implementation pipeline"):
                 above;
 * ``bf16``   -- BF16 bit helpers used to state expected outputs;
 * ``swiglu`` -- the MLP's SwiGLU, whose BF16 output the down projection
-                quantises (the fused SwiGLU + quantise operation).
+                quantises (the fused SwiGLU + quantise operation);
+* ``rmsnorm`` -- the RMSNorm whose BF16 output the QKV and gate/up
+                projections quantise (the fused RMSNorm + quantise
+                operation).
 
 It is test infrastructure: only ``tests/``, ``__graft_entry__.smoke()`` and
 the ``cpu_baseline`` leg of ``bench.py`` may import it. It shares no code with
 the HIP library and never imports it.
 """
 
-from . import bf16, fp8, quant, gemm, linear, swiglu  # noqa: F401
+from . import bf16, fp8, quant, gemm, linear, rmsnorm, swiglu  # noqa: F401

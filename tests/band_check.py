@@ -1,15 +1,15 @@
-"""Checks of a fused SwiGLU + quantise result against the oracle's band of
-accepted BF16 H values (oracle/swiglu.py). No arithmetic of the method here:
-scales and codes come from oracle.quant and oracle.fp8.
+"""Checks of a fused op + quantise result (SwiGLU, RMSNorm) against the
+oracle's band of accepted BF16 values of the op's output (oracle/swiglu.py,
+oracle/rmsnorm.py). No arithmetic of the method here: scales and codes come
+from oracle.quant and oracle.fp8.
 
 For every group (the whole tensor, 128 consecutive values along a row, or 128
 down a column) the accepted amax values are those of the band; the result's
 scale must be the scale of one of them (almost always there is one; a
-group whose largest values all sit in the band around zero of the deep
-negative gate tail has many). With
-that scale's multiplier, elements whose H is unique must carry exactly the
-oracle's code, and every other element a code whose value lies between the
-codes of the band's ends (codes are monotone in the value they encode).
+group whose largest values all sit in a band around zero has many). With
+that scale's multiplier, elements whose value is unique must carry exactly
+the oracle's code, and every other element a code whose value lies between
+the codes of the band's ends (codes are monotone in the value they encode).
 """
 
 import numpy as np

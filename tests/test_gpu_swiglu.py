@@ -1,7 +1,7 @@
 """GPU parity of the fused SwiGLU + quantise call (puro_swiglu_quantize_fp8)
 against the oracle (oracle/swiglu.py with oracle/quant.py), through the C
 ABI: codes and scales equal to the oracle's wherever H is unique, and valid
-for the band of accepted H elsewhere (tests/swiglu_check.py)."""
+for the band of accepted H elsewhere (tests/band_check.py)."""
 
 import numpy as np
 import pytest
@@ -9,7 +9,7 @@ import pytest
 from oracle import fp8, swiglu
 from paper_2608_27370_amd import inputs
 
-import swiglu_check
+import band_check
 from gpu_util import host, to_dev_bf16
 
 pytestmark = pytest.mark.gpu
@@ -48,13 +48,13 @@ def _check_all(r, gu, cols, fmt, mode, rnd, what):
     n = 0
     if mode == TENSOR:
         if r["q"] is not None:
-            n += swiglu_check.check(r["q"], r["scale"], mid, lo, hi, un, f, rule, None, what + " q")
+            n += band_check.check(r["q"], r["scale"], mid, lo, hi, un, f, rule, None, what + " q")
         if r["qT"] is not None:
-            n += swiglu_check.check(r["qT"].T, r["scale"], mid, lo, hi, un, f, rule, None, what + " qT")
+            n += band_check.check(r["qT"].T, r["scale"], mid, lo, hi, un, f, rule, None, what + " qT")
     if mode == ROW:
-        n += swiglu_check.check(r["q"], r["scale"], mid, lo, hi, un, f, rule, 1, what + " q")
+        n += band_check.check(r["q"], r["scale"], mid, lo, hi, un, f, rule, 1, what + " q")
     if (mode == ROW and r["qT"] is not None) or mode == COL:
-        n += swiglu_check.check(r["qT"].T, r["scaleT"], mid, lo, hi, un, f, rule, 0, what + " qT")
+        n += band_check.check(r["qT"].T, r["scaleT"], mid, lo, hi, un, f, rule, 0, what + " qT")
     return n
 
 
@@ -135,19 +135,19 @@ def test_mlp_full_size(P, mode, rnd):
         # codes of sampled rows and of sampled columns (qT rows)
         mid, lo, hi = swiglu.swiglu_bf16_band(gu, F)
         un = swiglu.unique_mask(lo, hi)
-        ta = swiglu_check.amax_band(lo, hi)
-        swiglu_check.check(r["q"][rws], r["scale"], mid[rws], lo[rws], hi[rws], un[rws], f, rule, None,
+        ta = band_check.amax_band(lo, hi)
+        band_check.check(r["q"][rws], r["scale"], mid[rws], lo[rws], hi[rws], un[rws], f, rule, None,
                            "full q rows", tensor_amax=ta)
         cols_idx = np.concatenate([np.arange(c, c + 128) for c in cls])
-        swiglu_check.check(r["qT"][cols_idx].T, r["scale"], mid[:, cols_idx], lo[:, cols_idx], hi[:, cols_idx],
+        band_check.check(r["qT"][cols_idx].T, r["scale"], mid[:, cols_idx], lo[:, cols_idx], hi[:, cols_idx],
                            un[:, cols_idx], f, rule, None, "full qT cols", tensor_amax=ta)
         return
     gr = np.ascontiguousarray(np.concatenate([gu[rws, :F], gu[rws, F:2 * F]], axis=1))
     mid, lo, hi = swiglu.swiglu_bf16_band(gr, F)
-    swiglu_check.check(r["q"][rws], r["scale"][rws], mid, lo, hi, swiglu.unique_mask(lo, hi), f, rule, 1,
+    band_check.check(r["q"][rws], r["scale"][rws], mid, lo, hi, swiglu.unique_mask(lo, hi), f, rule, 1,
                        "full 1x128 rows")
     cols_idx = np.concatenate([np.arange(c, c + 128) for c in cls])
     gc = np.ascontiguousarray(np.concatenate([gu[:, cols_idx], gu[:, F + cols_idx]], axis=1))
     mid, lo, hi = swiglu.swiglu_bf16_band(gc, cols_idx.size)
-    swiglu_check.check(r["qT"][cols_idx].T, r["scaleT"][cols_idx], mid, lo, hi, swiglu.unique_mask(lo, hi), f,
+    band_check.check(r["qT"][cols_idx].T, r["scaleT"][cols_idx], mid, lo, hi, swiglu.unique_mask(lo, hi), f,
                        rule, 0, "full 128x1 cols")

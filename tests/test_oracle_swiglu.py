@@ -1,5 +1,5 @@
 """Pins of the SwiGLU oracle (oracle/swiglu.py) and of the band check used by
-the fused SwiGLU + quantise parity tests (tests/swiglu_check.py).
+the fused SwiGLU + quantise parity tests (tests/band_check.py).
 
 silu(g) = g / (1 + e^-g) is pinned by the identity silu(g) - silu(-g) = g, by
 the library routine scipy.special.expit (silu(g) = g * expit(g)), and by its
@@ -13,7 +13,7 @@ import pytest
 from scipy.special import expit
 
 from oracle import bf16, quant, swiglu
-from tests import swiglu_check
+from tests import band_check
 
 
 def bits(x):
@@ -97,18 +97,18 @@ def test_band_check_accepts_oracle_and_rejects_mistakes(axis, rule):
     else:
         qT, s = quant.quantize_cols_128x1(mid, fmt, rule)
         q = qT.T
-    swiglu_check.check(q, s, mid, lo, hi, un, fmt, rule, axis, "oracle")
+    band_check.check(q, s, mid, lo, hi, un, fmt, rule, axis, "oracle")
     # a wrong code where H is unique
     i = tuple(np.argwhere(un & (q != 0))[0])
     q2 = q.copy()
     q2[i] ^= 0x01
     with pytest.raises(AssertionError):
-        swiglu_check.check(q2, s, mid, lo, hi, un, fmt, rule, axis, "planted code")
+        band_check.check(q2, s, mid, lo, hi, un, fmt, rule, axis, "planted code")
     # a wrong scale
     s2 = np.array(s, dtype=np.float32).reshape(-1).copy()
     s2[0] *= 2
     with pytest.raises(AssertionError):
-        swiglu_check.check(q, s2, mid, lo, hi, un, fmt, rule, axis, "planted scale")
+        band_check.check(q, s2, mid, lo, hi, un, fmt, rule, axis, "planted scale")
     # H taken without the up half (u = 1) must be caught
     gu1 = np.concatenate([gu[:, :C], bits(np.ones((R, C)))], axis=1)
     m1, _, _ = swiglu.swiglu_bf16_band(gu1, C)
@@ -120,4 +120,4 @@ def test_band_check_accepts_oracle_and_rejects_mistakes(axis, rule):
         q1T, s1 = quant.quantize_cols_128x1(m1, fmt, rule)
         q1 = q1T.T
     with pytest.raises(AssertionError):
-        swiglu_check.check(q1, s1, mid, lo, hi, un, fmt, rule, axis, "planted operand")
+        band_check.check(q1, s1, mid, lo, hi, un, fmt, rule, axis, "planted operand")
