@@ -44,11 +44,11 @@ def parse():
                     help="instead of the headline step, time every workload (the five Qwen2-1.5B-shaped ones "
                          "and the paper's own 1.7B shapes under both power-of-two scale rules) next to the "
                          "same GEMMs in BF16, and report the FP8 errors of the two rules; one JSON line each")
-    ap.add_argument("--only", choices=("step",) + CALLS + ("copy",) + SWIGLU_CALLS,
+    ap.add_argument("--only", choices=("step",) + CALLS + ("copy",) + SWIGLU_CALLS + RMSNORM_CALLS,
                     help="run just this call (or a whole step) warmup + steps times and print its average "
                          "time, for profilers; 'copy' is a plain 256 MiB device copy that calibrates "
-                         "the HBM byte counters; swiglu_* are the fused SwiGLU + quantise calls of the "
-                         "8192-token MLP")
+                         "the HBM byte counters; swiglu_* and rmsnorm_* are the fused SwiGLU / RMSNorm + "
+                         "quantise calls of the 8192-token MLP and QKV input")
     return ap.parse_args()
 
 
@@ -75,6 +75,46 @@ def cpu_baseline(tokens, reps):
 
 CALLS = ("quantize_x", "quantize_w", "fprop", "quantize_dy", "dgrad", "wgrad")
 SWIGLU_CALLS = ("swiglu_tensor", "swiglu_groups")
+RMSNORM_CALLS = ("rmsnorm_tensor", "rmsnorm_groups")
+
+
+def rmsnorm_workload(torch, puro, M=8192, d=1536):
+    """The fused RMSNorm + quantise of the QKV projection's input: x [M, d]
+    drawn on the device (N(0,1), 1% of the channels x20), gamma ~ N(1, 0.1^2),
+    eps 1e-6, E4M3 with q and qT, per-tensor and 1x128 + 128x1 groups.
+    Returns {name: (fused call, unfused call, algorithmic bytes)}; unfused is
+    torch's BF16 RMSNorm, then puro_quantize_fp8 of its output. Algorithmic
+    bytes: x read once (2 B) and q, qT written (2 B) per element."""
+    dev = torch.device("cuda", 0)
+    g = torch.Generator(device=dev)
+    g.manual_seed(1)
+    x = torch.randn(M, d, generator=g, device=dev)
+    x[:, torch.randperm(d, generator=g, device=dev)[:d // 100]] *= 20.0
+    x = x.to(torch.bfloat16)
+    gamma = (1.0 + 0.1 * torch.randn(d, generator=g, device=dev)).to(torch.bfloat16)
+    E4 = puro.E4M3
+    outs = {"q": torch.empty(M, d, dtype=torch.uint8, device=dev), "qT": torch.empty(d, M, dtype=torch.uint8, device=dev),
+            "rstd": torch.empty(M, dtype=torch.float32, device=dev)}
+    ts = dict(outs, scale=torch.empty(1, dtype=torch.float32, device=dev))
+    gs = dict(outs, scale=torch.empty(M, d // 128, dtype=torch.float32, device=dev),
+              scaleT=torch.empty(d, M // 128, dtype=torch.float32, device=dev))
+    ws = torch.empty(max(puro.lib().puro_rmsnorm_quantize_workspace_size(M, d),
+                         puro.lib().puro_quantize_workspace_size(M, d)), dtype=torch.uint8, device=dev)
+
+    def unfused(mode, rnd, out):
+        def fn():
+            y = torch.nn.functional.rms_norm(x, (d,), gamma, 1e-6)
+            puro.quantize_fp8(y, E4, mode=mode, rnd=rnd, want_qT=True, out=out, ws=ws)
+        return fn
+    nbytes = M * d * 4.0
+    return {
+        "rmsnorm_tensor": (lambda: puro.rmsnorm_quantize_fp8(x, gamma, 1e-6, E4, puro.SCALE_TENSOR, puro.SCALE_FP32,
+                                                             want_qT=True, out=ts, ws=ws),
+                           unfused(puro.SCALE_TENSOR, puro.SCALE_FP32, ts), nbytes),
+        "rmsnorm_groups": (lambda: puro.rmsnorm_quantize_fp8(x, gamma, 1e-6, E4, puro.SCALE_ROW_1x128, puro.SCALE_POW2,
+                                                             want_qT=True, out=gs, ws=ws),
+                           unfused(puro.SCALE_ROW_1x128, puro.SCALE_POW2, gs), nbytes),
+    }
 
 
 def swiglu_workload(torch, puro, M=8192):
@@ -181,6 +221,9 @@ def run_only(args, torch, stream, step, make_calls):
     if args.only in SWIGLU_CALLS:
         from paper_2608_27370_amd import puro
         fn, label = swiglu_workload(torch, puro)[args.only][0], "fused SwiGLU + quantise (%s)" % args.only
+    elif args.only in RMSNORM_CALLS:
+        from paper_2608_27370_amd import puro
+        fn, label = rmsnorm_workload(torch, puro)[args.only][0], "fused RMSNorm + quantise (%s)" % args.only
     elif args.only == "copy":
         src = torch.empty(COPY_BYTES // 4, dtype=torch.float32, device=stream.device).fill_(1.0)
         dst = torch.empty_like(src)
@@ -396,10 +439,13 @@ def run_suite(args):
         S.compare("paper_layer_m8192_%s" % rule, paper, rc, reps)
     del paper
     torch.cuda.empty_cache()
-    # the MLP's SwiGLU fused with the down projection's input quantisation
-    for name, (fused, unfused, nbytes) in swiglu_workload(torch, puro).items():
+    # the MLP's SwiGLU fused with the down projection's input quantisation,
+    # and the RMSNorm fused with the QKV projection's
+    work = dict(("mlp_%s_m8192" % k, v) for k, v in swiglu_workload(torch, puro).items())
+    work.update(("qkv_input_%s_m8192" % k, v) for k, v in rmsnorm_workload(torch, puro).items())
+    for name, (fused, unfused, nbytes) in work.items():
         us_f, us_u = S.time_us(fused, 50), S.time_us(unfused, 50)
-        print(json.dumps({"workload": "mlp_%s_m8192" % name, "fused_us": round(us_f, 2), "unfused_us": round(us_u, 2),
+        print(json.dumps({"workload": name, "fused_us": round(us_f, 2), "unfused_us": round(us_u, 2),
                           "fused_over_unfused": round(us_u / us_f, 3), "algorithmic_bytes": nbytes,
                           "fused_gbs": round(nbytes / us_f / 1e3, 1),
                           "fused_frac_hbm": round(nbytes / us_f / 1e3 / HBM_PEAK_GBS, 4)}), flush=True)

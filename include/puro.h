@@ -153,6 +153,38 @@ puro_status puro_swiglu_quantize_fp8(const uint16_t* gu, int64_t rows, int64_t c
                                      uint8_t* q, float* scale, uint8_t* qT, float* scaleT, void* ws,
                                      size_t ws_bytes, hipStream_t stream);
 
+/* ------------------------------------------------ RMSNorm + quantise ---
+ * Every attention and MLP block of the paper's model (the Qwen3-1.7B
+ * architecture, Section 2) starts with an RMSNorm whose output is the input
+ * of the QKV or gate/up projection; the norm stays BF16 and the projection
+ * quantises its input right before its GEMM (Section 3.2, Appendix C
+ * precision flow). This call fuses the two: for x [rows, cols] (row pitch
+ * ld elements) and the norm's weight gamma [cols] (BF16) it computes, per
+ * row, rstd = 1 / sqrt(mean(x^2) + eps) in binary32 (written to rstd[rows],
+ * float, for the norm's backward), forms y = x * rstd * gamma in binary32,
+ * rounds y to BF16 (nearest even) and quantises that y exactly as
+ * puro_quantize_fp8 would quantise a BF16 tensor holding it, without
+ * writing y. The binary32 sum of squares is taken in this library's order;
+ * another order can move rstd, and so y's last BF16 bit, slightly.
+ *
+ * Modes: TENSOR (q and/or qT; scale[0]; rnd FP32, POW2 or POW2_FLOOR),
+ * ROW_1x128 (q, scale and optionally the 128x1 column-grouped qT, scaleT)
+ * and COL_128x1 (qT, scaleT), with the layouts of puro_quantize_fp8.
+ * BLOCK_128x128 returns PURO_ERR_UNSUPPORTED. eps must be finite and
+ * >= 0 (else PURO_ERR_UNSUPPORTED).
+ *
+ * Requirements: those of puro_quantize_fp8 for x; cols > 0 when rows > 0;
+ * gamma and rstd non-NULL and 16-byte aligned when rows > 0. ws:
+ * puro_rmsnorm_quantize_workspace_size(rows, cols) bytes (used in TENSOR
+ * mode). All pointers are device memory owned by the caller; nothing is
+ * allocated or synchronised. */
+size_t puro_rmsnorm_quantize_workspace_size(int64_t rows, int64_t cols);
+puro_status puro_rmsnorm_quantize_fp8(const uint16_t* x, const uint16_t* gamma, int64_t rows, int64_t cols,
+                                      int64_t ld, float eps, puro_fp8_format fmt, puro_scale_mode mode,
+                                      puro_scale_rounding rnd, uint8_t* q, float* scale, uint8_t* qT,
+                                      float* scaleT, float* rstd, void* ws, size_t ws_bytes,
+                                      hipStream_t stream);
+
 /* ---------------------------------------------------------------- GEMM ---
  * D[m, n] = sum_k A[m, k] * B[n, k] with FP32 accumulation (Section 3.2:
  * the Fprop, Dgrad and Wgrad GEMMs of a linear layer run on FP8 operands).

@@ -92,16 +92,34 @@ namespace {
 
 // puro_quantize_fp8 with a choice of grouped-scale layout (kmajor: k-block-
 // major, as the linear layer keeps its scales for the GEMM).
-// swiglu: x is a fused gate/up output [rows, 2 cols] and the values
-// quantised are H = BF16(silu(gate) * up) [rows, cols].
+// The values a quantisation encodes: the BF16 tensor x itself; the SwiGLU
+// H = BF16(silu(gate) * up) [rows, cols] of a fused gate/up output x [rows,
+// 2 cols]; or the RMSNorm y = BF16(x * rstd * gamma) of x [rows, cols], whose
+// per-row rstd is written too.
+struct Source {
+    enum Kind { kBf16, kSwiglu, kRmsnorm } kind = kBf16;
+    const uint16_t* gamma = nullptr;
+    float* rstd = nullptr;
+    float eps = 0.0f;
+};
+
 puro_status quantize_impl(const uint16_t* x, int64_t rows, int64_t cols, int64_t ld, puro_fp8_format fmt,
                           puro_scale_mode mode, puro_scale_rounding rnd, const float* amax_in, uint8_t* q,
                           float* scale, uint8_t* qT, float* scaleT, void* ws, size_t ws_bytes, int kmajor,
-                          hipStream_t stream, bool swiglu = false) {
+                          hipStream_t stream, Source src = Source()) {
+    const bool swiglu = src.kind == Source::kSwiglu, rms = src.kind == Source::kRmsnorm;
     if (cols < 0) return PURO_ERR_SHAPE;
     puro_status st = check_bf16_matrix(x, rows, swiglu ? 2 * cols : cols, ld);
     if (st != PURO_OK) return st;
-    if (swiglu && (amax_in || mode == PURO_SCALE_BLOCK_128x128)) return PURO_ERR_UNSUPPORTED;
+    if ((swiglu || rms) && (amax_in || mode == PURO_SCALE_BLOCK_128x128)) return PURO_ERR_UNSUPPORTED;
+    if (rms) {
+        // a row needs its columns (the mean of an empty row is undefined)
+        if (rows > 0 && cols == 0) return PURO_ERR_SHAPE;
+        if (!(src.eps >= 0.0f) || !(src.eps <= 3.4028235e38f)) return PURO_ERR_UNSUPPORTED;
+        if (rows > 0 && (!src.gamma || !src.rstd)) return PURO_ERR_NULL;
+        if (rows > 0 && (!aligned16(src.gamma) || (reinterpret_cast<uintptr_t>(src.rstd) & 15) != 0))
+            return PURO_ERR_ALIGN;
+    }
     if (!fmt_ok(fmt) || (rnd != PURO_SCALE_FP32 && rnd != PURO_SCALE_POW2 && rnd != PURO_SCALE_POW2_FLOOR))
         return PURO_ERR_UNSUPPORTED;
     const bool pow2 = rnd == PURO_SCALE_POW2 || rnd == PURO_SCALE_POW2_FLOOR;
@@ -115,6 +133,8 @@ puro_status quantize_impl(const uint16_t* x, int64_t rows, int64_t cols, int64_t
     a.supplied = amax_in != nullptr;
     a.pow2 = rnd == PURO_SCALE_POW2 ? 1 : (rnd == PURO_SCALE_POW2_FLOOR ? 2 : 0);
     a.kmajor = kmajor;
+    a.gamma = src.gamma;
+    a.rstd = src.rstd;
     // outputs of an empty tensor are never written (torch hands out NULL for them)
     const bool empty = rows == 0 || cols == 0;
     int qmode;
@@ -146,6 +166,16 @@ puro_status quantize_impl(const uint16_t* x, int64_t rows, int64_t cols, int64_t
         break;
     default:
         return PURO_ERR_UNSUPPORTED;
+    }
+    if (rms) {
+        if (qmode == kQTensor) {
+            if (!ws) return PURO_ERR_NULL;
+            if (ws_bytes < rmsnorm_ws_bytes(rows)) return PURO_ERR_WORKSPACE;
+        } else if (rows == 0) {
+            return PURO_OK;
+        }
+        launch_rmsnorm_quantize(fmt, qmode, a, src.eps, ws, stream);
+        return launched();
     }
     if (qmode == kQTensor && !amax_in) {
         if (!ws) return PURO_ERR_NULL;
@@ -181,8 +211,29 @@ puro_status puro_swiglu_quantize_fp8(const uint16_t* gu, int64_t rows, int64_t c
                                      puro_fp8_format fmt, puro_scale_mode mode, puro_scale_rounding rnd,
                                      uint8_t* q, float* scale, uint8_t* qT, float* scaleT, void* ws,
                                      size_t ws_bytes, hipStream_t stream) {
+    Source src;
+    src.kind = Source::kSwiglu;
     return quantize_impl(gu, rows, cols, ld, fmt, mode, rnd, nullptr, q, scale, qT, scaleT, ws, ws_bytes, 0,
-                         stream, true);
+                         stream, src);
+}
+
+// --------------------------------------------------- RMSNorm + quantise
+size_t puro_rmsnorm_quantize_workspace_size(int64_t rows, int64_t cols) {
+    if (rows < 0 || cols < 0) return 0;
+    return rmsnorm_ws_bytes(rows);
+}
+
+puro_status puro_rmsnorm_quantize_fp8(const uint16_t* x, const uint16_t* gamma, int64_t rows, int64_t cols,
+                                      int64_t ld, float eps, puro_fp8_format fmt, puro_scale_mode mode,
+                                      puro_scale_rounding rnd, uint8_t* q, float* scale, uint8_t* qT,
+                                      float* scaleT, float* rstd, void* ws, size_t ws_bytes, hipStream_t stream) {
+    Source src;
+    src.kind = Source::kRmsnorm;
+    src.gamma = gamma;
+    src.rstd = rstd;
+    src.eps = eps;
+    return quantize_impl(x, rows, cols, ld, fmt, mode, rnd, nullptr, q, scale, qT, scaleT, ws, ws_bytes, 0,
+                         stream, src);
 }
 
 // ------------------------------------------------------------------- GEMM

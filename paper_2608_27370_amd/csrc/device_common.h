@@ -68,6 +68,14 @@ __device__ __forceinline__ void swiglu8(const uint32_t g[4], const uint32_t u[4]
         h[i] = pack_bf16x2(swiglu1(bf16lo(g[i]), bf16lo(u[i])), swiglu1(bf16hi(g[i]), bf16hi(u[i])));
 }
 
+// Eight RMSNorm outputs, BF16 (round to nearest even): x * r * gamma in
+// binary32 from four words of x, the row's r = rstd and four words of gamma.
+__device__ __forceinline__ void rmsnorm8(const uint32_t x[4], float r, const uint32_t g[4], uint32_t y[4]) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+        y[i] = pack_bf16x2(bf16lo(x[i]) * r * bf16lo(g[i]), bf16hi(x[i]) * r * bf16hi(g[i]));
+}
+
 // Hardware conversion of two binary32 values to two FP8 codes (RNE), written
 // into byte pair HI (false: bytes 0-1, true: bytes 2-3) of `old`. In range it
 // rounds exactly like the encoding this library defines; it does not

@@ -49,6 +49,10 @@ struct QuantArgs {
     // grouped modes: scale arrays k-block-major (the group index along the
     // quantised copy's columns outermost) instead of row-major
     int kmajor;
+    // RMSNorm source: the per-row reciprocal RMS (written by the row pass)
+    // and the norm's weight, BF16 [cols]
+    const float* rstd;
+    const uint16_t* gamma;
 };
 
 // Workspace of a per-tensor quantisation that computes its own amax.
@@ -65,6 +69,13 @@ void launch_quantize_tensor_pair(int fmt, QuantArgs a0, void* ws0, QuantArgs a1,
 // Grouped modes, or per-tensor with a.amax set; swiglu as above (not in
 // 128x128 block mode).
 void launch_quantize(int fmt, int mode, const QuantArgs& a, hipStream_t stream, bool swiglu = false);
+
+// RMSNorm + quantise: y = BF16(x * rstd * gamma) per row of a.x [rows, cols]
+// (rstd = 1 / sqrt(mean(x^2) + eps), written to a.rstd), quantised like a
+// BF16 tensor holding y in `mode` (kQTensor, kQRow or kQCol). ws holds
+// rmsnorm_ws_bytes(rows) bytes (the per-tensor partial maxima).
+size_t rmsnorm_ws_bytes(int64_t rows);
+void launch_rmsnorm_quantize(int fmt, int mode, QuantArgs a, float eps, void* ws, hipStream_t stream);
 
 // ---- GEMM (gemm.hip) ----------------------------------------------------------
 

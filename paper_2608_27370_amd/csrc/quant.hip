@@ -52,11 +52,12 @@ __device__ __forceinline__ uint32_t block_max(uint32_t v, uint32_t* red) {
 }
 
 // ---------------------------------------------------------------- amax ---
-// Sources of the values a pass reads: the BF16 tensor itself, or the SwiGLU
-// of a fused gate/up output [rows, 2 cols] (gate = columns [0, cols), up =
+// Sources of the values a pass reads: the BF16 tensor itself; the SwiGLU of a
+// fused gate/up output [rows, 2 cols] (gate = columns [0, cols), up =
 // columns [cols, 2 cols)), rounded to BF16 as the tensor H = silu(gate) * up
-// would hold it.
-enum : int { kSrcBf16 = 0, kSrcSwiglu = 1 };
+// would hold it; or the RMSNorm y = x * rstd * gamma of x [rows, cols],
+// rounded to BF16 (rstd per row from the row pass, gamma per column).
+enum : int { kSrcBf16 = 0, kSrcSwiglu = 1, kSrcRmsnorm = 2 };
 
 // Partial maxima of one or two tensors in one launch: blocks [0, j0.P) cover
 // the rows of the first tensor in P contiguous ranges, the rest the second.
@@ -118,6 +119,58 @@ __global__ __launch_bounds__(kThreads) void amax_finalize_kernel(const uint32_t*
     if (threadIdx.x == 0) *amax = __uint_as_float(m << 16);
 }
 
+// ------------------------------------------------------------ RMSNorm ---
+// One wave per row, four rows per block: the row's sum of squares in binary32
+// (each lane over its 8-column chunks in order, then a butterfly across the
+// wave), rstd = 1 / sqrt(sum / cols + eps) stored per row; with AMAX, a second
+// sweep over the row (now in cache) forms y = BF16(x * rstd * gamma) and the
+// block writes the largest |y| pattern of its rows as a partial maximum.
+template <bool AMAX>
+__global__ __launch_bounds__(kThreads) void rmsnorm_rows_kernel(const uint16_t* __restrict__ x, int64_t rows,
+                                                                int64_t cols, int64_t ld,
+                                                                const uint16_t* __restrict__ gamma, float eps,
+                                                                float* __restrict__ rstd,
+                                                                uint32_t* __restrict__ partial) {
+    __shared__ uint32_t red[4];
+    const int lane = threadIdx.x & 63;
+    const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    const int64_t cpr = cols / 8;
+    const bool live = row < rows;
+    const uint16_t* xr = x + (live ? row : 0) * ld;
+    float ss = 0.0f;
+    if (live) {
+        for (int64_t c = lane; c < cpr; c += 64) {
+            const uint4 v = *reinterpret_cast<const uint4*>(xr + c * 8);
+            const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const float lo = bf16lo(w[i]), hi = bf16hi(w[i]);
+                ss = fmaf(lo, lo, ss);
+                ss = fmaf(hi, hi, ss);
+            }
+        }
+    }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) ss += __shfl_xor(ss, o, 64);
+    const float r = 1.0f / sqrtf(ss / (float)cols + eps);
+    if (live && lane == 0) rstd[row] = r;
+    if constexpr (AMAX) {
+        uint32_t m = 0;
+        if (live) {
+            for (int64_t c = lane; c < cpr; c += 64) {
+                const uint4 v = *reinterpret_cast<const uint4*>(xr + c * 8);
+                const uint4 gv = *reinterpret_cast<const uint4*>(gamma + c * 8);
+                const uint32_t w[4] = {v.x, v.y, v.z, v.w}, gw[4] = {gv.x, gv.y, gv.z, gv.w};
+                uint32_t y[4];
+                rmsnorm8(w, r, gw, y);
+                m = max(m, absmax_bits8(y));
+            }
+        }
+        m = block_max(m, red);
+        if (threadIdx.x == 0) partial[blockIdx.x] = m;
+    }
+}
+
 // ------------------------------------------------------------ quantise ---
 struct Tile {
     int cc, rg;       // column chunk (8 columns) and row group (8 rows) of this thread
@@ -177,6 +230,19 @@ __device__ __forceinline__ void load_8x8(const QuantArgs& a, const Tile& t, uint
             const uint32_t g[4] = {w[i][0], w[i][1], w[i][2], w[i][3]};
             swiglu8(g, wu[i], w[i]);
         }
+    }
+    if constexpr (SRC == kSrcRmsnorm) {
+        // the rows' rstd (zeros past the last row) and the columns' gamma
+        const __amdgpu_buffer_rsrc_t rr = buffer_rsrc(a.rstd, (uint32_t)(a.rows * 4));
+        const __amdgpu_buffer_rsrc_t rg = buffer_rsrc(a.gamma, (uint32_t)(a.cols * 2));
+        const uint32_t roff = (uint32_t)(t.row0 * 4);
+        const v4i r0 = __builtin_amdgcn_raw_buffer_load_b128(rr, roff, 0, 0);
+        const v4i r1 = __builtin_amdgcn_raw_buffer_load_b128(rr, roff + 16, 0, 0);
+        const v4i gv = __builtin_amdgcn_raw_buffer_load_b128(rg, t.col_ok ? (uint32_t)(t.col * 2) : kOOB, 0, 0);
+        const uint32_t gw[4] = {(uint32_t)gv.x, (uint32_t)gv.y, (uint32_t)gv.z, (uint32_t)gv.w};
+        const int rs[8] = {r0.x, r0.y, r0.z, r0.w, r1.x, r1.y, r1.z, r1.w};
+#pragma unroll
+        for (int i = 0; i < 8; ++i) rmsnorm8(w[i], __int_as_float(rs[i]), gw, w[i]);
     }
 }
 
@@ -622,6 +688,27 @@ void launch_quantize_tensor_pair(int fmt, QuantArgs a0, void* ws0, QuantArgs a1,
         quant_tensor_kernel<kE4M3, kSrcBf16><<<grid, kThreads, 0, stream>>>(a0, a1, (int)t0, (int)gx0, (int)gx1);
     else
         quant_tensor_kernel<kE5M2, kSrcBf16><<<grid, kThreads, 0, stream>>>(a0, a1, (int)t0, (int)gx0, (int)gx1);
+}
+
+size_t rmsnorm_ws_bytes(int64_t rows) {
+    const int64_t P = rows > 0 ? (rows + 3) / 4 : 0;
+    return ((size_t)P * sizeof(uint32_t) + 255) / 256 * 256 + sizeof(float);
+}
+
+void launch_rmsnorm_quantize(int fmt, int mode, QuantArgs a, float eps, void* ws, hipStream_t stream) {
+    const int64_t P = a.rows > 0 ? (a.rows + 3) / 4 : 0;
+    uint32_t* partial = reinterpret_cast<uint32_t*>(ws);
+    if (P > 0) {
+        if (mode == kQTensor)
+            rmsnorm_rows_kernel<true><<<(unsigned)P, kThreads, 0, stream>>>(a.x, a.rows, a.cols, a.ld, a.gamma, eps,
+                                                                           const_cast<float*>(a.rstd), partial);
+        else
+            rmsnorm_rows_kernel<false><<<(unsigned)P, kThreads, 0, stream>>>(a.x, a.rows, a.cols, a.ld, a.gamma, eps,
+                                                                            const_cast<float*>(a.rstd), partial);
+    }
+    if (mode == kQTensor) amax_source(a, (int)P, ws, stream);
+    if (fmt == kE4M3) launch_quantize_fmt<kE4M3, kSrcRmsnorm>(mode, a, stream);
+    else launch_quantize_fmt<kE5M2, kSrcRmsnorm>(mode, a, stream);
 }
 
 }  // namespace puro

@@ -115,6 +115,14 @@ def mlp_gate_up(M=8192):
     return normal(rng(0, 3, 6), (M, 2 * MLP), 1.7)
 
 
+def norm_input(M=8192, d=HIDDEN):
+    """The residual stream an RMSNorm reads before the QKV projection
+    [M, d] (N(0,1) with 1% of the channels x20, like the MLP inputs) and the
+    norm's weight [d] ~ N(1, 0.1^2)."""
+    return dict(x=with_outlier_columns(rng(0, 7, 0), (M, d)),
+                gamma=bf16_from_f64(1.0 + 0.1 * rng(0, 7, 1).standard_normal(d)))
+
+
 def layer_linear(layer, j, M=16384):
     name, N, K = LAYER_LINEARS[j]
     return dict(name=name,

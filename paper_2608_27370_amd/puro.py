@@ -57,6 +57,9 @@ _SIGS = {
     "puro_quantize_fp8": (_i, [_p, _i64, _i64, _i64, _i, _i, _i, _p, _p, _p, _p, _p, _p, _sz, _p]),
     "puro_swiglu_quantize_workspace_size": (_sz, [_i64, _i64]),
     "puro_swiglu_quantize_fp8": (_i, [_p, _i64, _i64, _i64, _i, _i, _i, _p, _p, _p, _p, _p, _sz, _p]),
+    "puro_rmsnorm_quantize_workspace_size": (_sz, [_i64, _i64]),
+    "puro_rmsnorm_quantize_fp8": (_i, [_p, _p, _i64, _i64, _i64, ctypes.c_float, _i, _i, _i, _p, _p, _p, _p, _p,
+                                       _p, _sz, _p]),
     "puro_fp8_gemm_workspace_size": (_sz, [_i64, _i64, _i64, _i]),
     "puro_fp8_gemm_plan": (_i, [_i64, _i64, _i64, _i, _i, ctypes.POINTER(_i), ctypes.POINTER(_i),
                                 ctypes.POINTER(_i), ctypes.POINTER(_i), ctypes.POINTER(_i)]),
@@ -175,6 +178,53 @@ def quantize_fp8(x, fmt, mode=SCALE_TENSOR, rnd=SCALE_FP32, amax_in=None, want_q
         _ptr(x), rows, cols, _ld(x), fmt, mode, rnd, _ptr(amax_in), _ptr(q), _ptr(scale), _ptr(qT),
         _ptr(scaleT), _ptr(w), nb, _stream()))
     return dict(q=q, scale=scale, qT=qT, scaleT=scaleT)
+
+
+def _quant_outputs(rows, cols, mode, want_q, want_qT, out, dev):
+    """Output tensors of a quantisation (supplied ones from `out` kept)."""
+    out = dict(out or {})
+    G = 128
+    if mode == SCALE_COL_128x1:
+        want_q, want_qT = False, True
+    q = out.get("q") if want_q else None
+    if want_q and q is None:
+        q = torch.empty(rows, cols, dtype=torch.uint8, device=dev)
+    qT = out.get("qT") if want_qT else None
+    if want_qT and qT is None:
+        qT = torch.empty(cols, rows, dtype=torch.uint8, device=dev)
+    scale, scaleT = out.get("scale"), out.get("scaleT")
+    if mode == SCALE_TENSOR:
+        scale = scale if scale is not None else torch.empty(1, dtype=torch.float32, device=dev)
+        scaleT = None
+    elif mode == SCALE_ROW_1x128:
+        scale = scale if scale is not None else torch.empty(rows, cols // G, dtype=torch.float32, device=dev)
+        if want_qT and scaleT is None:
+            scaleT = torch.empty(cols, rows // G, dtype=torch.float32, device=dev)
+    elif mode == SCALE_COL_128x1:
+        scale = None
+        scaleT = scaleT if scaleT is not None else torch.empty(cols, rows // G, dtype=torch.float32, device=dev)
+    if not want_qT:
+        scaleT = None
+    return q, scale, qT, scaleT
+
+
+# ---------------------------------------------------- RMSNorm + quantise
+def rmsnorm_quantize_fp8(x, gamma, eps, fmt, mode=SCALE_TENSOR, rnd=SCALE_FP32, want_q=True, want_qT=False,
+                         out=None, ws=None):
+    """Quantise y = BF16(x * rstd * gamma) (RMSNorm of each row of x) without
+    writing y; returns dict(q, scale, qT, scaleT, rstd) with rstd [rows]
+    float32 (out may also supply "rstd")."""
+    rows, cols = x.shape
+    dev = x.device
+    q, scale, qT, scaleT = _quant_outputs(rows, cols, mode, want_q, want_qT, out, dev)
+    rstd = (out or {}).get("rstd")
+    if rstd is None:
+        rstd = torch.empty(rows, dtype=torch.float32, device=dev)
+    w, nb = _ws(lib().puro_rmsnorm_quantize_workspace_size(rows, cols), ws, dev)
+    _check("puro_rmsnorm_quantize_fp8", lib().puro_rmsnorm_quantize_fp8(
+        _ptr(x), _ptr(gamma), rows, cols, _ld(x), float(eps), fmt, mode, rnd, _ptr(q), _ptr(scale), _ptr(qT),
+        _ptr(scaleT), _ptr(rstd), _ptr(w), nb, _stream()))
+    return dict(q=q, scale=scale, qT=qT, scaleT=scaleT, rstd=rstd)
 
 
 # ----------------------------------------------------- SwiGLU + quantise

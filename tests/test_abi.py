@@ -202,3 +202,26 @@ def test_swiglu_quantize_validation(puro):
     # per-tensor without workspace for the amax pass
     assert f(FAKE, 4096, 4096, 8192, 0, 0, 0, FAKE, FAKE, None, None, FAKE, 0, None) == ERR_WORKSPACE
     assert L.puro_swiglu_quantize_workspace_size(4096, 4096) == L.puro_quantize_workspace_size(4096, 4096)
+
+
+def test_rmsnorm_quantize_validation(puro):
+    L = puro.lib()
+    f = L.puro_rmsnorm_quantize_fp8
+    big = 1 << 20
+    # x, gamma, rstd NULL
+    assert f(None, FAKE, 16, 128, 128, 1e-6, 0, 0, 0, FAKE, FAKE, None, None, FAKE, FAKE, big, None) == ERR_NULL
+    assert f(FAKE, None, 16, 128, 128, 1e-6, 0, 0, 0, FAKE, FAKE, None, None, FAKE, FAKE, big, None) == ERR_NULL
+    assert f(FAKE, FAKE, 16, 128, 128, 1e-6, 0, 0, 0, FAKE, FAKE, None, None, None, FAKE, big, None) == ERR_NULL
+    # misaligned gamma or rstd; cols % 16
+    assert f(FAKE, FAKE + 4, 16, 128, 128, 1e-6, 0, 0, 0, FAKE, FAKE, None, None, FAKE, FAKE, big, None) == ERR_ALIGN
+    assert f(FAKE, FAKE, 16, 128, 128, 1e-6, 0, 0, 0, FAKE, FAKE, None, None, FAKE + 4, FAKE, big, None) == ERR_ALIGN
+    assert f(FAKE, FAKE, 16, 24, 24, 1e-6, 0, 0, 0, FAKE, FAKE, None, None, FAKE, FAKE, big, None) == ERR_ALIGN
+    # eps negative or NaN; 128x128 blocks; a row without columns
+    assert f(FAKE, FAKE, 16, 128, 128, -1.0, 0, 0, 0, FAKE, FAKE, None, None, FAKE, FAKE, big, None) == ERR_UNSUPPORTED
+    assert f(FAKE, FAKE, 16, 128, 128, float("nan"), 0, 0, 0, FAKE, FAKE, None, None, FAKE, FAKE, big,
+             None) == ERR_UNSUPPORTED
+    assert f(FAKE, FAKE, 128, 128, 128, 1e-6, 0, 3, 1, FAKE, FAKE, None, None, FAKE, None, 0, None) == ERR_UNSUPPORTED
+    assert f(FAKE, FAKE, 16, 0, 0, 1e-6, 0, 0, 0, FAKE, FAKE, None, None, FAKE, FAKE, big, None) == ERR_SHAPE
+    # per-tensor without workspace
+    assert f(FAKE, FAKE, 4096, 1536, 1536, 1e-6, 0, 0, 0, FAKE, FAKE, None, None, FAKE, FAKE, 0, None) == ERR_WORKSPACE
+    assert L.puro_rmsnorm_quantize_workspace_size(8192, 1536) >= 2048 * 4 + 4
