@@ -26,6 +26,9 @@ Readings where the paper is silent (each restated in the design notes):
   the float64 evaluation; the quantisation of every accepted H is the
   quantisers' (``oracle.quant``).
 
+The backward (the gate/up projection's dY, quantised inside the op that
+produces it) follows below with readings of its own.
+
 Parity unpinned by the paper (it prints no SwiGLU values); pinned by the
 closed forms and library special cases in tests/test_oracle_swiglu.py.
 """
@@ -79,6 +82,55 @@ def swiglu_bf16_band(gu_bits, cols):
         lo = bf16.from_f64_rne(t - d)
         hi = bf16.from_f64_rne(t + d)
     return mid, lo, hi
+
+
+# ---- backward: the gate/up projection's output gradient --------------------
+#
+# Readings (the paper states no SwiGLU detail; Section 3.2 quantises each
+# GEMM's dY right before Dgrad and Wgrad):
+#
+# * From dH [R, C] and the saved gate/up output gu [R, 2C], the gradient of
+#   the gate/up output is dgu [R, 2C] = [dg | du] with
+#   dg = dH * u * silu'(g), du = dH * silu(g), silu'(g) = s (1 + g (1 - s)),
+#   s = 1 / (1 + e^-g); each evaluated in binary32 and rounded once to BF16.
+# * Accepted values: relative EPS as in the forward, plus for dg an absolute
+#   2**-20 * |dH * u|: silu' is a difference near its zero (g ~ -1.28),
+#   where a few binary32 ulps of its terms (about 1 in size) are not small
+#   against the result; plus the forward's allowances (2**-148 absolute, and
+#   zero where e^-g overflows, |dH| * max(1, |u|) * TINY).
+BWD_ABS = 2.0 ** -20
+
+
+def dsilu_f64(g):
+    """silu'(g) = s (1 + g (1 - s)) with s = 1 / (1 + e^-g), float64."""
+    g = np.asarray(g, dtype=np.float64)
+    with np.errstate(over="ignore", invalid="ignore"):
+        sg = 1.0 / (1.0 + np.exp(-g))
+        return sg * (1.0 + g * (1.0 - sg))
+
+
+def swiglu_bwd_f64(dh_bits, gu_bits, cols):
+    """[dg | du] [R, 2 cols] in float64."""
+    g, u = split(gu_bits, cols)
+    with np.errstate(invalid="ignore"):
+        dh = bf16.to_f32(np.asarray(dh_bits, dtype=np.uint16)[:, :cols]).astype(np.float64)
+    with np.errstate(over="ignore", invalid="ignore"):
+        return np.concatenate([dh * u * dsilu_f64(g), dh * silu_f64(g)], axis=1)
+
+
+def swiglu_bwd_bf16_band(dh_bits, gu_bits, cols):
+    """(mid, lo, hi) BF16 bit patterns of [dg | du] [R, 2 cols], as
+    ``swiglu_bf16_band`` states them for H."""
+    g, u = split(gu_bits, cols)
+    with np.errstate(invalid="ignore"):
+        dh = bf16.to_f32(np.asarray(dh_bits, dtype=np.uint16)[:, :cols]).astype(np.float64)
+    with np.errstate(over="ignore", invalid="ignore"):
+        t = swiglu_bwd_f64(dh_bits, gu_bits, cols)
+        deep = np.where(g < -87.0, TINY * np.abs(dh) * np.maximum(1.0, np.abs(u)), 0.0)
+        extra = np.concatenate([BWD_ABS * np.abs(dh * u) + deep, deep], axis=1)
+        d = EPS * np.abs(t) + 2.0 ** -148 + extra
+        d = np.where(np.isfinite(t), d, 0.0)
+        return bf16.from_f64_rne(t), bf16.from_f64_rne(t - d), bf16.from_f64_rne(t + d)
 
 
 def unique_mask(lo_bits, hi_bits):

@@ -121,3 +121,44 @@ def test_band_check_accepts_oracle_and_rejects_mistakes(axis, rule):
         q1 = q1T.T
     with pytest.raises(AssertionError):
         band_check.check(q1, s1, mid, lo, hi, un, fmt, rule, axis, "planted operand")
+
+
+def test_dsilu_identities_and_finite_differences():
+    g = np.linspace(-30, 30, 6001)
+    d = swiglu.dsilu_f64(g)
+    # d/dg [silu(g) - silu(-g)] = d/dg g = 1
+    assert np.all(np.abs(d + swiglu.dsilu_f64(-g) - 1.0) <= 1e-13)
+    assert swiglu.dsilu_f64(0.0) == 0.5
+    # central differences of the forward oracle
+    h = 1e-5
+    fd = (swiglu.silu_f64(g + h) - swiglu.silu_f64(g - h)) / (2 * h)
+    assert np.all(np.abs(fd - d) <= 1e-8)
+    assert swiglu.dsilu_f64(40.0) == 1.0 and abs(swiglu.dsilu_f64(-40.0)) < 1e-15
+    # silu' vanishes at the minimum of silu (g ~ -1.2785)
+    gg = np.linspace(-1.3, -1.25, 50001)
+    assert abs(gg[np.argmin(np.abs(swiglu.dsilu_f64(gg)))] + 1.27846) < 1e-4
+
+
+def test_backward_layout_and_band():
+    rng = np.random.default_rng(4)
+    R, C = 64, 128
+    gu = bits(rng.standard_normal((R, 2 * C)) * 1.7)
+    dh = bits(rng.standard_normal((R, C)) * 1e-3)
+    t = swiglu.swiglu_bwd_f64(dh, gu, C)
+    g, u = swiglu.split(gu, C)
+    dhf = bf16.to_f32(dh).astype(np.float64)
+    np.testing.assert_allclose(t[:, C:], dhf * g * expit(g), rtol=1e-14, atol=1e-300)
+    sg = expit(g)
+    np.testing.assert_allclose(t[:, :C], dhf * u * (sg + g * sg * (1 - sg)), rtol=1e-12, atol=1e-300)
+    mid, lo, hi = swiglu.swiglu_bwd_bf16_band(dh, gu, C)
+    assert mid.shape == (R, 2 * C)
+    lo_f, hi_f, mid_f = (bf16.to_f32(b) for b in (lo, hi, mid))
+    assert np.all(lo_f <= mid_f) and np.all(mid_f <= hi_f)
+    un = swiglu.unique_mask(lo, hi)
+    assert 0.9 < un.mean() < 1.0
+    # at the zero of silu' the absolute allowance covers binary32 ulps of its terms
+    gz = bits([[-1.28125]])                       # the BF16 value nearest the zero
+    m, l, h = swiglu.swiglu_bwd_bf16_band(bits([[1.0]]), np.concatenate([gz, bits([[1.0]])], axis=1), 1)
+    tz = swiglu.dsilu_f64(bf16.to_f32(gz).astype(np.float64))[0, 0]
+    assert abs(tz) < 2e-3
+    assert bf16.to_f32(l)[0, 0] <= tz - 2.0 ** -21 and bf16.to_f32(h)[0, 0] >= tz + 2.0 ** -21
