@@ -74,7 +74,7 @@ def cpu_baseline(tokens, reps):
 
 
 CALLS = ("quantize_x", "quantize_w", "fprop", "quantize_dy", "dgrad", "wgrad")
-SWIGLU_CALLS = ("swiglu_tensor", "swiglu_groups")
+SWIGLU_CALLS = ("swiglu_tensor", "swiglu_groups", "swiglu_bwd_groups")
 RMSNORM_CALLS = ("rmsnorm_tensor", "rmsnorm_groups")
 
 
@@ -124,7 +124,12 @@ def swiglu_workload(torch, puro, M=8192):
     128x1 power-of-two groups. Returns {name: (fused call, unfused call,
     algorithmic bytes)}; unfused is torch's BF16 silu and multiply, then
     puro_quantize_fp8 of the BF16 H. Algorithmic bytes: gate and up read
-    once (4 B per H element) and one byte per element for each of q and qT."""
+    once (4 B per H element) and one byte per element for each of q and qT.
+    Also the backward (swiglu_bwd_groups): dgu [M, 17920] from dH [M, 8960]
+    and the gate/up output, 1x128 + 128x1 groups; unfused is torch's binary32
+    arithmetic of the same formulas into a BF16 dgu, then puro_quantize_fp8.
+    Its algorithmic bytes: dH, g and u read once (6 B per dH element) and q,
+    qT of both halves written (4 B)."""
     from paper_2608_27370_amd import inputs
     F = inputs.MLP
     dev = torch.device("cuda", 0)
@@ -145,7 +150,26 @@ def swiglu_workload(torch, puro, M=8192):
             puro.quantize_fp8(Hbuf, E4, mode=mode, rnd=rnd, want_qT=True, out=out, ws=ws)
         return fn
     nbytes = M * F * 6.0
+    dh = (torch.randn(M, F, generator=g, device=dev) * 1e-3).to(torch.bfloat16)
+    dgu = torch.empty(M, 2 * F, dtype=torch.bfloat16, device=dev)
+    bs = {"q": torch.empty(M, 2 * F, dtype=torch.uint8, device=dev),
+          "qT": torch.empty(2 * F, M, dtype=torch.uint8, device=dev),
+          "scale": torch.empty(M, 2 * F // 128, dtype=torch.float32, device=dev),
+          "scaleT": torch.empty(2 * F, M // 128, dtype=torch.float32, device=dev)}
+    wsb = torch.empty(max(1, puro.lib().puro_swiglu_bwd_quantize_workspace_size(M, F),
+                          puro.lib().puro_quantize_workspace_size(M, 2 * F)), dtype=torch.uint8, device=dev)
+
+    def unfused_bwd():
+        gg, uu = gu[:, :F].float(), gu[:, F:].float()
+        sg = torch.sigmoid(gg)
+        dhf = dh.float()
+        dgu[:, :F] = dhf * uu * (sg * (1.0 + gg * (1.0 - sg)))
+        dgu[:, F:] = dhf * gg * sg
+        puro.quantize_fp8(dgu, E4, mode=puro.SCALE_ROW_1x128, rnd=puro.SCALE_POW2, want_qT=True, out=bs, ws=wsb)
     return {
+        "swiglu_bwd_groups": (lambda: puro.swiglu_bwd_quantize_fp8(dh, gu, E4, puro.SCALE_ROW_1x128, puro.SCALE_POW2,
+                                                                   want_qT=True, out=bs, ws=wsb),
+                              unfused_bwd, M * F * 10.0),
         "swiglu_tensor": (lambda: puro.swiglu_quantize_fp8(gu, F, E4, puro.SCALE_TENSOR, puro.SCALE_FP32,
                                                            want_qT=True, out=ts, ws=ws),
                           unfused(puro.SCALE_TENSOR, puro.SCALE_FP32, ts), nbytes),

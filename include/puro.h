@@ -153,6 +153,34 @@ puro_status puro_swiglu_quantize_fp8(const uint16_t* gu, int64_t rows, int64_t c
                                      uint8_t* q, float* scale, uint8_t* qT, float* scaleT, void* ws,
                                      size_t ws_bytes, hipStream_t stream);
 
+/* ---------------------------------------- SwiGLU backward + quantise ---
+ * The gate/up projection's Dgrad and Wgrad take the gradient of its output
+ * quantised (Section 3.2); that gradient is the SwiGLU's backward. From dH
+ * [rows, cols] (the down projection's Dgrad output; row pitch ld_dh) and
+ * the saved gate/up output gu [rows, 2 cols] (gate = columns [0, cols), up =
+ * columns [cols, 2 cols); row pitch ld_gu) this call forms dgu [rows,
+ * 2 cols] = [dg | du] with dg = dH * u * silu'(g), silu'(g) = s (1 + g (1 - s)),
+ * s = 1 / (1 + e^-g), and du = dH * silu(g), each in binary32 rounded once to
+ * BF16, and quantises dgu exactly as puro_quantize_fp8 would quantise a BF16
+ * tensor holding it, without writing it: q [rows, 2 cols] for Dgrad and the
+ * transposed qT [2 cols, rows] for Wgrad.
+ *
+ * Modes: TENSOR (q and/or qT; scale[0]; rnd FP32, POW2 or POW2_FLOOR),
+ * ROW_1x128 (q, scale [rows, 2 cols / 128] and optionally the 128x1
+ * column-grouped qT, scaleT) and COL_128x1 (qT, scaleT); BLOCK_128x128
+ * returns PURO_ERR_UNSUPPORTED.
+ *
+ * Requirements: dH [rows, cols] and gu [rows, 2 cols] meet puro_quantize_fp8's
+ * requirements for x; cols % 8 == 0 (2 cols % 16 == 0); the grouped
+ * dimension(s) of dgu % 128 == 0. ws: puro_swiglu_bwd_quantize_workspace_size
+ * (rows, cols) bytes (used in TENSOR mode). All pointers are device memory
+ * owned by the caller; nothing is allocated or synchronised. */
+size_t puro_swiglu_bwd_quantize_workspace_size(int64_t rows, int64_t cols);
+puro_status puro_swiglu_bwd_quantize_fp8(const uint16_t* dh, int64_t ld_dh, const uint16_t* gu, int64_t ld_gu,
+                                         int64_t rows, int64_t cols, puro_fp8_format fmt, puro_scale_mode mode,
+                                         puro_scale_rounding rnd, uint8_t* q, float* scale, uint8_t* qT,
+                                         float* scaleT, void* ws, size_t ws_bytes, hipStream_t stream);
+
 /* ------------------------------------------------ RMSNorm + quantise ---
  * Every attention and MLP block of the paper's model (the Qwen3-1.7B
  * architecture, Section 2) starts with an RMSNorm whose output is the input

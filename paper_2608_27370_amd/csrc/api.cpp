@@ -97,10 +97,13 @@ namespace {
 // 2 cols]; or the RMSNorm y = BF16(x * rstd * gamma) of x [rows, cols], whose
 // per-row rstd is written too.
 struct Source {
-    enum Kind { kBf16, kSwiglu, kRmsnorm } kind = kBf16;
+    enum Kind { kBf16, kSwiglu, kRmsnorm, kSwigluBwd } kind = kBf16;
     const uint16_t* gamma = nullptr;
     float* rstd = nullptr;
     float eps = 0.0f;
+    // the SwiGLU backward's saved gate/up output (x is then dH)
+    const uint16_t* gu = nullptr;
+    int64_t ld_gu = 0;
 };
 
 puro_status quantize_impl(const uint16_t* x, int64_t rows, int64_t cols, int64_t ld, puro_fp8_format fmt,
@@ -108,10 +111,17 @@ puro_status quantize_impl(const uint16_t* x, int64_t rows, int64_t cols, int64_t
                           float* scale, uint8_t* qT, float* scaleT, void* ws, size_t ws_bytes, int kmajor,
                           hipStream_t stream, Source src = Source()) {
     const bool swiglu = src.kind == Source::kSwiglu, rms = src.kind == Source::kRmsnorm;
+    const bool bwd = src.kind == Source::kSwigluBwd;
     if (cols < 0) return PURO_ERR_SHAPE;
-    puro_status st = check_bf16_matrix(x, rows, swiglu ? 2 * cols : cols, ld);
+    // x's columns: 2 cols for the SwiGLU's gate/up input, cols / 2 for the backward's dH
+    puro_status st = check_bf16_matrix(x, rows, swiglu ? 2 * cols : (bwd ? cols / 2 : cols), ld);
     if (st != PURO_OK) return st;
-    if ((swiglu || rms) && (amax_in || mode == PURO_SCALE_BLOCK_128x128)) return PURO_ERR_UNSUPPORTED;
+    if (bwd) {
+        st = check_bf16_matrix(src.gu, rows, cols, src.ld_gu);
+        if (st != PURO_OK) return st;
+        if (src.ld_gu >= ((int64_t)1 << 23)) return PURO_ERR_SHAPE;
+    }
+    if ((swiglu || rms || bwd) && (amax_in || mode == PURO_SCALE_BLOCK_128x128)) return PURO_ERR_UNSUPPORTED;
     if (rms) {
         // a row needs its columns (the mean of an empty row is undefined)
         if (rows > 0 && cols == 0) return PURO_ERR_SHAPE;
@@ -135,6 +145,8 @@ puro_status quantize_impl(const uint16_t* x, int64_t rows, int64_t cols, int64_t
     a.kmajor = kmajor;
     a.gamma = src.gamma;
     a.rstd = src.rstd;
+    a.x2 = src.gu;
+    a.ld2 = src.ld_gu;
     // outputs of an empty tensor are never written (torch hands out NULL for them)
     const bool empty = rows == 0 || cols == 0;
     int qmode;
@@ -177,6 +189,16 @@ puro_status quantize_impl(const uint16_t* x, int64_t rows, int64_t cols, int64_t
         launch_rmsnorm_quantize(fmt, qmode, a, src.eps, ws, stream);
         return launched();
     }
+    if (bwd) {
+        if (qmode == kQTensor) {
+            if (!ws) return PURO_ERR_NULL;
+            if (ws_bytes < swiglu_bwd_ws_bytes(rows, cols)) return PURO_ERR_WORKSPACE;
+        } else if (empty) {
+            return PURO_OK;
+        }
+        launch_swiglu_bwd_quantize(fmt, qmode, a, ws, stream);
+        return launched();
+    }
     if (qmode == kQTensor && !amax_in) {
         if (!ws) return PURO_ERR_NULL;
         if (ws_bytes < quant_tensor_ws_bytes(rows, cols)) return PURO_ERR_WORKSPACE;
@@ -215,6 +237,25 @@ puro_status puro_swiglu_quantize_fp8(const uint16_t* gu, int64_t rows, int64_t c
     src.kind = Source::kSwiglu;
     return quantize_impl(gu, rows, cols, ld, fmt, mode, rnd, nullptr, q, scale, qT, scaleT, ws, ws_bytes, 0,
                          stream, src);
+}
+
+// ------------------------------------------- SwiGLU backward + quantise
+size_t puro_swiglu_bwd_quantize_workspace_size(int64_t rows, int64_t cols) {
+    if (rows < 0 || cols < 0) return 0;
+    return swiglu_bwd_ws_bytes(rows, 2 * cols);
+}
+
+puro_status puro_swiglu_bwd_quantize_fp8(const uint16_t* dh, int64_t ld_dh, const uint16_t* gu, int64_t ld_gu,
+                                         int64_t rows, int64_t cols, puro_fp8_format fmt, puro_scale_mode mode,
+                                         puro_scale_rounding rnd, uint8_t* q, float* scale, uint8_t* qT,
+                                         float* scaleT, void* ws, size_t ws_bytes, hipStream_t stream) {
+    if (cols < 0 || cols > ((int64_t)1 << 30)) return PURO_ERR_SHAPE;
+    Source src;
+    src.kind = Source::kSwigluBwd;
+    src.gu = gu;
+    src.ld_gu = ld_gu;
+    return quantize_impl(dh, rows, 2 * cols, ld_dh, fmt, mode, rnd, nullptr, q, scale, qT, scaleT, ws, ws_bytes,
+                         0, stream, src);
 }
 
 // --------------------------------------------------- RMSNorm + quantise

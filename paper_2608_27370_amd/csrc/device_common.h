@@ -68,6 +68,15 @@ __device__ __forceinline__ void swiglu8(const uint32_t g[4], const uint32_t u[4]
         h[i] = pack_bf16x2(swiglu1(bf16lo(g[i]), bf16lo(u[i])), swiglu1(bf16hi(g[i]), bf16hi(u[i])));
 }
 
+// The SwiGLU's backward for one element in binary32: from dH and the saved
+// gate g and up u, dg = dH * u * silu'(g) with silu'(g) = s (1 + g (1 - s)),
+// s = 1 / (1 + e^-g) (the reciprocal instruction), or du = dH * silu(g) =
+// dH * g * s.
+__device__ __forceinline__ float swiglu_bwd1(float dh, float g, float u, bool dg) {
+    const float sg = __builtin_amdgcn_rcpf(1.0f + exp_f32(-g));
+    return dg ? dh * u * (sg * fmaf(g, 1.0f - sg, 1.0f)) : dh * (g * sg);
+}
+
 // Eight RMSNorm outputs, BF16 (round to nearest even): x * r * gamma in
 // binary32 from four words of x, the row's r = rstd and four words of gamma.
 __device__ __forceinline__ void rmsnorm8(const uint32_t x[4], float r, const uint32_t g[4], uint32_t y[4]) {

@@ -53,6 +53,10 @@ struct QuantArgs {
     // and the norm's weight, BF16 [cols]
     const float* rstd;
     const uint16_t* gamma;
+    // SwiGLU backward source: the saved gate/up output [rows, cols] (x is
+    // then dH [rows, cols / 2]) and its row pitch
+    const uint16_t* x2;
+    int64_t ld2;
 };
 
 // Workspace of a per-tensor quantisation that computes its own amax.
@@ -76,6 +80,13 @@ void launch_quantize(int fmt, int mode, const QuantArgs& a, hipStream_t stream, 
 // rmsnorm_ws_bytes(rows) bytes (the per-tensor partial maxima).
 size_t rmsnorm_ws_bytes(int64_t rows);
 void launch_rmsnorm_quantize(int fmt, int mode, QuantArgs a, float eps, void* ws, hipStream_t stream);
+
+// SwiGLU backward + quantise: the gate/up output's gradient [dg | du]
+// [rows, cols] (dg = dH u silu'(g), du = dH silu(g), BF16) from a.x = dH
+// [rows, cols / 2] and a.x2 = the gate/up output [rows, cols], quantised in
+// `mode` (kQTensor, kQRow or kQCol). ws holds swiglu_bwd_ws_bytes bytes.
+size_t swiglu_bwd_ws_bytes(int64_t rows, int64_t cols);
+void launch_swiglu_bwd_quantize(int fmt, int mode, QuantArgs a, void* ws, hipStream_t stream);
 
 // ---- GEMM (gemm.hip) ----------------------------------------------------------
 

@@ -55,9 +55,11 @@ __device__ __forceinline__ uint32_t block_max(uint32_t v, uint32_t* red) {
 // Sources of the values a pass reads: the BF16 tensor itself; the SwiGLU of a
 // fused gate/up output [rows, 2 cols] (gate = columns [0, cols), up =
 // columns [cols, 2 cols)), rounded to BF16 as the tensor H = silu(gate) * up
-// would hold it; or the RMSNorm y = x * rstd * gamma of x [rows, cols],
-// rounded to BF16 (rstd per row from the row pass, gamma per column).
-enum : int { kSrcBf16 = 0, kSrcSwiglu = 1, kSrcRmsnorm = 2 };
+// would hold it; the RMSNorm y = x * rstd * gamma of x [rows, cols],
+// rounded to BF16 (rstd per row from the row pass, gamma per column); or the
+// SwiGLU's backward [dg | du] [rows, cols] from dH [rows, cols / 2] and the
+// saved gate/up output, rounded to BF16.
+enum : int { kSrcBf16 = 0, kSrcSwiglu = 1, kSrcRmsnorm = 2, kSrcSwigluBwd = 3 };
 
 // Partial maxima of one or two tensors in one launch: blocks [0, j0.P) cover
 // the rows of the first tensor in P contiguous ranges, the rest the second.
@@ -205,7 +207,44 @@ constexpr uint32_t kOOB = 0x80000000u;   // an offset beyond every descriptor's 
 // the SwiGLU source each value is computed from the gate and up values at the
 // same position of the two halves of a row (zeros outside give silu(0) * 0 = 0).
 template <int SRC>
+__device__ __forceinline__ void load_8x8(const QuantArgs& a, const Tile& t, uint32_t w[8][4]);
+
+// The SwiGLU backward source: the thread's 8 columns of [dg | du] come from
+// the same 8 columns c of dH and of the gate half (g), and for dg of the up
+// half (u, columns F + c); a chunk never straddles F = cols / 2 (F % 8 == 0).
+__device__ __forceinline__ void load_swiglu_bwd_8x8(const QuantArgs& a, const Tile& t, uint32_t w[8][4]) {
+    const int64_t F = a.cols / 2;
+    const int64_t tr0 = t.row0 - t.rg * 8;
+    const int64_t vr = a.cols == 0 ? 0 : max((int64_t)0, min((int64_t)kTile, a.rows - tr0));
+    const uint32_t bh = vr == 0 ? 0u : (uint32_t)(((vr - 1) * a.ld + F) * 2);
+    const uint32_t bg = vr == 0 ? 0u : (uint32_t)(((vr - 1) * a.ld2 + 2 * F) * 2);
+    const __amdgpu_buffer_rsrc_t rh = buffer_rsrc(vr == 0 ? a.x : a.x + tr0 * a.ld, bh);
+    const __amdgpu_buffer_rsrc_t rg = buffer_rsrc(vr == 0 ? a.x2 : a.x2 + tr0 * a.ld2, bg);
+    const bool dg = t.col < F;
+    const int64_t c = dg ? t.col : t.col - F;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        const int64_t r = t.rg * 8 + i;
+        const v4i h = __builtin_amdgcn_raw_buffer_load_b128(rh, t.col_ok ? (uint32_t)((r * a.ld + c) * 2) : kOOB, 0, 0);
+        const v4i g = __builtin_amdgcn_raw_buffer_load_b128(rg, t.col_ok ? (uint32_t)((r * a.ld2 + c) * 2) : kOOB, 0, 0);
+        const v4i u = __builtin_amdgcn_raw_buffer_load_b128(
+            rg, (t.col_ok && dg) ? (uint32_t)((r * a.ld2 + F + c) * 2) : kOOB, 0, 0);
+        const uint32_t hw[4] = {(uint32_t)h.x, (uint32_t)h.y, (uint32_t)h.z, (uint32_t)h.w};
+        const uint32_t gw[4] = {(uint32_t)g.x, (uint32_t)g.y, (uint32_t)g.z, (uint32_t)g.w};
+        const uint32_t uw[4] = {(uint32_t)u.x, (uint32_t)u.y, (uint32_t)u.z, (uint32_t)u.w};
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            w[i][j] = pack_bf16x2(swiglu_bwd1(bf16lo(hw[j]), bf16lo(gw[j]), bf16lo(uw[j]), dg),
+                                  swiglu_bwd1(bf16hi(hw[j]), bf16hi(gw[j]), bf16hi(uw[j]), dg));
+    }
+}
+
+template <int SRC>
 __device__ __forceinline__ void load_8x8(const QuantArgs& a, const Tile& t, uint32_t w[8][4]) {
+    if constexpr (SRC == kSrcSwigluBwd) {
+        load_swiglu_bwd_8x8(a, t, w);
+        return;
+    }
     const int64_t tr0 = t.row0 - t.rg * 8;                        // the tile's first row
     const int64_t vr = a.cols == 0 ? 0 : max((int64_t)0, min((int64_t)kTile, a.rows - tr0));
     // rows tr0 .. tr0 + vr - 1: the last one ends at column cols (2 cols with the SwiGLU source)
@@ -390,6 +429,22 @@ __device__ __forceinline__ float tensor_amax(const QuantArgs& a, const PartialSh
     for (int u = 0; u < kMaxInlinePartials / kThreads; ++u) m = max(m, p.v[u]);
     m = block_max(m, red);
     return __uint_as_float(m << 16);
+}
+
+// Partial maxima of a source's values, one per 128x128 tile (1-D grid over
+// the tiles, row-major): the amax pass of a per-tensor quantisation whose
+// values are formed from several inputs.
+template <int SRC>
+__global__ __launch_bounds__(kThreads) void tile_amax_kernel(QuantArgs a, int gx, uint32_t* partial) {
+    __shared__ uint32_t red[4];
+    const Tile t = tile_coords(a.cols, (int)blockIdx.x % gx, (int)blockIdx.x / gx);
+    uint32_t w[8][4];
+    load_8x8<SRC>(a, t, w);
+    uint32_t m = 0;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) m = max(m, absmax_bits8(w[i]));
+    m = block_max(m, red);
+    if (threadIdx.x == 0) partial[blockIdx.x] = m;
 }
 
 // Per-tensor quantisation of one or two tensors in one launch (1-D grid:
@@ -709,6 +764,26 @@ void launch_rmsnorm_quantize(int fmt, int mode, QuantArgs a, float eps, void* ws
     if (mode == kQTensor) amax_source(a, (int)P, ws, stream);
     if (fmt == kE4M3) launch_quantize_fmt<kE4M3, kSrcRmsnorm>(mode, a, stream);
     else launch_quantize_fmt<kE5M2, kSrcRmsnorm>(mode, a, stream);
+}
+
+size_t swiglu_bwd_ws_bytes(int64_t rows, int64_t cols) {
+    const int64_t P = tiles_x(cols) * tiles_y(rows);
+    return ((size_t)P * sizeof(uint32_t) + 255) / 256 * 256 + sizeof(float);
+}
+
+void launch_swiglu_bwd_quantize(int fmt, int mode, QuantArgs a, void* ws, hipStream_t stream) {
+    if (mode == kQTensor) {
+        const int64_t gx = tiles_x(a.cols), P = gx * tiles_y(a.rows);
+        if (a.rows > 0 && a.cols > 0) {
+            tile_amax_kernel<kSrcSwigluBwd><<<(unsigned)P, kThreads, 0, stream>>>(a, (int)gx,
+                                                                                 reinterpret_cast<uint32_t*>(ws));
+            amax_source(a, (int)P, ws, stream);
+        } else {
+            amax_source(a, 0, ws, stream);
+        }
+    }
+    if (fmt == kE4M3) launch_quantize_fmt<kE4M3, kSrcSwigluBwd>(mode, a, stream);
+    else launch_quantize_fmt<kE5M2, kSrcSwigluBwd>(mode, a, stream);
 }
 
 }  // namespace puro

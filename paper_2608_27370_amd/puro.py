@@ -57,6 +57,8 @@ _SIGS = {
     "puro_quantize_fp8": (_i, [_p, _i64, _i64, _i64, _i, _i, _i, _p, _p, _p, _p, _p, _p, _sz, _p]),
     "puro_swiglu_quantize_workspace_size": (_sz, [_i64, _i64]),
     "puro_swiglu_quantize_fp8": (_i, [_p, _i64, _i64, _i64, _i, _i, _i, _p, _p, _p, _p, _p, _sz, _p]),
+    "puro_swiglu_bwd_quantize_workspace_size": (_sz, [_i64, _i64]),
+    "puro_swiglu_bwd_quantize_fp8": (_i, [_p, _i64, _p, _i64, _i64, _i64, _i, _i, _i, _p, _p, _p, _p, _p, _sz, _p]),
     "puro_rmsnorm_quantize_workspace_size": (_sz, [_i64, _i64]),
     "puro_rmsnorm_quantize_fp8": (_i, [_p, _p, _i64, _i64, _i64, ctypes.c_float, _i, _i, _i, _p, _p, _p, _p, _p,
                                        _p, _sz, _p]),
@@ -206,6 +208,23 @@ def _quant_outputs(rows, cols, mode, want_q, want_qT, out, dev):
     if not want_qT:
         scaleT = None
     return q, scale, qT, scaleT
+
+
+# -------------------------------------------- SwiGLU backward + quantise
+def swiglu_bwd_quantize_fp8(dh, gu, fmt, mode=SCALE_TENSOR, rnd=SCALE_FP32, want_q=True, want_qT=False,
+                            out=None, ws=None):
+    """Quantise dgu = [dH u silu'(g) | dH silu(g)] [rows, 2 cols] from dH
+    [rows, cols] and the saved gate/up output gu [rows, 2 cols] without
+    writing dgu; returns dict(q, scale, qT, scaleT)."""
+    rows, cols = dh.shape
+    assert gu.shape[0] == rows and gu.shape[1] >= 2 * cols
+    dev = dh.device
+    q, scale, qT, scaleT = _quant_outputs(rows, 2 * cols, mode, want_q, want_qT, out, dev)
+    w, nb = _ws(lib().puro_swiglu_bwd_quantize_workspace_size(rows, cols), ws, dev)
+    _check("puro_swiglu_bwd_quantize_fp8", lib().puro_swiglu_bwd_quantize_fp8(
+        _ptr(dh), _ld(dh), _ptr(gu), _ld(gu), rows, cols, fmt, mode, rnd, _ptr(q), _ptr(scale), _ptr(qT),
+        _ptr(scaleT), _ptr(w), nb, _stream()))
+    return dict(q=q, scale=scale, qT=qT, scaleT=scaleT)
 
 
 # ---------------------------------------------------- RMSNorm + quantise

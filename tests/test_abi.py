@@ -225,3 +225,21 @@ def test_rmsnorm_quantize_validation(puro):
     # per-tensor without workspace
     assert f(FAKE, FAKE, 4096, 1536, 1536, 1e-6, 0, 0, 0, FAKE, FAKE, None, None, FAKE, FAKE, 0, None) == ERR_WORKSPACE
     assert L.puro_rmsnorm_quantize_workspace_size(8192, 1536) >= 2048 * 4 + 4
+
+
+def test_swiglu_bwd_quantize_validation(puro):
+    L = puro.lib()
+    f = L.puro_swiglu_bwd_quantize_fp8
+    big = 1 << 20
+    # dH or gu NULL; gu's pitch shorter than its two halves
+    assert f(None, 128, FAKE, 256, 16, 128, 0, 0, 0, FAKE, FAKE, None, None, FAKE, big, None) == ERR_NULL
+    assert f(FAKE, 128, None, 256, 16, 128, 0, 0, 0, FAKE, FAKE, None, None, FAKE, big, None) == ERR_NULL
+    assert f(FAKE, 128, FAKE, 200, 16, 128, 0, 0, 0, FAKE, FAKE, None, None, FAKE, big, None) == ERR_SHAPE
+    # cols % 8, misaligned gu
+    assert f(FAKE, 12, FAKE, 24, 16, 12, 0, 0, 0, FAKE, FAKE, None, None, FAKE, big, None) == ERR_ALIGN
+    assert f(FAKE, 128, FAKE + 8, 256, 16, 128, 0, 0, 0, FAKE, FAKE, None, None, FAKE, big, None) == ERR_ALIGN
+    # 128x128 blocks; 1x128 groups need 2 cols % 128
+    assert f(FAKE, 128, FAKE, 256, 128, 128, 0, 3, 1, FAKE, FAKE, None, None, None, 0, None) == ERR_UNSUPPORTED
+    assert f(FAKE, 96, FAKE, 192, 128, 96, 0, 1, 1, FAKE, FAKE, None, None, None, 0, None) == ERR_ALIGN
+    # per-tensor without workspace
+    assert f(FAKE, 4096, FAKE, 8192, 4096, 4096, 0, 0, 0, FAKE, FAKE, None, None, FAKE, 0, None) == ERR_WORKSPACE
