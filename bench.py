@@ -465,6 +465,27 @@ def run_suite(args):
     torch.cuda.empty_cache()
     # the MLP's SwiGLU fused with the down projection's input quantisation,
     # and the RMSNorm fused with the QKV projection's
+    # the BF16 epilogues: QKV's bias, the O projection's residual add (in place)
+    for name, (M, N, K), bias, resid in (("qkv_fprop_bias_m8192", (8192, Q, H), True, False),
+                                         ("o_fprop_residual_m8192", (8192, H, H), False, True)):
+        xq = S.normal((M, K)).view(torch.uint8)[:, :K].contiguous() & 0x77      # finite E4M3 codes
+        wq = S.normal((N, K)).view(torch.uint8)[:, :K].contiguous() & 0x77
+        one = torch.ones(1, dtype=torch.float32, device=S.dev)
+        A, B = puro.operand(xq, E4, puro.SCALE_TENSOR, one), puro.operand(wq, E4, puro.SCALE_TENSOR, one)
+        b = S.normal((N,)) if bias else None
+        r = S.normal((M, N)) if resid else None
+        D = torch.empty(M, N, dtype=torch.bfloat16, device=S.dev)
+        ws = torch.empty(max(1, puro.fp8_gemm_workspace_size(M, N, K, puro.OUT_BF16)), dtype=torch.uint8, device=S.dev)
+        if resid:
+            fused = lambda: puro.fp8_gemm_epilogue(A, M, B, N, K, residual=r, D=r, ws=ws)
+            unfused = lambda: r.add_(puro.fp8_gemm(A, M, B, N, K, puro.OUT_BF16, D=D, ws=ws))
+        else:
+            fused = lambda: puro.fp8_gemm_epilogue(A, M, B, N, K, bias=b, D=D, ws=ws)
+            unfused = lambda: puro.fp8_gemm(A, M, B, N, K, puro.OUT_BF16, D=D, ws=ws).add_(b)
+        us_f, us_u = S.time_us(fused, 50), S.time_us(unfused, 50)
+        print(json.dumps({"workload": name, "fused_us": round(us_f, 2), "unfused_us": round(us_u, 2),
+                          "fused_over_unfused": round(us_u / us_f, 3),
+                          "fused_tflops": round(2.0 * M * N * K / us_f / 1e6, 1)}), flush=True)
     work = dict(("mlp_%s_m8192" % k, v) for k, v in swiglu_workload(torch, puro).items())
     work.update(("qkv_input_%s_m8192" % k, v) for k, v in rmsnorm_workload(torch, puro).items())
     for name, (fused, unfused, nbytes) in work.items():

@@ -258,6 +258,21 @@ puro_status puro_fp8_gemm(int64_t M, int64_t N, int64_t K,
                           void* D, puro_out_dtype d_type, int64_t ldd, int accumulate,
                           void* ws, size_t ws_bytes, hipStream_t stream);
 
+/* GEMM with the BF16 bias / residual epilogue of the linear layers around
+ * the FP8 GEMMs: D = BF16(alpha * acc + bias[n] + residual[m, n]), the sum
+ * in binary32 and one rounding (BF16 output only; either term may be NULL).
+ * Qwen2's QKV projection carries a bias, and the attention output and MLP
+ * down projections add into the residual stream, which stays BF16 (Appendix
+ * C precision flow): fusing the add removes a BF16 read and write of Y.
+ * bias: BF16 [N], 16-byte aligned. residual: BF16 [M, N] with row pitch
+ * ldr >= N, ldr % 4 == 0, 16-byte aligned; it may be D itself (ldr == ldd,
+ * an in-place residual add) but must not otherwise overlap D. Operands,
+ * scales, workspace and errors as puro_fp8_gemm; accumulate is not offered. */
+puro_status puro_fp8_gemm_epilogue(int64_t M, int64_t N, int64_t K, const puro_fp8_operand* A,
+                                   const puro_fp8_operand* B, uint16_t* D, int64_t ldd, const uint16_t* bias,
+                                   const uint16_t* residual, int64_t ldr, void* ws, size_t ws_bytes,
+                                   hipStream_t stream);
+
 /* -------------------------------------------------------- linear layer ---
  * Y = X W^T with X [M, K] and W [N, K] in BF16 (dense rows), and its backward
  * pass, as a sequence of the calls above (Section 3.2; Appendix C).

@@ -107,6 +107,24 @@ def gemm_entries(ms, ns, a, a_fmt, a_scale, a_mode, b, b_fmt, b_scale, b_mode):
     return ref, den
 
 
+def epilogue(ref, den, bias=None, residual=None):
+    """The BF16 bias / residual epilogue of a linear layer's GEMM (the bias
+    of Qwen2's QKV projection; the residual stream the attention output and
+    MLP down projections add into, BF16 per the Appendix C precision flow):
+    the exact value ref + bias + residual, and its tolerance scale
+    den + |bias| + |residual| (every binary32 addition of the epilogue rounds
+    by at most 2**-24 of the magnitudes summed). bias and residual are
+    float64 values broadcast against ref (None: absent)."""
+    ref = np.asarray(ref, dtype=np.float64)
+    den = np.asarray(den, dtype=np.float64)
+    for t in (bias, residual):
+        if t is not None:
+            t = np.asarray(t, dtype=np.float64)
+            ref = ref + t
+            den = den + np.abs(t)
+    return ref, den
+
+
 def _scale_of(scale, mode, i, kb):
     s = np.asarray(scale, dtype=np.float32)
     if mode == "tensor":

@@ -326,9 +326,11 @@ static puro_status check_operand(const puro_fp8_operand* o, int64_t rows, int64_
 namespace {
 
 // puro_fp8_gemm with a choice of grouped-scale layout per operand.
+// bias / residual: the BF16 epilogue (both NULL: none).
 puro_status gemm_impl(int64_t M, int64_t N, int64_t K, const puro_fp8_operand* A, const puro_fp8_operand* B,
                       void* D, puro_out_dtype d_type, int64_t ldd, int accumulate, void* ws, size_t ws_bytes,
-                      int a_kmajor, int b_kmajor, hipStream_t stream) {
+                      int a_kmajor, int b_kmajor, hipStream_t stream, const uint16_t* bias = nullptr,
+                      const uint16_t* residual = nullptr, int64_t ldr = 0) {
     if (M < 0 || N < 0 || K < 0) return PURO_ERR_SHAPE;
     if (M > INT32_MAX / 2 || N > INT32_MAX / 2 || K > INT32_MAX / 2) return PURO_ERR_SHAPE;
     int sa = 0, sb = 0;
@@ -342,7 +344,21 @@ puro_status gemm_impl(int64_t M, int64_t N, int64_t K, const puro_fp8_operand* A
     if (M == 0 || N == 0) return PURO_OK;
     if (!D) return PURO_ERR_NULL;
     if ((ldd % 4) != 0 || !aligned16(D)) return PURO_ERR_ALIGN;
-    const int out = d_type == PURO_OUT_FP32 ? kOutF32 : kOutBF16;
+    const bool epi = bias || residual;
+    if (epi) {
+        if (d_type != PURO_OUT_BF16 || accumulate) return PURO_ERR_UNSUPPORTED;
+        if (bias && !aligned16(bias)) return PURO_ERR_ALIGN;
+        if (residual && (ldr < N)) return PURO_ERR_SHAPE;
+        if (residual && (!aligned16(residual) || (ldr % 4) != 0)) return PURO_ERR_ALIGN;
+        // the residual may be D itself (an in-place residual add), but not overlap it otherwise
+        if (residual && residual != D) {
+            const uintptr_t r0 = (uintptr_t)residual, r1 = r0 + (uintptr_t)(((M - 1) * ldr + N) * 2);
+            const uintptr_t d0 = (uintptr_t)D, d1 = d0 + (uintptr_t)(((M - 1) * ldd + N) * 2);
+            if (r0 < d1 && d0 < r1) return PURO_ERR_SHAPE;
+        }
+        if (residual == D && ldr != ldd) return PURO_ERR_SHAPE;
+    }
+    const int out = d_type == PURO_OUT_FP32 ? kOutF32 : (epi ? kOutBF16Epi : kOutBF16);
     const size_t need = gemm_workspace_bytes(M, N, K, out);
     if (need > 0 && !ws) return PURO_ERR_NULL;
     if (ws_bytes < need) return PURO_ERR_WORKSPACE;
@@ -352,6 +368,7 @@ puro_status gemm_impl(int64_t M, int64_t N, int64_t K, const puro_fp8_operand* A
     g.B = B->data; g.ldb = B->ld; g.fb = B->fmt; g.sb_mode = sb; g.sb = B->scale;
     g.D = D; g.ldd = ldd; g.out = out; g.accumulate = accumulate != 0;
     g.sa_kmajor = a_kmajor; g.sb_kmajor = b_kmajor;
+    g.bias = bias; g.residual = residual; g.ldr = ldr;
     launch_gemm(g, ws, stream);
     return launched();
 }
@@ -364,6 +381,13 @@ puro_status puro_fp8_gemm(int64_t M, int64_t N, int64_t K, const puro_fp8_operan
                           const puro_fp8_operand* B, void* D, puro_out_dtype d_type, int64_t ldd,
                           int accumulate, void* ws, size_t ws_bytes, hipStream_t stream) {
     return gemm_impl(M, N, K, A, B, D, d_type, ldd, accumulate, ws, ws_bytes, 0, 0, stream);
+}
+
+puro_status puro_fp8_gemm_epilogue(int64_t M, int64_t N, int64_t K, const puro_fp8_operand* A,
+                                   const puro_fp8_operand* B, uint16_t* D, int64_t ldd, const uint16_t* bias,
+                                   const uint16_t* residual, int64_t ldr, void* ws, size_t ws_bytes,
+                                   hipStream_t stream) {
+    return gemm_impl(M, N, K, A, B, D, PURO_OUT_BF16, ldd, 0, ws, ws_bytes, 0, 0, stream, bias, residual, ldr);
 }
 
 // ----------------------------------------------------------- linear layer

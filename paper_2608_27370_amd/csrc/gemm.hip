@@ -71,7 +71,31 @@ struct Params {
     int tiles_m, tiles_n;
     int accumulate;
     float alpha;               // host-known part of the per-tensor scale (1)
+    const uint16_t* bias;      // OUT kOutBF16Epi: optional bias [N] and residual [M, N] (pitch ldr)
+    const uint16_t* residual;
+    int64_t ldr;
 };
+
+// The bias / residual epilogue: the BF16 bias of columns n..n+3 and the BF16
+// residual of row m at those columns added to four binary32 results (the
+// sum stays binary32 until the output's one rounding).
+__device__ __forceinline__ void add_epilogue4(float4& v, const uint16_t* bias, const uint16_t* residual,
+                                              int64_t ldr, int64_t m, int64_t n) {
+    if (bias) {
+        const uint2 b = *reinterpret_cast<const uint2*>(bias + n);
+        v.x += bf16lo(b.x); v.y += bf16hi(b.x); v.z += bf16lo(b.y); v.w += bf16hi(b.y);
+    }
+    if (residual) {
+        const uint2 r = *reinterpret_cast<const uint2*>(residual + m * ldr + n);
+        v.x += bf16lo(r.x); v.y += bf16hi(r.x); v.z += bf16lo(r.y); v.w += bf16hi(r.y);
+    }
+}
+__device__ __forceinline__ float add_epilogue1(float v, const uint16_t* bias, const uint16_t* residual, int64_t ldr,
+                                               int64_t m, int64_t n) {
+    if (bias) v += __uint_as_float((uint32_t)bias[n] << 16);
+    if (residual) v += __uint_as_float((uint32_t)residual[m * ldr + n] << 16);
+    return v;
+}
 
 __device__ __forceinline__ uint32_t e8m0_of(float s) { return (__float_as_uint(s) >> 23) & 0xFFu; }
 
@@ -497,6 +521,7 @@ __global__ __launch_bounds__(WM * WN * 64 * (PROD ? 2 : 1)) void gemm_fp8_kernel
                     *reinterpret_cast<float4*>(part + m * p.N + n) = w;
                 } else {
                     w.x *= alpha; w.y *= alpha; w.z *= alpha; w.w *= alpha;
+                    if constexpr (OUT == kOutBF16Epi) add_epilogue4(w, p.bias, p.residual, p.ldr, m, n);
                     if constexpr (OUT == kOutF32)
                         *reinterpret_cast<float4*>(reinterpret_cast<float*>(p.D) + m * p.ldd + n) = w;
                     else
@@ -521,6 +546,7 @@ __global__ __launch_bounds__(WM * WN * 64 * (PROD ? 2 : 1)) void gemm_fp8_kernel
             }
             v.x *= alpha; v.y *= alpha; v.z *= alpha; v.w *= alpha;
             if (n + 3 < p.N) {
+                if constexpr (OUT == kOutBF16Epi) add_epilogue4(v, p.bias, p.residual, p.ldr, m, n);
                 if constexpr (OUT == kOutF32) {
                     float4* dst = reinterpret_cast<float4*>(reinterpret_cast<float*>(p.D) + (int64_t)m * p.ldd + n);
                     if (p.accumulate) {
@@ -547,7 +573,9 @@ __global__ __launch_bounds__(WM * WN * 64 * (PROD ? 2 : 1)) void gemm_fp8_kernel
                         *dst = p.accumulate ? *dst + vv[t] : vv[t];
                     } else {
                         uint16_t* dst = reinterpret_cast<uint16_t*>(p.D) + (int64_t)m * p.ldd + n + t;
-                        *dst = to_bf16(p.accumulate ? vv[t] + __uint_as_float((uint32_t)*dst << 16) : vv[t]);
+                        float o = p.accumulate ? vv[t] + __uint_as_float((uint32_t)*dst << 16) : vv[t];
+                        if constexpr (OUT == kOutBF16Epi) o = add_epilogue1(o, p.bias, p.residual, p.ldr, m, n + t);
+                        *dst = to_bf16(o);
                     }
                 }
             }
@@ -560,7 +588,8 @@ template <int OUT>
 __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restrict__ partial, int splits,
                                                             int M, int N, const float* sa, const float* sb,
                                                             int a_tensor, int b_tensor, void* D,
-                                                            int64_t ldd, int accumulate) {
+                                                            int64_t ldd, int accumulate, const uint16_t* bias,
+                                                            const uint16_t* residual, int64_t ldr) {
     const int64_t nq = N / 4;
     const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (idx >= (int64_t)M * nq) return;
@@ -575,6 +604,7 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restr
         s.x += t.x; s.y += t.y; s.z += t.z; s.w += t.w;
     }
     s.x *= alpha; s.y *= alpha; s.z *= alpha; s.w *= alpha;
+    if constexpr (OUT == kOutBF16Epi) add_epilogue4(s, bias, residual, ldr, m, n);
     if constexpr (OUT == kOutF32) {
         float* dst = reinterpret_cast<float*>(D) + m * ldd + n;
         if (accumulate) {
@@ -684,6 +714,8 @@ template <int BM, int BN, int WM, int WN, int SL, int NST, int PROD, int FA, int
 void launch_tile(const Params& prm, int out, bool grouped, int grid, hipStream_t stream) {
     if (out == 2) launch_cfg<BM, BN, WM, WN, SL, NST, PROD, FA, FB, 2>(prm, grouped, grid, stream);
     else if (out == kOutF32) launch_cfg<BM, BN, WM, WN, SL, NST, PROD, FA, FB, kOutF32>(prm, grouped, grid, stream);
+    else if (out == kOutBF16Epi)
+        launch_cfg<BM, BN, WM, WN, SL, NST, PROD, FA, FB, kOutBF16Epi>(prm, grouped, grid, stream);
     else launch_cfg<BM, BN, WM, WN, SL, NST, PROD, FA, FB, kOutBF16>(prm, grouped, grid, stream);
 }
 
@@ -730,6 +762,9 @@ void run_plan(const GemmProblem& g, const Plan& pl, void* ws, hipStream_t stream
     prm.tiles_n = (int)((g.N + t.bn - 1) / t.bn);
     prm.accumulate = g.accumulate;
     prm.alpha = 1.0f;
+    prm.bias = g.bias;
+    prm.residual = g.residual;
+    prm.ldr = g.ldr;
     const bool grouped = g.sa_mode != kSTensor || g.sb_mode != kSTensor;
     const int out = pl.splits > 1 ? 2 : g.out;
     const int grid = prm.tiles_m * prm.tiles_n * pl.splits;
@@ -743,11 +778,15 @@ void run_plan(const GemmProblem& g, const Plan& pl, void* ws, hipStream_t stream
         if (g.out == kOutF32)
             splitk_reduce_kernel<kOutF32><<<blocks, 256, 0, stream>>>(
                 prm.partial, pl.splits, prm.M, prm.N, g.sa, g.sb, g.sa_mode == kSTensor,
-                g.sb_mode == kSTensor, g.D, g.ldd, g.accumulate);
+                g.sb_mode == kSTensor, g.D, g.ldd, g.accumulate, nullptr, nullptr, 0);
+        else if (g.out == kOutBF16Epi)
+            splitk_reduce_kernel<kOutBF16Epi><<<blocks, 256, 0, stream>>>(
+                prm.partial, pl.splits, prm.M, prm.N, g.sa, g.sb, g.sa_mode == kSTensor,
+                g.sb_mode == kSTensor, g.D, g.ldd, 0, g.bias, g.residual, g.ldr);
         else
             splitk_reduce_kernel<kOutBF16><<<blocks, 256, 0, stream>>>(
                 prm.partial, pl.splits, prm.M, prm.N, g.sa, g.sb, g.sa_mode == kSTensor,
-                g.sb_mode == kSTensor, g.D, g.ldd, g.accumulate);
+                g.sb_mode == kSTensor, g.D, g.ldd, g.accumulate, nullptr, nullptr, 0);
     }
 }
 

@@ -91,7 +91,9 @@ void launch_swiglu_bwd_quantize(int fmt, int mode, QuantArgs a, void* ws, hipStr
 // ---- GEMM (gemm.hip) ----------------------------------------------------------
 
 enum ScaleMode : int { kSTensor = 0, kSRow = 1, kSBlock = 2 };
-enum OutKind : int { kOutBF16 = 0, kOutF32 = 1 };
+// kOutBF16Epi: BF16 output with the bias / residual epilogue (the partial
+// sums of a split-K plan are kind 2, internal to the GEMM).
+enum OutKind : int { kOutBF16 = 0, kOutF32 = 1, kOutBF16Epi = 3 };
 
 struct GemmProblem {
     int64_t M, N, K;
@@ -110,6 +112,11 @@ struct GemmProblem {
     // grouped scales stored k-block-major ([K/128][rows] or [K/128][rows/128])
     // instead of row-major ([rows][K/128] or [rows/128][K/128])
     int sa_kmajor, sb_kmajor;
+    // kOutBF16Epi: D = BF16(alpha * acc + bias[n] + residual[m, n]), either
+    // term optional (NULL); residual row pitch ldr (residual may be D itself)
+    const uint16_t* bias;
+    const uint16_t* residual;
+    int64_t ldr;
 };
 
 // Workspace the GEMM needs for split-K partial sums (0 when it runs unsplit).

@@ -67,6 +67,8 @@ _SIGS = {
                                 ctypes.POINTER(_i), ctypes.POINTER(_i), ctypes.POINTER(_i)]),
     "puro_fp8_gemm": (_i, [_i64, _i64, _i64, ctypes.POINTER(Operand), ctypes.POINTER(Operand),
                            _p, _i, _i64, _i, _p, _sz, _p]),
+    "puro_fp8_gemm_epilogue": (_i, [_i64, _i64, _i64, ctypes.POINTER(Operand), ctypes.POINTER(Operand),
+                                    _p, _i64, _p, _p, _i64, _p, _sz, _p]),
     "puro_linear_saved_bytes": (_sz, [_i64, _i64, _i64, ctypes.POINTER(Recipe), ctypes.POINTER(_sz * 4)]),
     "puro_linear_fwd_workspace_size": (_sz, [_i64, _i64, _i64, ctypes.POINTER(Recipe)]),
     "puro_linear_bwd_workspace_size": (_sz, [_i64, _i64, _i64, ctypes.POINTER(Recipe)]),
@@ -315,6 +317,21 @@ def fp8_gemm(A, a_rows, B, b_rows, K, out_dtype=OUT_BF16, D=None, accumulate=Fal
     _check("puro_fp8_gemm", lib().puro_fp8_gemm(M, N, K, ctypes.byref(A), ctypes.byref(B), _ptr(D),
                                                 out_dtype, _ld(D), int(bool(accumulate)), _ptr(w), nb,
                                                 _stream()))
+    return D
+
+
+def fp8_gemm_epilogue(A, a_rows, B, b_rows, K, bias=None, residual=None, D=None, ws=None):
+    """D[M, N] = BF16(sum_k A[m, k] B[n, k] + bias[n] + residual[m, n]) (bias
+    and residual BF16, optional; residual may be D itself)."""
+    M, N = a_rows, b_rows
+    dev = torch.device("cuda", torch.cuda.current_device())
+    if D is None:
+        D = torch.empty(M, N, dtype=torch.bfloat16, device=dev)
+    w, nb = _ws(fp8_gemm_workspace_size(M, N, K, OUT_BF16), ws, dev)
+    ldr = _ld(residual) if residual is not None else 0
+    _check("puro_fp8_gemm_epilogue", lib().puro_fp8_gemm_epilogue(
+        M, N, K, ctypes.byref(A), ctypes.byref(B), _ptr(D), _ld(D), _ptr(bias), _ptr(residual), ldr, _ptr(w), nb,
+        _stream()))
     return D
 
 

@@ -243,3 +243,19 @@ def test_swiglu_bwd_quantize_validation(puro):
     assert f(FAKE, 96, FAKE, 192, 128, 96, 0, 1, 1, FAKE, FAKE, None, None, None, 0, None) == ERR_ALIGN
     # per-tensor without workspace
     assert f(FAKE, 4096, FAKE, 8192, 4096, 4096, 0, 0, 0, FAKE, FAKE, None, None, FAKE, 0, None) == ERR_WORKSPACE
+
+
+def test_gemm_epilogue_validation(puro):
+    L = puro.lib()
+    f = L.puro_fp8_gemm_epilogue
+    good = puro.Operand(FAKE, 256, 0, 0, FAKE)
+    big = 1 << 30
+    g = lambda *a: f(*a)
+    # misaligned bias / residual, a residual pitch below N or not a multiple of 4
+    assert g(16, 16, 256, good, good, FAKE, 16, FAKE + 2, None, 0, FAKE, big, None) == ERR_ALIGN
+    assert g(16, 16, 256, good, good, FAKE, 16, None, FAKE + 0x10000 + 8, 16, FAKE, big, None) == ERR_ALIGN
+    assert g(16, 16, 256, good, good, FAKE, 16, None, FAKE + 0x10000, 8, FAKE, big, None) == ERR_SHAPE
+    assert g(16, 16, 256, good, good, FAKE, 16, None, FAKE + 0x10000, 18, FAKE, big, None) == ERR_ALIGN
+    # a residual overlapping D without being D, and D itself with another pitch
+    assert g(16, 16, 256, good, good, FAKE, 16, None, FAKE + 64, 16, FAKE, big, None) == ERR_SHAPE
+    assert g(16, 16, 256, good, good, FAKE, 16, None, FAKE, 32, FAKE, big, None) == ERR_SHAPE

@@ -12,7 +12,7 @@ from oracle import bf16, fp8, gemm, quant
 from paper_2608_27370_amd import inputs
 
 import mfma_model
-from gpu_util import bf16_bits, check_bf16, check_fp32, host, to_dev
+from gpu_util import bf16_bits, check_bf16, check_fp32, host, to_dev, to_dev_bf16
 
 pytestmark = pytest.mark.gpu
 
@@ -264,3 +264,85 @@ def test_gemm_block_scales_change_between_blocks(P, shape):
             check_fp32(host(D)[ms, ns], ref, den, what=what, slack=slack)
         else:
             check_bf16(bf16_bits(D)[ms, ns], ref, den, what=what, slack=slack)
+
+
+def _epilogue_terms(seed, M, N, bias, residual):
+    rng = np.random.default_rng(seed)
+    b = inputs.bf16_from_f64(0.5 * rng.standard_normal(N)) if bias else None
+    r = inputs.bf16_from_f64(rng.standard_normal((M, N))) if residual else None
+    return b, r
+
+
+def _run_epi(P, a, fa, sa, am, b, fb, sb, bm, bias, resid, ld_pad=0, in_place=False):
+    M, K = a.shape
+    N = b.shape[0]
+    da, db = to_dev(a), to_dev(b)
+    dsa, dsb = to_dev(np.atleast_1d(np.asarray(sa, np.float32))), to_dev(np.atleast_1d(np.asarray(sb, np.float32)))
+    A = P.operand(da, fa, MODE[am], dsa)
+    B = P.operand(db, fb, MODE[bm], dsb)
+    import torch
+    D = torch.empty(M, N + ld_pad, dtype=torch.bfloat16, device="cuda")[:, :N]
+    dbias = to_dev_bf16(bias) if bias is not None else None
+    if in_place:
+        D.view(torch.int16).copy_(to_dev(resid.view(np.int16)))
+        dres = D
+    elif resid is not None:
+        # the residual with the same row pitch as D
+        dres = to_dev_bf16(np.pad(resid, ((0, 0), (0, ld_pad))))[:, :N]
+    else:
+        dres = None
+    return P.fp8_gemm_epilogue(A, M, B, N, K, bias=dbias, residual=dres, D=D)
+
+
+EPI_SHAPES = [(300, 520, 384), (200, 258, 208), (256, 256, 1024), (513, 260, 1040)]
+
+
+@pytest.mark.parametrize("shape", EPI_SHAPES, ids=lambda s: "x".join(map(str, s)))
+@pytest.mark.parametrize("terms", ["bias", "residual", "both", "in_place"])
+def test_gemm_epilogue(P, shape, terms):
+    """D = BF16(A B^T + bias + residual): every entry within the BF16 band
+    of the oracle's exact value (oracle/gemm.py's epilogue); ragged N, a
+    split-K shape (whose reduction kernel applies the epilogue), and the
+    residual being D itself."""
+    M, N, K = shape
+    a, sa = _operand_tensor(31, M, K, E4)
+    b, sb = _operand_tensor(32, N, K, E4, std=0.02)
+    bias, resid = _epilogue_terms(M + N, M, N, terms in ("bias", "both", "in_place"), terms != "bias")
+    D = _run_epi(P, a, E4, sa, "tensor", b, E4, sb, "tensor", bias, resid, ld_pad=(-N) % 4 + 4 * (N % 4 != 0),
+                 in_place=terms == "in_place")
+    op = (a, fp8.E4M3, sa, "tensor", b, fp8.E4M3, sb, "tensor")
+    ref, den = gemm.gemm(*op)
+    ref, den = gemm.epilogue(ref, den, None if bias is None else bf16.to_f32(bias)[None, :],
+                             None if resid is None else bf16.to_f32(resid))
+    check_bf16(bf16_bits(D), ref, den, what="epilogue %s %s plan %s" % (terms, shape, P.fp8_gemm_plan(M, N, K)),
+               slack=mfma_model.truncation_loss_full(*op))
+
+
+def test_gemm_epilogue_block_scales(P):
+    M, N, K = 256, 384, 512
+    a, sa = _operand_grouped(33, M, K, E4, "row")
+    b, sb = _operand_grouped(34, N, K, E4, "block", std=0.02)
+    bias, resid = _epilogue_terms(5, M, N, True, True)
+    D = _run_epi(P, a, E4, sa, "row", b, E4, sb, "block", bias, resid)
+    op = (a, fp8.E4M3, sa, "row", b, fp8.E4M3, sb, "block")
+    ref, den = gemm.gemm(*op)
+    ref, den = gemm.epilogue(ref, den, bf16.to_f32(bias)[None, :], bf16.to_f32(resid))
+    check_bf16(bf16_bits(D), ref, den, what="epilogue block scales", slack=mfma_model.truncation_loss_full(*op))
+
+
+def test_gemm_epilogue_qkv_bias_full_size(P):
+    """The Qwen2-1.5B QKV projection with its bias, 8192 x 2048 x 1536, in the
+    bench's launch configuration; 16 entries in every 256x256 tile plus the
+    whole first and last tiles."""
+    from gpu_util import sample_entries
+    d = inputs.qkv()
+    xq, _, sx, _ = quant.quantize_tensor(d["X"], fp8.E4M3)
+    wq, _, sw, _ = quant.quantize_tensor(d["W"], fp8.E4M3)
+    M, N, K = 8192, inputs.QKV_OUT, inputs.HIDDEN
+    bias, _ = _epilogue_terms(6, M, N, True, False)
+    D = _run_epi(P, xq, E4, sx, "tensor", wq, E4, sw, "tensor", bias, None)
+    ms, ns = sample_entries(M, N, np.random.default_rng(13))
+    op = (xq, fp8.E4M3, sx, "tensor", wq, fp8.E4M3, sw, "tensor")
+    ref, den = gemm.gemm_entries(ms, ns, *op)
+    ref, den = gemm.epilogue(ref, den, bf16.to_f32(bias)[ns])
+    check_bf16(bf16_bits(D)[ms, ns], ref, den, what="QKV + bias", slack=mfma_model.truncation_loss(ms, ns, *op))

@@ -178,3 +178,18 @@ def test_bf16_rounding_helper():
     assert bits[5] == 0x7F62 and bits[6] == 0x7F80 and bits[7] == 0x7F80
     assert bits[8] == 0x7FC0
     assert bits[9] == 0x0001 and bits[10] == 0x0000    # tie at half the smallest subnormal -> even
+
+
+def test_epilogue_closed_forms():
+    """A zero product leaves bias + residual; the tolerance scale grows by
+    their magnitudes; absent terms change nothing."""
+    rng = np.random.default_rng(12)
+    b = bf16.to_f32(bf16.from_f64_rne(rng.standard_normal(8))).astype(np.float64)
+    r = bf16.to_f32(bf16.from_f64_rne(rng.standard_normal((4, 8)))).astype(np.float64)
+    ref, den = gemm.epilogue(np.zeros((4, 8)), np.zeros((4, 8)), b, r)
+    np.testing.assert_array_equal(ref, b[None, :] + r)
+    np.testing.assert_array_equal(den, np.abs(b)[None, :] + np.abs(r))
+    x = rng.standard_normal((4, 8))
+    ref, den = gemm.epilogue(x, np.abs(x))
+    np.testing.assert_array_equal(ref, x)
+    np.testing.assert_array_equal(den, np.abs(x))
