@@ -39,6 +39,8 @@
 //  * Small grids split K into ranges whose FP32 partial sums a second kernel
 //    adds in a fixed order (deterministic).
 
+#include <type_traits>
+
 #include "device_common.h"
 #include "kernels.h"
 
@@ -95,6 +97,16 @@ __device__ __forceinline__ float add_epilogue1(float v, const uint16_t* bias, co
     if (bias) v += __uint_as_float((uint32_t)bias[n] << 16);
     if (residual) v += __uint_as_float((uint32_t)residual[m * ldr + n] << 16);
     return v;
+}
+
+// f(std::integral_constant<int, i>) for i = 0 .. N-1, each call with its own
+// compile-time index (no loop left for the unroller to decide on).
+template <int N, int I = 0, class F>
+__device__ __forceinline__ void static_for(F&& f) {
+    if constexpr (I < N) {
+        f(std::integral_constant<int, I>{});
+        static_for<N, I + 1>(f);
+    }
 }
 
 __device__ __forceinline__ uint32_t e8m0_of(float s) { return (__float_as_uint(s) >> 23) & 0xFFu; }
@@ -480,9 +492,23 @@ __global__ __launch_bounds__(WM * WN * 64 * (PROD ? 2 : 1)) void gemm_fp8_kernel
     // 4-column vectors everywhere: a branch-free path that issues all of a
     // pass's LDS reads before its stores
     const bool fast = m0 + BM <= p.M && n0 + BN <= p.N && (OUT == 2 || !p.accumulate);
-    __syncthreads();   // every wave is done with the last stage
+    // the bias of the lane's columns in the fast path below: lane chunk
+    // (it * 64 + lane) % ECPR repeats with period ECPR / gcd(64, ECPR) in it
+    constexpr int EP = ECPR / ((ECPR & -ECPR) < 64 ? (ECPR & -ECPR) : 64);
+    uint2 eb[OUT == kOutBF16Epi ? EP : 1];
+    if constexpr (OUT == kOutBF16Epi) {
+        const __amdgpu_buffer_rsrc_t rb = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<uint16_t*>(p.bias), 0, p.bias ? p.N * 2 : 0, 0x00020000);
 #pragma unroll
-    for (int pass = 0; pass < WTM / RPP; ++pass) {
+        for (int it = 0; it < EP; ++it)
+            eb[it] = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(
+                rb, (uint32_t)((ncol0 + ((it * 64 + lane) % ECPR) * 4) * 2), 0, 0));
+    }
+    __syncthreads();   // every wave is done with the last stage
+    // one pass per constant: the accumulators are indexed by the pass, and a
+    // loop the unroller leaves rolled would move them to scratch memory
+    static_for<WTM / RPP>([&](auto pass_c) __attribute__((always_inline)) {
+        constexpr int pass = decltype(pass_c)::value;
 #pragma unroll
         for (int ii = 0; ii < RPP / 32; ++ii) {
             const int i = pass * (RPP / 32) + ii;
@@ -503,33 +529,70 @@ __global__ __launch_bounds__(WM * WN * 64 * (PROD ? 2 : 1)) void gemm_fp8_kernel
         asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
         constexpr int IT = RPP * ECPR / 64;
         if (fast) {
-            float4 v[IT];
+            // the epilogue terms are loaded before the LDS reads of their
+            // group of iterations, so that their latency overlaps those reads
+            // and the group's stores wait once (a load issued after stores
+            // waits for them); buffer loads, so an absent term costs no
+            // branch and no traffic. Groups of at most 16 iterations keep the
+            // residual and the staged values in registers beside the
+            // accumulators of the passes still to come.
+            constexpr int EG = (OUT == kOutBF16Epi && IT > 16) ? IT / 2 : IT;
+            static_assert(IT % EG == 0, "epilogue groups");
 #pragma unroll
-            for (int it = 0; it < IT; ++it) {
-                const int q = it * 64 + lane;
-                const int r = q / ECPR, c = q % ECPR;
-                v[it] = *reinterpret_cast<const float4*>(ep + r * ROWB + ((c ^ (r & SWZ)) << 4));
-            }
+            for (int g0 = 0; g0 < IT; g0 += EG) {
+                uint2 er[OUT == kOutBF16Epi ? EG : 1];
+                if constexpr (OUT == kOutBF16Epi) {
+                    const int64_t mt = mrow0 + pass * RPP;           // the pass's first row
+                    const __amdgpu_buffer_rsrc_t rr = __builtin_amdgcn_make_buffer_rsrc(
+                        const_cast<uint16_t*>(p.residual ? p.residual + mt * p.ldr : p.residual), 0,
+                        p.residual ? (int)((RPP - 1) * p.ldr * 2 + (int64_t)(ncol0 + WTN) * 2) : 0, 0x00020000);
 #pragma unroll
-            for (int it = 0; it < IT; ++it) {
-                const int q = it * 64 + lane;
-                const int r = q / ECPR, c = q % ECPR;
-                const int64_t m = mrow0 + pass * RPP + r;
-                const int n = ncol0 + c * 4;
-                float4 w = v[it];
-                if constexpr (OUT == 2) {
-                    *reinterpret_cast<float4*>(part + m * p.N + n) = w;
-                } else {
-                    w.x *= alpha; w.y *= alpha; w.z *= alpha; w.w *= alpha;
-                    if constexpr (OUT == kOutBF16Epi) add_epilogue4(w, p.bias, p.residual, p.ldr, m, n);
-                    if constexpr (OUT == kOutF32)
-                        *reinterpret_cast<float4*>(reinterpret_cast<float*>(p.D) + m * p.ldd + n) = w;
-                    else
-                        *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(p.D) + m * p.ldd + n) =
-                            make_uint2(pack_bf16x2(w.x, w.y), pack_bf16x2(w.z, w.w));
+                    for (int e = 0; e < EG; ++e) {
+                        const int q = (g0 + e) * 64 + lane;
+                        const int r = q / ECPR, c = q % ECPR;
+                        er[e] = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(
+                            rr, (uint32_t)((r * p.ldr + ncol0 + c * 4) * 2), 0, 0));
+                    }
+                }
+                float4 v[EG];
+#pragma unroll
+                for (int e = 0; e < EG; ++e) {
+                    const int q = (g0 + e) * 64 + lane;
+                    const int r = q / ECPR, c = q % ECPR;
+                    v[e] = *reinterpret_cast<const float4*>(ep + r * ROWB + ((c ^ (r & SWZ)) << 4));
+                }
+#pragma unroll
+                for (int e = 0; e < EG; ++e) {
+                    const int it = g0 + e;
+                    const int q = it * 64 + lane;
+                    const int r = q / ECPR, c = q % ECPR;
+                    const int64_t m = mrow0 + pass * RPP + r;
+                    const int n = ncol0 + c * 4;
+                    float4 w = v[e];
+                    if constexpr (OUT == 2) {
+                        *reinterpret_cast<float4*>(part + m * p.N + n) = w;
+                    } else {
+                        w.x *= alpha; w.y *= alpha; w.z *= alpha; w.w *= alpha;
+                        if constexpr (OUT == kOutBF16Epi) {
+                            // each term only when given: adding +0 would turn a -0 sum into +0
+                            if (p.bias) {
+                                const uint2 b = eb[it % EP];
+                                w.x += bf16lo(b.x); w.y += bf16hi(b.x); w.z += bf16lo(b.y); w.w += bf16hi(b.y);
+                            }
+                            if (p.residual) {
+                                const uint2 rv = er[e];
+                                w.x += bf16lo(rv.x); w.y += bf16hi(rv.x); w.z += bf16lo(rv.y); w.w += bf16hi(rv.y);
+                            }
+                        }
+                        if constexpr (OUT == kOutF32)
+                            *reinterpret_cast<float4*>(reinterpret_cast<float*>(p.D) + m * p.ldd + n) = w;
+                        else
+                            *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(p.D) + m * p.ldd + n) =
+                                make_uint2(pack_bf16x2(w.x, w.y), pack_bf16x2(w.z, w.w));
+                    }
                 }
             }
-            continue;
+            return;
         }
 #pragma unroll
         for (int it = 0; it < IT; ++it) {
@@ -580,7 +643,7 @@ __global__ __launch_bounds__(WM * WN * 64 * (PROD ? 2 : 1)) void gemm_fp8_kernel
                 }
             }
         }
-    }
+    });
 }
 
 // Fixed-order sum of the split-K partials, scaling and output conversion.
