@@ -9,8 +9,9 @@ the timed region.
 
 Prints one JSON line: the metric (TFLOP/s of fwd + dgrad + wgrad GEMM work per
 step time), a per-call breakdown and a roofline entry for the dominant kernel
-(each call timed with HIP events on its stream around back-to-back launches),
-and the CPU oracle timed on a sample of the same workload.
+(each call timed with HIP events on its stream around back-to-back launches;
+also per launch, as median, p10 and p90, warm and after a fill that evicts the
+caches), and the CPU oracle timed on a sample of the same workload.
 """
 
 import argparse
@@ -507,6 +508,7 @@ def main():
     if args.suite:
         run_suite(args)
         return
+    import numpy as np
     import torch
     from paper_2608_27370_amd import inputs, puro
 
@@ -517,7 +519,6 @@ def main():
     d = inputs.qkv(M=M)
 
     def up(bits):
-        import numpy as np
         return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).to(dev).view(torch.bfloat16)
 
     X, W, dY = up(d["X"]), up(d["W"]), up(d["dY"])
@@ -574,6 +575,23 @@ def main():
     # behind the queue, as in the step)
     kernels = calls(torch, puro, dev, M, N, K, X, W, dY, Y, dX, dW, saved)
     reps = max(20, args.steps // 2)
+    # per-launch samples: each call bracketed by its own pair of events
+    # (median, p10, p90), warm (back to back) and cold (after a 512 MiB fill
+    # that evicts the 256 MB MALL and the L2s)
+    pairs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+
+    def sampled(fn, cold):
+        for a, b in pairs:
+            if cold:
+                flush.zero_()
+            a.record(stream)
+            fn()
+            b.record(stream)
+        torch.cuda.synchronize()
+        us = np.sort([a.elapsed_time(b) * 1e3 for a, b in pairs])
+        return {k: round(float(np.percentile(us, q)), 2) for k, q in (("p10", 10), ("median", 50), ("p90", 90))}
+
     breakdown = []
     for _, name, fn, flops, nbytes, launches in kernels:
         for _ in range(3):
@@ -585,7 +603,8 @@ def main():
         e1.record(stream)
         torch.cuda.synchronize()
         us = e0.elapsed_time(e1) / reps * 1e3
-        row = {"call": name, "us": round(us, 2), "launches": launches}
+        row = {"call": name, "us": round(us, 2), "launches": launches,
+               "per_launch_us": sampled(fn, False), "cold_per_launch_us": sampled(fn, True)}
         if flops:
             row["tflops"] = round(flops / (us * 1e-6) / 1e12, 1)
         if nbytes:
