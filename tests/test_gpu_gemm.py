@@ -318,6 +318,38 @@ def test_gemm_epilogue(P, shape, terms):
                slack=mfma_model.truncation_loss_full(*op))
 
 
+# The epilogue on the tile configurations the shapes above do not reach:
+# 256x192 (bias repeating with period 3 over a lane's store iterations), and
+# 128x128 with a 4-deep ring and producer waves, alone and split over K.
+EPI_TILE_CASES = [
+    # (M, N, K, tile_m, tile_n, stages, splits, in_place, full_tiles)
+    (8192, 1536, 1536, 256, 192, 2, 1, True, True),
+    (2048, 1536, 2048, 128, 128, 4, 1, False, True),
+    (1024, 768, 8192, 128, 128, 4, 4, True, False),
+]
+
+
+@pytest.mark.parametrize("case", EPI_TILE_CASES, ids=lambda c: "x".join(map(str, c[:3])))
+def test_gemm_epilogue_tile_configs(P, case):
+    """Bias plus residual (in place on D where marked) on sampled entries:
+    16 in every 256x256 block, plus the whole first and last blocks where
+    marked."""
+    from gpu_util import sample_entries
+    M, N, K, tm, tn, st, sp, in_place, full = case
+    plan = P.fp8_gemm_plan(M, N, K)
+    assert (plan["tile_m"], plan["tile_n"], plan["stages"], plan["splits"]) == (tm, tn, st, sp), plan
+    a, sa = _operand_tensor(41, M, K, E4)
+    b, sb = _operand_tensor(42, N, K, E4, std=0.02)
+    bias, resid = _epilogue_terms(43, M, N, True, True)
+    D = _run_epi(P, a, E4, sa, "tensor", b, E4, sb, "tensor", bias, resid, in_place=in_place)
+    ms, ns = sample_entries(M, N, np.random.default_rng(44), per_tile=16 if full else 64, full_tiles=full)
+    op = (a, fp8.E4M3, sa, "tensor", b, fp8.E4M3, sb, "tensor")
+    ref, den = gemm.gemm_entries(ms, ns, *op)
+    ref, den = gemm.epilogue(ref, den, bf16.to_f32(bias)[ns], bf16.to_f32(resid)[ms, ns])
+    check_bf16(bf16_bits(D)[ms, ns], ref, den, what="epilogue %s plan %s" % (case[:3], plan),
+               slack=mfma_model.truncation_loss(ms, ns, *op))
+
+
 def test_gemm_epilogue_block_scales(P):
     M, N, K = 256, 384, 512
     a, sa = _operand_grouped(33, M, K, E4, "row")
