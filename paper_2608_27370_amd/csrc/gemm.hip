@@ -765,7 +765,10 @@ Plan make_plan(int64_t M, int64_t N, int64_t K, bool grouped) {
 
 template <int BM, int BN, int WM, int WN, int SL, int NST, int PROD, int FA, int FB, int OUT>
 void launch_cfg(const Params& prm, bool grouped, int grid, hipStream_t stream) {
-    constexpr int GM = 8;
+    // tile rows per group of the XCD ranges: the QKV Wgrad's 24-tile ranges
+    // become 4 x 6 tiles (10 operand panels per XCD instead of 11 at 8),
+    // and the 32-tile ranges of one-tile-per-CU GEMMs stay at 12 panels
+    constexpr int GM = 4;
     constexpr int threads = WM * WN * 64 * (PROD ? 2 : 1);
     if (grouped)
         gemm_fp8_kernel<BM, BN, WM, WN, FA, FB, OUT, true, GM, SL, NST, PROD != 0><<<grid, threads, 0, stream>>>(prm);
