@@ -10,8 +10,8 @@ the timed region.
 Prints one JSON line: the metric (TFLOP/s of fwd + dgrad + wgrad GEMM work per
 step time), a per-call breakdown and a roofline entry for the dominant kernel
 (each call timed with HIP events on its stream around back-to-back launches;
-also per launch, as median, p10 and p90, warm and after a fill that evicts the
-caches), and the CPU oracle timed on a sample of the same workload.
+also per launch, as median, p10 and p90, and with --cold after a fill that
+evicts the caches), and the CPU oracle timed on a sample of the same workload.
 """
 
 import argparse
@@ -38,6 +38,9 @@ def parse():
     ap.add_argument("--cpu-tokens", type=int, default=8192,
                     help="tokens of the workload the CPU oracle is timed on (0: skip)")
     ap.add_argument("--cpu-reps", type=int, default=4, help="repetitions of the CPU oracle sample")
+    ap.add_argument("--cold", action="store_true",
+                    help="also time every call after a 512 MiB fill that evicts the MALL and the L2s "
+                         "(kept out of the default run, whose kernel trace profiles warm launches)")
     ap.add_argument("--graph", action="store_true",
                     help="replay the step captured in a HIP graph instead of launching its kernels one by one "
                          "(measured no faster: the launches are not host-bound)")
@@ -576,10 +579,10 @@ def main():
     kernels = calls(torch, puro, dev, M, N, K, X, W, dY, Y, dX, dW, saved)
     reps = max(20, args.steps // 2)
     # per-launch samples: each call bracketed by its own pair of events
-    # (median, p10, p90), warm (back to back) and cold (after a 512 MiB fill
-    # that evicts the 256 MB MALL and the L2s)
+    # (median, p10, p90), warm (back to back) and, with --cold, after a
+    # 512 MiB fill that evicts the 256 MB MALL and the L2s
     pairs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
-    flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev) if args.cold else None
 
     def sampled(fn, cold):
         for a, b in pairs:
@@ -603,8 +606,9 @@ def main():
         e1.record(stream)
         torch.cuda.synchronize()
         us = e0.elapsed_time(e1) / reps * 1e3
-        row = {"call": name, "us": round(us, 2), "launches": launches,
-               "per_launch_us": sampled(fn, False), "cold_per_launch_us": sampled(fn, True)}
+        row = {"call": name, "us": round(us, 2), "launches": launches, "per_launch_us": sampled(fn, False)}
+        if args.cold:
+            row["cold_per_launch_us"] = sampled(fn, True)
         if flops:
             row["tflops"] = round(flops / (us * 1e-6) / 1e12, 1)
         if nbytes:
