@@ -151,3 +151,31 @@ def test_quantize_is_deterministic(P):
     b = P.quantize_fp8(x, E4, P.SCALE_TENSOR, 0, want_qT=True)
     assert_bytes_equal(host(a["q"]), host(b["q"]))
     assert_bytes_equal(host(a["qT"]), host(b["qT"]))
+
+
+def test_quantize_largest_row_pitch(P):
+    """The largest row pitch the quantisers accept, ld = 2**23 - 8 elements:
+    inside a 128-row tile the byte offsets of the buffer loads reach about
+    2**31, the edge of their 32-bit arithmetic. Per-tensor (q, qT) and
+    1x128 + 128x1 groups on a 256 x 256 window of a 4.3 GB allocation."""
+    import torch
+    rows, cols, ld = 256, 256, (1 << 23) - 8
+    x = inputs.case(15, (rows, cols), kind="outliers")
+    big = torch.empty(rows, ld, dtype=torch.int16, device="cuda")
+    big[:, :cols].copy_(torch.from_numpy(x.view(np.int16)).cuda())
+    d = big.view(torch.bfloat16)[:, :cols]
+    assert d.stride(0) == ld
+    r = P.quantize_fp8(d, E4, P.SCALE_TENSOR, 0, want_q=True, want_qT=True)
+    q, qT, s, _ = quant.quantize_tensor(x, fp8.E4M3, rule=RULE[0])
+    assert_f32_bits_equal(host(r["scale"]), np.array([s]), "scale")
+    assert_bytes_equal(host(r["q"]), q, "q")
+    assert_bytes_equal(host(r["qT"]), qT, "qT")
+    r = P.quantize_fp8(d, E4, P.SCALE_ROW_1x128, 1, want_q=True, want_qT=True)
+    q, s = quant.quantize_rows_1x128(x, fp8.E4M3, RULE[1])
+    qT, sT = quant.quantize_cols_128x1(x, fp8.E4M3, RULE[1])
+    assert_bytes_equal(host(r["q"]), q, "row q")
+    assert_f32_bits_equal(host(r["scale"]), s, "row scale")
+    assert_bytes_equal(host(r["qT"]), qT, "col qT")
+    assert_f32_bits_equal(host(r["scaleT"]), sT, "col scaleT")
+    del big, d
+    torch.cuda.empty_cache()
