@@ -265,7 +265,7 @@ puro_status puro_fp8_gemm(int64_t M, int64_t N, int64_t K,
  * down projections add into the residual stream, which stays BF16 (Appendix
  * C precision flow): fusing the add removes a BF16 read and write of Y.
  * bias: BF16 [N], 16-byte aligned. residual: BF16 [M, N] with row pitch
- * ldr >= N, ldr % 4 == 0, 16-byte aligned; it may be D itself (ldr == ldd,
+ * N <= ldr <= 2^22, ldr % 4 == 0, 16-byte aligned; it may be D itself (ldr == ldd,
  * an in-place residual add) but must not otherwise overlap D. Operands,
  * scales, workspace and errors as puro_fp8_gemm; accumulate is not offered. */
 puro_status puro_fp8_gemm_epilogue(int64_t M, int64_t N, int64_t K, const puro_fp8_operand* A,

@@ -348,7 +348,8 @@ puro_status gemm_impl(int64_t M, int64_t N, int64_t K, const puro_fp8_operand* A
     if (epi) {
         if (d_type != PURO_OUT_BF16 || accumulate) return PURO_ERR_UNSUPPORTED;
         if (bias && !aligned16(bias)) return PURO_ERR_ALIGN;
-        if (residual && (ldr < N)) return PURO_ERR_SHAPE;
+        // ldr as the operands' pitch: buffer offsets over a tile's rows stay below 2^31
+        if (residual && (ldr < N || ldr > ((int64_t)1 << 22))) return PURO_ERR_SHAPE;
         if (residual && (!aligned16(residual) || (ldr % 4) != 0)) return PURO_ERR_ALIGN;
         // the residual may be D itself (an in-place residual add), but not overlap it otherwise
         if (residual && residual != D) {

@@ -256,6 +256,8 @@ def test_gemm_epilogue_validation(puro):
     assert g(16, 16, 256, good, good, FAKE, 16, None, FAKE + 0x10000 + 8, 16, FAKE, big, None) == ERR_ALIGN
     assert g(16, 16, 256, good, good, FAKE, 16, None, FAKE + 0x10000, 8, FAKE, big, None) == ERR_SHAPE
     assert g(16, 16, 256, good, good, FAKE, 16, None, FAKE + 0x10000, 18, FAKE, big, None) == ERR_ALIGN
+    # a residual pitch beyond the operands' limit, 2^22
+    assert g(16, 16, 256, good, good, FAKE, 16, None, FAKE + 0x10000, (1 << 22) + 4, FAKE, big, None) == ERR_SHAPE
     # a residual overlapping D without being D, and D itself with another pitch
     assert g(16, 16, 256, good, good, FAKE, 16, None, FAKE + 64, 16, FAKE, big, None) == ERR_SHAPE
     assert g(16, 16, 256, good, good, FAKE, 16, None, FAKE, 32, FAKE, big, None) == ERR_SHAPE
