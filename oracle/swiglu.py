@@ -19,9 +19,11 @@ Readings where the paper is silent (each restated in the design notes):
   H is not unique in its last BF16 bit: any BF16 value that an evaluation
   with relative error at most EPS = 2**-20 (plus 2**-148 absolute, for
   results in binary32's subnormal range) could round to is accepted; where
-  1 / (1 + e^-g) leaves binary32's normal range or e^-g overflows (g < -87),
-  zero is accepted as well (the exact H is then below TINY * max(1, |u|),
-  TINY = 2**-118). Where exactly one BF16
+  e^-g overflows binary32 (g < -ln(FLT_MAX) = -88.72), a binary32
+  evaluation of g / (1 + e^-g) is -0, so zero is accepted as well (the exact
+  H is then below TINY * max(1, |u|), TINY = 2**-120). Above that point every
+  step of a binary32 evaluation stays finite and, with gradual underflow,
+  non-zero, and so must H. Where exactly one BF16
   value is accepted (almost everywhere) H is that value, rounded once from
   the float64 evaluation; the quantisation of every accepted H is the
   quantisers' (``oracle.quant``).
@@ -38,7 +40,9 @@ import numpy as np
 from . import bf16
 
 EPS = 2.0 ** -20
-TINY = 2.0 ** -118
+TINY = 2.0 ** -120
+# e^-g overflows binary32 for g below -ln(FLT_MAX)
+G_OVERFLOW = -float(np.log(np.float64(np.finfo(np.float32).max)))
 
 
 def split(gu_bits, cols):
@@ -76,7 +80,7 @@ def swiglu_bf16_band(gu_bits, cols):
     g, u = split(gu_bits, cols)
     with np.errstate(over="ignore", invalid="ignore"):
         t = silu_f64(g) * u
-        d = EPS * np.abs(t) + 2.0 ** -148 + np.where(g < -87.0, TINY * np.maximum(1.0, np.abs(u)), 0.0)
+        d = EPS * np.abs(t) + 2.0 ** -148 + np.where(g < G_OVERFLOW, TINY * np.maximum(1.0, np.abs(u)), 0.0)
         d = np.where(np.isfinite(t), d, 0.0)        # infinities are exact
         mid = bf16.from_f64_rne(t)
         lo = bf16.from_f64_rne(t - d)
@@ -94,10 +98,15 @@ def swiglu_bf16_band(gu_bits, cols):
 #   dg = dH * u * silu'(g), du = dH * silu(g), silu'(g) = s (1 + g (1 - s)),
 #   s = 1 / (1 + e^-g); each evaluated in binary32 and rounded once to BF16.
 # * Accepted values: relative EPS as in the forward, plus for dg an absolute
-#   2**-20 * |dH * u|: silu' is a difference near its zero (g ~ -1.28),
-#   where a few binary32 ulps of its terms (about 1 in size) are not small
-#   against the result; plus the forward's allowances (2**-148 absolute, and
-#   zero where e^-g overflows, |dH| * max(1, |u|) * TINY).
+#   2**-20 * |dH * u| * s**2 * |g| * min(1, 2**21 (1 - s)): silu' =
+#   s (1 + g (1 - s)) is a difference near its zero (g ~ -1.28). In a binary32
+#   evaluation every rounding is a few ulps of the result (covered by EPS)
+#   except the error of 1 - s, which reaches silu' multiplied by s |g| and is
+#   a few ulps of s (s * 2**-22 at most) or, where s rounds to 1, 1 - s
+#   itself; the allowance covers s**2 |g| min(2**-22, 2 (1 - s)) four times;
+#   plus the forward's allowances (2**-148 absolute, and
+#   zero where e^-g overflows binary32, g < G_OVERFLOW: there s = 0 in
+#   binary32 and both halves vanish; |dH| * max(1, |u|) * TINY bounds them).
 BWD_ABS = 2.0 ** -20
 
 
@@ -126,8 +135,12 @@ def swiglu_bwd_bf16_band(dh_bits, gu_bits, cols):
         dh = bf16.to_f32(np.asarray(dh_bits, dtype=np.uint16)[:, :cols]).astype(np.float64)
     with np.errstate(over="ignore", invalid="ignore"):
         t = swiglu_bwd_f64(dh_bits, gu_bits, cols)
-        deep = np.where(g < -87.0, TINY * np.abs(dh) * np.maximum(1.0, np.abs(u)), 0.0)
-        extra = np.concatenate([BWD_ABS * np.abs(dh * u) + deep, deep], axis=1)
+        deep = np.where(g < G_OVERFLOW, TINY * np.abs(dh) * np.maximum(1.0, np.abs(u)), 0.0)
+        sg = 1.0 / (1.0 + np.exp(-g))
+        near_zero = np.where(np.isfinite(g),
+                             BWD_ABS * np.abs(dh * u) * sg * sg * np.abs(g) * np.minimum(1.0, 2.0 ** 21 * (1.0 - sg)),
+                             0.0)
+        extra = np.concatenate([near_zero + deep, deep], axis=1)
         d = EPS * np.abs(t) + 2.0 ** -148 + extra
         d = np.where(np.isfinite(t), d, 0.0)
         return bf16.from_f64_rne(t), bf16.from_f64_rne(t - d), bf16.from_f64_rne(t + d)

@@ -156,9 +156,83 @@ def test_backward_layout_and_band():
     assert np.all(lo_f <= mid_f) and np.all(mid_f <= hi_f)
     un = swiglu.unique_mask(lo, hi)
     assert 0.9 < un.mean() < 1.0
-    # at the zero of silu' the absolute allowance covers binary32 ulps of its terms
+    # at the zero of silu' the absolute allowance covers the error a binary32
+    # evaluation makes there (s^2 |g| times a few 2^-24 in 1 - s: about 2^-26)
     gz = bits([[-1.28125]])                       # the BF16 value nearest the zero
     m, l, h = swiglu.swiglu_bwd_bf16_band(bits([[1.0]]), np.concatenate([gz, bits([[1.0]])], axis=1), 1)
     tz = swiglu.dsilu_f64(bf16.to_f32(gz).astype(np.float64))[0, 0]
     assert abs(tz) < 2e-3
-    assert bf16.to_f32(l)[0, 0] <= tz - 2.0 ** -21 and bf16.to_f32(h)[0, 0] >= tz + 2.0 ** -21
+    lo_f, hi_f = bf16.to_f32(l)[0, 0], bf16.to_f32(h)[0, 0]
+    for e in (-2.0 ** -25, 2.0 ** -25):
+        v = bf16.to_f32(bf16.from_f64_rne(np.array([tz + e])))[0]
+        assert lo_f <= v <= hi_f
+
+
+def _every_gate_value():
+    """Every finite BF16 pattern as float32 gate values."""
+    g = np.arange(65536, dtype=np.uint32).astype(np.uint16)
+    g32 = bf16.to_f32(g)
+    return g[np.isfinite(g32)], g32[np.isfinite(g32)]
+
+
+def _in_band(h_bits, lo, hi):
+    h, l, u = (bf16.to_f32(b).astype(np.float64) for b in (h_bits, lo, hi))
+    return (l <= h) & (h <= u)
+
+
+@pytest.mark.parametrize("u", [1.0, -3.0, 2.0 ** -10, 300.0])
+def test_band_holds_ieee_binary32_evaluation(u):
+    """The reading evaluates silu(g) u = g / (1 + e^-g) * u in binary32. numpy's
+    float32 arithmetic is IEEE binary32 with gradual underflow, so its result,
+    rounded to BF16, must lie in the band for every finite gate value; and
+    wherever that BF16 value is non-zero the band must exclude zero. In
+    particular zero is accepted only where e^-g overflows binary32 (there the
+    binary32 quotient is -0): for g in [-88.72, -64) a binary32 evaluation is
+    non-zero and so must a kernel's be."""
+    gb, g32 = _every_gate_value()
+    C = gb.size
+    ub = bits(np.full(C, u))
+    with np.errstate(over="ignore", invalid="ignore", under="ignore"):
+        u32 = bf16.to_f32(ub)
+        h32 = (g32 / (np.float32(1.0) + np.exp(-g32))) * u32
+    assert h32.dtype == np.float32
+    h = bf16.from_f64_rne(h32.astype(np.float64))
+    mid, lo, hi = swiglu.swiglu_bf16_band(np.concatenate([gb, ub])[None, :], C)
+    ok = _in_band(h[None, :], lo, hi)
+    assert ok.all(), g32[~ok[0]][:8]
+    nz = bf16.to_f32(h) != 0
+    zero_in = (bf16.to_f32(lo)[0] <= 0) & (0 <= bf16.to_f32(hi)[0])
+    assert not (nz & zero_in).any(), g32[nz & zero_in][:8]
+    # the tail in question: non-zero below -64 down to the overflow point
+    tail = (g32 >= swiglu.G_OVERFLOW) & (g32 < -64)
+    assert tail.sum() > 10 and nz[tail].all()
+    # where e^-g overflows binary32 the float32 result is a zero, and the bound
+    # TINY * max(1, |u|) on the exact value holds
+    deep = g32 < swiglu.G_OVERFLOW
+    assert (h32[deep] == 0).all()
+    assert (np.abs(swiglu.silu_f64(g32[deep].astype(np.float64))) < swiglu.TINY).all()
+
+
+@pytest.mark.parametrize("dh,u", [(1e-3, 1.0), (1.0, -3.0), (2.0 ** -10, 300.0)])
+def test_backward_band_holds_ieee_binary32_evaluation(dh, u):
+    """The backward's halves dg = dH u s (1 + g (1 - s)) and du = dH g s with
+    s = 1 / (1 + e^-g), evaluated in binary32 by numpy, lie in the band for
+    every finite gate value, and the band excludes zero wherever that
+    evaluation is non-zero in BF16."""
+    gb, g32 = _every_gate_value()
+    C = gb.size
+    ub, dhb = bits(np.full(C, u)), bits(np.full(C, dh))
+    with np.errstate(over="ignore", invalid="ignore", under="ignore"):
+        u32, dh32 = bf16.to_f32(ub), bf16.to_f32(dhb)
+        s = np.float32(1.0) / (np.float32(1.0) + np.exp(-g32))
+        dg = dh32 * u32 * (s * (np.float32(1.0) + g32 * (np.float32(1.0) - s)))
+        du = dh32 * (g32 * s)
+    h = bf16.from_f64_rne(np.concatenate([dg, du]).astype(np.float64))[None, :]
+    mid, lo, hi = swiglu.swiglu_bwd_bf16_band(dhb[None, :], np.concatenate([gb, ub])[None, :], C)
+    ok = _in_band(h, lo, hi)
+    assert ok.all(), np.concatenate([g32, g32])[~ok[0]][:8]
+    nz = bf16.to_f32(h)[0] != 0
+    zero_in = (bf16.to_f32(lo)[0] <= 0) & (0 <= bf16.to_f32(hi)[0])
+    assert not (nz & zero_in).any()
+    tail = np.concatenate([(g32 >= swiglu.G_OVERFLOW) & (g32 < -64)] * 2)
+    assert nz[tail].all()
