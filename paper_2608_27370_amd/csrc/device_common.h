@@ -51,12 +51,49 @@ __device__ __forceinline__ float exp_f32(float x) {
     return __builtin_amdgcn_exp2f(t) * (1.0f + err * kLn2);
 }
 
+// e^x as m * 2^n, m in [1, 2) within about 2 ulp, n an integer: the exp2
+// instruction only ever sees the fraction of x log2 e, so results that lie
+// below binary32's normal range (where that instruction flushes to zero) keep
+// their significand. For finite x with |x| < 2^24.
+__device__ __forceinline__ float exp_split(float x, int& n) {
+    constexpr float kL2eHi = 1.44269502162933349609375f;
+    constexpr float kL2eLo = 1.925962989e-8f;
+    constexpr float kLn2 = 0.693147180559945309f;
+    const float t = x * kL2eHi;
+    const float err = fmaf(x, kL2eHi, -t) + x * kL2eLo;
+    const float fl = floorf(t);
+    n = (int)fl;
+    return __builtin_amdgcn_exp2f(t - fl) * (1.0f + err * kLn2);
+}
+
+// Gate values below kDeepGate take the scaled evaluation: there 1 + e^-g equals
+// e^-g in binary32, so silu(g) = g e^g, and e^g and the reciprocal of 1 + e^-g
+// approach or leave binary32's normal range. Below kFarGate the result is
+// zero in binary32 (|silu(g)| < 2^-270), and e^-g overflows in the direct
+// evaluation, which then gives -0 as binary32 arithmetic does.
+constexpr float kDeepGate = -64.0f;
+constexpr float kFarGate = -192.0f;
+
+// x * y * z * e^g for g in [kFarGate, kDeepGate): the factors' significands
+// multiplied (magnitude in [1/8, 2)) and the exponents added, then one ldexp,
+// which rounds once (correctly into the subnormal range) instead of flushing;
+// no intermediate product overflows or underflows.
+__device__ __forceinline__ float mul_exp_deep(float x, float y, float z, float g) {
+    int n, ex, ey, ez;
+    const float m = exp_split(g, n);
+    const float mx = __builtin_frexpf(x, &ex);
+    const float my = __builtin_frexpf(y, &ey);
+    const float mz = __builtin_frexpf(z, &ez);
+    return __builtin_ldexpf(mx * my * mz * m, n + ex + ey + ez);
+}
+
 // SwiGLU of one gate/up pair in binary32: silu(g) * u with silu(g) = g / (1 + e^-g),
 // the quotient as g times the reciprocal instruction's 1 / (1 + e^-g) (about
-// 1 ulp); altogether within about 5 ulp of the exact value. For g below about
-// -87.3 the reciprocal falls below binary32's normal range and may flush, and
-// for g < -88.72 e^-g overflows: silu(g) is then -0.
+// 1 ulp); altogether within about 5 ulp of the exact value. Deep in the
+// negative tail (g < -64) silu(g) u = g u e^g in the scaled form above, so
+// that no step flushes a value below binary32's normal range to zero.
 __device__ __forceinline__ float swiglu1(float g, float u) {
+    if (g < kDeepGate && g >= kFarGate) return mul_exp_deep(g, u, 1.0f, g);
     return g * __builtin_amdgcn_rcpf(1.0f + exp_f32(-g)) * u;
 }
 
@@ -71,8 +108,10 @@ __device__ __forceinline__ void swiglu8(const uint32_t g[4], const uint32_t u[4]
 // The SwiGLU's backward for one element in binary32: from dH and the saved
 // gate g and up u, dg = dH * u * silu'(g) with silu'(g) = s (1 + g (1 - s)),
 // s = 1 / (1 + e^-g) (the reciprocal instruction), or du = dH * silu(g) =
-// dH * g * s.
+// dH * g * s. Deep in the negative tail (g < -64, where s = e^g and 1 - s = 1
+// in binary32) dg = dH u e^g (1 + g) and du = dH g e^g in the scaled form.
 __device__ __forceinline__ float swiglu_bwd1(float dh, float g, float u, bool dg) {
+    if (g < kDeepGate && g >= kFarGate) return dg ? mul_exp_deep(dh, u, 1.0f + g, g) : mul_exp_deep(dh, g, 1.0f, g);
     const float sg = __builtin_amdgcn_rcpf(1.0f + exp_f32(-g));
     return dg ? dh * u * (sg * fmaf(g, 1.0f - sg, 1.0f)) : dh * (g * sg);
 }
