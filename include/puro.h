@@ -313,7 +313,10 @@ size_t puro_linear_fwd_workspace_size(int64_t M, int64_t N, int64_t K, const pur
 size_t puro_linear_bwd_workspace_size(int64_t M, int64_t N, int64_t K, const puro_linear_recipe* recipe);
 
 /* Forward: quantise X and W, Y [M, N] (BF16) = Fprop, fill `saved`.
- * Requirements: M, N, K multiples of 16 (of 128 when blockwise). */
+ * Requirements: M, N, K multiples of 16 (of 128 when blockwise) and at most
+ * 2^22 (each is the row pitch of an FP8 operand of one of the three GEMMs);
+ * larger sizes return PURO_ERR_SHAPE before anything is enqueued (this also
+ * holds for the backward). */
 puro_status puro_linear_fwd(const uint16_t* X, const uint16_t* W, int64_t M, int64_t N, int64_t K,
                             const puro_linear_recipe* recipe, uint16_t* Y,
                             const puro_linear_saved* saved, void* ws, size_t ws_bytes,

@@ -13,6 +13,9 @@ namespace {
 
 constexpr int64_t kGroup = 128;
 constexpr size_t kAlign = 256;
+// largest FP8 operand row pitch of the GEMM (bytes): buffer offsets over a
+// 256-row tile stay below 2^31
+constexpr int64_t kMaxPitch = (int64_t)1 << 22;
 
 inline size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 inline bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
@@ -310,7 +313,7 @@ static puro_status check_operand(const puro_fp8_operand* o, int64_t rows, int64_
     if (o->ld < K) return PURO_ERR_SHAPE;
     if ((o->ld % 16) != 0 || !aligned16(o->data)) return PURO_ERR_ALIGN;
     // buffer offsets within one tile of 256 rows stay below 2^31
-    if (o->ld > ((int64_t)1 << 22)) return PURO_ERR_SHAPE;
+    if (o->ld > kMaxPitch) return PURO_ERR_SHAPE;
     switch (o->mode) {
     case PURO_SCALE_TENSOR: *smode = kSTensor; break;
     case PURO_SCALE_ROW_1x128: *smode = kSRow; break;
@@ -349,7 +352,7 @@ puro_status gemm_impl(int64_t M, int64_t N, int64_t K, const puro_fp8_operand* A
         if (d_type != PURO_OUT_BF16 || accumulate) return PURO_ERR_UNSUPPORTED;
         if (bias && !aligned16(bias)) return PURO_ERR_ALIGN;
         // ldr as the operands' pitch: buffer offsets over a tile's rows stay below 2^31
-        if (residual && (ldr < N || ldr > ((int64_t)1 << 22))) return PURO_ERR_SHAPE;
+        if (residual && (ldr < N || ldr > kMaxPitch)) return PURO_ERR_SHAPE;
         if (residual && (!aligned16(residual) || (ldr % 4) != 0)) return PURO_ERR_ALIGN;
         // the residual may be D itself (an in-place residual add), but not overlap it otherwise
         if (residual && residual != D) {
@@ -408,6 +411,10 @@ bool recipe_ok(const puro_linear_recipe* r) {
 puro_status check_linear_dims(int64_t M, int64_t N, int64_t K, const puro_linear_recipe* r) {
     if (!recipe_ok(r)) return PURO_ERR_UNSUPPORTED;
     if (M < 0 || N < 0 || K < 0) return PURO_ERR_SHAPE;
+    // each of M, N and K is the row pitch of an FP8 operand of one of the
+    // three GEMMs (Xq, dYq, the transposed copies), limited to 2^22 bytes;
+    // rejected here, before the quantisers write anything
+    if (M > kMaxPitch || N > kMaxPitch || K > kMaxPitch) return PURO_ERR_SHAPE;
     const int64_t g = r->blockwise ? kGroup : 16;
     if ((M % g) != 0 || (N % g) != 0 || (K % g) != 0) return PURO_ERR_ALIGN;
     return PURO_OK;

@@ -150,6 +150,16 @@ def test_linear_validation(puro):
     need = L.puro_linear_bwd_workspace_size(256, 256, 256, byref(rb))
     assert L.puro_linear_bwd(FAKE, byref(s), 256, 256, 256, byref(rb), FAKE, FAKE, 0, FAKE, need - 1, None) \
         == ERR_WORKSPACE
+    # every dimension is an FP8 operand pitch of one of the GEMMs: above 2^22
+    # the call fails before the quantisers run (with the NULL and FAKE buffers
+    # here, anything enqueued would fault or fail to launch)
+    big = (1 << 22) + 128
+    for dims in ((256, 256, big), (256, big, 256), (big, 256, 256)):
+        for r in (rc, rb):
+            assert L.puro_linear_fwd(FAKE, FAKE, *dims, byref(r), FAKE, byref(s), FAKE, 1 << 62, None) == ERR_SHAPE
+            assert L.puro_linear_bwd(FAKE, byref(s), *dims, byref(r), FAKE, FAKE, 0, FAKE, 1 << 62, None) \
+                == ERR_SHAPE
+            assert L.puro_linear_fwd_workspace_size(*dims, byref(r)) == 0
     sizes = (ctypes.c_size_t * 4)()
     total = L.puro_linear_saved_bytes(256, 512, 384, byref(rb), byref(sizes))
     assert list(sizes) == [384 * 256, 384 * 2 * 4, 384 * 512, 3 * 4 * 4] and total == sum(sizes)
