@@ -1,6 +1,7 @@
 """Build libpuro.so (HIP for gfx950) in-tree with hipcc.
 
-Each source compiles to an object in parallel; the objects link into
+Each source compiles to an object in parallel (the GEMM kernel once per
+variant); the objects link into
 ``paper_2608_27370_amd/libpuro.so``. Packed-FP32 instruction selection is
 disabled for all device code.
 """
@@ -16,16 +17,22 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libpuro.so")
-SOURCES = ("quant.hip", "gemm.hip", "api.cpp")
+# (source, object name, extra flags): the GEMM kernel is compiled once per
+# operand-format pair and scale kind, so that its instantiations build in parallel
+GEMM_VARIANTS = [(fa, fb, g) for fa in (0, 1) for fb in (0, 1) for g in (0, 1)]
+SOURCES = [("quant.hip", "quant", []), ("gemm.hip", "gemm", []), ("api.cpp", "api", [])] + [
+    ("gemm_kernel.hip", "gemm_kernel_%d%d%d" % v, ["-DPURO_FA=%d" % v[0], "-DPURO_FB=%d" % v[1], "-DPURO_GROUPED=%d" % v[2]])
+    for v in GEMM_VARIANTS]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
          "-I", INCLUDE, "-I", CSRC]
 
 
-def _compile(src):
-    obj = os.path.join(BUILD, src + ".o")
-    cmd = [HIPCC] + FLAGS + ["-c", os.path.join(CSRC, src), "-o", obj]
+def _compile(entry):
+    src, name, extra = entry
+    obj = os.path.join(BUILD, name + ".o")
+    cmd = [HIPCC] + FLAGS + extra + ["-c", os.path.join(CSRC, src), "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     # the host pass does not know the device-only target feature; that note is harmless
     err = "\n".join(l for l in r.stderr.splitlines() if "packed-fp32-ops" not in l)
@@ -36,7 +43,7 @@ def _compile(src):
 
 def build(verbose=False):
     os.makedirs(BUILD, exist_ok=True)
-    with concurrent.futures.ThreadPoolExecutor(len(SOURCES)) as ex:
+    with concurrent.futures.ThreadPoolExecutor(min(len(SOURCES), os.cpu_count() or 1)) as ex:
         objs = list(ex.map(_compile, SOURCES))
     tmp = LIB + ".tmp%d" % os.getpid()
     cmd = [HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp] + objs

@@ -1,650 +1,18 @@
-// Scaled FP8 GEMM for gfx950: D[m, n] = sum_k A[m, k] * B[n, k].
-//
-// Section 3.2 of the paper runs the Fprop, Dgrad and Wgrad GEMMs of every
-// linear layer on FP8 operands with higher-precision accumulation; operands
-// carry a per-tensor scale or power-of-two scales per 128 values along k
-// (per row, or per 128x128 block).
-//
-// Design (CDNA4):
-//  * Both operands reduction-contiguous ("TN"); Dgrad and Wgrad are posed
-//    this way by feeding the transposed FP8 copies the quantiser writes.
-//  * Four waves per workgroup, one per SIMD, in a 2x2 grid; workgroup tiles
-//    up to 256x256 (wave tiles up to 128x128, accumulators in AGPRs).
-//  * Operand tiles move global -> LDS by buffer_load ... lds (16 bytes per
-//    lane, no VGPR staging) in k slices of SL = 128 bytes: one 1 KB DMA load
-//    covers 8 rows x 128 bytes, whole cache lines. A ring of NST slices
-//    keeps the next ones in flight while one is multiplied.
-//  * Within a slice the wave works in 64-byte k steps; the fragments of
-//    the next step are read from LDS into a second register set while the
-//    MFMAs of the current one run, and the DMA loads are spread between
-//    the MFMAs too. The loop body has no branches and waits on constant
-//    counts; one barrier per slice.
-//  * LDS rows are XOR-swizzled in 16-byte chunks (conflict-free reads; the
-//    swizzle is applied on the global side because the DMA writes lane l at
-//    base + 16 l).
-//  * v_mfma_scale_f32_32x32x64_f8f6f4: 32x32 outputs per 64-long k step.
-//    Grouped scales become the instruction's E8M0 operands (exact powers of
-//    two, applied inside the MFMA); per-tensor scales multiply the FP32
-//    result once in the epilogue. The instruction is issued with the B tile
-//    as its first operand, so each lane's accumulators hold four consecutive
-//    output columns of one row.
-//  * Out-of-range rows and the k tail are zero-filled by the buffer
-//    descriptor's range check (num_records) rather than by branches.
-//  * Tiles are remapped so the eight XCDs (workgroups are dealt round-robin
-//    to them) each own a contiguous range of tiles, grouped by row panels to
-//    share operand panels in that XCD's L2.
-//  * The epilogue stages each wave's FP32 tile in the idle ring and stores
-//    whole rows; interior tiles take a branch-free path that issues all LDS
-//    reads of a pass before its stores.
-//  * Small grids split K into ranges whose FP32 partial sums a second kernel
-//    adds in a fixed order (deterministic).
+// Host side of the scaled FP8 GEMM: the plan for a problem (tile
+// configuration and k split), its launch, and the fixed-order split-K
+// reduction kernel. The GEMM kernel itself is in gemm_kernel.hip.
 
 #include <type_traits>
 
 #include "device_common.h"
+#include "gemm_common.h"
 #include "kernels.h"
 
 namespace puro {
 
+using namespace gemm_detail;
+
 namespace {
-
-typedef int v8i __attribute__((ext_vector_type(8)));
-typedef float v16f __attribute__((ext_vector_type(16)));
-typedef __attribute__((address_space(3))) void lds_void_t;
-
-constexpr int kBK = 128;                   // k block of the grouped scales (and of split-K ranges)
-constexpr uint32_t kRsrcWord3 = 0x00020000u;  // raw buffer, 32-bit data format
-constexpr uint32_t kOOB = 0x80000000u;     // offset that fails the range check
-
-struct Params {
-    const uint8_t* A;
-    const uint8_t* B;
-    const float* sa;
-    const float* sb;
-    void* D;
-    float* partial;
-    int64_t lda, ldb, ldd;
-    int M, N, K;
-    int a_mode, b_mode;
-    int a_kmajor, b_kmajor;    // grouped scales k-block-major rather than row-major
-    int ld_sa, ld_sb;          // scale pitch: K/128 (row-major) or the row (block) count (k-major)
-    uint32_t sa_bytes, sb_bytes;  // sizes of the scale arrays (grouped modes)
-    int ksteps, ksteps_per_split, splits;
-    int tiles_m, tiles_n;
-    int accumulate;
-    float alpha;               // host-known part of the per-tensor scale (1)
-    const uint16_t* bias;      // OUT kOutBF16Epi: optional bias [N] and residual [M, N] (pitch ldr)
-    const uint16_t* residual;
-    int64_t ldr;
-};
-
-// The bias / residual epilogue: the BF16 bias of columns n..n+3 and the BF16
-// residual of row m at those columns added to four binary32 results (the
-// sum stays binary32 until the output's one rounding).
-__device__ __forceinline__ void add_epilogue4(float4& v, const uint16_t* bias, const uint16_t* residual,
-                                              int64_t ldr, int64_t m, int64_t n) {
-    if (bias) {
-        const uint2 b = *reinterpret_cast<const uint2*>(bias + n);
-        v.x += bf16lo(b.x); v.y += bf16hi(b.x); v.z += bf16lo(b.y); v.w += bf16hi(b.y);
-    }
-    if (residual) {
-        const uint2 r = *reinterpret_cast<const uint2*>(residual + m * ldr + n);
-        v.x += bf16lo(r.x); v.y += bf16hi(r.x); v.z += bf16lo(r.y); v.w += bf16hi(r.y);
-    }
-}
-__device__ __forceinline__ float add_epilogue1(float v, const uint16_t* bias, const uint16_t* residual, int64_t ldr,
-                                               int64_t m, int64_t n) {
-    if (bias) v += __uint_as_float((uint32_t)bias[n] << 16);
-    if (residual) v += __uint_as_float((uint32_t)residual[m * ldr + n] << 16);
-    return v;
-}
-
-// f(std::integral_constant<int, i>) for i = 0 .. N-1, each call with its own
-// compile-time index (no loop left for the unroller to decide on).
-template <int N, int I = 0, class F>
-__device__ __forceinline__ void static_for(F&& f) {
-    if constexpr (I < N) {
-        f(std::integral_constant<int, I>{});
-        static_for<N, I + 1>(f);
-    }
-}
-
-__device__ __forceinline__ uint32_t e8m0_of(float s) { return (__float_as_uint(s) >> 23) & 0xFFu; }
-
-
-typedef int v4i __attribute__((ext_vector_type(4)));
-
-// Raw buffer descriptor (base, num_records bytes; 32-bit data format); every
-// field is made wave-uniform so that it lives in SGPRs.
-__device__ __forceinline__ v4i make_rsrc(const void* base, uint32_t bytes) {
-    const uint64_t a = (uint64_t)base;
-    v4i r;
-    r.x = __builtin_amdgcn_readfirstlane((int)(uint32_t)a);
-    r.y = __builtin_amdgcn_readfirstlane((int)((a >> 32) & 0xFFFFu));
-    r.z = __builtin_amdgcn_readfirstlane((int)bytes);
-    r.w = (int)kRsrcWord3;
-    return r;
-}
-
-// LDS byte address of a __shared__ object (the value M0 takes for a DMA).
-__device__ __forceinline__ uint32_t lds_addr(const void* p) {
-    return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) uint8_t*)p;
-}
-
-// Global -> LDS DMA of BYTES (16 or 4) per lane: lane l's data lands at
-// LDS address lds + BYTES * l; offsets at or beyond the descriptor's
-// num_records read as zero. Issued from inline assembly so that the
-// compiler, which cannot tell which LDS bytes a DMA writes, does not make
-// every later LDS read wait for it: the kernel waits explicitly
-// (s_waitcnt vmcnt(0) + barrier) before reading a stage. M0 is saved and
-// restored around the DMA (the compiler may keep a value there), and one wait
-// state separates the M0 write from the DMA that reads it.
-template <int BYTES>
-__device__ __forceinline__ void dma_to_lds(v4i rsrc, uint32_t lds, uint32_t voff) {
-    lds = (uint32_t)__builtin_amdgcn_readfirstlane((int)lds);   // wave-uniform by construction
-    uint32_t saved;
-    if constexpr (BYTES == 16)
-        asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\ts_nop 0\n\t"
-                     "buffer_load_dwordx4 %2, %3, 0 offen lds\n\ts_mov_b32 m0, %0"
-                     : "=&s"(saved) : "s"(lds), "v"(voff), "s"(rsrc) : "memory");
-    else
-        asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\ts_nop 0\n\t"
-                     "buffer_load_dword %2, %3, 0 offen lds\n\ts_mov_b32 m0, %0"
-                     : "=&s"(saved) : "s"(lds), "v"(voff), "s"(rsrc) : "memory");
-}
-
-// PROD: the workgroup has NW more waves that only issue the global->LDS
-// loads (producers); the NW MFMA waves (consumers) then only read LDS and
-// multiply, so a load that cannot issue (the texture unit's queue full)
-// does not hold up their matrix instructions. Both kinds meet at the one
-// barrier per slice.
-template <int BM, int BN, int WM, int WN, int FA, int FB, int OUT, bool GROUPED, int GM, int SL, int NST, bool PROD>
-__global__ __launch_bounds__(WM * WN * 64 * (PROD ? 2 : 1)) void gemm_fp8_kernel(Params p) {
-    constexpr int NW = WM * WN;
-    constexpr int WTM = BM / WM, WTN = BN / WN;
-    constexpr int FM = WTM / 32, FN = WTN / 32;
-    constexpr int KH = SL / 64;                     // 64-byte MFMA k steps per slice
-    constexpr int A_BYTES = BM * SL, B_BYTES = BN * SL;
-    constexpr int STAGE = A_BYTES + B_BYTES;        // one SL-byte k slice of both tiles
-    // 1 KB DMA loads (RPL rows of SL bytes) per wave and slice; when the row
-    // blocks do not divide evenly, the surplus loads repeat earlier blocks
-    // (the same bytes to the same place), so every wave issues the same
-    // number of loads and can wait on an exact count
-    constexpr int RPL = 1024 / SL;                  // rows per DMA load
-    constexpr int CPR = SL / 16;                    // 16-byte chunks per LDS row
-    constexpr int A_BLK = BM / RPL, B_BLK = BN / RPL;
-    constexpr int A_PER = (A_BLK + NW - 1) / NW, B_PER = (B_BLK + NW - 1) / NW;
-    constexpr int SC_BLK = (BM + BN) / 64;          // 64 scales per 4-byte DMA load
-    constexpr int SC_PER = GROUPED ? (SC_BLK + NW - 1) / NW : 0;
-    constexpr int LOADS = A_PER + B_PER + SC_PER;
-    static_assert(SL == 64 || SL == 128, "slice width");
-    static_assert(BM % 32 == 0 && BN % 32 == 0 && (BM + BN) % 64 == 0, "tile shape");
-    static_assert(NST >= 2 && (NST - 1) * LOADS <= 63, "pipeline depth");
-
-    __shared__ __attribute__((aligned(1024))) uint8_t smem[NST * STAGE];
-    // grouped scales of a slice's rows (A then B), float, DMA'd like the operands
-    __shared__ __attribute__((aligned(16))) float ssc[GROUPED ? NST * (BM + BN) : 1];
-
-    const int tid = threadIdx.x;
-    const int lane = tid & 63;
-    const int wave_id = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const bool producer = PROD && wave_id >= NW;
-    // consumer waves 0..NW-1; a producer takes the DMA share of consumer wave_id - NW
-    const int wave = producer ? wave_id - NW : wave_id;
-    const int wm = wave / WN, wn = wave % WN;
-
-    // ---- tile index: contiguous ranges per XCD, grouped by GM row panels
-    const int T = gridDim.x;
-    const int b = blockIdx.x;
-    const int lt = (T % 8 == 0) ? (b % 8) * (T / 8) + b / 8 : b;
-    const int per_split = p.tiles_m * p.tiles_n;
-    const int ks = lt / per_split;
-    const int rem = lt - ks * per_split;
-    const int group = rem / (GM * p.tiles_n);
-    const int first_m = group * GM;
-    const int gsz = min(GM, p.tiles_m - first_m);
-    const int r2 = rem - group * GM * p.tiles_n;
-    const int tm = first_m + r2 % gsz, tn = r2 / gsz;
-    const int m0 = tm * BM, n0 = tn * BN;
-    // per-tensor scales, applied to the FP32 sums in the epilogue (loaded
-    // here so that their latency hides behind the main loop)
-    float alpha = p.alpha;
-    if (OUT != 2) {
-        if (p.a_mode == kSTensor) alpha *= p.sa[0];
-        if (p.b_mode == kSTensor) alpha *= p.sb[0];
-    }
-    // k slices [s0, s1) of SL bytes: this split's 128-wide k blocks
-    constexpr int SPB = kBK / SL;                   // slices per 128-wide k block
-    const int s0 = SPB * ks * p.ksteps_per_split;
-    const int s1 = SPB * min((ks + 1) * p.ksteps_per_split, p.ksteps);
-
-    const int valid_m = min(BM, p.M - m0), valid_n = min(BN, p.N - n0);
-    const v4i ra = make_rsrc(p.A + (int64_t)m0 * p.lda, (uint32_t)(valid_m * p.lda));
-    const v4i rb = make_rsrc(p.B + (int64_t)n0 * p.ldb, (uint32_t)(valid_n * p.ldb));
-
-    // LDS layout of a slice: row r of a tile is SL bytes (CPR 16-byte chunks)
-    // and its logical chunk c sits at position c ^ key(r). The 16 (or 8)
-    // lanes of a ds_read_b128 phase read 16 (8) consecutive rows at the same
-    // logical chunk; the keys make them hit distinct banks with 64 (32)
-    // four-byte banks:
-    //  * SL = 64, key(r) = ((r >> 1) & 3) ^ ((r >> 3) & 1): of 16 consecutive
-    //    rows, those sharing a 64-byte position in a 256-byte bank line get
-    //    distinct keys, and so do those of 8 rows in a 128-byte line;
-    //  * SL = 128, key(r) = (r & 7) ^ ((r >> 3) & 1): of 16 consecutive rows
-    //    the 8 even (odd) ones, which share the lower (upper) half of a
-    //    256-byte bank line, get distinct keys, and 8 consecutive rows in a
-    //    128-byte line get the keys 0..7.
-    // Lane l of a DMA load fills row RPL * blk + l / CPR at position l % CPR,
-    // so it fetches the logical chunk (l % CPR) ^ key(row) of that row.
-    auto row_key = [](int r) { return SL == 64 ? ((r >> 1) & 3) ^ ((r >> 3) & 1) : (r & 7) ^ ((r >> 3) & 1); };
-    // logical k byte a lane fetches in a load of an even / odd row block
-    const int kch0 = ((lane % CPR) ^ row_key(lane / CPR)) * 16;
-    const int kch1 = ((lane % CPR) ^ row_key(RPL + lane / CPR)) * 16;
-    const uint32_t rowA = (uint32_t)((lane / CPR) * p.lda), rowB = (uint32_t)((lane / CPR) * p.ldb);
-    const uint32_t blkA = (uint32_t)(RPL * p.lda), blkB = (uint32_t)(RPL * p.ldb);
-    const uint32_t smem_lds = lds_addr(smem);
-    const uint32_t ssc_lds = lds_addr(ssc);
-
-    v4i rsa{}, rsb{};
-    // Scale load j of this wave brings entries 64 t .. 64 t + 63 (t = its
-    // chunk) of a slice's scale vector: BM entries for A, then BN for B. A
-    // row-scaled operand has one entry per tile row, a block-scaled one one
-    // per 128-row block (entries past that are unused). The element lane l
-    // loads for k block kb is sc_base[j] + kb * sc_kstride[j] (row-major
-    // scales: stride 1; k-major: the array's row pitch), or nothing when
-    // sc_base[j] < 0; all of it is fixed before the main loop.
-    int sc_base[SC_PER > 0 ? SC_PER : 1], sc_kstride[SC_PER > 0 ? SC_PER : 1];
-    bool sc_is_a[SC_PER > 0 ? SC_PER : 1];
-    if constexpr (GROUPED) {
-        rsa = make_rsrc(p.sa, p.a_mode == kSTensor ? 0u : p.sa_bytes);
-        rsb = make_rsrc(p.sb, p.b_mode == kSTensor ? 0u : p.sb_bytes);
-#pragma unroll
-        for (int j = 0; j < SC_PER; ++j) {
-            const int t = (wave * SC_PER + j) % SC_BLK;
-            const bool is_a = t * 64 < BM;
-            const int r = t * 64 + lane - (is_a ? 0 : BM);
-            const int mode = is_a ? p.a_mode : p.b_mode;
-            const bool km = is_a ? p.a_kmajor : p.b_kmajor;
-            const int ld = is_a ? p.ld_sa : p.ld_sb;
-            const int row0 = is_a ? m0 : n0;
-            const int rows = is_a ? p.M : p.N;
-            int unit = -1;   // row (row scales) or 128-row block (block scales) of this lane's entry
-            if (mode == kSBlock) {
-                // the 128-row blocks the tile's rows touch: from row0's to (row0 + BM - 1)'s
-                const int b = (row0 >> 7) + r;
-                const int last = (row0 + (is_a ? BM : BN) - 1) >> 7;
-                if (b <= last && b < (rows + 127) >> 7) unit = b;
-            } else if (mode == kSRow) {
-                if (row0 + r < rows) unit = row0 + r;
-            }
-            sc_is_a[j] = is_a;
-            sc_base[j] = unit < 0 ? -1 : (km ? unit : unit * ld);
-            sc_kstride[j] = km ? ld : 1;
-        }
-    }
-    (void)sc_base; (void)sc_kstride; (void)sc_is_a;
-
-    // DMA load q (0 <= q < LOADS) of this wave for slice `sl` into ring
-    // stage `st`. With `valid` false the load still issues (so that every
-    // wave always has the same number in flight and waits on constant
-    // counts) but reads out of range: no memory traffic, zeros into a stage
-    // no later slice uses.
-    auto dma_one = [&](int st, int sl, int q, bool valid) __attribute__((always_inline)) {
-        const int k0 = sl * SL;
-        const uint32_t sbase = smem_lds + st * STAGE;
-        if (q < A_PER + B_PER) {
-            const bool is_a = q < A_PER;
-            const int blk = is_a ? (wave * A_PER + q) % A_BLK : (wave * B_PER + (q - A_PER)) % B_BLK;
-            const int kch = (blk & 1) ? kch1 : kch0;
-            // the k tail (K % SL != 0) also reads out of range on purpose: zeros
-            const uint32_t off = (valid && k0 + kch < p.K) ? (uint32_t)(k0 + kch) : kOOB;
-            if (is_a) dma_to_lds<16>(ra, sbase + blk * 1024, rowA + blk * blkA + off);
-            else dma_to_lds<16>(rb, sbase + A_BYTES + blk * 1024, rowB + blk * blkB + off);
-        } else if constexpr (GROUPED) {
-            const int j = q - A_PER - B_PER;
-            const int t = (wave * SC_PER + j) % SC_BLK;
-            const int kb = sl / SPB;
-            const uint32_t soff = (valid && sc_base[j] >= 0) ? (uint32_t)(sc_base[j] + kb * sc_kstride[j]) * 4u : kOOB;
-            const uint32_t dst = ssc_lds + (st * (BM + BN) + t * 64) * 4;
-            dma_to_lds<4>(sc_is_a[j] ? rsa : rsb, dst, soff);
-        }
-    };
-
-    v16f acc[FM][FN];
-#pragma unroll
-    for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int j = 0; j < FN; ++j)
-#pragma unroll
-            for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
-
-    const int fr = lane & 31;                 // fragment row of this lane
-    const int c0 = (lane >> 5) * 2;           // first of this lane's two chunks in a 64-byte k step
-    // key of the lane's fragment rows (fragments start at multiples of 32)
-    const int key = row_key(fr);
-
-    // The operand fragments of one 64-byte k step as this wave holds them:
-    // for each 32-row fragment (A fragments first) 32 bytes of k per lane,
-    // bytes 32 (l >> 5) .. + 31 of the step in row l & 31, from two 16-byte
-    // LDS reads; and the E8M0 scale of each fragment row.
-    struct Frags {
-        v8i f[FM + FN];
-        uint32_t sc[FM + FN];
-    };
-    // the LDS entry of each fragment row's scale within a stage's scale
-    // vector (block scales: the row's 128-row block counted from the block
-    // of the tile's first row, which need not start a block when the tile
-    // is 192 rows), and whether the operand has grouped scales at all
-    int sc_off[FM + FN];
-    bool sc_on[FM + FN];
-#pragma unroll
-    for (int fi = 0; fi < FM + FN; ++fi) {
-        const bool is_a = fi < FM;
-        const int r = is_a ? wm * WTM + fi * 32 + fr : wn * WTN + (fi - FM) * 32 + fr;   // tile row
-        const int row0 = is_a ? m0 : n0;
-        const int mode = is_a ? p.a_mode : p.b_mode;
-        sc_off[fi] = (is_a ? 0 : BM) + (mode == kSBlock ? ((row0 + r) >> 7) - (row0 >> 7) : r);
-        sc_on[fi] = mode != kSTensor;
-    }
-    // read piece t of k step h of the slice in stage st: t < FM + FN are
-    // the operand fragments, the rest the scales
-    constexpr int NPIECE = (FM + FN) * (GROUPED ? 2 : 1);
-    auto read_piece = [&](Frags& f, int st, int h, int t) __attribute__((always_inline)) {
-        if (t < FM + FN) {
-            const uint8_t* row = t < FM ? smem + st * STAGE + (wm * WTM + t * 32 + fr) * SL
-                                        : smem + st * STAGE + A_BYTES + (wn * WTN + (t - FM) * 32 + fr) * SL;
-            const int cc = 4 * h + c0;
-            const v4i lo = *reinterpret_cast<const v4i*>(row + ((cc ^ key) << 4));
-            const v4i hi = *reinterpret_cast<const v4i*>(row + (((cc + 1) ^ key) << 4));
-            f.f[t] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-        } else {
-            const int fi = t - (FM + FN);
-            const uint32_t e = e8m0_of(ssc[st * (BM + BN) + sc_off[fi]]);
-            f.sc[fi] = sc_on[fi] ? e : 127u;
-        }
-    };
-    auto mfma_one = [&](const Frags& f, int t) __attribute__((always_inline)) {
-        const int i = t / FN, j = t % FN;
-        if constexpr (GROUPED)
-            acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
-                f.f[FM + j], f.f[i], acc[i][j], FB, FA, 0, (int)f.sc[FM + j], 0, (int)f.sc[i]);
-        else
-            acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
-                f.f[FM + j], f.f[i], acc[i][j], FB, FA, 0, 127, 0, 127);
-    };
-
-    // One pipeline step: the MFMAs of k step h of slice sl (fragments in
-    // `cur`, read during the previous step) with the LDS reads of the next
-    // k step (into `nxt`) and, in a slice's last k step, the DMA loads of
-    // slice sl + NST interleaved between them, so that LDS and memory
-    // latency hide behind the MFMAs.
-    // Before the reads of the next slice (in its last k step) a wave waits
-    // until at most NST - 2 slices of its DMA loads remain in flight (every
-    // wave always has NST - 1 in flight then, so its loads of slice sl + 1
-    // have landed) and until its reads of slice sl are complete
-    // (lgkmcnt(0)). After the barrier every wave is at that point: slice
-    // sl + 1 is in LDS and the stage of slice sl is free for the DMA of slice
-    // sl + NST. The loop body has no branches: reads past the last slice
-    // fetch stale LDS data that is never used, and DMA loads past it read
-    // nothing.
-    constexpr int NMFMA = FM * FN;
-    auto step = [&](int sl, int h, Frags& cur, Frags& nxt) __attribute__((always_inline)) {
-        const bool last = h == KH - 1;
-        if (last) {
-            if constexpr (PROD)
-                asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-            else
-                asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)" :: "n"((NST - 2) * LOADS) : "memory");
-            __syncthreads();
-        }
-        const int st = (sl - s0) % NST;
-        const int rst = last ? (sl + 1 - s0) % NST : st;   // stage and k step read into nxt
-        const int rh = last ? 0 : h + 1;
-        const bool refill = sl + NST < s1;
-        // read piece u goes after MFMA u * NMFMA / NPIECE, DMA load q after
-        // MFMA q * NMFMA / LOADS (constant loop bounds, so that everything
-        // unrolls and the fragments stay in registers)
-#pragma unroll
-        for (int t = 0; t < NMFMA; ++t) {
-            mfma_one(cur, t);
-#pragma unroll
-            for (int u = 0; u < NPIECE; ++u)
-                if (u * NMFMA / NPIECE == t) read_piece(nxt, rst, rh, u);
-            if (last && !PROD) {
-#pragma unroll
-                for (int q = 0; q < LOADS; ++q)
-                    if (q * NMFMA / LOADS == t) dma_one(st, sl + NST, q, refill);
-            }
-            __builtin_amdgcn_sched_barrier(0);
-        }
-    };
-
-    // prologue: slices s0 .. s0 + NST - 1 in flight, then k step 0 of slice s0 read
-    if (!PROD || producer) {
-#pragma unroll
-        for (int t = 0; t < NST; ++t)
-#pragma unroll
-            for (int q = 0; q < LOADS; ++q) dma_one(t, s0 + t, q, s0 + t < s1);
-        asm volatile("s_waitcnt vmcnt(%0)" :: "n"((NST - 1) * LOADS) : "memory");
-    }
-    __syncthreads();
-    if constexpr (PROD) {
-        if (producer) {
-            // per slice: slice sl + 1 landed, then (after the barrier at which
-            // the consumers have read all of slice sl) its stage refilled with
-            // slice sl + NST; the same barriers as the consumers' loop and
-            // epilogue
-            for (int sl = s0; sl < s1; ++sl) {
-                asm volatile("s_waitcnt vmcnt(%0)" :: "n"((NST - 2) * LOADS) : "memory");
-                __syncthreads();
-                const int st = (sl - s0) % NST;
-#pragma unroll
-                for (int q = 0; q < LOADS; ++q) dma_one(st, sl + NST, q, sl + NST < s1);
-            }
-            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-            __syncthreads();   // the epilogue's barrier: the ring is idle
-            return;
-        }
-    }
-    Frags F0, F1;
-#pragma unroll
-    for (int t = 0; t < NPIECE; ++t) read_piece(F0, 0, 0, t);
-    if constexpr (KH == 2) {
-        for (int sl = s0; sl < s1; ++sl) {
-            step(sl, 0, F0, F1);
-            step(sl, 1, F1, F0);
-        }
-    } else {
-        int sl = s0;
-        for (; sl + 1 < s1; sl += 2) {
-            step(sl, 0, F0, F1);
-            step(sl + 1, 0, F1, F0);
-        }
-        if (sl < s1) step(sl, 0, F0, F1);
-    }
-    // the loads issued for slices past the end write zeros into the ring,
-    // which the epilogue reuses: let them land first
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-
-    // ---- epilogue. Lane l holds, for fragment (i, j), wave-tile row
-    // i*32 + (l & 31) and columns j*32 + 8g + 4(l >> 5) + {0..3}, g = 0..3.
-    // Written straight to memory that would scatter 16-byte pieces over 32
-    // rows per store; instead each wave stages its FP32 tile in its own part
-    // of the (now idle) stage buffers, 16-byte chunks XOR-swizzled by row so
-    // that both the writes and the row reads are free of bank conflicts, and
-    // then stores whole rows: consecutive lanes on consecutive 16-byte chunks
-    // (4 FP32 values), converted and scaled on the way out.
-    constexpr int ROWB = WTN * 4;                 // bytes of one staged wave-tile row (FP32)
-    constexpr int ECPR = ROWB / 16;               // 16-byte chunks per staged row
-    constexpr int REGION = NST * STAGE / NW;      // LDS bytes per wave
-    constexpr int RFIT = REGION / ROWB;          // rows that fit in the region
-    // rows per pass: WTM halved until it fits
-    constexpr int RPP = WTM <= RFIT ? WTM : (WTM / 2 <= RFIT ? WTM / 2 : WTM / 4);
-    // XOR key of the chunk swizzle: 16 distinct keys when rows have 16*k chunks, else 8
-    constexpr int SWZ = (ECPR % 16 == 0) ? 15 : 7;
-    static_assert(RPP >= 32 && WTM % RPP == 0 && (RPP * ECPR) % 64 == 0, "epilogue tiling");
-    static_assert(ECPR % 8 == 0, "row swizzle needs 8k chunks per row");
-    uint8_t* ep = smem + wave * REGION;
-    const int mrow0 = m0 + wm * WTM;
-    const int ncol0 = n0 + wn * WTN;
-    float* const part = p.partial + (int64_t)ks * p.M * p.N;
-    // a tile inside the matrix whose sums overwrite the output stores whole
-    // 4-column vectors everywhere: a branch-free path that issues all of a
-    // pass's LDS reads before its stores
-    const bool fast = m0 + BM <= p.M && n0 + BN <= p.N && (OUT == 2 || !p.accumulate);
-    // the bias of the lane's columns in the fast path below: lane chunk
-    // (it * 64 + lane) % ECPR repeats with period ECPR / gcd(64, ECPR) in it
-    constexpr int EP = ECPR / ((ECPR & -ECPR) < 64 ? (ECPR & -ECPR) : 64);
-    uint2 eb[OUT == kOutBF16Epi ? EP : 1];
-    if constexpr (OUT == kOutBF16Epi) {
-        const __amdgpu_buffer_rsrc_t rb = __builtin_amdgcn_make_buffer_rsrc(
-            const_cast<uint16_t*>(p.bias), 0, p.bias ? p.N * 2 : 0, 0x00020000);
-#pragma unroll
-        for (int it = 0; it < EP; ++it)
-            eb[it] = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(
-                rb, (uint32_t)((ncol0 + ((it * 64 + lane) % ECPR) * 4) * 2), 0, 0));
-    }
-    __syncthreads();   // every wave is done with the last stage
-    // one pass per constant: the accumulators are indexed by the pass, and a
-    // loop the unroller leaves rolled would move them to scratch memory
-    static_for<WTM / RPP>([&](auto pass_c) __attribute__((always_inline)) {
-        constexpr int pass = decltype(pass_c)::value;
-#pragma unroll
-        for (int ii = 0; ii < RPP / 32; ++ii) {
-            const int i = pass * (RPP / 32) + ii;
-            const int r = ii * 32 + (lane & 31);
-#pragma unroll
-            for (int j = 0; j < FN; ++j)
-#pragma unroll
-                for (int g = 0; g < 4; ++g) {
-                    const int chunk = j * 8 + g * 2 + (lane >> 5);
-                    float4 v = make_float4(acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2],
-                                           acc[i][j][4 * g + 3]);
-                    *reinterpret_cast<float4*>(ep + r * ROWB + ((chunk ^ (r & SWZ)) << 4)) = v;
-                }
-        }
-        // the region belongs to this wave alone: once its own writes are
-        // done other lanes of the wave may read them (and the next pass
-        // writes only after this pass's reads have returned their data)
-        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-        constexpr int IT = RPP * ECPR / 64;
-        if (fast) {
-            // the epilogue terms are loaded before the LDS reads of their
-            // group of iterations, so that their latency overlaps those reads
-            // and the group's stores wait once (a load issued after stores
-            // waits for them); buffer loads, so an absent term costs no
-            // branch and no traffic. Groups of at most 16 iterations keep the
-            // residual and the staged values in registers beside the
-            // accumulators of the passes still to come.
-            constexpr int EG = (OUT == kOutBF16Epi && IT > 16) ? IT / 2 : IT;
-            static_assert(IT % EG == 0, "epilogue groups");
-#pragma unroll
-            for (int g0 = 0; g0 < IT; g0 += EG) {
-                uint2 er[OUT == kOutBF16Epi ? EG : 1];
-                if constexpr (OUT == kOutBF16Epi) {
-                    const int64_t mt = mrow0 + pass * RPP;           // the pass's first row
-                    const __amdgpu_buffer_rsrc_t rr = __builtin_amdgcn_make_buffer_rsrc(
-                        const_cast<uint16_t*>(p.residual ? p.residual + mt * p.ldr : p.residual), 0,
-                        p.residual ? (int)((RPP - 1) * p.ldr * 2 + (int64_t)(ncol0 + WTN) * 2) : 0, 0x00020000);
-#pragma unroll
-                    for (int e = 0; e < EG; ++e) {
-                        const int q = (g0 + e) * 64 + lane;
-                        const int r = q / ECPR, c = q % ECPR;
-                        er[e] = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(
-                            rr, (uint32_t)((r * p.ldr + ncol0 + c * 4) * 2), 0, 0));
-                    }
-                }
-                float4 v[EG];
-#pragma unroll
-                for (int e = 0; e < EG; ++e) {
-                    const int q = (g0 + e) * 64 + lane;
-                    const int r = q / ECPR, c = q % ECPR;
-                    v[e] = *reinterpret_cast<const float4*>(ep + r * ROWB + ((c ^ (r & SWZ)) << 4));
-                }
-#pragma unroll
-                for (int e = 0; e < EG; ++e) {
-                    const int it = g0 + e;
-                    const int q = it * 64 + lane;
-                    const int r = q / ECPR, c = q % ECPR;
-                    const int64_t m = mrow0 + pass * RPP + r;
-                    const int n = ncol0 + c * 4;
-                    float4 w = v[e];
-                    if constexpr (OUT == 2) {
-                        *reinterpret_cast<float4*>(part + m * p.N + n) = w;
-                    } else {
-                        w.x *= alpha; w.y *= alpha; w.z *= alpha; w.w *= alpha;
-                        if constexpr (OUT == kOutBF16Epi) {
-                            // each term only when given: adding +0 would turn a -0 sum into +0
-                            if (p.bias) {
-                                const uint2 b = eb[it % EP];
-                                w.x += bf16lo(b.x); w.y += bf16hi(b.x); w.z += bf16lo(b.y); w.w += bf16hi(b.y);
-                            }
-                            if (p.residual) {
-                                const uint2 rv = er[e];
-                                w.x += bf16lo(rv.x); w.y += bf16hi(rv.x); w.z += bf16lo(rv.y); w.w += bf16hi(rv.y);
-                            }
-                        }
-                        if constexpr (OUT == kOutF32)
-                            *reinterpret_cast<float4*>(reinterpret_cast<float*>(p.D) + m * p.ldd + n) = w;
-                        else
-                            *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(p.D) + m * p.ldd + n) =
-                                make_uint2(pack_bf16x2(w.x, w.y), pack_bf16x2(w.z, w.w));
-                    }
-                }
-            }
-            return;
-        }
-#pragma unroll
-        for (int it = 0; it < IT; ++it) {
-            const int q = it * 64 + lane;
-            const int r = q / ECPR, c = q % ECPR;
-            float4 v = *reinterpret_cast<const float4*>(ep + r * ROWB + ((c ^ (r & SWZ)) << 4));
-            const int m = mrow0 + pass * RPP + r;
-            const int n = ncol0 + c * 4;
-            if (m >= p.M || n >= p.N) continue;
-            if constexpr (OUT == 2) {
-                // split-K partial sums, dense [splits][M][N] FP32 (N % 4 == 0)
-                *reinterpret_cast<float4*>(part + (int64_t)m * p.N + n) = v;
-                continue;
-            }
-            v.x *= alpha; v.y *= alpha; v.z *= alpha; v.w *= alpha;
-            if (n + 3 < p.N) {
-                if constexpr (OUT == kOutBF16Epi) add_epilogue4(v, p.bias, p.residual, p.ldr, m, n);
-                if constexpr (OUT == kOutF32) {
-                    float4* dst = reinterpret_cast<float4*>(reinterpret_cast<float*>(p.D) + (int64_t)m * p.ldd + n);
-                    if (p.accumulate) {
-                        const float4 o = *dst;
-                        v.x += o.x; v.y += o.y; v.z += o.z; v.w += o.w;
-                    }
-                    *dst = v;
-                } else {
-                    uint2* dst = reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(p.D) + (int64_t)m * p.ldd + n);
-                    if (p.accumulate) {
-                        const uint2 o = *dst;
-                        v.x += bf16lo(o.x); v.y += bf16hi(o.x); v.z += bf16lo(o.y); v.w += bf16hi(o.y);
-                    }
-                    *dst = make_uint2(pack_bf16x2(v.x, v.y), pack_bf16x2(v.z, v.w));
-                }
-            } else {
-                // ragged right edge: element by element
-                const float vv[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-                for (int t = 0; t < 4; ++t) {
-                    if (n + t >= p.N) continue;
-                    if constexpr (OUT == kOutF32) {
-                        float* dst = reinterpret_cast<float*>(p.D) + (int64_t)m * p.ldd + n + t;
-                        *dst = p.accumulate ? *dst + vv[t] : vv[t];
-                    } else {
-                        uint16_t* dst = reinterpret_cast<uint16_t*>(p.D) + (int64_t)m * p.ldd + n + t;
-                        float o = p.accumulate ? vv[t] + __uint_as_float((uint32_t)*dst << 16) : vv[t];
-                        if constexpr (OUT == kOutBF16Epi) o = add_epilogue1(o, p.bias, p.residual, p.ldr, m, n + t);
-                        *dst = to_bf16(o);
-                    }
-                }
-            }
-        }
-    });
-}
 
 // Fixed-order sum of the split-K partials, scaling and output conversion.
 template <int OUT>
@@ -687,31 +55,6 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restr
 
 // ---- tile configurations and the plan for a problem ---------------------------
 
-struct TileCfg {
-    int bm, bn;          // workgroup tile
-    int wm, wn;          // wave grid (wave tile bm/wm x bn/wn)
-    int sl, nst;         // k bytes per pipeline slice, ring stages
-    int prod;            // producer waves issue the global->LDS loads
-    float fixed_us;      // time model: per wave of work units ...
-    float slice_us;      // ... plus per k slice of a unit (MI355X, all CUs busy)
-};
-// Four MFMA waves (one per SIMD) in a 2x2 grid. The large wave tiles need
-// the least LDS traffic per MFMA (128x128: 16 MFMAs per 16 KB of fragment
-// reads); the 128x128 tiles give more work units on narrow problems, with a
-// deep ring (one workgroup per CU) or a short one (two per CU). A 128x128
-// tile moves as many bytes global->LDS per k slice as the texture unit
-// passes (about 64 B per clock per CU) while its MFMAs run, so its loads
-// often wait for queue space: the deep-ring variant adds four producer waves
-// that issue them (the tile's registers leave room for two waves per SIMD),
-// 15-20% faster on long-K Wgrad than issuing them from the MFMA waves. The
-// time constants are least-squares fits to measured kernel times on the
-// Qwen2-1.5B layer shapes.
-#define PURO_TILE_LIST(X)                                 \
-    X(0, 256, 256, 2, 2, 128, 2, 0, 7.86f, 1.322f)        \
-    X(1, 256, 192, 2, 2, 128, 2, 0, 6.37f, 1.120f)        \
-    X(2, 128, 128, 2, 2, 128, 4, 1, 6.65f, 0.379f)        \
-    X(3, 128, 128, 2, 2, 128, 2, 0, 4.37f, 0.803f)
-#define PURO_TILE_ROW(i, bm, bn, wm, wn, sl, nst, prod, f, s) {bm, bn, wm, wn, sl, nst, prod, f, s},
 constexpr TileCfg kTiles[] = {PURO_TILE_LIST(PURO_TILE_ROW)};
 constexpr int kNumTiles = sizeof(kTiles) / sizeof(kTiles[0]);
 constexpr int kCUs = 256;
@@ -763,36 +106,6 @@ Plan make_plan(int64_t M, int64_t N, int64_t K, bool grouped) {
     return best;
 }
 
-template <int BM, int BN, int WM, int WN, int SL, int NST, int PROD, int FA, int FB, int OUT>
-void launch_cfg(const Params& prm, bool grouped, int grid, hipStream_t stream) {
-    // tile rows per group of the XCD ranges: the QKV Wgrad's 24-tile ranges
-    // become 4 x 6 tiles (10 operand panels per XCD instead of 11 at 8),
-    // and the 32-tile ranges of one-tile-per-CU GEMMs stay at 12 panels
-    constexpr int GM = 4;
-    constexpr int threads = WM * WN * 64 * (PROD ? 2 : 1);
-    if (grouped)
-        gemm_fp8_kernel<BM, BN, WM, WN, FA, FB, OUT, true, GM, SL, NST, PROD != 0><<<grid, threads, 0, stream>>>(prm);
-    else
-        gemm_fp8_kernel<BM, BN, WM, WN, FA, FB, OUT, false, GM, SL, NST, PROD != 0><<<grid, threads, 0, stream>>>(prm);
-}
-
-template <int BM, int BN, int WM, int WN, int SL, int NST, int PROD, int FA, int FB>
-void launch_tile(const Params& prm, int out, bool grouped, int grid, hipStream_t stream) {
-    if (out == 2) launch_cfg<BM, BN, WM, WN, SL, NST, PROD, FA, FB, 2>(prm, grouped, grid, stream);
-    else if (out == kOutF32) launch_cfg<BM, BN, WM, WN, SL, NST, PROD, FA, FB, kOutF32>(prm, grouped, grid, stream);
-    else if (out == kOutBF16Epi)
-        launch_cfg<BM, BN, WM, WN, SL, NST, PROD, FA, FB, kOutBF16Epi>(prm, grouped, grid, stream);
-    else launch_cfg<BM, BN, WM, WN, SL, NST, PROD, FA, FB, kOutBF16>(prm, grouped, grid, stream);
-}
-
-template <int FA, int FB>
-void launch_fmt(const Params& prm, int cfg, int out, bool grouped, int grid, hipStream_t stream) {
-#define PURO_TILE_CASE(i, bm, bn, wm, wn, sl, nst, prod, f, s) \
-    case i: launch_tile<bm, bn, wm, wn, sl, nst, prod, FA, FB>(prm, out, grouped, grid, stream); break;
-    switch (cfg) { PURO_TILE_LIST(PURO_TILE_CASE) }
-#undef PURO_TILE_CASE
-}
-
 size_t plan_workspace_bytes(int64_t M, int64_t N, const Plan& pl) {
     if (pl.splits <= 1) return 0;
     return (size_t)pl.splits * (size_t)M * (size_t)N * sizeof(float);
@@ -834,10 +147,17 @@ void run_plan(const GemmProblem& g, const Plan& pl, void* ws, hipStream_t stream
     const bool grouped = g.sa_mode != kSTensor || g.sb_mode != kSTensor;
     const int out = pl.splits > 1 ? 2 : g.out;
     const int grid = prm.tiles_m * prm.tiles_n * pl.splits;
-    if (g.fa == kE4M3 && g.fb == kE4M3) launch_fmt<kE4M3, kE4M3>(prm, pl.cfg, out, grouped, grid, stream);
-    else if (g.fa == kE5M2 && g.fb == kE4M3) launch_fmt<kE5M2, kE4M3>(prm, pl.cfg, out, grouped, grid, stream);
-    else if (g.fa == kE4M3 && g.fb == kE5M2) launch_fmt<kE4M3, kE5M2>(prm, pl.cfg, out, grouped, grid, stream);
-    else launch_fmt<kE5M2, kE5M2>(prm, pl.cfg, out, grouped, grid, stream);
+    auto launch = [&](auto fa, auto fb) {
+        constexpr int FA = decltype(fa)::value, FB = decltype(fb)::value;
+        if (grouped) launch_variant<FA, FB, true>(prm, pl.cfg, out, grid, stream);
+        else launch_variant<FA, FB, false>(prm, pl.cfg, out, grid, stream);
+    };
+    using E4 = std::integral_constant<int, kE4M3>;
+    using E5 = std::integral_constant<int, kE5M2>;
+    if (g.fa == kE4M3 && g.fb == kE4M3) launch(E4{}, E4{});
+    else if (g.fa == kE5M2 && g.fb == kE4M3) launch(E5{}, E4{});
+    else if (g.fa == kE4M3 && g.fb == kE5M2) launch(E4{}, E5{});
+    else launch(E5{}, E5{});
     if (pl.splits > 1) {
         const int64_t n = g.M * (g.N / 4);
         const int blocks = (int)((n + 255) / 256);

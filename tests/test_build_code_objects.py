@@ -42,7 +42,7 @@ def _kernels(obj):
 def _objects():
     tools = all(os.access(os.path.join(LLVM, t), os.X_OK)
                 for t in ("llvm-objcopy", "clang-offload-bundler", "llvm-readelf"))
-    objs = sorted(glob.glob(os.path.join(BUILD, "*.hip.o")))
+    objs = [o for o in sorted(glob.glob(os.path.join(BUILD, "*.o"))) if not o.endswith("api.o")]
     if not tools or not objs:
         pytest.skip("needs the built objects (paper_2608_27370_amd/build.py) and the ROCm LLVM tools")
     return objs
