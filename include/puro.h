@@ -63,8 +63,22 @@ typedef enum {
     PURO_SCALE_TENSOR = 0,        /* one scale                                          */
     PURO_SCALE_ROW_1x128 = 1,     /* one scale per row per 128 consecutive columns      */
     PURO_SCALE_COL_128x1 = 2,     /* one scale per column per 128 consecutive rows      */
-    PURO_SCALE_BLOCK_128x128 = 3  /* one scale per 128x128 block                        */
+    PURO_SCALE_BLOCK_128x128 = 3, /* one scale per 128x128 block                        */
+    PURO_SCALE_KMAJOR = 0x100     /* layout flag of the grouped modes (below)           */
 } puro_scale_mode;
+
+/* PURO_SCALE_KMAJOR is a layout flag of the grouped modes, OR-ed into a puro_scale_mode argument
+ * (the quantise calls) or into puro_fp8_operand.mode (the GEMM): the scale
+ * array is stored k-block-major, the index of the 128-wide group along the
+ * reduction dimension of the GEMM that reads the codes outermost. Without it
+ * grouped scales are row-major. The GEMM then loads each k block's scales as
+ * one contiguous run; the linear layer keeps its scales this way. Layouts:
+ *   quantise ROW_1x128:     scale  [cols/128][rows], scaleT [rows/128][cols]
+ *   quantise COL_128x1:     scaleT [rows/128][cols]
+ *   quantise BLOCK_128x128: scale  [cols/128][rows/128], scaleT [rows/128][cols/128]
+ *   GEMM operand [rows, K]: ROW_1x128 scale[(k/128) * rows + row],
+ *                           BLOCK_128x128 scale[(k/128) * ceil(rows/128) + row/128]
+ * With TENSOR it is PURO_ERR_UNSUPPORTED. */
 
 /* Scale value rule. Section 3.2: block scales are powers of two (the
  * exponent-only E8M0 representation of MXFP8). */
@@ -237,7 +251,7 @@ typedef struct {
     const uint8_t* data;
     int64_t ld;
     puro_fp8_format fmt;
-    puro_scale_mode mode;   /* TENSOR, ROW_1x128 or BLOCK_128x128 */
+    puro_scale_mode mode;   /* TENSOR, ROW_1x128 or BLOCK_128x128; grouped ones may carry PURO_SCALE_KMAJOR */
     const float* scale;
 } puro_fp8_operand;
 

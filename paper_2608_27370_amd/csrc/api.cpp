@@ -93,9 +93,8 @@ size_t puro_quantize_workspace_size(int64_t rows, int64_t cols) {
 
 namespace {
 
-// puro_quantize_fp8 with a choice of grouped-scale layout (kmajor: k-block-
-// major, as the linear layer keeps its scales for the GEMM).
-// The values a quantisation encodes: the BF16 tensor x itself; the SwiGLU
+// puro_quantize_fp8 and the fused quantise calls (the mode may carry the
+// k-block-major layout flag). The values a quantisation encodes: the BF16 tensor x itself; the SwiGLU
 // H = BF16(silu(gate) * up) [rows, cols] of a fused gate/up output x [rows,
 // 2 cols]; or the RMSNorm y = BF16(x * rstd * gamma) of x [rows, cols], whose
 // per-row rstd is written too.
@@ -110,9 +109,13 @@ struct Source {
 };
 
 puro_status quantize_impl(const uint16_t* x, int64_t rows, int64_t cols, int64_t ld, puro_fp8_format fmt,
-                          puro_scale_mode mode, puro_scale_rounding rnd, const float* amax_in, uint8_t* q,
-                          float* scale, uint8_t* qT, float* scaleT, void* ws, size_t ws_bytes, int kmajor,
+                          puro_scale_mode mode_arg, puro_scale_rounding rnd, const float* amax_in, uint8_t* q,
+                          float* scale, uint8_t* qT, float* scaleT, void* ws, size_t ws_bytes,
                           hipStream_t stream, Source src = Source()) {
+    // the scale-layout flag of the grouped modes
+    const int kmajor = ((int)mode_arg & PURO_SCALE_KMAJOR) != 0;
+    const puro_scale_mode mode = (puro_scale_mode)((int)mode_arg & ~(int)PURO_SCALE_KMAJOR);
+    if (kmajor && mode == PURO_SCALE_TENSOR) return PURO_ERR_UNSUPPORTED;
     const bool swiglu = src.kind == Source::kSwiglu, rms = src.kind == Source::kRmsnorm;
     const bool bwd = src.kind == Source::kSwigluBwd;
     if (cols < 0) return PURO_ERR_SHAPE;
@@ -222,8 +225,7 @@ puro_status puro_quantize_fp8(const uint16_t* x, int64_t rows, int64_t cols, int
                               puro_fp8_format fmt, puro_scale_mode mode, puro_scale_rounding rnd,
                               const float* amax_in, uint8_t* q, float* scale, uint8_t* qT,
                               float* scaleT, void* ws, size_t ws_bytes, hipStream_t stream) {
-    return quantize_impl(x, rows, cols, ld, fmt, mode, rnd, amax_in, q, scale, qT, scaleT, ws, ws_bytes, 0,
-                         stream);
+    return quantize_impl(x, rows, cols, ld, fmt, mode, rnd, amax_in, q, scale, qT, scaleT, ws, ws_bytes, stream);
 }
 
 // ---------------------------------------------------- SwiGLU + quantise
@@ -238,8 +240,8 @@ puro_status puro_swiglu_quantize_fp8(const uint16_t* gu, int64_t rows, int64_t c
                                      size_t ws_bytes, hipStream_t stream) {
     Source src;
     src.kind = Source::kSwiglu;
-    return quantize_impl(gu, rows, cols, ld, fmt, mode, rnd, nullptr, q, scale, qT, scaleT, ws, ws_bytes, 0,
-                         stream, src);
+    return quantize_impl(gu, rows, cols, ld, fmt, mode, rnd, nullptr, q, scale, qT, scaleT, ws, ws_bytes, stream,
+                         src);
 }
 
 // ------------------------------------------- SwiGLU backward + quantise
@@ -258,7 +260,7 @@ puro_status puro_swiglu_bwd_quantize_fp8(const uint16_t* dh, int64_t ld_dh, cons
     src.gu = gu;
     src.ld_gu = ld_gu;
     return quantize_impl(dh, rows, 2 * cols, ld_dh, fmt, mode, rnd, nullptr, q, scale, qT, scaleT, ws, ws_bytes,
-                         0, stream, src);
+                         stream, src);
 }
 
 // --------------------------------------------------- RMSNorm + quantise
@@ -276,8 +278,8 @@ puro_status puro_rmsnorm_quantize_fp8(const uint16_t* x, const uint16_t* gamma, 
     src.gamma = gamma;
     src.rstd = rstd;
     src.eps = eps;
-    return quantize_impl(x, rows, cols, ld, fmt, mode, rnd, nullptr, q, scale, qT, scaleT, ws, ws_bytes, 0,
-                         stream, src);
+    return quantize_impl(x, rows, cols, ld, fmt, mode, rnd, nullptr, q, scale, qT, scaleT, ws, ws_bytes, stream,
+                         src);
 }
 
 // ------------------------------------------------------------------- GEMM
@@ -291,7 +293,8 @@ puro_status puro_fp8_gemm_plan(int64_t M, int64_t N, int64_t K, puro_scale_mode 
                                int* launches) {
     if (M < 0 || N < 0 || K < 0) return PURO_ERR_SHAPE;
     auto ok = [](puro_scale_mode m) {
-        return m == PURO_SCALE_TENSOR || m == PURO_SCALE_ROW_1x128 || m == PURO_SCALE_BLOCK_128x128;
+        const int g = (int)m & ~(int)PURO_SCALE_KMAJOR;
+        return m == PURO_SCALE_TENSOR || g == PURO_SCALE_ROW_1x128 || g == PURO_SCALE_BLOCK_128x128;
     };
     if (!ok(a_mode) || !ok(b_mode)) return PURO_ERR_UNSUPPORTED;
     int tm = 0, tn = 0, ns = 0, s = 1;
@@ -304,7 +307,7 @@ puro_status puro_fp8_gemm_plan(int64_t M, int64_t N, int64_t K, puro_scale_mode 
     return PURO_OK;
 }
 
-static puro_status check_operand(const puro_fp8_operand* o, int64_t rows, int64_t K, int* smode) {
+static puro_status check_operand(const puro_fp8_operand* o, int64_t rows, int64_t K, int* smode, int* kmajor) {
     if (!o) return PURO_ERR_NULL;
     // the scale is read whenever the operand has rows (also for K == 0, where
     // the result is a scaled empty sum); the data only when there is a k
@@ -314,8 +317,12 @@ static puro_status check_operand(const puro_fp8_operand* o, int64_t rows, int64_
     if ((o->ld % 16) != 0 || !aligned16(o->data)) return PURO_ERR_ALIGN;
     // buffer offsets within one tile of 256 rows stay below 2^31
     if (o->ld > kMaxPitch) return PURO_ERR_SHAPE;
-    switch (o->mode) {
-    case PURO_SCALE_TENSOR: *smode = kSTensor; break;
+    *kmajor = ((int)o->mode & PURO_SCALE_KMAJOR) != 0;
+    switch ((int)o->mode & ~(int)PURO_SCALE_KMAJOR) {
+    case PURO_SCALE_TENSOR:
+        if (*kmajor) return PURO_ERR_UNSUPPORTED;
+        *smode = kSTensor;
+        break;
     case PURO_SCALE_ROW_1x128: *smode = kSRow; break;
     case PURO_SCALE_BLOCK_128x128: *smode = kSBlock; break;
     default: return PURO_ERR_UNSUPPORTED;
@@ -332,14 +339,14 @@ namespace {
 // bias / residual: the BF16 epilogue (both NULL: none).
 puro_status gemm_impl(int64_t M, int64_t N, int64_t K, const puro_fp8_operand* A, const puro_fp8_operand* B,
                       void* D, puro_out_dtype d_type, int64_t ldd, int accumulate, void* ws, size_t ws_bytes,
-                      int a_kmajor, int b_kmajor, hipStream_t stream, const uint16_t* bias = nullptr,
-                      const uint16_t* residual = nullptr, int64_t ldr = 0) {
+                      hipStream_t stream, const uint16_t* bias = nullptr, const uint16_t* residual = nullptr,
+                      int64_t ldr = 0) {
     if (M < 0 || N < 0 || K < 0) return PURO_ERR_SHAPE;
     if (M > INT32_MAX / 2 || N > INT32_MAX / 2 || K > INT32_MAX / 2) return PURO_ERR_SHAPE;
-    int sa = 0, sb = 0;
-    puro_status st = check_operand(A, M, K, &sa);
+    int sa = 0, sb = 0, a_kmajor = 0, b_kmajor = 0;
+    puro_status st = check_operand(A, M, K, &sa, &a_kmajor);
     if (st != PURO_OK) return st;
-    st = check_operand(B, N, K, &sb);
+    st = check_operand(B, N, K, &sb, &b_kmajor);
     if (st != PURO_OK) return st;
     if (d_type != PURO_OUT_BF16 && d_type != PURO_OUT_FP32) return PURO_ERR_UNSUPPORTED;
     if ((K % 16) != 0) return PURO_ERR_ALIGN;
@@ -384,18 +391,23 @@ extern "C" {
 puro_status puro_fp8_gemm(int64_t M, int64_t N, int64_t K, const puro_fp8_operand* A,
                           const puro_fp8_operand* B, void* D, puro_out_dtype d_type, int64_t ldd,
                           int accumulate, void* ws, size_t ws_bytes, hipStream_t stream) {
-    return gemm_impl(M, N, K, A, B, D, d_type, ldd, accumulate, ws, ws_bytes, 0, 0, stream);
+    return gemm_impl(M, N, K, A, B, D, d_type, ldd, accumulate, ws, ws_bytes, stream);
 }
 
 puro_status puro_fp8_gemm_epilogue(int64_t M, int64_t N, int64_t K, const puro_fp8_operand* A,
                                    const puro_fp8_operand* B, uint16_t* D, int64_t ldd, const uint16_t* bias,
                                    const uint16_t* residual, int64_t ldr, void* ws, size_t ws_bytes,
                                    hipStream_t stream) {
-    return gemm_impl(M, N, K, A, B, D, PURO_OUT_BF16, ldd, 0, ws, ws_bytes, 0, 0, stream, bias, residual, ldr);
+    return gemm_impl(M, N, K, A, B, D, PURO_OUT_BF16, ldd, 0, ws, ws_bytes, stream, bias, residual, ldr);
 }
 
 // ----------------------------------------------------------- linear layer
 namespace {
+
+// The linear layer keeps its grouped scales k-block-major: the GEMMs load a
+// k slice's scales as contiguous runs.
+constexpr puro_scale_mode kRowKM = (puro_scale_mode)(PURO_SCALE_ROW_1x128 | PURO_SCALE_KMAJOR);
+constexpr puro_scale_mode kBlockKM = (puro_scale_mode)(PURO_SCALE_BLOCK_128x128 | PURO_SCALE_KMAJOR);
 
 // The power-of-two rule of a blockwise recipe.
 puro_scale_rounding block_rule(const puro_linear_recipe* r) {
@@ -531,19 +543,17 @@ puro_status puro_linear_fwd(const uint16_t* X, const uint16_t* W, int64_t M, int
         // column-grouped transposed copy kept for Wgrad.
         float* xs_row = reinterpret_cast<float*>(w8 + l.xs_row);
         float* w_blk = reinterpret_cast<float*>(w8 + l.w_blk);
-        st = quantize_impl(X, M, K, K, r->x_fmt, PURO_SCALE_ROW_1x128, block_rule(r), nullptr, xq, xs_row,
-                           saved->xq_t, saved->x_scale, nullptr, 0, 1, stream);
+        st = quantize_impl(X, M, K, K, r->x_fmt, kRowKM, block_rule(r), nullptr, xq, xs_row, saved->xq_t,
+                           saved->x_scale, nullptr, 0, stream);
         if (st != PURO_OK) return st;
         // W: 128x128 blocks, plus the transposed copy (same blocks) kept for Dgrad.
-        st = quantize_impl(W, N, K, K, r->w_fmt, PURO_SCALE_BLOCK_128x128, block_rule(r), nullptr, wq, w_blk,
-                           saved->wq_t, saved->w_scale, nullptr, 0, 1, stream);
+        st = quantize_impl(W, N, K, K, r->w_fmt, kBlockKM, block_rule(r), nullptr, wq, w_blk, saved->wq_t,
+                           saved->w_scale, nullptr, 0, stream);
         if (st != PURO_OK) return st;
-        A = puro_fp8_operand{xq, K, r->x_fmt, PURO_SCALE_ROW_1x128, xs_row};
-        B = puro_fp8_operand{wq, K, r->w_fmt, PURO_SCALE_BLOCK_128x128, w_blk};
+        A = puro_fp8_operand{xq, K, r->x_fmt, kRowKM, xs_row};
+        B = puro_fp8_operand{wq, K, r->w_fmt, kBlockKM, w_blk};
     }
-    // blockwise scales are kept k-block-major: the GEMM loads a slice's scales as contiguous runs
-    const int km = r->blockwise ? 1 : 0;
-    return gemm_impl(M, N, K, &A, &B, Y, PURO_OUT_BF16, N, 0, w8 + l.gemm, ws_bytes - l.gemm, km, km, stream);
+    return gemm_impl(M, N, K, &A, &B, Y, PURO_OUT_BF16, N, 0, w8 + l.gemm, ws_bytes - l.gemm, stream);
 }
 
 puro_status puro_linear_bwd(const uint16_t* dY, const puro_linear_saved* saved, int64_t M, int64_t N,
@@ -577,21 +587,20 @@ puro_status puro_linear_bwd(const uint16_t* dY, const puro_linear_saved* saved, 
         wA = puro_fp8_operand{dyq_t, M, r->dy_fmt, PURO_SCALE_TENSOR, dys};
         wB = puro_fp8_operand{saved->xq_t, M, r->x_fmt, PURO_SCALE_TENSOR, saved->x_scale};
     } else {
-        st = quantize_impl(dY, M, N, N, r->dy_fmt, PURO_SCALE_ROW_1x128, block_rule(r), nullptr, dyq, dys,
-                           dyq_t, dys_t, nullptr, 0, 1, stream);
+        st = quantize_impl(dY, M, N, N, r->dy_fmt, kRowKM, block_rule(r), nullptr, dyq, dys, dyq_t, dys_t, nullptr,
+                           0, stream);
         if (st != PURO_OK) return st;
-        dA = puro_fp8_operand{dyq, N, r->dy_fmt, PURO_SCALE_ROW_1x128, dys};
-        dB = puro_fp8_operand{saved->wq_t, N, r->w_fmt, PURO_SCALE_BLOCK_128x128, saved->w_scale};
-        wA = puro_fp8_operand{dyq_t, M, r->dy_fmt, PURO_SCALE_ROW_1x128, dys_t};
-        wB = puro_fp8_operand{saved->xq_t, M, r->x_fmt, PURO_SCALE_ROW_1x128, saved->x_scale};
+        dA = puro_fp8_operand{dyq, N, r->dy_fmt, kRowKM, dys};
+        dB = puro_fp8_operand{saved->wq_t, N, r->w_fmt, kBlockKM, saved->w_scale};
+        wA = puro_fp8_operand{dyq_t, M, r->dy_fmt, kRowKM, dys_t};
+        wB = puro_fp8_operand{saved->xq_t, M, r->x_fmt, kRowKM, saved->x_scale};
     }
-    const int km = r->blockwise ? 1 : 0;
     if (dX) {
-        st = gemm_impl(M, K, N, &dA, &dB, dX, PURO_OUT_BF16, K, 0, gws, gws_bytes, km, km, stream);
+        st = gemm_impl(M, K, N, &dA, &dB, dX, PURO_OUT_BF16, K, 0, gws, gws_bytes, stream);
         if (st != PURO_OK) return st;
     }
     if (dW) {
-        st = gemm_impl(N, K, M, &wA, &wB, dW, PURO_OUT_FP32, K, accumulate_dW, gws, gws_bytes, km, km, stream);
+        st = gemm_impl(N, K, M, &wA, &wB, dW, PURO_OUT_FP32, K, accumulate_dW, gws, gws_bytes, stream);
         if (st != PURO_OK) return st;
     }
     return PURO_OK;

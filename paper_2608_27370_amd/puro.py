@@ -20,10 +20,9 @@ LIB_PATH = os.path.join(_HERE, "libpuro.so")
 
 E4M3, E5M2 = 0, 1
 SCALE_TENSOR, SCALE_ROW_1x128, SCALE_COL_128x1, SCALE_BLOCK_128x128 = 0, 1, 2, 3
+SCALE_KMAJOR = 0x100    # OR-ed into a grouped mode: k-block-major scale arrays
 SCALE_FP32, SCALE_POW2, SCALE_POW2_FLOOR = 0, 1, 2
 OUT_BF16, OUT_FP32 = 0, 1
-
-FMAX = {E4M3: 448.0, E5M2: 57344.0}
 
 _i64, _sz, _p, _i = ctypes.c_int64, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_int
 
@@ -149,34 +148,7 @@ def quantize_fp8(x, fmt, mode=SCALE_TENSOR, rnd=SCALE_FP32, amax_in=None, want_q
     outputs are None). ``out`` may supply preallocated outputs."""
     rows, cols = x.shape
     dev = x.device
-    out = dict(out or {})
-    G = 128
-    if mode == SCALE_COL_128x1:
-        want_q, want_qT = False, True
-    q = out.get("q") if want_q else None
-    if want_q and q is None:
-        q = torch.empty(rows, cols, dtype=torch.uint8, device=dev)
-    qT = out.get("qT") if want_qT else None
-    if want_qT and qT is None:
-        qT = torch.empty(cols, rows, dtype=torch.uint8, device=dev)
-    scale = out.get("scale")
-    scaleT = out.get("scaleT")
-    if mode == SCALE_TENSOR:
-        scale = scale if scale is not None else torch.empty(1, dtype=torch.float32, device=dev)
-        scaleT = None
-    elif mode == SCALE_ROW_1x128:
-        scale = scale if scale is not None else torch.empty(rows, cols // G, dtype=torch.float32, device=dev)
-        if want_qT and scaleT is None:
-            scaleT = torch.empty(cols, rows // G, dtype=torch.float32, device=dev)
-    elif mode == SCALE_COL_128x1:
-        scale = None
-        scaleT = scaleT if scaleT is not None else torch.empty(cols, rows // G, dtype=torch.float32, device=dev)
-    elif mode == SCALE_BLOCK_128x128:
-        scale = scale if scale is not None else torch.empty(rows // G, cols // G, dtype=torch.float32, device=dev)
-        if want_qT and scaleT is None:
-            scaleT = torch.empty(cols // G, rows // G, dtype=torch.float32, device=dev)
-    if not want_qT:
-        scaleT = None
+    q, scale, qT, scaleT = _quant_outputs(rows, cols, mode, want_q, want_qT, out, dev)
     w, nb = _ws(lib().puro_quantize_workspace_size(rows, cols), ws, dev)
     _check("puro_quantize_fp8", lib().puro_quantize_fp8(
         _ptr(x), rows, cols, _ld(x), fmt, mode, rnd, _ptr(amax_in), _ptr(q), _ptr(scale), _ptr(qT),
@@ -185,10 +157,13 @@ def quantize_fp8(x, fmt, mode=SCALE_TENSOR, rnd=SCALE_FP32, amax_in=None, want_q
 
 
 def _quant_outputs(rows, cols, mode, want_q, want_qT, out, dev):
-    """Output tensors of a quantisation (supplied ones from `out` kept)."""
+    """Output tensors of a quantisation (supplied ones from `out` kept), in the
+    scale layout the mode's SCALE_KMAJOR flag selects."""
     out = dict(out or {})
     G = 128
-    if mode == SCALE_COL_128x1:
+    km = bool(mode & SCALE_KMAJOR)
+    base = mode & ~SCALE_KMAJOR
+    if base == SCALE_COL_128x1:
         want_q, want_qT = False, True
     q = out.get("q") if want_q else None
     if want_q and q is None:
@@ -197,16 +172,23 @@ def _quant_outputs(rows, cols, mode, want_q, want_qT, out, dev):
     if want_qT and qT is None:
         qT = torch.empty(cols, rows, dtype=torch.uint8, device=dev)
     scale, scaleT = out.get("scale"), out.get("scaleT")
-    if mode == SCALE_TENSOR:
+
+    def new(shape):
+        return torch.empty(*(shape[::-1] if km else shape), dtype=torch.float32, device=dev)
+    if base == SCALE_TENSOR:
         scale = scale if scale is not None else torch.empty(1, dtype=torch.float32, device=dev)
         scaleT = None
-    elif mode == SCALE_ROW_1x128:
-        scale = scale if scale is not None else torch.empty(rows, cols // G, dtype=torch.float32, device=dev)
+    elif base == SCALE_ROW_1x128:
+        scale = scale if scale is not None else new((rows, cols // G))
         if want_qT and scaleT is None:
-            scaleT = torch.empty(cols, rows // G, dtype=torch.float32, device=dev)
-    elif mode == SCALE_COL_128x1:
+            scaleT = new((cols, rows // G))
+    elif base == SCALE_COL_128x1:
         scale = None
-        scaleT = scaleT if scaleT is not None else torch.empty(cols, rows // G, dtype=torch.float32, device=dev)
+        scaleT = scaleT if scaleT is not None else new((cols, rows // G))
+    elif base == SCALE_BLOCK_128x128:
+        scale = scale if scale is not None else new((rows // G, cols // G))
+        if want_qT and scaleT is None:
+            scaleT = new((cols // G, rows // G))
     if not want_qT:
         scaleT = None
     return q, scale, qT, scaleT
@@ -257,29 +239,7 @@ def swiglu_quantize_fp8(gu, cols, fmt, mode=SCALE_TENSOR, rnd=SCALE_FP32, want_q
     rows = gu.shape[0]
     assert gu.shape[1] >= 2 * cols
     dev = gu.device
-    out = dict(out or {})
-    G = 128
-    if mode == SCALE_COL_128x1:
-        want_q, want_qT = False, True
-    q = out.get("q") if want_q else None
-    if want_q and q is None:
-        q = torch.empty(rows, cols, dtype=torch.uint8, device=dev)
-    qT = out.get("qT") if want_qT else None
-    if want_qT and qT is None:
-        qT = torch.empty(cols, rows, dtype=torch.uint8, device=dev)
-    scale, scaleT = out.get("scale"), out.get("scaleT")
-    if mode == SCALE_TENSOR:
-        scale = scale if scale is not None else torch.empty(1, dtype=torch.float32, device=dev)
-        scaleT = None
-    elif mode == SCALE_ROW_1x128:
-        scale = scale if scale is not None else torch.empty(rows, cols // G, dtype=torch.float32, device=dev)
-        if want_qT and scaleT is None:
-            scaleT = torch.empty(cols, rows // G, dtype=torch.float32, device=dev)
-    elif mode == SCALE_COL_128x1:
-        scale = None
-        scaleT = scaleT if scaleT is not None else torch.empty(cols, rows // G, dtype=torch.float32, device=dev)
-    if not want_qT:
-        scaleT = None
+    q, scale, qT, scaleT = _quant_outputs(rows, cols, mode, want_q, want_qT, out, dev)
     w, nb = _ws(lib().puro_swiglu_quantize_workspace_size(rows, cols), ws, dev)
     _check("puro_swiglu_quantize_fp8", lib().puro_swiglu_quantize_fp8(
         _ptr(gu), rows, cols, _ld(gu), fmt, mode, rnd, _ptr(q), _ptr(scale), _ptr(qT), _ptr(scaleT),

@@ -93,6 +93,10 @@ def test_quantize_validation(puro):
     assert q(FAKE, 16, 128, 1 << 23, 0, 0, 0, None, FAKE, FAKE, None, None, FAKE, big, None) == ERR_SHAPE
     # per-tensor without workspace for the amax pass
     assert q(FAKE, 4096, 4096, 4096, 0, 0, 0, None, FAKE, FAKE, None, None, FAKE, 0, None) == ERR_WORKSPACE
+    # the k-major layout flag belongs to the grouped modes
+    KM = puro.SCALE_KMAJOR
+    assert q(FAKE, 128, 128, 128, 0, 0 | KM, 0, None, FAKE, FAKE, None, None, FAKE, big, None) == ERR_UNSUPPORTED
+    assert q(FAKE, 128, 136, 136, 0, 1 | KM, 1, None, FAKE, FAKE, None, None, None, 0, None) == ERR_ALIGN
 
 
 def test_gemm_validation(puro):
@@ -114,6 +118,11 @@ def test_gemm_validation(puro):
     assert g(16, 16, 256, Op(FAKE, 256, 0, 0, None), good) == ERR_NULL
     assert g(16, 16, 0, Op(FAKE, 0, 0, 0, None), good) == ERR_NULL       # scale is read even for K == 0
     assert g(16, 16, 208, Op(FAKE, 208, 0, 1, FAKE), Op(FAKE, 208, 0, 0, FAKE)) == ERR_ALIGN  # grouped needs K % 128
+    KM = puro.SCALE_KMAJOR
+    assert g(16, 16, 256, Op(FAKE, 256, 0, KM, FAKE), good) == ERR_UNSUPPORTED      # k-major: grouped modes only
+    assert g(16, 16, 256, Op(FAKE, 256, 0, 2 | KM, FAKE), good) == ERR_UNSUPPORTED
+    assert g(16, 16, 208, Op(FAKE, 208, 0, 1 | KM, FAKE), Op(FAKE, 208, 0, 3 | KM, FAKE)) == ERR_ALIGN
+    assert puro.fp8_gemm_plan(4096, 4096, 4096, 1 | KM, 3 | KM)["launches"] == 1
     assert g(16, 16, 256, good, good, dt=4) == ERR_UNSUPPORTED
     assert g(16, 16, 256, good, good, ldd=8) == ERR_SHAPE
     assert g(16, 18, 256, good, good, ldd=18) == ERR_ALIGN

@@ -378,3 +378,27 @@ def test_gemm_epilogue_qkv_bias_full_size(P):
     ref, den = gemm.gemm_entries(ms, ns, *op)
     ref, den = gemm.epilogue(ref, den, bf16.to_f32(bias)[ns])
     check_bf16(bf16_bits(D)[ms, ns], ref, den, what="QKV + bias", slack=mfma_model.truncation_loss(ms, ns, *op))
+
+
+@pytest.mark.parametrize("am,bm", [("row", "block"), ("row", "row")])
+@pytest.mark.parametrize("shape", [(384, 264, 512), (256, 392, 1024)], ids=lambda s: "x".join(map(str, s)))
+def test_gemm_kmajor_scales(P, am, bm, shape):
+    """The k-block-major scale layout (PURO_SCALE_KMAJOR) is only a layout:
+    the same operands with their scale arrays transposed give bitwise the
+    same output, which matches the oracle."""
+    import torch
+    M, N, K = shape
+    a, sa = _operand_grouped(31, M, K, E4, am, kind="outliers")
+    b, sb = _operand_grouped(32, N, K, E4, bm, std=0.02)
+    da, db = to_dev(a), to_dev(b)
+    for out in (0, 1):
+        rm = P.fp8_gemm(P.operand(da, E4, MODE[am], to_dev(sa)), M, P.operand(db, E4, MODE[bm], to_dev(sb)), N, K,
+                        out)
+        km = P.fp8_gemm(P.operand(da, E4, MODE[am] | P.SCALE_KMAJOR, to_dev(np.ascontiguousarray(sa.T))), M,
+                        P.operand(db, E4, MODE[bm] | P.SCALE_KMAJOR, to_dev(np.ascontiguousarray(sb.T))), N, K, out)
+        torch.cuda.synchronize()
+        assert torch.equal(rm.view(torch.int16) if out == 0 else rm.view(torch.int32),
+                           km.view(torch.int16) if out == 0 else km.view(torch.int32))
+        op = (a, fp8.E4M3, sa, am, b, fp8.E4M3, sb, bm)
+        ref, den = gemm.gemm(*op)
+        _check(P, out, km, ref, den, "k-major %s/%s %s" % (am, bm, shape), op)

@@ -129,6 +129,15 @@ def test_quantize_rows_and_columns(P, fmt, shape, kind, specials, rnd):
     r = P.quantize_fp8(d, fmt, P.SCALE_COL_128x1, rnd)
     assert_bytes_equal(host(r["qT"]), qT, "col qT")
     assert_f32_bits_equal(host(r["scaleT"]), sT, "col scaleT")
+    # the k-block-major layout: the same codes, the scale arrays transposed
+    r = P.quantize_fp8(d, fmt, P.SCALE_ROW_1x128 | P.SCALE_KMAJOR, rnd, want_q=True, want_qT=True)
+    assert_bytes_equal(host(r["q"]), q, "row q (k-major)")
+    assert_f32_bits_equal(host(r["scale"]), s.T, "row scale (k-major)")
+    assert_bytes_equal(host(r["qT"]), qT, "col qT (k-major)")
+    assert_f32_bits_equal(host(r["scaleT"]), sT.T, "col scaleT (k-major)")
+    r = P.quantize_fp8(d, fmt, P.SCALE_COL_128x1 | P.SCALE_KMAJOR, rnd)
+    assert_bytes_equal(host(r["qT"]), qT, "col qT only (k-major)")
+    assert_f32_bits_equal(host(r["scaleT"]), sT.T, "col scaleT only (k-major)")
 
 
 @pytest.mark.parametrize("rnd", [1, 2], ids=["pow2", "pow2_floor"])
@@ -143,6 +152,11 @@ def test_quantize_blocks(P, fmt, shape, kind, specials, rnd):
     assert_f32_bits_equal(host(r["scale"]), s, "block scale")
     assert_bytes_equal(host(r["qT"]), qT, "block qT")
     assert_f32_bits_equal(host(r["scaleT"]), sT, "block scaleT")
+    r = P.quantize_fp8(to_dev_bf16(x), fmt, P.SCALE_BLOCK_128x128 | P.SCALE_KMAJOR, rnd, want_q=True, want_qT=True)
+    assert_bytes_equal(host(r["q"]), q, "block q (k-major)")
+    assert_f32_bits_equal(host(r["scale"]), s.T, "block scale (k-major)")
+    assert_bytes_equal(host(r["qT"]), qT, "block qT (k-major)")
+    assert_f32_bits_equal(host(r["scaleT"]), sT.T, "block scaleT (k-major)")
 
 
 def test_quantize_is_deterministic(P):
