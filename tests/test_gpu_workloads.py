@@ -38,16 +38,18 @@ def test_single_forward_256x1536x1536(P):
     assert_bytes_equal(host(saved["xq_t"]), osaved["xq_t"], "xq_t")
     assert_bytes_equal(host(saved["wq_t"]), osaved["wq_t"], "wq_t")
     assert_f32_bits_equal(host(saved["x_scale"]), np.array([osaved["x_scale"]]), "x scale")
-    check_bf16(bf16_bits(Y), y_ref, y_den, what="Y", slack=mfma_model.truncation_loss_full(*fprop))
+    # the plain bound max|err| / sum|ab| <= 1e-5 holds here and is asserted
+    check_bf16(bf16_bits(Y), y_ref, y_den, what="single forward Y", slack=mfma_model.truncation_loss_full(*fprop),
+               strict=True)
 
 
-def _entries_check(P, D, out, ms, ns, op, what):
+def _entries_check(P, D, out, ms, ns, op, what, strict=False):
     ref, den = gemm.gemm_entries(ms, ns, *op)
     slack = mfma_model.truncation_loss(ms, ns, *op)
     if out == 1:
-        check_fp32(host(D)[ms, ns], ref, den, what=what, slack=slack)
+        check_fp32(host(D)[ms, ns], ref, den, what=what, slack=slack, strict=strict)
     else:
-        check_bf16(bf16_bits(D)[ms, ns], ref, den, what=what, slack=slack)
+        check_bf16(bf16_bits(D)[ms, ns], ref, den, what=what, slack=slack, strict=strict)
 
 
 def test_qkv_projection_fwd_dgrad_wgrad(P):
@@ -65,10 +67,11 @@ def test_qkv_projection_fwd_dgrad_wgrad(P):
     assert_bytes_equal(host(saved["wq_t"]), osaved["wq_t"], "wq_t")
     assert_f32_bits_equal(host(saved["x_scale"]), np.array([osaved["x_scale"]]), "x scale")
     assert_f32_bits_equal(host(saved["w_scale"]), np.array([osaved["w_scale"]]), "w scale")
+    # the plain bound max|err| / sum|ab| <= 1e-5 holds on all three and is asserted
     g = np.random.default_rng(2)
     ms, ns = sample_entries(M, N, g)
-    _entries_check(P, Y, 0, ms, ns, fprop, "Y")
+    _entries_check(P, Y, 0, ms, ns, fprop, "qkv Y", strict=True)
     ms, ns = sample_entries(M, K, g)
-    _entries_check(P, dX, 0, ms, ns, dgrad, "dX")
+    _entries_check(P, dX, 0, ms, ns, dgrad, "qkv dX", strict=True)
     ms, ns = sample_entries(N, K, g)
-    _entries_check(P, dW, 1, ms, ns, wgrad, "dW")
+    _entries_check(P, dW, 1, ms, ns, wgrad, "qkv dW", strict=True)
