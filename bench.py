@@ -1,17 +1,26 @@
-"""Throughput of the FP8 linear layer's hot path on one MI355X.
+"""Throughput of the FP8 linear layers' hot path on one MI355X.
 
-A step is one pass of the whole path at the Qwen2-1.5B QKV-projection shape
-(M = 8192 tokens, K = 1536, N = 2048; per-tensor scales, X and W in E4M3, dY
-in E5M2): amax and quantisation of X and W, the Fprop GEMM, amax and
-quantisation of dY, the Dgrad and Wgrad GEMMs (puro_linear_fwd then
-puro_linear_bwd). Inputs are seeded synthetic tensors resident in HBM before
-the timed region.
+The default workload is one training step's linear layers of a 28-layer
+Qwen2-1.5B-shaped transformer at M = 16384 tokens (one GPU's share: two of
+the paper's 8192-token micro-batches): for every layer the QKV (2048 x
+1536), O (1536 x 1536), fused gate/up (17920 x 1536) and down (1536 x 8960)
+projections, forward in layer order and backward in reverse, with the
+paper's blockwise recipe (Section 3.2): X and dY in 1x128 groups along each
+GEMM's reduction dimension, W in 128x128 blocks, power-of-two scales, E4M3
+throughout. A step is puro_linear_fwd for the 112 linears, then
+puro_linear_bwd for them in reverse: amax and quantisation of every operand
+and the Fprop, Dgrad and Wgrad GEMMs. Every layer has its own seeded
+synthetic weights, activations and gradients (drawn on the device; weights
+~N(0, 0.02^2), activations ~N(0, 1), gradients ~N(0, (1e-3)^2)), resident in
+HBM before the timed region. ``--workload qkv`` times the per-tensor QKV
+projection step (M 8192) instead.
 
-Prints one JSON line: the metric (TFLOP/s of fwd + dgrad + wgrad GEMM work per
-step time), a per-call breakdown and a roofline entry for the dominant kernel
-(each call timed with HIP events on its stream around back-to-back launches;
-also per launch, as median, p10 and p90, and with --cold after a fill that
-evicts the caches), and the CPU oracle timed on a sample of the same workload.
+Prints one JSON line: the metric (TFLOP/s of fwd + dgrad + wgrad GEMM work
+per step time), the GEMM-only rate, a per-call breakdown (each kernel call
+of one layer timed with HIP events on its stream over back-to-back launches,
+and per launch as median / p10 / p90), a roofline entry for the dominant
+kernel, the shader clock sampled during the timed region, and the CPU
+oracle timed on a sample of the same workload.
 """
 
 import argparse
@@ -19,65 +28,164 @@ import hashlib
 import json
 import os
 import sys
+import threading
 import time
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
-FP8_PEAK_TFLOPS = 5000.0   # MI355X dense FP8 MFMA
+FP8_PEAK_TFLOPS = 5000.0   # MI355X dense FP8 MFMA (256 CUs x 8192 FLOP/clk x 2.4 GHz)
+PEAK_CLOCK_GHZ = 2.4
 HBM_PEAK_GBS = 8000.0      # MI355X HBM3E
 METRIC = "FP8 linear fwd+dgrad+wgrad TFLOP/s at Qwen2-1.5B shapes; % FP8 MFMA peak"
+# the paper's mixed-precision MFU denominator (Section 3.1.3): 72% of the
+# tensor-core work in FP8 at 419 TFLOP/s and 28% in BF16 at 209.5 on RTX 5090
+PAPER_FP8_SHARE, PAPER_FP8_PEAK, PAPER_BF16_PEAK = 0.72, 419.0, 209.5
+BF16_PEAK_TFLOPS = 2500.0  # MI355X dense BF16 MFMA
+
+
+def p_eff(fp8_share, fp8_peak, bf16_peak):
+    """Effective peak of a mixed FP8/BF16 workload (Section 3.1.3): the
+    harmonic mix (fp8_share / fp8_peak + (1 - fp8_share) / bf16_peak)^-1,
+    the rate at which that work would run with each part at its own peak."""
+    return 1.0 / (fp8_share / fp8_peak + (1.0 - fp8_share) / bf16_peak)
+
+
+WORKLOADS = ("layers28", "qkv")
+DEFAULTS = {"layers28": (20, 3), "qkv": (1000, 50)}   # (steps, warmup)
 
 
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=200)
-    ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--tokens", type=int, default=8192)
-    ap.add_argument("--cpu-tokens", type=int, default=8192,
-                    help="tokens of the workload the CPU oracle is timed on (0: skip)")
-    ap.add_argument("--cpu-reps", type=int, default=4, help="repetitions of the CPU oracle sample")
+    ap.add_argument("--workload", choices=WORKLOADS, default="layers28",
+                    help="layers28: the 28-layer blockwise step at M 16384 (default); "
+                         "qkv: the per-tensor QKV projection step at M 8192")
+    ap.add_argument("--steps", type=int, default=None)
+    ap.add_argument("--warmup", type=int, default=None)
+    ap.add_argument("--cpu-tokens", type=int, default=None,
+                    help="tokens per linear of the CPU oracle sample (0: skip)")
     ap.add_argument("--cold", action="store_true",
                     help="also time every call after a 512 MiB fill that evicts the MALL and the L2s "
                          "(kept out of the default run, whose kernel trace profiles warm launches)")
     ap.add_argument("--graph", action="store_true",
-                    help="replay the step captured in a HIP graph instead of launching its kernels one by one "
-                         "(measured no faster: the launches are not host-bound)")
+                    help="replay the step captured in a HIP graph instead of launching its kernels one by one")
     ap.add_argument("--suite", action="store_true",
                     help="instead of the headline step, time every workload (the five Qwen2-1.5B-shaped ones "
                          "and the paper's own 1.7B shapes under both power-of-two scale rules) next to the "
                          "same GEMMs in BF16, and report the FP8 errors of the two rules; one JSON line each")
-    ap.add_argument("--only", choices=("step",) + CALLS + ("copy",) + SWIGLU_CALLS + RMSNORM_CALLS,
-                    help="run just this call (or a whole step) warmup + steps times and print its average "
-                         "time, for profilers; 'copy' is a plain 256 MiB device copy that calibrates "
-                         "the HBM byte counters; swiglu_* and rmsnorm_* are the fused SwiGLU / RMSNorm + "
-                         "quantise calls of the 8192-token MLP and QKV input")
-    return ap.parse_args()
+    ap.add_argument("--only", default=None,
+                    help="run just this call of the workload's breakdown (its key, e.g. gate_up.fprop), "
+                         "'step', 'copy' (a plain 256 MiB device copy that calibrates the HBM byte counters) "
+                         "or a fused call (%s) warmup + steps times and print its average time, for profilers"
+                         % ", ".join(SWIGLU_CALLS + RMSNORM_CALLS))
+    a = ap.parse_args()
+    st, wu = DEFAULTS[a.workload]
+    a.steps = st if a.steps is None else a.steps
+    a.warmup = wu if a.warmup is None else a.warmup
+    if a.cpu_tokens is None:
+        a.cpu_tokens = 256 if a.workload == "layers28" else 8192
+    return a
 
 
-def cpu_baseline(tokens, reps):
-    """The oracle (test infrastructure, unmodified) on the first `tokens`
-    tokens of the same workload, `reps` times over: quantisation of X, W, dY
-    and the three FP64 GEMMs; reported as TFLOP/s of the sampled GEMM work."""
+def cpu_info():
+    model = None
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return model, os.cpu_count()
+
+
+def cpu_baseline(workload, tokens):
+    """The oracle (test infrastructure, unmodified) timed on a bounded sample
+    of the workload: the linear layer's quantisation and its three FP64 GEMMs
+    on the first `tokens` tokens; reported as TFLOP/s of the sampled GEMM
+    work (the rate the oracle would sustain on the whole step)."""
     from oracle import linear
     from paper_2608_27370_amd import inputs
-    d = inputs.qkv(M=tokens)
-    rc = linear.recipe("tensor")
-    t0 = time.perf_counter()
-    for _ in range(reps):
+    threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    model, ncpu = cpu_info()
+    flops = 0.0
+    if workload == "layers28":
+        rc = linear.recipe("block", dy_fmt="e4m3")
+        data = [inputs.layer_linear(0, j, M=tokens) for j in range(len(inputs.LAYER_LINEARS))]
+        t0 = time.perf_counter()
+        for d in data:
+            _, _, saved = linear.linear_fwd(d["X"], d["W"], rc)
+            linear.linear_bwd(d["dY"], saved, rc)
+            flops += 3 * 2.0 * tokens * d["W"].shape[0] * d["W"].shape[1]
+        dt = time.perf_counter() - t0
+        sample = ("oracle blockwise linear fwd+bwd of layer 0's four linears (qkv, o, gate/up, down) on the first "
+                  "%d of the 16384 tokens: quantisation and FP64 GEMMs; the rate applies to the whole 28-layer "
+                  "step, whose 128.8 TFLOP would take %.0f h at it" % (tokens, 0))
+    else:
+        d = inputs.qkv(M=tokens)
+        rc = linear.recipe("tensor")
+        t0 = time.perf_counter()
         _, _, saved = linear.linear_fwd(d["X"], d["W"], rc)
         linear.linear_bwd(d["dY"], saved, rc)
-    dt = time.perf_counter() - t0
-    flops = reps * 3 * 2.0 * tokens * inputs.QKV_OUT * inputs.HIDDEN
-    threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
-    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
-            "seconds": round(dt, 2),
-            "sample": "oracle linear fwd+bwd on %d of the 8192 tokens (X[%d,1536], W[2048,1536], dY[%d,2048]), "
-                      "%d times; FP64 GEMMs on %d OpenMP threads" % (tokens, tokens, tokens, reps, threads)}
+        dt = time.perf_counter() - t0
+        flops = 3 * 2.0 * tokens * inputs.QKV_OUT * inputs.HIDDEN
+        sample = "oracle per-tensor linear fwd+bwd on %d of the 8192 tokens of the QKV projection" % tokens
+    value = flops / dt / 1e12
+    if workload == "layers28":
+        sample = sample.replace("take 0 h", "take %.0f h" % (128.8 / value / 3600.0))
+    return {"value": value, "unit": "TFLOP/s", "cores": threads, "kind": "oracle", "seconds": round(dt, 2),
+            "cpu_model": model, "nproc": ncpu, "sample": sample + "; FP64 GEMMs on %d OpenMP threads" % threads}
 
 
-CALLS = ("quantize_x", "quantize_w", "fprop", "quantize_dy", "dgrad", "wgrad")
+class ClockSampler:
+    """The GFX clock sampled through amdsmi every few milliseconds while
+    running (None when amdsmi is unavailable)."""
+
+    def __init__(self, period_s=0.005):
+        self.samples, self.period, self._stop = [], period_s, threading.Event()
+        self.handle = None
+        try:
+            import amdsmi
+            amdsmi.amdsmi_init()
+            self.amdsmi = amdsmi
+            self.handle = amdsmi.amdsmi_get_processor_handles()[0]
+            self.read()
+        except Exception:
+            self.handle = None
+
+    def read(self):
+        info = self.amdsmi.amdsmi_get_clock_info(self.handle, self.amdsmi.AmdSmiClkType.GFX)
+        return float(info["clk"])
+
+    def _run(self):
+        while not self._stop.is_set():
+            try:
+                self.samples.append(self.read())
+            except Exception:
+                return
+            time.sleep(self.period)
+
+    def __enter__(self):
+        if self.handle is not None:
+            self.thread = threading.Thread(target=self._run, daemon=True)
+            self.thread.start()
+        return self
+
+    def __exit__(self, *exc):
+        if self.handle is not None:
+            self._stop.set()
+            self.thread.join()
+
+    def summary(self):
+        import numpy as np
+        if not self.samples:
+            return None
+        s = np.array(self.samples)
+        return {"median_mhz": float(np.median(s)), "p10_mhz": float(np.percentile(s, 10)),
+                "p90_mhz": float(np.percentile(s, 90)), "samples": int(s.size), "source": "amdsmi GFX clock"}
+
+
 SWIGLU_CALLS = ("swiglu_tensor", "swiglu_groups", "swiglu_bwd_groups")
 RMSNORM_CALLS = ("rmsnorm_tensor", "rmsnorm_groups")
 
@@ -183,95 +291,209 @@ def swiglu_workload(torch, puro, M=8192):
     }
 
 
-def calls(torch, puro, dev, M, N, K, X, W, dY, Y, dX, dW, saved):
-    """The step's calls one at a time, on buffers of their own, as
-    (key, label, fn, flops, algorithmic bytes, kernel launches) rows."""
-    xq = torch.empty(M, K, dtype=torch.uint8, device=dev)
-    wq = torch.empty(N, K, dtype=torch.uint8, device=dev)
-    dyq = torch.empty(M, N, dtype=torch.uint8, device=dev)
-    dyqT = torch.empty(N, M, dtype=torch.uint8, device=dev)
-    sx = torch.empty(1, dtype=torch.float32, device=dev)
-    sw = torch.empty(1, dtype=torch.float32, device=dev)
-    sdy = torch.empty(1, dtype=torch.float32, device=dev)
-    qws = torch.empty(max(1, puro.lib().puro_quantize_workspace_size(M, N)), dtype=torch.uint8, device=dev)
-    gws = torch.empty(max(1, max(puro.fp8_gemm_workspace_size(M, N, K, 0), puro.fp8_gemm_workspace_size(M, K, N, 0),
-                                 puro.fp8_gemm_workspace_size(N, K, M, 1))), dtype=torch.uint8, device=dev)
-    A_f = puro.operand(xq, puro.E4M3, puro.SCALE_TENSOR, sx)
-    B_f = puro.operand(wq, puro.E4M3, puro.SCALE_TENSOR, sw)
-    A_d = puro.operand(dyq, puro.E5M2, puro.SCALE_TENSOR, sdy)
-    B_d = puro.operand(saved["wq_t"], puro.E4M3, puro.SCALE_TENSOR, sw)
-    A_w = puro.operand(dyqT, puro.E5M2, puro.SCALE_TENSOR, sdy)
-    B_w = puro.operand(saved["xq_t"], puro.E4M3, puro.SCALE_TENSOR, sx)
-    # quantisation moves 2 B read + 1 B (q) + 1 B (qT) written per element
-    return [
-        ("quantize_x", "quantize X (amax + encode, q and qT)", lambda: puro.quantize_fp8(
-            X, puro.E4M3, out=dict(q=xq, scale=sx, qT=saved["xq_t"]), want_qT=True, ws=qws), None,
-         M * K * 4.0, 2),
-        ("quantize_w", "quantize W (amax + encode, q and qT)", lambda: puro.quantize_fp8(
-            W, puro.E4M3, out=dict(q=wq, scale=sw, qT=saved["wq_t"]), want_qT=True, ws=qws), None,
-         N * K * 4.0, 2),
-        ("fprop", "fprop GEMM %dx%dx%d" % (M, N, K),
-         lambda: puro.fp8_gemm(A_f, M, B_f, N, K, puro.OUT_BF16, D=Y, ws=gws), 2.0 * M * N * K, None,
-         puro.fp8_gemm_plan(M, N, K)["launches"]),
-        ("quantize_dy", "quantize dY (amax + encode, q and qT)", lambda: puro.quantize_fp8(
-            dY, puro.E5M2, out=dict(q=dyq, scale=sdy, qT=dyqT), want_qT=True, ws=qws), None, M * N * 4.0, 2),
-        ("dgrad", "dgrad GEMM %dx%dx%d" % (M, K, N),
-         lambda: puro.fp8_gemm(A_d, M, B_d, K, N, puro.OUT_BF16, D=dX, ws=gws), 2.0 * M * N * K, None,
-         puro.fp8_gemm_plan(M, K, N)["launches"]),
-        ("wgrad", "wgrad GEMM %dx%dx%d" % (N, K, M),
-         lambda: puro.fp8_gemm(A_w, N, B_w, K, M, puro.OUT_FP32, D=dW, ws=gws), 2.0 * M * N * K, None,
-         puro.fp8_gemm_plan(N, K, M)["launches"]),
-    ]
+class Call:
+    """One kernel call of a step's breakdown: `count` times per step."""
+
+    def __init__(self, key, label, fn, flops=None, nbytes=None, launches=1, count=1):
+        self.key, self.label, self.fn = key, label, fn
+        self.flops, self.nbytes, self.launches, self.count = flops, nbytes, launches, count
+
+
+class Layers28:
+    """The 28-layer blockwise step at M = 16384 (see the module docstring)."""
+
+    name = "layers28_blockwise_m16384"
+    M = 16384
+
+    def __init__(self, torch, puro):
+        from paper_2608_27370_amd import inputs
+        self.torch, self.P, self.inputs = torch, puro, inputs
+        P, M = puro, self.M
+        dev = torch.device("cuda", 0)
+        self.dev = dev
+        self.rc = P.LinearRecipe(P.E4M3, P.E4M3, P.E4M3, 1, P.SCALE_POW2)
+        gen = torch.Generator(device=dev)
+        gen.manual_seed(4)
+
+        def normal(shape, std):
+            return (torch.randn(shape, generator=gen, device=dev) * std).to(torch.bfloat16)
+        self.kinds = inputs.LAYER_LINEARS
+        self.layers = []
+        for _ in range(inputs.LAYERS):
+            row = []
+            for name, N, K in self.kinds:
+                row.append(dict(X=normal((M, K), 1.0), W=normal((N, K), 0.02), dY=normal((M, N), 1e-3),
+                                saved=P.linear_saved(M, N, K, self.rc, dev)))
+            self.layers.append(row)
+        # outputs of one kind share their buffers across layers (overwritten)
+        self.outs = [dict(Y=torch.empty(M, N, dtype=torch.bfloat16, device=dev),
+                          dX=torch.empty(M, K, dtype=torch.bfloat16, device=dev),
+                          dW=torch.empty(N, K, dtype=torch.float32, device=dev)) for _, N, K in self.kinds]
+        self.wsf = torch.empty(max(P.linear_fwd_workspace_size(M, N, K, self.rc) for _, N, K in self.kinds),
+                               dtype=torch.uint8, device=dev)
+        self.wsb = torch.empty(max(P.linear_bwd_workspace_size(M, N, K, self.rc) for _, N, K in self.kinds),
+                               dtype=torch.uint8, device=dev)
+        self.gemm_flops = sum(3 * 2.0 * M * N * K for _, N, K in self.kinds) * inputs.LAYERS
+        self.config = {"workload": self.name, "layers": inputs.LAYERS, "tokens": M,
+                       "linears": {n: [N, K] for n, N, K in self.kinds},
+                       "recipe": "blockwise: X, dY 1x128 groups along each GEMM's reduction dim, W 128x128 blocks, "
+                                 "power-of-two scales, E4M3 throughout; BF16 Y/dX, FP32 dW"}
+
+    def step(self):
+        P = self.P
+        for row in self.layers:
+            for j, lin in enumerate(row):
+                P.linear_fwd(lin["X"], lin["W"], self.rc, Y=self.outs[j]["Y"], saved=lin["saved"], ws=self.wsf)
+        for row in reversed(self.layers):
+            for j in reversed(range(len(row))):
+                lin, o = row[j], self.outs[j]
+                P.linear_bwd(lin["dY"], lin["saved"], self.rc, lin["X"].shape[1], dX=o["dX"], dW=o["dW"],
+                             ws=self.wsb)
+
+    def calls(self):
+        """The kernels of each linear kind (layer 0's tensors), called as the
+        linear layer calls them: the same quantisers and GEMMs with the same
+        k-block-major scale layouts; each occurs 28 times per step."""
+        torch, P, M = self.torch, self.P, self.M
+        E4, KM = P.E4M3, P.SCALE_KMAJOR
+        ROW, BLK = P.SCALE_ROW_1x128 | KM, P.SCALE_BLOCK_128x128 | KM
+        L = len(self.layers)
+        out = []
+        for j, (name, N, K) in enumerate(self.kinds):
+            lin, o = self.layers[0][j], self.outs[j]
+            sv, dev = lin["saved"], self.dev
+            u8 = lambda *s: torch.empty(*s, dtype=torch.uint8, device=dev)
+            f32 = lambda *s: torch.empty(*s, dtype=torch.float32, device=dev)
+            xq, xs = u8(M, K), f32(K // 128, M)
+            wq, wb = u8(N, K), f32(K // 128, N // 128)
+            dyq, dys, dyqT, dysT = u8(M, N), f32(N // 128, M), u8(N, M), f32(M // 128, N)
+            gws = torch.empty(max(1, P.fp8_gemm_workspace_size(M, N, K, 0), P.fp8_gemm_workspace_size(M, K, N, 0),
+                                  P.fp8_gemm_workspace_size(N, K, M, 1)), dtype=torch.uint8, device=dev)
+            A_f, B_f = P.operand(xq, E4, ROW, xs), P.operand(wq, E4, BLK, wb)
+            A_d, B_d = P.operand(dyq, E4, ROW, dys), P.operand(sv["wq_t"], E4, BLK, sv["w_scale"])
+            A_w, B_w = P.operand(dyqT, E4, ROW, dysT), P.operand(sv["xq_t"], E4, ROW, sv["x_scale"])
+            X, W, dY = lin["X"], lin["W"], lin["dY"]
+            grp = 2.0 * 4 / 128          # two scale arrays of 4 B per 128 elements
+            fl = 2.0 * M * N * K
+
+            def q(x, mode, o_):
+                return lambda: P.quantize_fp8(x, E4, mode, P.SCALE_POW2, want_qT=True, out=o_)
+
+            def gemm(A, m, B, n, k, kind, D, w):
+                return lambda: P.fp8_gemm(A, m, B, n, k, kind, D=D, ws=w)
+            plan = lambda m, n, k: P.fp8_gemm_plan(m, n, k, P.SCALE_ROW_1x128, P.SCALE_BLOCK_128x128)["launches"]
+            planw = lambda m, n, k: P.fp8_gemm_plan(m, n, k, P.SCALE_ROW_1x128, P.SCALE_ROW_1x128)["launches"]
+            out += [
+                Call(name + ".quantize_x", "%s: quantize X [%d,%d] (1x128 rows + 128x1 columns, one read)" % (name, M, K),
+                     q(X, ROW, dict(q=xq, scale=xs, qT=sv["xq_t"], scaleT=sv["x_scale"])),
+                     nbytes=M * K * (4.0 + grp), count=L),
+                Call(name + ".quantize_w", "%s: quantize W [%d,%d] (128x128 blocks + transposed copy)" % (name, N, K),
+                     q(W, BLK, dict(q=wq, scale=wb, qT=sv["wq_t"], scaleT=sv["w_scale"])),
+                     nbytes=N * K * 4.0, count=L),
+                Call(name + ".fprop", "%s: fprop GEMM %dx%dx%d" % (name, M, N, K),
+                     gemm(A_f, M, B_f, N, K, P.OUT_BF16, o["Y"], gws),
+                     flops=fl, launches=plan(M, N, K), count=L),
+                Call(name + ".quantize_dy", "%s: quantize dY [%d,%d] (1x128 rows + 128x1 columns, one read)" % (name, M, N),
+                     q(dY, ROW, dict(q=dyq, scale=dys, qT=dyqT, scaleT=dysT)), nbytes=M * N * (4.0 + grp), count=L),
+                Call(name + ".dgrad", "%s: dgrad GEMM %dx%dx%d" % (name, M, K, N),
+                     gemm(A_d, M, B_d, K, N, P.OUT_BF16, o["dX"], gws),
+                     flops=fl, launches=plan(M, K, N), count=L),
+                Call(name + ".wgrad", "%s: wgrad GEMM %dx%dx%d" % (name, N, K, M),
+                     gemm(A_w, N, B_w, K, M, P.OUT_FP32, o["dW"], gws),
+                     flops=fl, launches=planw(N, K, M), count=L),
+            ]
+        return out
+
+
+class Qkv:
+    """The per-tensor QKV projection step at M = 8192 (X, W E4M3; dY E5M2)."""
+
+    name = "qkv_projection_fwd_dgrad_wgrad"
+
+    def __init__(self, torch, puro, M=8192):
+        import numpy as np
+        from paper_2608_27370_amd import inputs
+        self.torch, self.P = torch, puro
+        dev = torch.device("cuda", 0)
+        self.dev = dev
+        self.M, self.K, self.N = M, inputs.HIDDEN, inputs.QKV_OUT
+        d = inputs.qkv(M=M)
+
+        def up(bits):
+            return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).to(dev).view(torch.bfloat16)
+        self.X, self.W, self.dY = up(d["X"]), up(d["W"]), up(d["dY"])
+        P, M, K, N = puro, self.M, self.K, self.N
+        self.rc = P.LinearRecipe(P.E4M3, P.E4M3, P.E5M2, 0, P.SCALE_FP32)
+        self.saved = P.linear_saved(M, N, K, self.rc, dev)
+        self.Y = torch.empty(M, N, dtype=torch.bfloat16, device=dev)
+        self.dX = torch.empty(M, K, dtype=torch.bfloat16, device=dev)
+        self.dW = torch.empty(N, K, dtype=torch.float32, device=dev)
+        self.wsf = torch.empty(max(1, P.linear_fwd_workspace_size(M, N, K, self.rc)), dtype=torch.uint8, device=dev)
+        self.wsb = torch.empty(max(1, P.linear_bwd_workspace_size(M, N, K, self.rc)), dtype=torch.uint8, device=dev)
+        self.gemm_flops = 3 * 2.0 * M * N * K
+        self.config = {"workload": self.name, "M": M, "K": K, "N": N,
+                       "recipe": "per-tensor scales, X/W E4M3, dY E5M2, BF16 Y/dX, FP32 dW"}
+
+    def step(self):
+        P = self.P
+        P.linear_fwd(self.X, self.W, self.rc, Y=self.Y, saved=self.saved, ws=self.wsf)
+        P.linear_bwd(self.dY, self.saved, self.rc, self.K, dX=self.dX, dW=self.dW, ws=self.wsb)
+
+    def calls(self):
+        torch, P, M, N, K, dev = self.torch, self.P, self.M, self.N, self.K, self.dev
+        xq = torch.empty(M, K, dtype=torch.uint8, device=dev)
+        wq = torch.empty(N, K, dtype=torch.uint8, device=dev)
+        dyq = torch.empty(M, N, dtype=torch.uint8, device=dev)
+        dyqT = torch.empty(N, M, dtype=torch.uint8, device=dev)
+        sx, sw, sdy = (torch.empty(1, dtype=torch.float32, device=dev) for _ in range(3))
+        qws = torch.empty(max(1, P.lib().puro_quantize_workspace_size(M, N)), dtype=torch.uint8, device=dev)
+        gws = torch.empty(max(1, P.fp8_gemm_workspace_size(M, N, K, 0), P.fp8_gemm_workspace_size(M, K, N, 0),
+                              P.fp8_gemm_workspace_size(N, K, M, 1)), dtype=torch.uint8, device=dev)
+        sv = self.saved
+        A_f, B_f = P.operand(xq, P.E4M3, P.SCALE_TENSOR, sx), P.operand(wq, P.E4M3, P.SCALE_TENSOR, sw)
+        A_d, B_d = P.operand(dyq, P.E5M2, P.SCALE_TENSOR, sdy), P.operand(sv["wq_t"], P.E4M3, P.SCALE_TENSOR, sw)
+        A_w, B_w = P.operand(dyqT, P.E5M2, P.SCALE_TENSOR, sdy), P.operand(sv["xq_t"], P.E4M3, P.SCALE_TENSOR, sx)
+        fl = 2.0 * M * N * K
+        # quantisation moves 2 B read + 1 B (q) + 1 B (qT) written per element
+        return [
+            Call("quantize_x", "quantize X (amax + encode, q and qT)", lambda: P.quantize_fp8(
+                self.X, P.E4M3, out=dict(q=xq, scale=sx, qT=sv["xq_t"]), want_qT=True, ws=qws),
+                nbytes=M * K * 4.0, launches=2),
+            Call("quantize_w", "quantize W (amax + encode, q and qT)", lambda: P.quantize_fp8(
+                self.W, P.E4M3, out=dict(q=wq, scale=sw, qT=sv["wq_t"]), want_qT=True, ws=qws),
+                nbytes=N * K * 4.0, launches=2),
+            Call("fprop", "fprop GEMM %dx%dx%d" % (M, N, K),
+                 lambda: P.fp8_gemm(A_f, M, B_f, N, K, P.OUT_BF16, D=self.Y, ws=gws), flops=fl,
+                 launches=P.fp8_gemm_plan(M, N, K)["launches"]),
+            Call("quantize_dy", "quantize dY (amax + encode, q and qT)", lambda: P.quantize_fp8(
+                self.dY, P.E5M2, out=dict(q=dyq, scale=sdy, qT=dyqT), want_qT=True, ws=qws),
+                nbytes=M * N * 4.0, launches=2),
+            Call("dgrad", "dgrad GEMM %dx%dx%d" % (M, K, N),
+                 lambda: P.fp8_gemm(A_d, M, B_d, K, N, P.OUT_BF16, D=self.dX, ws=gws), flops=fl,
+                 launches=P.fp8_gemm_plan(M, K, N)["launches"]),
+            Call("wgrad", "wgrad GEMM %dx%dx%d" % (N, K, M),
+                 lambda: P.fp8_gemm(A_w, N, B_w, K, M, P.OUT_FP32, D=self.dW, ws=gws), flops=fl,
+                 launches=P.fp8_gemm_plan(N, K, M)["launches"]),
+        ]
 
 
 COPY_BYTES = 256 << 20
-TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "hbm_bytes_qkv.md")
 
 
-def profiled_traffic(call):
-    """HBM-side bytes per launch of `call` at the 8192-token workload, from the
-    committed rocprofv3 FETCH_SIZE / WRITE_SIZE summary (scaled by its copy
-    calibration); None when that summary is missing or any source it was
-    measured on has changed since."""
+def profiled(workload, key, field):
+    """A per-launch figure (`field`: "bytes" = HBM-side bytes from rocprofv3
+    FETCH_SIZE / WRITE_SIZE scaled by the copy calibration) of call `key`,
+    from the committed summary profiles/hbm_bytes_<workload>.md; None when it
+    is missing or any source it was measured on has changed since."""
     try:
-        text = open(TRAFFIC_PROFILE).read()
+        text = open(os.path.join(ROOT, "profiles", "hbm_bytes_%s.md" % workload)).read()
         d = json.loads(text.split("```json", 1)[1].split("```", 1)[0])
         for path, digest in d["sources"].items():
             if hashlib.sha256(open(os.path.join(ROOT, path), "rb").read()).hexdigest() != digest:
                 return None
-        return d["calls"][call]["bytes"]
+        return d["calls"][key][field]
     except (OSError, IndexError, KeyError, ValueError):
         return None
-
-
-def run_only(args, torch, stream, step, make_calls):
-    """Profiling mode: one call (or the whole step) warmup + steps times."""
-    if args.only in SWIGLU_CALLS:
-        from paper_2608_27370_amd import puro
-        fn, label = swiglu_workload(torch, puro)[args.only][0], "fused SwiGLU + quantise (%s)" % args.only
-    elif args.only in RMSNORM_CALLS:
-        from paper_2608_27370_amd import puro
-        fn, label = rmsnorm_workload(torch, puro)[args.only][0], "fused RMSNorm + quantise (%s)" % args.only
-    elif args.only == "copy":
-        src = torch.empty(COPY_BYTES // 4, dtype=torch.float32, device=stream.device).fill_(1.0)
-        dst = torch.empty_like(src)
-        fn, label = (lambda: dst.copy_(src)), "plain device copy of %d bytes" % COPY_BYTES
-    elif args.only == "step":
-        fn, label = step, "linear fwd + bwd step"
-    else:
-        row = [r for r in make_calls() if r[0] == args.only][0]
-        fn, label = row[2], row[1]
-    for _ in range(args.warmup):
-        fn()
-    torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record(stream)
-    for _ in range(args.steps):
-        fn()
-    e1.record(stream)
-    torch.cuda.synchronize()
-    print(json.dumps({"only": args.only, "call": label, "launches": args.steps,
-                      "us_per_call": round(e0.elapsed_time(e1) / max(1, args.steps) * 1e3, 2)}))
 
 
 class Suite:
@@ -500,89 +722,51 @@ def run_suite(args):
                           "fused_frac_hbm": round(nbytes / us_f / 1e3 / HBM_PEAK_GBS, 4)}), flush=True)
 
 
-def main():
-    args = parse()
-    if args.gpus != 1:
-        print("bench.py runs on one GPU only: this build measures the single-GPU share of the data-"
-              "parallel path (every rank runs the same layer on its own tokens); --gpus %d is not "
-              "supported" % args.gpus, file=sys.stderr)
-        sys.exit(2)
-
-    if args.suite:
-        run_suite(args)
-        return
-    import numpy as np
-    import torch
-    from paper_2608_27370_amd import inputs, puro
-
-    puro.lib()
-    dev = torch.device("cuda", 0)
-    torch.cuda.set_device(dev)
-    M, K, N = args.tokens, inputs.HIDDEN, inputs.QKV_OUT
-    d = inputs.qkv(M=M)
-
-    def up(bits):
-        return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).to(dev).view(torch.bfloat16)
-
-    X, W, dY = up(d["X"]), up(d["W"]), up(d["dY"])
-    rc = puro.LinearRecipe(puro.E4M3, puro.E4M3, puro.E5M2, 0, puro.SCALE_FP32)
-    saved = puro.linear_saved(M, N, K, rc, dev)
-    Y = torch.empty(M, N, dtype=torch.bfloat16, device=dev)
-    dX = torch.empty(M, K, dtype=torch.bfloat16, device=dev)
-    dW = torch.empty(N, K, dtype=torch.float32, device=dev)
-    wsf = torch.empty(max(1, puro.linear_fwd_workspace_size(M, N, K, rc)), dtype=torch.uint8, device=dev)
-    wsb = torch.empty(max(1, puro.linear_bwd_workspace_size(M, N, K, rc)), dtype=torch.uint8, device=dev)
-
-    def step():
-        puro.linear_fwd(X, W, rc, Y=Y, saved=saved, ws=wsf)
-        puro.linear_bwd(dY, saved, rc, K, dX=dX, dW=dW, ws=wsb)
-
+def run_only(args, torch, W):
+    """Profiling mode: one call (or the whole step) warmup + steps times."""
     stream = torch.cuda.current_stream()
-    if args.only:
-        run_only(args, torch, stream, step, lambda: calls(torch, puro, dev, M, N, K, X, W, dY, Y, dX, dW, saved))
-        return
+    if args.only in SWIGLU_CALLS:
+        from paper_2608_27370_amd import puro
+        fn, label = swiglu_workload(torch, puro)[args.only][0], "fused SwiGLU + quantise (%s)" % args.only
+    elif args.only in RMSNORM_CALLS:
+        from paper_2608_27370_amd import puro
+        fn, label = rmsnorm_workload(torch, puro)[args.only][0], "fused RMSNorm + quantise (%s)" % args.only
+    elif args.only == "copy":
+        src = torch.empty(COPY_BYTES // 4, dtype=torch.float32, device=stream.device).fill_(1.0)
+        dst = torch.empty_like(src)
+        fn, label = (lambda: dst.copy_(src)), "plain device copy of %d bytes" % COPY_BYTES
+    elif args.only == "step":
+        fn, label = W.step, "%s step" % W.name
+    else:
+        rows = [c for c in W.calls() if c.key == args.only]
+        if not rows:
+            sys.exit("unknown --only %r; calls of %s: %s" % (args.only, W.name,
+                                                             ", ".join(c.key for c in W.calls())))
+        fn, label = rows[0].fn, rows[0].label
     for _ in range(args.warmup):
-        step()
+        fn()
     torch.cuda.synchronize()
-    run = step
-    if args.graph:
-        # the step's launches captured once in a HIP graph and replayed: the
-        # same kernels on the same buffers, without per-launch host overhead
-        side = torch.cuda.Stream()
-        side.wait_stream(stream)
-        with torch.cuda.stream(side):
-            step()
-        stream.wait_stream(side)
-        torch.cuda.synchronize()
-        graph = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(graph):
-            step()
-        run = graph.replay
-        for _ in range(args.warmup):
-            run()
-        torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    t0 = time.perf_counter()
     e0.record(stream)
     for _ in range(args.steps):
-        run()
+        fn()
     e1.record(stream)
     torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    ms_per_step = e0.elapsed_time(e1) / args.steps
-    gemm_flops = 3 * 2.0 * M * N * K
-    value = gemm_flops / (ms_per_step * 1e-3) / 1e12
+    print(json.dumps({"only": args.only, "call": label, "launches": args.steps,
+                      "us_per_call": round(e0.elapsed_time(e1) / max(1, args.steps) * 1e3, 2)}), flush=True)
 
-    # each call on its own, timed over back-to-back launches between two
-    # events on the stream they run on (so that host launch latency hides
-    # behind the queue, as in the step)
-    kernels = calls(torch, puro, dev, M, N, K, X, W, dY, Y, dX, dW, saved)
-    reps = max(20, args.steps // 2)
-    # per-launch samples: each call bracketed by its own pair of events
-    # (median, p10, p90), warm (back to back) and, with --cold, after a
-    # 512 MiB fill that evicts the 256 MB MALL and the L2s
+
+def breakdown(args, torch, W, stream):
+    """Each call of the workload timed on the stream it runs on: back-to-back
+    launches between two events (the mean), and each launch bracketed by its
+    own events (median, p10, p90), warm and with --cold after a 512 MiB fill
+    that evicts the 256 MB MALL and the L2s."""
+    import numpy as np
+    calls = W.calls()
+    reps = 20
     pairs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
-    flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev) if args.cold else None
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device=W.dev) if args.cold else None
 
     def sampled(fn, cold):
         for a, b in pairs:
@@ -594,44 +778,101 @@ def main():
         torch.cuda.synchronize()
         us = np.sort([a.elapsed_time(b) * 1e3 for a, b in pairs])
         return {k: round(float(np.percentile(us, q)), 2) for k, q in (("p10", 10), ("median", 50), ("p90", 90))}
-
-    breakdown = []
-    for _, name, fn, flops, nbytes, launches in kernels:
+    rows = []
+    for c in calls:
         for _ in range(3):
-            fn()
+            c.fn()
         torch.cuda.synchronize()
         e0.record(stream)
         for _ in range(reps):
-            fn()
+            c.fn()
         e1.record(stream)
         torch.cuda.synchronize()
         us = e0.elapsed_time(e1) / reps * 1e3
-        row = {"call": name, "us": round(us, 2), "launches": launches, "per_launch_us": sampled(fn, False)}
+        row = {"call": c.label, "key": c.key, "us": round(us, 2), "per_step": c.count,
+               "launches": c.launches, "per_launch_us": sampled(c.fn, False)}
         if args.cold:
-            row["cold_per_launch_us"] = sampled(fn, True)
-        if flops:
-            row["tflops"] = round(flops / (us * 1e-6) / 1e12, 1)
-        if nbytes:
-            row["gbs_algorithmic"] = round(nbytes / (us * 1e-6) / 1e9, 1)
-        breakdown.append(row)
-    gemm_rows = [r for r in breakdown if "tflops" in r]
-    gemm_us = sum(r["us"] for r in gemm_rows)
-    # dominant kernel: the slowest call that is a single kernel launch
-    single = [(r, k) for r, k in zip(breakdown, kernels) if k[5] == 1]
-    dom, dom_k = max(single, key=lambda rk: rk[0]["us"])
-    traffic = profiled_traffic(dom_k[0]) if M == 8192 else None
+            row["cold_per_launch_us"] = sampled(c.fn, True)
+        if c.flops:
+            row["tflops"] = round(c.flops / (us * 1e-6) / 1e12, 1)
+            row["frac_fp8_peak"] = round(c.flops / (us * 1e-6) / 1e12 / FP8_PEAK_TFLOPS, 4)
+        if c.nbytes:
+            row["gbs_algorithmic"] = round(c.nbytes / (us * 1e-6) / 1e9, 1)
+            row["frac_hbm_peak"] = round(c.nbytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)
+        rows.append(row)
+    return calls, rows
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print("bench.py runs on one GPU only: this build measures the single-GPU share of the data-"
+              "parallel path (every rank runs the same layers on its own tokens); --gpus %d is not "
+              "supported" % args.gpus, file=sys.stderr)
+        sys.exit(2)
+    if args.suite:
+        run_suite(args)
+        return
+    import torch
+    from paper_2608_27370_amd import puro
+
+    puro.lib()
+    torch.cuda.set_device(0)
+    W = (Layers28 if args.workload == "layers28" else Qkv)(torch, puro)
+    if args.only:
+        run_only(args, torch, W)
+        return
+    stream = torch.cuda.current_stream()
+    for _ in range(args.warmup):
+        W.step()
+    torch.cuda.synchronize()
+    run = W.step
+    if args.graph:
+        # the step's launches captured once in a HIP graph and replayed
+        side = torch.cuda.Stream()
+        side.wait_stream(stream)
+        with torch.cuda.stream(side):
+            W.step()
+        stream.wait_stream(side)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            W.step()
+        run = graph.replay
+        for _ in range(args.warmup):
+            run()
+        torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    with ClockSampler() as clock:
+        t0 = time.perf_counter()
+        e0.record(stream)
+        for _ in range(args.steps):
+            run()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+    ms_per_step = e0.elapsed_time(e1) / args.steps
+    value = W.gemm_flops / (ms_per_step * 1e-3) / 1e12
+
+    calls, rows = breakdown(args, torch, W, stream)
+    gemm_us = sum(r["us"] * r["per_step"] for r in rows if "tflops" in r)
+    sum_us = sum(r["us"] * r["per_step"] for r in rows)
+    # dominant kernel: the single-launch call with the largest share of a step
+    single = [(r, c) for r, c in zip(rows, calls) if c.launches == 1]
+    dom, dom_c = max(single, key=lambda rc: rc[0]["us"] * rc[0]["per_step"])
     if "tflops" in dom:
         roofline = {"bound": "mfma", "kernel": dom["call"], "achieved": dom["tflops"], "peak": FP8_PEAK_TFLOPS,
                     "unit": "TFLOP/s", "frac": round(dom["tflops"] / FP8_PEAK_TFLOPS, 4),
-                    "algorithmic_flops_per_launch": dom_k[3]}
+                    "algorithmic_flops_per_launch": dom_c.flops}
     else:
         roofline = {"bound": "hbm", "kernel": dom["call"], "achieved": dom["gbs_algorithmic"], "peak": HBM_PEAK_GBS,
                     "unit": "GB/s", "frac": round(dom["gbs_algorithmic"] / HBM_PEAK_GBS, 4),
-                    "algorithmic_bytes_per_launch": dom_k[4]}
+                    "algorithmic_bytes_per_launch": dom_c.nbytes}
     roofline["us_per_launch"] = dom["us"]
-    roofline["traffic"] = traffic
+    roofline["share_of_step"] = round(dom["us"] * dom["per_step"] / (ms_per_step * 1e3), 4)
+    roofline["traffic"] = profiled(args.workload, dom_c.key, "bytes")
     roofline["traffic_unit"] = "HBM-side bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)"
-
+    clk = clock.summary()
     out = {
         "metric": METRIC,
         "value": round(value, 2),
@@ -645,18 +886,26 @@ def main():
         "vs_baseline": None,
         "dtype": "fp8",
         "data": "synthetic",
-        "config": {"workload": "qkv_projection_fwd_dgrad_wgrad", "M": M, "K": K, "N": N,
-                   "recipe": "per-tensor scales, X/W E4M3, dY E5M2, BF16 Y/dX, FP32 dW",
-                   "launch": "hip_graph" if args.graph else "eager"},
+        "config": dict(W.config, launch="hip_graph" if args.graph else "eager"),
         "pct_fp8_peak": round(100 * value / FP8_PEAK_TFLOPS, 2),
-        "gemm_only_tflops": round(gemm_flops / (gemm_us * 1e-6) / 1e12, 1),
-        "breakdown": breakdown,
+        "gemm_only_tflops": round(W.gemm_flops / (gemm_us * 1e-6) / 1e12, 1),
+        "gemm_only_pct_fp8_peak": round(100 * W.gemm_flops / (gemm_us * 1e-6) / 1e12 / FP8_PEAK_TFLOPS, 2),
+        "breakdown_sum_ms": round(sum_us / 1e3, 3),
+        "breakdown": rows,
         "roofline": roofline,
+        "clock": clk,
         "wall_s_timed": round(wall, 3),
+        "mfu_context": {"paper_p_eff_tflops": round(p_eff(PAPER_FP8_SHARE, PAPER_FP8_PEAK, PAPER_BF16_PEAK), 2),
+                        "mi355x_p_eff_tflops_at_paper_mix": round(p_eff(PAPER_FP8_SHARE, FP8_PEAK_TFLOPS,
+                                                                        BF16_PEAK_TFLOPS), 1),
+                        "fp8_share_of_this_step": 1.0},
     }
+    if clk:
+        ghz = clk["median_mhz"] / 1e3
+        out["pct_fp8_peak_at_measured_clock"] = round(100 * value / (FP8_PEAK_TFLOPS * ghz / PEAK_CLOCK_GHZ), 2)
     if args.cpu_tokens > 0:
-        out["cpu_baseline"] = cpu_baseline(args.cpu_tokens, args.cpu_reps)
-    print(json.dumps(out))
+        out["cpu_baseline"] = cpu_baseline(args.workload, args.cpu_tokens)
+    print(json.dumps(out), flush=True)
 
 
 if __name__ == "__main__":
