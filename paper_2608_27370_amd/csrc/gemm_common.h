@@ -27,6 +27,7 @@ struct Params {
     int ld_sa, ld_sb;          // scale pitch: K/128 (row-major) or the row (block) count (k-major)
     uint32_t sa_bytes, sb_bytes;  // sizes of the scale arrays (grouped modes)
     int ksteps, ksteps_per_split, splits;
+    int gm;                    // tile rows per group within an XCD's range of tiles
     int tiles_m, tiles_n;
     int accumulate;
     float alpha;               // host-known part of the per-tensor scale (1)

@@ -126,7 +126,7 @@ __device__ __forceinline__ void dma_to_lds(v4i rsrc, uint32_t lds, uint32_t voff
 // multiply, so a load that cannot issue (the texture unit's queue full)
 // does not hold up their matrix instructions. Both kinds meet at the one
 // barrier per slice.
-template <int BM, int BN, int WM, int WN, int FA, int FB, int OUT, bool GROUPED, int GM, int SL, int NST, bool PROD>
+template <int BM, int BN, int WM, int WN, int FA, int FB, int OUT, bool GROUPED, int SL, int NST, bool PROD>
 __global__ __launch_bounds__(WM * WN * 64 * (PROD ? 2 : 1)) void gemm_fp8_kernel(Params p) {
     constexpr int NW = WM * WN;
     constexpr int WTM = BM / WM, WTN = BN / WN;
@@ -161,17 +161,17 @@ __global__ __launch_bounds__(WM * WN * 64 * (PROD ? 2 : 1)) void gemm_fp8_kernel
     const int wave = producer ? wave_id - NW : wave_id;
     const int wm = wave / WN, wn = wave % WN;
 
-    // ---- tile index: contiguous ranges per XCD, grouped by GM row panels
+    // ---- tile index: contiguous ranges per XCD, grouped by p.gm row panels
     const int T = gridDim.x;
     const int b = blockIdx.x;
     const int lt = (T % 8 == 0) ? (b % 8) * (T / 8) + b / 8 : b;
     const int per_split = p.tiles_m * p.tiles_n;
     const int ks = lt / per_split;
     const int rem = lt - ks * per_split;
-    const int group = rem / (GM * p.tiles_n);
-    const int first_m = group * GM;
-    const int gsz = min(GM, p.tiles_m - first_m);
-    const int r2 = rem - group * GM * p.tiles_n;
+    const int group = rem / (p.gm * p.tiles_n);
+    const int first_m = group * p.gm;
+    const int gsz = min(p.gm, p.tiles_m - first_m);
+    const int r2 = rem - group * p.gm * p.tiles_n;
     const int tm = first_m + r2 % gsz, tn = r2 / gsz;
     const int m0 = tm * BM, n0 = tn * BN;
     // per-tensor scales, applied to the FP32 sums in the epilogue (loaded
@@ -616,15 +616,11 @@ __global__ __launch_bounds__(WM * WN * 64 * (PROD ? 2 : 1)) void gemm_fp8_kernel
 
 template <int BM, int BN, int WM, int WN, int SL, int NST, int PROD, int FA, int FB, int OUT>
 void launch_cfg(const Params& prm, bool grouped, int grid, hipStream_t stream) {
-    // tile rows per group of the XCD ranges: the QKV Wgrad's 24-tile ranges
-    // become 4 x 6 tiles (10 operand panels per XCD instead of 11 at 8),
-    // and the 32-tile ranges of one-tile-per-CU GEMMs stay at 12 panels
-    constexpr int GM = 4;
     constexpr int threads = WM * WN * 64 * (PROD ? 2 : 1);
     if (grouped)
-        gemm_fp8_kernel<BM, BN, WM, WN, FA, FB, OUT, true, GM, SL, NST, PROD != 0><<<grid, threads, 0, stream>>>(prm);
+        gemm_fp8_kernel<BM, BN, WM, WN, FA, FB, OUT, true, SL, NST, PROD != 0><<<grid, threads, 0, stream>>>(prm);
     else
-        gemm_fp8_kernel<BM, BN, WM, WN, FA, FB, OUT, false, GM, SL, NST, PROD != 0><<<grid, threads, 0, stream>>>(prm);
+        gemm_fp8_kernel<BM, BN, WM, WN, FA, FB, OUT, false, SL, NST, PROD != 0><<<grid, threads, 0, stream>>>(prm);
 }
 
 template <int BM, int BN, int WM, int WN, int SL, int NST, int PROD, int FA, int FB>
