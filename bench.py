@@ -305,9 +305,10 @@ class Layers28:
     name = "layers28_blockwise_m16384"
     M = 16384
 
-    def __init__(self, torch, puro):
+    def __init__(self, torch, puro, layers=None):
         from paper_2608_27370_amd import inputs
         self.torch, self.P, self.inputs = torch, puro, inputs
+        nl = inputs.LAYERS if layers is None else layers
         P, M = puro, self.M
         dev = torch.device("cuda", 0)
         self.dev = dev
@@ -319,7 +320,7 @@ class Layers28:
             return (torch.randn(shape, generator=gen, device=dev) * std).to(torch.bfloat16)
         self.kinds = inputs.LAYER_LINEARS
         self.layers = []
-        for _ in range(inputs.LAYERS):
+        for _ in range(nl):
             row = []
             for name, N, K in self.kinds:
                 row.append(dict(X=normal((M, K), 1.0), W=normal((N, K), 0.02), dY=normal((M, N), 1e-3),
@@ -333,8 +334,8 @@ class Layers28:
                                dtype=torch.uint8, device=dev)
         self.wsb = torch.empty(max(P.linear_bwd_workspace_size(M, N, K, self.rc) for _, N, K in self.kinds),
                                dtype=torch.uint8, device=dev)
-        self.gemm_flops = sum(3 * 2.0 * M * N * K for _, N, K in self.kinds) * inputs.LAYERS
-        self.config = {"workload": self.name, "layers": inputs.LAYERS, "tokens": M,
+        self.gemm_flops = sum(3 * 2.0 * M * N * K for _, N, K in self.kinds) * nl
+        self.config = {"workload": self.name, "layers": nl, "tokens": M,
                        "linears": {n: [N, K] for n, N, K in self.kinds},
                        "recipe": "blockwise: X, dY 1x128 groups along each GEMM's reduction dim, W 128x128 blocks, "
                                  "power-of-two scales, E4M3 throughout; BF16 Y/dX, FP32 dW"}
@@ -357,7 +358,7 @@ class Layers28:
         torch, P, M = self.torch, self.P, self.M
         E4, KM = P.E4M3, P.SCALE_KMAJOR
         ROW, BLK = P.SCALE_ROW_1x128 | KM, P.SCALE_BLOCK_128x128 | KM
-        L = len(self.layers)
+        L = self.inputs.LAYERS       # each kind's calls occur once per layer of the step
         out = []
         for j, (name, N, K) in enumerate(self.kinds):
             lin, o = self.layers[0][j], self.outs[j]
@@ -818,7 +819,11 @@ def main():
 
     puro.lib()
     torch.cuda.set_device(0)
-    W = (Layers28 if args.workload == "layers28" else Qkv)(torch, puro)
+    if args.workload == "layers28":
+        # a single call profiles layer 0's tensors; a step needs every layer
+        W = Layers28(torch, puro, layers=1 if args.only and args.only != "step" else None)
+    else:
+        W = Qkv(torch, puro)
     if args.only:
         run_only(args, torch, W)
         return
