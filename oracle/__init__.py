@@ -18,11 +18,13 @@ Training", and Appendix C, "FP8 implementation pipeline"):
                 quantises (the fused SwiGLU + quantise operation);
 * ``rmsnorm`` -- the RMSNorm whose BF16 output the QKV and gate/up
                 projections quantise (the fused RMSNorm + quantise
-                operation).
+                operation);
+* ``lm_head`` -- the language-model head with its cross-entropy loss,
+                forward and backward.
 
 It is test infrastructure: only ``tests/``, ``__graft_entry__.smoke()`` and
 the ``cpu_baseline`` leg of ``bench.py`` may import it. It shares no code with
 the HIP library and never imports it.
 """
 
-from . import bf16, fp8, quant, gemm, linear, rmsnorm, swiglu  # noqa: F401
+from . import bf16, fp8, quant, gemm, linear, rmsnorm, swiglu, lm_head  # noqa: F401
