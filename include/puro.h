@@ -137,6 +137,25 @@ puro_status puro_quantize_fp8(const uint16_t* x, int64_t rows, int64_t cols, int
                               uint8_t* qT, float* scaleT, void* ws, size_t ws_bytes,
                               hipStream_t stream);
 
+/* For callers that cannot allocate (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc): puro_quantize_fp8 without
+ * a workspace. The per-tensor mode's amax pass keeps its partial maxima in a
+ * library-owned static device array of PURO_QUANTIZE_STATIC_SCRATCH_BYTES
+ * (32 KiB) on each GPU it runs on, held until the process ends (its address is
+ * looked up on the first such call on a device); nothing is allocated or freed.
+ * Every call on one GPU shares that array: calls that overlap on one GPU (on
+ * different streams, or from different threads without ordering) race and
+ * may give wrong scales; order them on one stream. The partials are written
+ * in full by each call, so nothing needs clearing. Sizes whose partials would
+ * not fit return PURO_ERR_WORKSPACE (the quantiser uses at most 4096 partials,
+ * which always fit). Arguments, outputs and errors otherwise as
+ * puro_quantize_fp8; grouped modes and a supplied amax use no scratch. */
+#define PURO_QUANTIZE_STATIC_SCRATCH_BYTES 32768
+puro_status puro_quantize_fp8_static(const uint16_t* x, int64_t rows, int64_t cols, int64_t ld,
+                                     puro_fp8_format fmt, puro_scale_mode mode, puro_scale_rounding rnd,
+                                     const float* amax_in, uint8_t* q, float* scale, uint8_t* qT, float* scaleT,
+                                     hipStream_t stream);
+
 /* ------------------------------------------------- SwiGLU + quantise ---
  * The MLP of the paper's model (the Qwen3-1.7B architecture, Section 2)
  * computes down(silu(gate(x)) * up(x)); the hidden flow stays BF16 and the

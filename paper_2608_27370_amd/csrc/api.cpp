@@ -111,7 +111,7 @@ struct Source {
 puro_status quantize_impl(const uint16_t* x, int64_t rows, int64_t cols, int64_t ld, puro_fp8_format fmt,
                           puro_scale_mode mode_arg, puro_scale_rounding rnd, const float* amax_in, uint8_t* q,
                           float* scale, uint8_t* qT, float* scaleT, void* ws, size_t ws_bytes,
-                          hipStream_t stream, Source src = Source()) {
+                          hipStream_t stream, Source src = Source(), bool static_ws = false) {
     // the scale-layout flag of the grouped modes
     const int kmajor = ((int)mode_arg & PURO_SCALE_KMAJOR) != 0;
     const puro_scale_mode mode = (puro_scale_mode)((int)mode_arg & ~(int)PURO_SCALE_KMAJOR);
@@ -206,6 +206,12 @@ puro_status quantize_impl(const uint16_t* x, int64_t rows, int64_t cols, int64_t
         return launched();
     }
     if (qmode == kQTensor && !amax_in) {
+        if (static_ws) {
+            // the library's own scratch (arguments are valid by now)
+            if (quant_tensor_ws_bytes(rows, cols) > kStaticScratchBytes) return PURO_ERR_WORKSPACE;
+            if (static_scratch(&ws) != hipSuccess) return PURO_ERR_HIP;
+            ws_bytes = kStaticScratchBytes;
+        }
         if (!ws) return PURO_ERR_NULL;
         if (ws_bytes < quant_tensor_ws_bytes(rows, cols)) return PURO_ERR_WORKSPACE;
         launch_quantize_tensor(fmt, a, ws, stream, swiglu);
@@ -226,6 +232,16 @@ puro_status puro_quantize_fp8(const uint16_t* x, int64_t rows, int64_t cols, int
                               const float* amax_in, uint8_t* q, float* scale, uint8_t* qT,
                               float* scaleT, void* ws, size_t ws_bytes, hipStream_t stream) {
     return quantize_impl(x, rows, cols, ld, fmt, mode, rnd, amax_in, q, scale, qT, scaleT, ws, ws_bytes, stream);
+}
+
+static_assert(PURO_QUANTIZE_STATIC_SCRATCH_BYTES == kStaticScratchBytes, "scratch size");
+
+puro_status puro_quantize_fp8_static(const uint16_t* x, int64_t rows, int64_t cols, int64_t ld,
+                                     puro_fp8_format fmt, puro_scale_mode mode, puro_scale_rounding rnd,
+                                     const float* amax_in, uint8_t* q, float* scale, uint8_t* qT, float* scaleT,
+                                     hipStream_t stream) {
+    return quantize_impl(x, rows, cols, ld, fmt, mode, rnd, amax_in, q, scale, qT, scaleT, nullptr, 0, stream,
+                         Source(), true);
 }
 
 // ---------------------------------------------------- SwiGLU + quantise

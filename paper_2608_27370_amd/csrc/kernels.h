@@ -61,6 +61,11 @@ struct QuantArgs {
 
 // Workspace of a per-tensor quantisation that computes its own amax.
 size_t quant_tensor_ws_bytes(int64_t rows, int64_t cols);
+
+// Size of the library's own per-GPU scratch array (quant.hip), and its
+// device address on the current device (looked up once per device).
+constexpr size_t kStaticScratchBytes = 32768;
+hipError_t static_scratch(void** ptr);
 // Per-tensor quantisation with the tensor's own amax: the partial maxima
 // pass, then the quantise pass (which reduces them, or reads the amax a
 // one-block reduction wrote). ws holds quant_tensor_ws_bytes.

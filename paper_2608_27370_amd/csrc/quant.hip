@@ -20,6 +20,8 @@
 // outside a tensor, so they carry no branches and never wait on each other.
 
 #include <algorithm>
+#include <atomic>
+#include <mutex>
 
 #include "device_common.h"
 #include "kernels.h"
@@ -784,6 +786,40 @@ void launch_swiglu_bwd_quantize(int fmt, int mode, QuantArgs a, void* ws, hipStr
     }
     if (fmt == kE4M3) launch_quantize_fmt<kE4M3, kSrcSwigluBwd>(mode, a, stream);
     else launch_quantize_fmt<kE5M2, kSrcSwigluBwd>(mode, a, stream);
+}
+
+// ---- scratch for callers that cannot allocate ------------------------------
+// puro_quantize_fp8_static keeps the per-tensor amax pass's partial maxima
+// (and the reduced amax) here instead of in a caller workspace: a file-scope
+// device array, one copy per GPU the library runs on, held until the process
+// ends. Host code never passes the array's name to a kernel (there it is a
+// host-side stand-in): it looks up each device's address once, with that
+// device current, and passes that.
+namespace {
+__device__ __attribute__((aligned(256))) uint8_t scratch[kStaticScratchBytes];
+constexpr int kMaxDevices = 64;
+std::atomic<void*> g_scratch_ptr[kMaxDevices];
+std::mutex g_scratch_mu;
+}  // namespace
+
+hipError_t static_scratch(void** ptr) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    void* p = g_scratch_ptr[dev].load(std::memory_order_acquire);
+    if (!p) {
+        std::lock_guard<std::mutex> lock(g_scratch_mu);
+        p = g_scratch_ptr[dev].load(std::memory_order_acquire);
+        if (!p) {
+            e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+            if (e != hipSuccess) return e;
+            if (!p) return hipErrorInvalidSymbol;
+            g_scratch_ptr[dev].store(p, std::memory_order_release);
+        }
+    }
+    *ptr = p;
+    return hipSuccess;
 }
 
 }  // namespace puro

@@ -54,6 +54,7 @@ _SIGS = {
     "puro_amax": (_i, [_p, _i64, _i64, _i64, _p, _p, _sz, _p]),
     "puro_quantize_workspace_size": (_sz, [_i64, _i64]),
     "puro_quantize_fp8": (_i, [_p, _i64, _i64, _i64, _i, _i, _i, _p, _p, _p, _p, _p, _p, _sz, _p]),
+    "puro_quantize_fp8_static": (_i, [_p, _i64, _i64, _i64, _i, _i, _i, _p, _p, _p, _p, _p, _p]),
     "puro_swiglu_quantize_workspace_size": (_sz, [_i64, _i64]),
     "puro_swiglu_quantize_fp8": (_i, [_p, _i64, _i64, _i64, _i, _i, _i, _p, _p, _p, _p, _p, _sz, _p]),
     "puro_swiglu_bwd_quantize_workspace_size": (_sz, [_i64, _i64]),
@@ -153,6 +154,19 @@ def quantize_fp8(x, fmt, mode=SCALE_TENSOR, rnd=SCALE_FP32, amax_in=None, want_q
     _check("puro_quantize_fp8", lib().puro_quantize_fp8(
         _ptr(x), rows, cols, _ld(x), fmt, mode, rnd, _ptr(amax_in), _ptr(q), _ptr(scale), _ptr(qT),
         _ptr(scaleT), _ptr(w), nb, _stream()))
+    return dict(q=q, scale=scale, qT=qT, scaleT=scaleT)
+
+
+def quantize_fp8_static(x, fmt, mode=SCALE_TENSOR, rnd=SCALE_FP32, amax_in=None, want_q=True, want_qT=False,
+                        out=None):
+    """quantize_fp8 through the allocation-free entry point (the library's
+    own per-GPU scratch instead of a workspace); pass preallocated ``out``
+    tensors to allocate nothing at all."""
+    rows, cols = x.shape
+    q, scale, qT, scaleT = _quant_outputs(rows, cols, mode, want_q, want_qT, out, x.device)
+    _check("puro_quantize_fp8_static", lib().puro_quantize_fp8_static(
+        _ptr(x), rows, cols, _ld(x), fmt, mode, rnd, _ptr(amax_in), _ptr(q), _ptr(scale), _ptr(qT),
+        _ptr(scaleT), _stream()))
     return dict(q=q, scale=scale, qT=qT, scaleT=scaleT)
 
 

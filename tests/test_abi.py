@@ -99,6 +99,19 @@ def test_quantize_validation(puro):
     assert q(FAKE, 128, 136, 136, 0, 1 | KM, 1, None, FAKE, FAKE, None, None, None, 0, None) == ERR_ALIGN
 
 
+def test_static_quantize_validation(puro):
+    """The allocation-free quantise validates like puro_quantize_fp8 and
+    returns before any HIP call (none is possible here: no GPU)."""
+    L = puro.lib()
+    q = lambda *a: L.puro_quantize_fp8_static(*a)
+    assert q(FAKE, 128, 128, 128, 7, 0, 0, None, FAKE, FAKE, None, None, None) == ERR_UNSUPPORTED
+    assert q(None, 128, 128, 128, 0, 0, 0, None, FAKE, FAKE, None, None, None) == ERR_NULL
+    assert q(FAKE, 128, 128, 128, 0, 0, 0, None, None, None, None, None, None) == ERR_NULL
+    assert q(FAKE, 16, 24, 24, 0, 0, 0, None, FAKE, FAKE, None, None, None) == ERR_ALIGN
+    assert q(FAKE, 16, 128, 1 << 23, 0, 0, 0, None, FAKE, FAKE, None, None, None) == ERR_SHAPE
+    assert q(FAKE, 128, 128, 128, 0, 1, 0, None, FAKE, FAKE, None, None, None) == ERR_UNSUPPORTED
+
+
 def test_gemm_validation(puro):
     L = puro.lib()
     Op = puro.Operand
