@@ -20,11 +20,13 @@ Training", and Appendix C, "FP8 implementation pipeline"):
                 projections quantise (the fused RMSNorm + quantise
                 operation);
 * ``lm_head`` -- the language-model head with its cross-entropy loss,
-                forward and backward.
+                forward and backward;
+* ``muonh``  -- the MuonH optimiser step of one matrix: momentum,
+                Newton-Schulz orthogonalisation and the hyperball update.
 
 It is test infrastructure: only ``tests/``, ``__graft_entry__.smoke()`` and
 the ``cpu_baseline`` leg of ``bench.py`` may import it. It shares no code with
 the HIP library and never imports it.
 """
 
-from . import bf16, fp8, quant, gemm, linear, rmsnorm, swiglu, lm_head  # noqa: F401
+from . import bf16, fp8, quant, gemm, linear, rmsnorm, swiglu, lm_head, muonh  # noqa: F401
