@@ -13,7 +13,11 @@ and the Fprop, Dgrad and Wgrad GEMMs. Every layer has its own seeded
 synthetic weights, activations and gradients (drawn on the device; weights
 ~N(0, 0.02^2), activations ~N(0, 1), gradients ~N(0, (1e-3)^2)), resident in
 HBM before the timed region. ``--workload qkv`` times the per-tensor QKV
-projection step (M 8192) instead.
+projection step (M 8192) instead; ``lm_head_bf16`` / ``lm_head_fp8`` the fused
+LM head with its cross-entropy loss, forward and backward, at M 8192, V
+151936, K 1536 (BF16 as the paper runs it, or the blockwise FP8 recipe);
+``muonh28`` one MuonH optimiser step of the 28 layers' QKV, O, gate/up and down
+matrices (Section 3.3), one call per kind.
 
 Prints one JSON line: the metric (TFLOP/s of fwd + dgrad + wgrad GEMM work
 per step time), the GEMM-only rate, a per-call breakdown (each kernel call
@@ -51,8 +55,9 @@ def p_eff(fp8_share, fp8_peak, bf16_peak):
     return 1.0 / (fp8_share / fp8_peak + (1.0 - fp8_share) / bf16_peak)
 
 
-WORKLOADS = ("layers28", "qkv")
-DEFAULTS = {"layers28": (20, 3), "qkv": (1000, 50)}   # (steps, warmup)
+WORKLOADS = ("layers28", "qkv", "lm_head_bf16", "lm_head_fp8", "muonh28")
+DEFAULTS = {"layers28": (20, 3), "qkv": (1000, 50), "lm_head_bf16": (20, 3), "lm_head_fp8": (20, 3),
+            "muonh28": (10, 2)}   # (steps, warmup)
 
 
 def parse():
@@ -60,7 +65,9 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--workload", choices=WORKLOADS, default="layers28",
                     help="layers28: the 28-layer blockwise step at M 16384 (default); "
-                         "qkv: the per-tensor QKV projection step at M 8192")
+                         "qkv: the per-tensor QKV projection step at M 8192; lm_head_bf16 / lm_head_fp8: the "
+                         "fused LM head + cross-entropy at M 8192, V 151936; muonh28: one MuonH step of the "
+                         "28 layers' matrices")
     ap.add_argument("--steps", type=int, default=None)
     ap.add_argument("--warmup", type=int, default=None)
     ap.add_argument("--cpu-tokens", type=int, default=None,
@@ -84,7 +91,7 @@ def parse():
     a.steps = st if a.steps is None else a.steps
     a.warmup = wu if a.warmup is None else a.warmup
     if a.cpu_tokens is None:
-        a.cpu_tokens = 256 if a.workload == "layers28" else 8192
+        a.cpu_tokens = {"layers28": 256, "qkv": 8192}.get(a.workload, 0)
     return a
 
 
@@ -140,11 +147,13 @@ def cpu_baseline(workload, tokens):
 
 class ClockSampler:
     """The GFX clock sampled through amdsmi every few milliseconds while
-    running (None when amdsmi is unavailable)."""
+    running: the mean over the XCDs of the metrics table's current GFX
+    clocks, or (where the table has none) the clock-info reading; None when
+    amdsmi is unavailable."""
 
     def __init__(self, period_s=0.005):
         self.samples, self.period, self._stop = [], period_s, threading.Event()
-        self.handle = None
+        self.handle, self.source = None, None
         try:
             import amdsmi
             amdsmi.amdsmi_init()
@@ -155,7 +164,17 @@ class ClockSampler:
             self.handle = None
 
     def read(self):
+        try:
+            m = self.amdsmi.amdsmi_get_gpu_metrics_info(self.handle)
+            v = m.get("current_gfxclks")
+            vals = [float(x) for x in v if isinstance(x, (int, float)) and 0 < x < 65535] if isinstance(v, list) else []
+            if vals:
+                self.source = "amdsmi metrics current_gfxclks, mean over %d XCDs" % len(vals)
+                return sum(vals) / len(vals)
+        except Exception:
+            pass
         info = self.amdsmi.amdsmi_get_clock_info(self.handle, self.amdsmi.AmdSmiClkType.GFX)
+        self.source = "amdsmi clock info GFX"
         return float(info["clk"])
 
     def _run(self):
@@ -183,7 +202,7 @@ class ClockSampler:
             return None
         s = np.array(self.samples)
         return {"median_mhz": float(np.median(s)), "p10_mhz": float(np.percentile(s, 10)),
-                "p90_mhz": float(np.percentile(s, 90)), "samples": int(s.size), "source": "amdsmi GFX clock"}
+                "p90_mhz": float(np.percentile(s, 90)), "samples": int(s.size), "source": self.source}
 
 
 SWIGLU_CALLS = ("swiglu_tensor", "swiglu_groups", "swiglu_bwd_groups")
@@ -292,11 +311,13 @@ def swiglu_workload(torch, puro, M=8192):
 
 
 class Call:
-    """One kernel call of a step's breakdown: `count` times per step."""
+    """One kernel call of a step's breakdown: `count` times per step; `peak`
+    is the MFMA peak its FLOPs are priced against."""
 
-    def __init__(self, key, label, fn, flops=None, nbytes=None, launches=1, count=1):
+    def __init__(self, key, label, fn, flops=None, nbytes=None, launches=1, count=1, peak=FP8_PEAK_TFLOPS):
         self.key, self.label, self.fn = key, label, fn
         self.flops, self.nbytes, self.launches, self.count = flops, nbytes, launches, count
+        self.peak = peak
 
 
 class Layers28:
@@ -476,6 +497,126 @@ class Qkv:
                  lambda: P.fp8_gemm(A_w, N, B_w, K, M, P.OUT_FP32, D=self.dW, ws=gws), flops=fl,
                  launches=P.fp8_gemm_plan(N, K, M)["launches"]),
         ]
+
+
+class LmHead:
+    """The fused LM head + cross-entropy at M 8192 tokens, V 151936, K 1536:
+    forward (lse and loss) then backward (dX, dW) per step. X ~ Student-t(3),
+    W ~ N(0, 0.02^2), targets uniform, drawn on the device. The algorithmic
+    work is the three GEMMs' 6 M V K; the backward recomputes the logits (2 M V
+    K more), which the rate does not count."""
+
+    def __init__(self, torch, puro, recipe, M=8192):
+        from paper_2608_27370_amd import inputs
+        self.torch, self.P = torch, puro
+        dev = torch.device("cuda", 0)
+        self.dev = dev
+        self.M, self.V, self.K = M, inputs.VOCAB, inputs.HIDDEN
+        self.recipe = recipe
+        gen = torch.Generator(device=dev)
+        gen.manual_seed(5)
+        M, V, K = self.M, self.V, self.K
+        chi = torch.randn(M, K, 3, generator=gen, device=dev).square().sum(-1) / 3.0
+        self.X = (torch.randn(M, K, generator=gen, device=dev) / chi.sqrt()).to(torch.bfloat16)
+        self.W = (torch.randn(V, K, generator=gen, device=dev) * 0.02).to(torch.bfloat16)
+        self.t = torch.randint(0, V, (M,), generator=gen, device=dev, dtype=torch.int32)
+        self.lse = torch.empty(M, dtype=torch.float32, device=dev)
+        self.loss = torch.empty(M, dtype=torch.float32, device=dev)
+        self.dX = torch.empty(M, K, dtype=torch.bfloat16, device=dev)
+        self.dW = torch.empty(V, K, dtype=torch.float32, device=dev)
+        self.wsf = torch.empty(puro.lm_head_ce_workspace_size(M, V, K, recipe, False), dtype=torch.uint8, device=dev)
+        self.wsb = torch.empty(puro.lm_head_ce_workspace_size(M, V, K, recipe, True), dtype=torch.uint8, device=dev)
+        fp8 = recipe == puro.LM_HEAD_FP8
+        self.name = "lm_head_ce_%s_m%d_v%d" % ("fp8" if fp8 else "bf16", M, V)
+        self.flops = 6.0 * M * V * K
+        self.peak = FP8_PEAK_TFLOPS if fp8 else BF16_PEAK_TFLOPS
+        self.dtype = "fp8" if fp8 else "bf16"
+        self.metric = "LM head + cross-entropy fwd+bwd TFLOP/s (6 M V K per step) at Qwen2-1.5B shapes"
+        self.config = {"workload": self.name, "tokens": M, "vocab": V, "hidden": K,
+                       "recipe": ("blockwise FP8: X 1x128 rows / 128x1 columns, W 128x128 blocks, dz BF16 then "
+                                  "1x128 + 128x1, E4M3, power-of-two scales" if fp8 else
+                                  "BF16 operands, binary32 accumulation, dz BF16"),
+                       "logits": "never stored: forward reduces them to (max, sum exp) per 128-column block in "
+                                 "the GEMM epilogue; backward recomputes them per 16384-column chunk"}
+
+    def step(self):
+        P = self.P
+        P.lm_head_ce_fwd(self.X, self.W, self.t, self.recipe, lse=self.lse, loss=self.loss, ws=self.wsf)
+        P.lm_head_ce_bwd(self.X, self.W, self.t, self.lse, self.recipe, grad_scale=1.0 / self.M, dX=self.dX,
+                         dW=self.dW, ws=self.wsb)
+
+    def calls(self):
+        P, M, V, K = self.P, self.M, self.V, self.K
+        fl = 2.0 * M * V * K
+        return [
+            Call("fwd", "forward: logits GEMM with the (max, sum exp) epilogue, lse per row%s" %
+                 (", X and W quantised" if self.dtype == "fp8" else ""),
+                 lambda: P.lm_head_ce_fwd(self.X, self.W, self.t, self.recipe, lse=self.lse, loss=self.loss,
+                                          ws=self.wsf), flops=fl, launches=0, peak=self.peak),
+            Call("bwd", "backward: per 16384-column chunk the logits GEMM with the softmax-gradient epilogue, "
+                 "then dX and dW GEMMs (4 M V K executed, 4 M V K counted)",
+                 lambda: P.lm_head_ce_bwd(self.X, self.W, self.t, self.lse, self.recipe, grad_scale=1.0 / M,
+                                          dX=self.dX, dW=self.dW, ws=self.wsb), flops=2 * fl, launches=0,
+                 peak=self.peak),
+        ]
+
+
+class MuonH28:
+    """One MuonH step (Section 3.3) of the 28 layers' wrapped matrices: per
+    kind (QKV 2048x1536, O 1536x1536, gate/up 17920x1536, down 1536x8960) one
+    call on the 28 matrices stored back to back (FP32 W, G, momentum; W ~
+    N(0, 0.02^2), G and momentum ~ N(0, (1e-3)^2), drawn on the device). The
+    algorithmic work is the Newton-Schulz products: per matrix and step (r <=
+    c its oriented shape) 2 r^2 c for X X^T, 2 r^3 for A A^T, 2 r^2 c for B X,
+    five steps."""
+
+    name = "muonh_28_layers_qwen2_1p5b"
+
+    def __init__(self, torch, puro):
+        from paper_2608_27370_amd import inputs
+        self.torch, self.P = torch, puro
+        dev = torch.device("cuda", 0)
+        self.dev = dev
+        gen = torch.Generator(device=dev)
+        gen.manual_seed(7)
+        L = inputs.LAYERS
+        self.kinds = inputs.LAYER_LINEARS
+        self.mats = []
+        self.flops = 0.0
+        for name, rows, cols in self.kinds:
+            W = torch.randn(L, rows, cols, generator=gen, device=dev) * 0.02
+            G = torch.randn(L, rows, cols, generator=gen, device=dev) * 1e-3
+            buf = torch.randn(L, rows, cols, generator=gen, device=dev) * 1e-3
+            R = torch.linalg.vector_norm(W.double(), dim=(1, 2)).float()
+            wb = torch.empty(L, rows, cols, dtype=torch.bfloat16, device=dev)
+            ws = torch.empty(puro.lib().puro_muonh_workspace_size(L, rows, cols), dtype=torch.uint8, device=dev)
+            r, c = min(rows, cols), max(rows, cols)
+            fl = L * 5 * (4.0 * r * r * c + 2.0 * r ** 3)
+            self.flops += fl
+            self.mats.append(dict(name=name, W=W, G=G, buf=buf, R=R, wb=wb, ws=ws, flops=fl, shape=(rows, cols)))
+        self.peak = BF16_PEAK_TFLOPS
+        self.dtype = "bf16"
+        self.metric = "MuonH optimiser step: Newton-Schulz TFLOP/s over the 28 layers' matrices (BF16 MFMA)"
+        self.config = {"workload": self.name, "layers": L, "matrices": {n: [r, c] for n, r, c in self.kinds},
+                       "newton_schulz": "5 quintic steps in BF16, (a, b, c) = (3.4445, -4.7750, 2.0315)",
+                       "state": "FP32 W, G, momentum (mu 0.95, Nesterov); BF16 copy of W' written"}
+
+    def _call(self, m):
+        P = self.P
+        return lambda: P.muonh_step(m["W"], m["G"], m["buf"], m["R"], 1e-3, w_bf16=m["wb"], ws=m["ws"])
+
+    def step(self):
+        for m in self.mats:
+            self._call(m)()
+
+    def calls(self):
+        out = []
+        for m in self.mats:
+            rows, cols = m["shape"]
+            out.append(Call(m["name"], "%s: MuonH step of 28 [%d,%d] matrices (momentum, 5 Newton-Schulz steps of "
+                            "3 batched BF16 GEMMs + transpose, hyperball)" % (m["name"], rows, cols),
+                            self._call(m), flops=m["flops"], launches=0, peak=BF16_PEAK_TFLOPS))
+        return out
 
 
 COPY_BYTES = 256 << 20
@@ -796,7 +937,8 @@ def breakdown(args, torch, W, stream):
             row["cold_per_launch_us"] = sampled(c.fn, True)
         if c.flops:
             row["tflops"] = round(c.flops / (us * 1e-6) / 1e12, 1)
-            row["frac_fp8_peak"] = round(c.flops / (us * 1e-6) / 1e12 / FP8_PEAK_TFLOPS, 4)
+            row["frac_%s_peak" % ("fp8" if c.peak == FP8_PEAK_TFLOPS else "bf16")] = round(
+                c.flops / (us * 1e-6) / 1e12 / c.peak, 4)
         if c.nbytes:
             row["gbs_algorithmic"] = round(c.nbytes / (us * 1e-6) / 1e9, 1)
             row["frac_hbm_peak"] = round(c.nbytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)
@@ -822,8 +964,15 @@ def main():
     if args.workload == "layers28":
         # a single call profiles layer 0's tensors; a step needs every layer
         W = Layers28(torch, puro, layers=1 if args.only and args.only != "step" else None)
-    else:
+    elif args.workload == "qkv":
         W = Qkv(torch, puro)
+    elif args.workload.startswith("lm_head"):
+        W = LmHead(torch, puro, puro.LM_HEAD_FP8 if args.workload == "lm_head_fp8" else puro.LM_HEAD_BF16)
+    else:
+        W = MuonH28(torch, puro)
+    flops = getattr(W, "flops", None) or W.gemm_flops
+    peak = getattr(W, "peak", FP8_PEAK_TFLOPS)
+    dtype = getattr(W, "dtype", "fp8")
     if args.only:
         run_only(args, torch, W)
         return
@@ -857,18 +1006,21 @@ def main():
         torch.cuda.synchronize()
         wall = time.perf_counter() - t0
     ms_per_step = e0.elapsed_time(e1) / args.steps
-    value = W.gemm_flops / (ms_per_step * 1e-3) / 1e12
+    value = flops / (ms_per_step * 1e-3) / 1e12
 
     calls, rows = breakdown(args, torch, W, stream)
     gemm_us = sum(r["us"] * r["per_step"] for r in rows if "tflops" in r)
     sum_us = sum(r["us"] * r["per_step"] for r in rows)
     # dominant kernel: the single-launch call with the largest share of a step
-    single = [(r, c) for r, c in zip(rows, calls) if c.launches == 1]
+    # (workloads whose calls are entry points of several kernels: the call)
+    single = [(r, c) for r, c in zip(rows, calls) if c.launches == 1] or list(zip(rows, calls))
     dom, dom_c = max(single, key=lambda rc: rc[0]["us"] * rc[0]["per_step"])
     if "tflops" in dom:
-        roofline = {"bound": "mfma", "kernel": dom["call"], "achieved": dom["tflops"], "peak": FP8_PEAK_TFLOPS,
-                    "unit": "TFLOP/s", "frac": round(dom["tflops"] / FP8_PEAK_TFLOPS, 4),
+        roofline = {"bound": "mfma", "kernel": dom["call"], "achieved": dom["tflops"], "peak": dom_c.peak,
+                    "unit": "TFLOP/s", "frac": round(dom["tflops"] / dom_c.peak, 4),
                     "algorithmic_flops_per_launch": dom_c.flops}
+        if dom_c.launches != 1:
+            roofline["note"] = "an entry point of several kernels; its kernels' own times are in the profiles"
     else:
         roofline = {"bound": "hbm", "kernel": dom["call"], "achieved": dom["gbs_algorithmic"], "peak": HBM_PEAK_GBS,
                     "unit": "GB/s", "frac": round(dom["gbs_algorithmic"] / HBM_PEAK_GBS, 4),
@@ -879,7 +1031,7 @@ def main():
     roofline["traffic_unit"] = "HBM-side bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)"
     clk = clock.summary()
     out = {
-        "metric": METRIC,
+        "metric": getattr(W, "metric", METRIC),
         "value": round(value, 2),
         "unit": "TFLOP/s",
         "n_gpus": 1,
@@ -889,12 +1041,12 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "fp8",
+        "dtype": dtype,
         "data": "synthetic",
         "config": dict(W.config, launch="hip_graph" if args.graph else "eager"),
-        "pct_fp8_peak": round(100 * value / FP8_PEAK_TFLOPS, 2),
-        "gemm_only_tflops": round(W.gemm_flops / (gemm_us * 1e-6) / 1e12, 1),
-        "gemm_only_pct_fp8_peak": round(100 * W.gemm_flops / (gemm_us * 1e-6) / 1e12 / FP8_PEAK_TFLOPS, 2),
+        "pct_%s_peak" % dtype: round(100 * value / peak, 2),
+        "gemm_only_tflops": round(flops / (gemm_us * 1e-6) / 1e12, 1),
+        "gemm_only_pct_%s_peak" % dtype: round(100 * flops / (gemm_us * 1e-6) / 1e12 / peak, 2),
         "breakdown_sum_ms": round(sum_us / 1e3, 3),
         "breakdown": rows,
         "roofline": roofline,
@@ -903,11 +1055,11 @@ def main():
         "mfu_context": {"paper_p_eff_tflops": round(p_eff(PAPER_FP8_SHARE, PAPER_FP8_PEAK, PAPER_BF16_PEAK), 2),
                         "mi355x_p_eff_tflops_at_paper_mix": round(p_eff(PAPER_FP8_SHARE, FP8_PEAK_TFLOPS,
                                                                         BF16_PEAK_TFLOPS), 1),
-                        "fp8_share_of_this_step": 1.0},
+                        "fp8_share_of_this_step": 1.0 if dtype == "fp8" else 0.0},
     }
     if clk:
         ghz = clk["median_mhz"] / 1e3
-        out["pct_fp8_peak_at_measured_clock"] = round(100 * value / (FP8_PEAK_TFLOPS * ghz / PEAK_CLOCK_GHZ), 2)
+        out["pct_%s_peak_at_measured_clock" % dtype] = round(100 * value / (peak * ghz / PEAK_CLOCK_GHZ), 2)
     if args.cpu_tokens > 0:
         out["cpu_baseline"] = cpu_baseline(args.workload, args.cpu_tokens)
     print(json.dumps(out), flush=True)

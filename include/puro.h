@@ -363,6 +363,77 @@ puro_status puro_linear_bwd(const uint16_t* dY, const puro_linear_saved* saved,
                             uint16_t* dX, float* dW, int accumulate_dW,
                             void* ws, size_t ws_bytes, hipStream_t stream);
 
+/* ------------------------------------- LM head with cross-entropy loss ---
+ * Section 3.1.3 of the paper names the language-model head as the layer whose
+ * cost sets the pipeline's last stage apart; Appendix C keeps it in BF16. For
+ * hidden states X [M, K] and the output embedding W [V, K] (BF16, dense rows)
+ * and one target vocabulary id per row, targets [M] (int32):
+ *   forward:  z = X W^T; lse[m] = log sum_v exp(z[m, v]); loss[m] = lse[m] - z[m, t_m]
+ *   backward: dz = g (exp(z - lse) - onehot(t)); dX = dz W (BF16 [M, K]);
+ *             dW = dz^T X (FP32 [V, K], overwritten)
+ * The logits are never stored: the forward reduces each 128-column block of
+ * the GEMM's output tile to (max, sum exp) in its epilogue; the backward
+ * recomputes the logits in chunks of 16384 vocabulary columns and writes only
+ * the chunk's dz (BF16) to the workspace. g is the loss's upstream gradient
+ * (1 for the sum over tokens, 1/M for their mean).
+ * Recipes: PURO_LM_HEAD_BF16 (BF16 GEMMs with binary32 accumulation, dz
+ * rounded to BF16), PURO_LM_HEAD_FP8 (Section 3.2's blockwise recipe: X in
+ * 1x128 groups, W in 128x128 blocks, each dz chunk rounded to BF16 and then
+ * in 1x128 + 128x1 groups; E4M3, power-of-two scales).
+ * Requirements: M, V, K positive multiples of 128, at most 2^21; X, W, lse,
+ * loss, dX, dW 16-byte aligned; targets in [0, V) (a row whose target lies
+ * outside gets loss NaN and no onehot term). lse and loss are FP32 [M]. ws:
+ * puro_lm_head_ce_workspace_size(M, V, K, recipe, backward) bytes (the
+ * backward's includes the quantised or transposed operands and one chunk). All
+ * pointers are device memory owned by the caller; nothing is allocated or
+ * synchronised; invalid arguments return before anything is enqueued. */
+typedef enum { PURO_LM_HEAD_BF16 = 0, PURO_LM_HEAD_FP8 = 1 } puro_lm_head_recipe;
+size_t puro_lm_head_ce_workspace_size(int64_t M, int64_t V, int64_t K, puro_lm_head_recipe recipe, int backward);
+puro_status puro_lm_head_ce_fwd(const uint16_t* X, const uint16_t* W, const int32_t* targets, int64_t M,
+                                int64_t V, int64_t K, puro_lm_head_recipe recipe, float* lse, float* loss,
+                                void* ws, size_t ws_bytes, hipStream_t stream);
+puro_status puro_lm_head_ce_bwd(const uint16_t* X, const uint16_t* W, const int32_t* targets, const float* lse,
+                                int64_t M, int64_t V, int64_t K, puro_lm_head_recipe recipe, float grad_scale,
+                                uint16_t* dX, float* dW, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* ---------------------------------------------------------------- MuonH ---
+ * Section 3.3 (Hyperball Optimization), equation hyperball-update: a wrapped
+ * matrix keeps its initial Frobenius radius R; with the Muon update u and the
+ * weight learning rate eta,
+ *     W~ = W - eta R u / ||u||_F,    W' = R W~ / ||W~||_F.
+ * The paper takes Muon from its training framework; the Muon update here is
+ * the published method's:
+ *     buf' = mu buf + (1 - mu) G;  V = (1 - mu) G + mu buf' (nesterov) or buf'
+ *     X_0 = V / (||V||_F + 1e-7), transposed when rows > cols;
+ *     ns_steps times: A = X X^T, B = b A + c A A^T, X = a X + B X,
+ *     (a, b, c) = (3.4445, -4.7750, 2.0315); u = X (turned back).
+ * FP32 state (W, G, buf), each momentum product and sum rounded to binary32
+ * in that order with (1 - mu) rounded first; Newton-Schulz in BF16 with
+ * binary32 accumulation, each of A, B and X rounded once to BF16; the
+ * hyperball step from the BF16 u in binary32 with double-precision norms.
+ *
+ * puro_muonh_step updates `count` matrices of one shape stored back to back:
+ * W [count][rows][cols] (FP32, in place), buf (FP32, in place), G (FP32),
+ * radius [count] (FP32 device array: each matrix's R). Optional outputs:
+ * w_bf16 (BF16 copy of W'), u_out (BF16 u, W's layout). ns_steps: 5 in the
+ * method; 0 applies the hyperball step to X_0 (a test hook). u = 0 (all of V
+ * zero) leaves W's direction and only projects it. rows, cols: positive
+ * multiples of 128, at most 2^21; count in [1, 65535]; pointers 16-byte
+ * aligned device memory owned by the caller. ws:
+ * puro_muonh_workspace_size(count, rows, cols) bytes. Matrices may not
+ * overlap W, G, buf or the outputs.
+ *
+ * puro_newton_schulz_bf16 runs `steps` Newton-Schulz steps on X [count][r][c]
+ * (BF16, r <= c, already normalised) into out (same layout); the steps of
+ * puro_muonh_step, exposed for per-step checks. */
+size_t puro_muonh_workspace_size(int64_t count, int64_t rows, int64_t cols);
+puro_status puro_muonh_step(int64_t count, int64_t rows, int64_t cols, float* W, uint16_t* w_bf16, const float* G,
+                            float* buf, const float* radius, float mu, int nesterov, float eta, int ns_steps,
+                            uint16_t* u_out, void* ws, size_t ws_bytes, hipStream_t stream);
+size_t puro_newton_schulz_workspace_size(int64_t count, int64_t r, int64_t c);
+puro_status puro_newton_schulz_bf16(int64_t count, int64_t r, int64_t c, const uint16_t* X, int steps,
+                                    uint16_t* out, void* ws, size_t ws_bytes, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -19,8 +19,9 @@ BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libpuro.so")
 # (source, object name, extra flags): the GEMM kernel is compiled once per
 # operand-format pair and scale kind, so that its instantiations build in parallel
-GEMM_VARIANTS = [(fa, fb, g) for fa in (0, 1) for fb in (0, 1) for g in (0, 1)]
-SOURCES = [("quant.hip", "quant", []), ("gemm.hip", "gemm", []), ("api.cpp", "api", [])] + [
+GEMM_VARIANTS = [(fa, fb, g) for fa in (0, 1) for fb in (0, 1) for g in (0, 1)] + [(2, 2, 0)]   # + BF16
+SOURCES = [("quant.hip", "quant", []), ("gemm.hip", "gemm", []), ("lm_head.hip", "lm_head", []),
+           ("transpose.hip", "transpose", []), ("muonh.hip", "muonh", []), ("api.cpp", "api", [])] + [
     ("gemm_kernel.hip", "gemm_kernel_%d%d%d" % v, ["-DPURO_FA=%d" % v[0], "-DPURO_FB=%d" % v[1], "-DPURO_GROUPED=%d" % v[2]])
     for v in GEMM_VARIANTS]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

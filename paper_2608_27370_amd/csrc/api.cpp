@@ -623,3 +623,116 @@ puro_status puro_linear_bwd(const uint16_t* dY, const puro_linear_saved* saved, 
 }
 
 }  // extern "C"
+
+// ------------------------------------------ LM head with cross-entropy loss
+namespace {
+
+puro_status check_lm_head(const uint16_t* X, const uint16_t* W, const int32_t* targets, int64_t M, int64_t V,
+                          int64_t K, puro_lm_head_recipe r) {
+    if (r != PURO_LM_HEAD_BF16 && r != PURO_LM_HEAD_FP8) return PURO_ERR_UNSUPPORTED;
+    if (M <= 0 || V <= 0 || K <= 0) return PURO_ERR_SHAPE;
+    // BF16 operand pitches (2 M, 2 V, 2 K bytes for the transposed copies) within 2^22
+    const int64_t lim = (int64_t)1 << 21;
+    if (M > lim || V > lim || K > lim) return PURO_ERR_SHAPE;
+    if ((M % kGroup) != 0 || (V % kGroup) != 0 || (K % kGroup) != 0) return PURO_ERR_ALIGN;
+    if (!X || !W || !targets) return PURO_ERR_NULL;
+    if (!aligned16(X) || !aligned16(W) || ((uintptr_t)targets & 3) != 0) return PURO_ERR_ALIGN;
+    return PURO_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t puro_lm_head_ce_workspace_size(int64_t M, int64_t V, int64_t K, puro_lm_head_recipe recipe, int backward) {
+    if (check_lm_head(reinterpret_cast<const uint16_t*>(16), reinterpret_cast<const uint16_t*>(16),
+                      reinterpret_cast<const int32_t*>(16), M, V, K, recipe) != PURO_OK)
+        return 0;
+    return lm_head_ws_bytes(M, V, K, recipe == PURO_LM_HEAD_FP8, backward != 0);
+}
+
+puro_status puro_lm_head_ce_fwd(const uint16_t* X, const uint16_t* W, const int32_t* targets, int64_t M,
+                                int64_t V, int64_t K, puro_lm_head_recipe recipe, float* lse, float* loss,
+                                void* ws, size_t ws_bytes, hipStream_t stream) {
+    puro_status st = check_lm_head(X, W, targets, M, V, K, recipe);
+    if (st != PURO_OK) return st;
+    if (!lse || !loss || !ws) return PURO_ERR_NULL;
+    if (!aligned16(lse) || !aligned16(loss)) return PURO_ERR_ALIGN;
+    if (ws_bytes < lm_head_ws_bytes(M, V, K, recipe == PURO_LM_HEAD_FP8, false)) return PURO_ERR_WORKSPACE;
+    launch_lm_head_fwd(X, W, targets, M, V, K, recipe == PURO_LM_HEAD_FP8, lse, loss, ws, stream);
+    return launched();
+}
+
+puro_status puro_lm_head_ce_bwd(const uint16_t* X, const uint16_t* W, const int32_t* targets, const float* lse,
+                                int64_t M, int64_t V, int64_t K, puro_lm_head_recipe recipe, float grad_scale,
+                                uint16_t* dX, float* dW, void* ws, size_t ws_bytes, hipStream_t stream) {
+    puro_status st = check_lm_head(X, W, targets, M, V, K, recipe);
+    if (st != PURO_OK) return st;
+    if (!lse || !dX || !dW || !ws) return PURO_ERR_NULL;
+    if (!aligned16(lse) || !aligned16(dX) || !aligned16(dW)) return PURO_ERR_ALIGN;
+    if (!(grad_scale == grad_scale) || grad_scale > 3.4028235e38f || grad_scale < -3.4028235e38f)
+        return PURO_ERR_UNSUPPORTED;
+    if (ws_bytes < lm_head_ws_bytes(M, V, K, recipe == PURO_LM_HEAD_FP8, true)) return PURO_ERR_WORKSPACE;
+    launch_lm_head_bwd(X, W, targets, lse, M, V, K, recipe == PURO_LM_HEAD_FP8, grad_scale, dX, dW, ws, stream);
+    return launched();
+}
+
+}  // extern "C"
+
+// ------------------------------------------------------------------- MuonH
+namespace {
+
+puro_status check_muonh_shape(int64_t count, int64_t rows, int64_t cols) {
+    if (count <= 0 || rows <= 0 || cols <= 0) return PURO_ERR_SHAPE;
+    const int64_t lim = (int64_t)1 << 21;
+    if (count > 65535 || rows > lim || cols > lim) return PURO_ERR_SHAPE;
+    if ((rows % kGroup) != 0 || (cols % kGroup) != 0) return PURO_ERR_ALIGN;
+    return PURO_OK;
+}
+
+bool finite_f32(float v) { return v == v && v <= 3.4028235e38f && v >= -3.4028235e38f; }
+
+}  // namespace
+
+extern "C" {
+
+size_t puro_muonh_workspace_size(int64_t count, int64_t rows, int64_t cols) {
+    if (check_muonh_shape(count, rows, cols) != PURO_OK) return 0;
+    return muonh_ws_bytes(count, rows, cols);
+}
+
+puro_status puro_muonh_step(int64_t count, int64_t rows, int64_t cols, float* W, uint16_t* w_bf16, const float* G,
+                            float* buf, const float* radius, float mu, int nesterov, float eta, int ns_steps,
+                            uint16_t* u_out, void* ws, size_t ws_bytes, hipStream_t stream) {
+    puro_status st = check_muonh_shape(count, rows, cols);
+    if (st != PURO_OK) return st;
+    if (!W || !G || !buf || !radius || !ws) return PURO_ERR_NULL;
+    if (!aligned16(W) || !aligned16(G) || !aligned16(buf) || ((uintptr_t)radius & 3) != 0 ||
+        (w_bf16 && !aligned16(w_bf16)) || (u_out && !aligned16(u_out)))
+        return PURO_ERR_ALIGN;
+    if (!finite_f32(mu) || !finite_f32(eta) || ns_steps < 0 || ns_steps > 64) return PURO_ERR_UNSUPPORTED;
+    if (ws_bytes < muonh_ws_bytes(count, rows, cols)) return PURO_ERR_WORKSPACE;
+    launch_muonh_step(count, rows, cols, W, w_bf16, G, buf, radius, mu, nesterov != 0, eta, ns_steps, u_out, ws,
+                      stream);
+    return launched();
+}
+
+size_t puro_newton_schulz_workspace_size(int64_t count, int64_t r, int64_t c) {
+    if (check_muonh_shape(count, r, c) != PURO_OK || r > c) return 0;
+    return newton_schulz_ws_bytes(count, r, c);
+}
+
+puro_status puro_newton_schulz_bf16(int64_t count, int64_t r, int64_t c, const uint16_t* X, int steps,
+                                    uint16_t* out, void* ws, size_t ws_bytes, hipStream_t stream) {
+    puro_status st = check_muonh_shape(count, r, c);
+    if (st != PURO_OK) return st;
+    if (r > c) return PURO_ERR_SHAPE;
+    if (!X || !out || !ws) return PURO_ERR_NULL;
+    if (!aligned16(X) || !aligned16(out)) return PURO_ERR_ALIGN;
+    if (steps < 0 || steps > 64) return PURO_ERR_UNSUPPORTED;
+    if (ws_bytes < newton_schulz_ws_bytes(count, r, c)) return PURO_ERR_WORKSPACE;
+    launch_newton_schulz(X, count, r, c, steps, out, ws, stream);
+    return launched();
+}
+
+}  // extern "C"

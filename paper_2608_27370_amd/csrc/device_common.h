@@ -7,8 +7,9 @@
 namespace puro {
 
 // FP8 format ids; the values double as the MFMA operand-format selectors of
-// the gfx950 f8f6f4 instructions (0 = E4M3, 1 = E5M2).
-enum : int { kE4M3 = 0, kE5M2 = 1 };
+// the gfx950 f8f6f4 instructions (0 = E4M3, 1 = E5M2). kBF16 marks BF16
+// GEMM operands (the 32x32x16 BF16 matrix instruction).
+enum : int { kE4M3 = 0, kE5M2 = 1, kBF16 = 2 };
 
 template <int FMT> struct Fp8Traits;
 template <> struct Fp8Traits<kE4M3> {

@@ -30,10 +30,23 @@ struct Params {
     int gm;                    // tile rows per group within an XCD's range of tiles
     int tiles_m, tiles_n;
     int accumulate;
-    float alpha;               // host-known part of the per-tensor scale (1)
+    float alpha;               // host-known factor of the sums (with the per-tensor scales)
     const uint16_t* bias;      // OUT kOutBF16Epi: optional bias [N] and residual [M, N] (pitch ldr)
     const uint16_t* residual;
     int64_t ldr;
+    float res_scale;           // factor of the residual
+    int batch;                 // problems of one launch: A, B, D advance by bsa, bsb, bsd bytes,
+    int64_t bsa, bsb, bsd;     // the residual by bsr elements, the split-K partials by
+    int64_t bsr;               // splits * M * N floats
+
+    // LM-head output kinds (kOutLseStats, kOutSoftmaxGrad; 128-column wave tiles)
+    const int32_t* targets;    // target vocabulary id per row
+    int col0;                  // vocabulary column of this GEMM's column 0
+    float2* stats;             // [M][stats_ld]: (max, sum exp(z - max)) per 128-column block
+    int64_t stats_ld;
+    float* zt;                 // [M]: the target's logit
+    const float* lse;          // [M]
+    float grad_scale;
 };
 
 struct TileCfg {
@@ -65,21 +78,24 @@ struct TileCfg {
 // The bias / residual epilogue: the BF16 bias of columns n..n+3 and the BF16
 // residual of row m at those columns added to four binary32 results (the
 // sum stays binary32 until the output's one rounding).
+// The residual is multiplied by rs in the same fused step as its addition
+// (rs = 1 adds it exactly as a plain sum).
 __device__ __forceinline__ void add_epilogue4(float4& v, const uint16_t* bias, const uint16_t* residual,
-                                              int64_t ldr, int64_t m, int64_t n) {
+                                              int64_t ldr, int64_t m, int64_t n, float rs) {
     if (bias) {
         const uint2 b = *reinterpret_cast<const uint2*>(bias + n);
         v.x += bf16lo(b.x); v.y += bf16hi(b.x); v.z += bf16lo(b.y); v.w += bf16hi(b.y);
     }
     if (residual) {
         const uint2 r = *reinterpret_cast<const uint2*>(residual + m * ldr + n);
-        v.x += bf16lo(r.x); v.y += bf16hi(r.x); v.z += bf16lo(r.y); v.w += bf16hi(r.y);
+        v.x = fmaf(rs, bf16lo(r.x), v.x); v.y = fmaf(rs, bf16hi(r.x), v.y);
+        v.z = fmaf(rs, bf16lo(r.y), v.z); v.w = fmaf(rs, bf16hi(r.y), v.w);
     }
 }
 __device__ __forceinline__ float add_epilogue1(float v, const uint16_t* bias, const uint16_t* residual, int64_t ldr,
-                                               int64_t m, int64_t n) {
+                                               int64_t m, int64_t n, float rs) {
     if (bias) v += __uint_as_float((uint32_t)bias[n] << 16);
-    if (residual) v += __uint_as_float((uint32_t)residual[m * ldr + n] << 16);
+    if (residual) v = fmaf(rs, __uint_as_float((uint32_t)residual[m * ldr + n] << 16), v);
     return v;
 }
 

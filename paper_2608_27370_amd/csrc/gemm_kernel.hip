@@ -60,6 +60,7 @@ namespace {
 
 
 typedef int v8i __attribute__((ext_vector_type(8)));
+typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
 typedef float v16f __attribute__((ext_vector_type(16)));
 typedef __attribute__((address_space(3))) void lds_void_t;
 
@@ -164,8 +165,18 @@ __global__ __launch_bounds__(WM * WN * 64 * (PROD ? 2 : 1)) void gemm_fp8_kernel
     // ---- tile index: contiguous ranges per XCD, grouped by p.gm row panels
     const int T = gridDim.x;
     const int b = blockIdx.x;
-    const int lt = (T % 8 == 0) ? (b % 8) * (T / 8) + b / 8 : b;
+    int lt = (T % 8 == 0) ? (b % 8) * (T / 8) + b / 8 : b;
     const int per_split = p.tiles_m * p.tiles_n;
+    if (p.batch > 1) {
+        // problem bi of a batched launch: its operands, output and partials
+        const int bi = lt / (per_split * p.splits);
+        lt -= bi * per_split * p.splits;
+        p.A += bi * p.bsa;
+        p.B += bi * p.bsb;
+        p.D = reinterpret_cast<uint8_t*>(p.D) + bi * p.bsd;
+        if (p.residual) p.residual += bi * p.bsr;
+        p.partial += (int64_t)bi * p.splits * p.M * p.N;
+    }
     const int ks = lt / per_split;
     const int rem = lt - ks * per_split;
     const int group = rem / (p.gm * p.tiles_n);
@@ -333,7 +344,19 @@ __global__ __launch_bounds__(WM * WN * 64 * (PROD ? 2 : 1)) void gemm_fp8_kernel
     };
     auto mfma_one = [&](const Frags& f, int t) __attribute__((always_inline)) {
         const int i = t / FN, j = t % FN;
-        if constexpr (GROUPED)
+        if constexpr (FA == kBF16) {
+            // BF16: the lane's 32 bytes are 16 k values; each half feeds one
+            // 32x32x16 instruction. A and B split k the same way, so the two
+            // instructions together add every product of the 64-byte step.
+            const v4i blo = __builtin_shufflevector(f.f[FM + j], f.f[FM + j], 0, 1, 2, 3);
+            const v4i bhi = __builtin_shufflevector(f.f[FM + j], f.f[FM + j], 4, 5, 6, 7);
+            const v4i alo = __builtin_shufflevector(f.f[i], f.f[i], 0, 1, 2, 3);
+            const v4i ahi = __builtin_shufflevector(f.f[i], f.f[i], 4, 5, 6, 7);
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(v8bf, blo),
+                                                                __builtin_bit_cast(v8bf, alo), acc[i][j], 0, 0, 0);
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(v8bf, bhi),
+                                                                __builtin_bit_cast(v8bf, ahi), acc[i][j], 0, 0, 0);
+        } else if constexpr (GROUPED)
             acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
                 f.f[FM + j], f.f[i], acc[i][j], FB, FA, 0, (int)f.sc[FM + j], 0, (int)f.sc[i]);
         else
@@ -496,6 +519,63 @@ __global__ __launch_bounds__(WM * WN * 64 * (PROD ? 2 : 1)) void gemm_fp8_kernel
         // writes only after this pass's reads have returned their data)
         asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
         constexpr int IT = RPP * ECPR / 64;
+        if constexpr (OUT == kOutLseStats || OUT == kOutSoftmaxGrad) {
+            // LM-head epilogues on the staged tile. A wave-tile row is 128
+            // columns = 32 chunks, so lanes 0-31 read one row and lanes 32-63
+            // the next; row reductions are butterflies within 32 lanes.
+            // Every lane takes part in every shuffle (no early exits); rows
+            // past M and columns past N are masked.
+            static_assert(ECPR == 32, "LM-head epilogues take 128-column wave tiles");
+#pragma unroll 2
+            for (int it = 0; it < IT; ++it) {
+                const int q = it * 64 + lane;
+                const int r = q / ECPR, c = q % ECPR;
+                const float4 v = *reinterpret_cast<const float4*>(ep + r * ROWB + ((c ^ (r & SWZ)) << 4));
+                const int64_t m = mrow0 + pass * RPP + r;
+                const int n = ncol0 + c * 4;
+                const bool row_ok = m < p.M;
+                const int64_t mr = row_ok ? m : 0;
+                const float e[4] = {v.x * alpha, v.y * alpha, v.z * alpha, v.w * alpha};
+                const int tgt = p.targets[mr] - p.col0;      // the target's column in this GEMM
+                if constexpr (OUT == kOutLseStats) {
+                    float mx = -__builtin_inff();
+#pragma unroll
+                    for (int t = 0; t < 4; ++t)
+                        if (n + t < p.N) mx = fmaxf(mx, e[t]);
+#pragma unroll
+                    for (int o = 16; o >= 1; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 64));
+                    float sum = 0.0f;
+#pragma unroll
+                    for (int t = 0; t < 4; ++t)
+                        if (n + t < p.N) sum += exp_f32(e[t] - mx);
+#pragma unroll
+                    for (int o = 16; o >= 1; o >>= 1) sum += __shfl_xor(sum, o, 64);
+                    // a wave tile wholly past N (the ragged last tile) has no block
+                    if (row_ok && (lane & 31) == 0 && ncol0 < p.N)
+                        p.stats[m * p.stats_ld + ncol0 / 128] = make_float2(mx, sum);
+#pragma unroll
+                    for (int t = 0; t < 4; ++t)
+                        if (row_ok && n + t == tgt && n + t < p.N) p.zt[m] = e[t];
+                } else {
+                    const float l = p.lse[mr];
+                    float d[4];
+#pragma unroll
+                    for (int t = 0; t < 4; ++t)
+                        d[t] = p.grad_scale * (exp_f32(e[t] - l) - (n + t == tgt ? 1.0f : 0.0f));
+                    if (row_ok) {
+                        uint16_t* dst = reinterpret_cast<uint16_t*>(p.D) + m * p.ldd + n;
+                        if (n + 3 < p.N) {
+                            *reinterpret_cast<uint2*>(dst) = make_uint2(pack_bf16x2(d[0], d[1]), pack_bf16x2(d[2], d[3]));
+                        } else {
+#pragma unroll
+                            for (int t = 0; t < 4; ++t)
+                                if (n + t < p.N) dst[t] = to_bf16(d[t]);
+                        }
+                    }
+                }
+            }
+            return;
+        }
         if (fast) {
             // the epilogue terms are loaded before the LDS reads of their
             // group of iterations, so that their latency overlaps those reads
@@ -549,7 +629,9 @@ __global__ __launch_bounds__(WM * WN * 64 * (PROD ? 2 : 1)) void gemm_fp8_kernel
                             }
                             if (p.residual) {
                                 const uint2 rv = er[e];
-                                w.x += bf16lo(rv.x); w.y += bf16hi(rv.x); w.z += bf16lo(rv.y); w.w += bf16hi(rv.y);
+                                const float rs = p.res_scale;
+                                w.x = fmaf(rs, bf16lo(rv.x), w.x); w.y = fmaf(rs, bf16hi(rv.x), w.y);
+                                w.z = fmaf(rs, bf16lo(rv.y), w.z); w.w = fmaf(rs, bf16hi(rv.y), w.w);
                             }
                         }
                         if constexpr (OUT == kOutF32)
@@ -577,7 +659,7 @@ __global__ __launch_bounds__(WM * WN * 64 * (PROD ? 2 : 1)) void gemm_fp8_kernel
             }
             v.x *= alpha; v.y *= alpha; v.z *= alpha; v.w *= alpha;
             if (n + 3 < p.N) {
-                if constexpr (OUT == kOutBF16Epi) add_epilogue4(v, p.bias, p.residual, p.ldr, m, n);
+                if constexpr (OUT == kOutBF16Epi) add_epilogue4(v, p.bias, p.residual, p.ldr, m, n, p.res_scale);
                 if constexpr (OUT == kOutF32) {
                     float4* dst = reinterpret_cast<float4*>(reinterpret_cast<float*>(p.D) + (int64_t)m * p.ldd + n);
                     if (p.accumulate) {
@@ -605,7 +687,7 @@ __global__ __launch_bounds__(WM * WN * 64 * (PROD ? 2 : 1)) void gemm_fp8_kernel
                     } else {
                         uint16_t* dst = reinterpret_cast<uint16_t*>(p.D) + (int64_t)m * p.ldd + n + t;
                         float o = p.accumulate ? vv[t] + __uint_as_float((uint32_t)*dst << 16) : vv[t];
-                        if constexpr (OUT == kOutBF16Epi) o = add_epilogue1(o, p.bias, p.residual, p.ldr, m, n + t);
+                        if constexpr (OUT == kOutBF16Epi) o = add_epilogue1(o, p.bias, p.residual, p.ldr, m, n + t, p.res_scale);
                         *dst = to_bf16(o);
                     }
                 }
@@ -614,31 +696,35 @@ __global__ __launch_bounds__(WM * WN * 64 * (PROD ? 2 : 1)) void gemm_fp8_kernel
     });
 }
 
-template <int BM, int BN, int WM, int WN, int SL, int NST, int PROD, int FA, int FB, int OUT>
-void launch_cfg(const Params& prm, bool grouped, int grid, hipStream_t stream) {
+template <int BM, int BN, int WM, int WN, int SL, int NST, int PROD, int FA, int FB, bool GROUPED, int OUT>
+void launch_cfg(const Params& prm, int grid, hipStream_t stream) {
     constexpr int threads = WM * WN * 64 * (PROD ? 2 : 1);
-    if (grouped)
-        gemm_fp8_kernel<BM, BN, WM, WN, FA, FB, OUT, true, SL, NST, PROD != 0><<<grid, threads, 0, stream>>>(prm);
-    else
-        gemm_fp8_kernel<BM, BN, WM, WN, FA, FB, OUT, false, SL, NST, PROD != 0><<<grid, threads, 0, stream>>>(prm);
+    gemm_fp8_kernel<BM, BN, WM, WN, FA, FB, OUT, GROUPED, SL, NST, PROD != 0><<<grid, threads, 0, stream>>>(prm);
 }
 
-template <int BM, int BN, int WM, int WN, int SL, int NST, int PROD, int FA, int FB>
-void launch_tile(const Params& prm, int out, bool grouped, int grid, hipStream_t stream) {
-    if (out == 2) launch_cfg<BM, BN, WM, WN, SL, NST, PROD, FA, FB, 2>(prm, grouped, grid, stream);
-    else if (out == kOutF32) launch_cfg<BM, BN, WM, WN, SL, NST, PROD, FA, FB, kOutF32>(prm, grouped, grid, stream);
+template <int BM, int BN, int WM, int WN, int SL, int NST, int PROD, int FA, int FB, bool GROUPED>
+void launch_tile(const Params& prm, int out, int grid, hipStream_t stream) {
+    // the LM-head kinds exist for BF16 operands and blockwise E4M3 operands,
+    // on 128-column wave tiles
+    constexpr bool lm = (FA == kBF16 && FB == kBF16 && !GROUPED) || (FA == kE4M3 && FB == kE4M3 && GROUPED);
+    if (out == 2) launch_cfg<BM, BN, WM, WN, SL, NST, PROD, FA, FB, GROUPED, 2>(prm, grid, stream);
+    else if (out == kOutF32) launch_cfg<BM, BN, WM, WN, SL, NST, PROD, FA, FB, GROUPED, kOutF32>(prm, grid, stream);
     else if (out == kOutBF16Epi)
-        launch_cfg<BM, BN, WM, WN, SL, NST, PROD, FA, FB, kOutBF16Epi>(prm, grouped, grid, stream);
-    else launch_cfg<BM, BN, WM, WN, SL, NST, PROD, FA, FB, kOutBF16>(prm, grouped, grid, stream);
+        launch_cfg<BM, BN, WM, WN, SL, NST, PROD, FA, FB, GROUPED, kOutBF16Epi>(prm, grid, stream);
+    else if (out == kOutLseStats || out == kOutSoftmaxGrad) {
+        if constexpr (lm && BN / WN == 128) {
+            if (out == kOutLseStats) launch_cfg<BM, BN, WM, WN, SL, NST, PROD, FA, FB, GROUPED, kOutLseStats>(prm, grid, stream);
+            else launch_cfg<BM, BN, WM, WN, SL, NST, PROD, FA, FB, GROUPED, kOutSoftmaxGrad>(prm, grid, stream);
+        }
+    } else launch_cfg<BM, BN, WM, WN, SL, NST, PROD, FA, FB, GROUPED, kOutBF16>(prm, grid, stream);
 }
-
 
 }  // namespace
 
 template <int FA, int FB, bool GROUPED>
 void launch_variant(const Params& prm, int cfg, int out, int grid, hipStream_t stream) {
 #define PURO_TILE_CASE(i, bm, bn, wm, wn, sl, nst, prod, f, s) \
-    case i: launch_tile<bm, bn, wm, wn, sl, nst, prod, FA, FB>(prm, out, GROUPED, grid, stream); break;
+    case i: launch_tile<bm, bn, wm, wn, sl, nst, prod, FA, FB, GROUPED>(prm, out, grid, stream); break;
     switch (cfg) { PURO_TILE_LIST(PURO_TILE_CASE) }
 #undef PURO_TILE_CASE
 }

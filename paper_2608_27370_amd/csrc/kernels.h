@@ -95,11 +95,17 @@ void launch_swiglu_bwd_quantize(int fmt, int mode, QuantArgs a, void* ws, hipStr
 
 // ---- GEMM (gemm.hip) ----------------------------------------------------------
 
-enum ScaleMode : int { kSTensor = 0, kSRow = 1, kSBlock = 2 };
+// kSNone: an operand without scales (BF16 operands).
+enum ScaleMode : int { kSTensor = 0, kSRow = 1, kSBlock = 2, kSNone = 3 };
 // kOutBF16Epi: BF16 output with the bias / residual epilogue (the partial
-// sums of a split-K plan are kind 2, internal to the GEMM).
-enum OutKind : int { kOutBF16 = 0, kOutF32 = 1, kOutBF16Epi = 3 };
+// sums of a split-K plan are kind 2, internal to the GEMM). The LM-head
+// kinds replace the output store: kOutLseStats writes per row and 128-column
+// block (max, sum of exp(z - max)) and the target's logit; kOutSoftmaxGrad
+// writes BF16 dz = g (exp(z - lse) - [column == target]).
+enum OutKind : int { kOutBF16 = 0, kOutF32 = 1, kOutBF16Epi = 3, kOutLseStats = 4, kOutSoftmaxGrad = 5 };
 
+// K, lda and ldb count operand elements (FP8 codes, or BF16 values when fa
+// and fb are kBF16, with scale modes kSNone).
 struct GemmProblem {
     int64_t M, N, K;
     const uint8_t* A;
@@ -117,19 +123,79 @@ struct GemmProblem {
     // grouped scales stored k-block-major ([K/128][rows] or [K/128][rows/128])
     // instead of row-major ([rows][K/128] or [rows/128][K/128])
     int sa_kmajor, sb_kmajor;
-    // kOutBF16Epi: D = BF16(alpha * acc + bias[n] + residual[m, n]), either
-    // term optional (NULL); residual row pitch ldr (residual may be D itself)
+    // kOutBF16Epi: D = BF16(alpha * acc + bias[n] + res_scale * residual[m, n]),
+    // either term optional (NULL); residual row pitch ldr (residual may be D
+    // itself). alpha multiplies the sums of every output kind (with the
+    // per-tensor scales).
     const uint16_t* bias;
     const uint16_t* residual;
     int64_t ldr;
+    float alpha = 1.0f, res_scale = 1.0f;
+    // `batch` independent problems of the same shape and scales: operand,
+    // output and residual b start bsa, bsb, bsd, bsr elements after those of
+    // problem 0
+    int batch = 1;
+    int64_t bsa = 0, bsb = 0, bsd = 0, bsr = 0;
+    // LM-head output kinds: the target vocabulary id of each row, the
+    // vocabulary column of this GEMM's column 0, and stats [M][stats_ld]
+    // with zt [M] (kOutLseStats) or lse [M] with the gradient scale
+    // (kOutSoftmaxGrad)
+    const int32_t* targets;
+    int col0;
+    float2* stats;
+    int64_t stats_ld;
+    float* zt;
+    const float* lse;
+    float grad_scale;
 };
 
-// Workspace the GEMM needs for split-K partial sums (0 when it runs unsplit).
-size_t gemm_workspace_bytes(int64_t M, int64_t N, int64_t K, int out);
+// Workspace the GEMM needs for split-K partial sums (0 when it runs unsplit);
+// K in bytes of an operand row (2 K for BF16 operands).
+size_t gemm_workspace_bytes(int64_t M, int64_t N, int64_t K, int out, int batch = 1);
 // The plan launch_gemm takes: tile, ring depth, k ranges.
 void gemm_plan(int64_t M, int64_t N, int64_t K, bool grouped, int* tile_m, int* tile_n, int* stages,
                int* splits);
 // Enqueue the GEMM; `ws` must hold gemm_workspace_bytes(...) bytes.
 void launch_gemm(const GemmProblem& p, void* ws, hipStream_t stream);
+
+// ---- BF16 transpose (transpose.hip) -------------------------------------------
+
+// dst [C, R] (pitch ldd) = src [R, C] (pitch lds), for `batch` problems whose
+// source and destination start bs_src and bs_dst elements after the previous one's.
+void transpose_bf16(const uint16_t* src, int64_t R, int64_t C, int64_t lds, uint16_t* dst, int64_t ldd,
+                    hipStream_t stream, int batch = 1, int64_t bs_src = 0, int64_t bs_dst = 0);
+
+// ---- LM head with cross-entropy (lm_head.hip) ---------------------------------
+
+// Vocabulary columns per chunk of the backward pass.
+constexpr int64_t kLmChunk = 16384;
+int64_t lm_head_chunk(int64_t V);
+// Workspace of the forward (bwd false) or backward pass; fp8: the blockwise
+// FP8 recipe, else BF16 operands. M, V, K multiples of 128.
+size_t lm_head_ws_bytes(int64_t M, int64_t V, int64_t K, int fp8, bool bwd);
+// lse [M] and loss [M] = lse - z_target from X [M, K], W [V, K] (BF16, dense
+// rows) and targets [M].
+void launch_lm_head_fwd(const uint16_t* X, const uint16_t* W, const int32_t* targets, int64_t M, int64_t V,
+                        int64_t K, int fp8, float* lse, float* loss, void* ws, hipStream_t stream);
+// dX [M, K] (BF16) and dW [V, K] (FP32) of grad_scale * loss, from lse.
+void launch_lm_head_bwd(const uint16_t* X, const uint16_t* W, const int32_t* targets, const float* lse, int64_t M,
+                        int64_t V, int64_t K, int fp8, float grad_scale, uint16_t* dX, float* dW, void* ws,
+                        hipStream_t stream);
+
+// ---- MuonH (muonh.hip) ---------------------------------------------------------
+
+// Workspace of one MuonH step of `count` [rows, cols] matrices (rows and cols
+// multiples of 128), and of Newton-Schulz on count [r, c] BF16 matrices (r <= c).
+size_t muonh_ws_bytes(int64_t count, int64_t rows, int64_t cols);
+size_t newton_schulz_ws_bytes(int64_t count, int64_t r, int64_t c);
+// out = NS^steps(X), X and out [count][r][c] BF16 (X already normalised).
+void launch_newton_schulz(const uint16_t* X, int64_t count, int64_t r, int64_t c, int steps, uint16_t* out,
+                          void* ws, hipStream_t stream);
+// One MuonH step: buf (FP32) takes the momentum update from G (FP32), W
+// (FP32) the hyperball update of radius[b] with the Newton-Schulz direction;
+// optional BF16 copies of W' (w_bf16) and of the direction (u_out).
+void launch_muonh_step(int64_t count, int64_t rows, int64_t cols, float* W, uint16_t* w_bf16, const float* G,
+                       float* buf, const float* radius, float mu, int nesterov, float eta, int steps,
+                       uint16_t* u_out, void* ws, hipStream_t stream);
 
 }  // namespace puro

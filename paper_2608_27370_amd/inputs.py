@@ -30,6 +30,12 @@ Workloads (M tokens, K input features, N output features):
   fused gate/up 12288x2048, down 2048x6144; X ~ N(0,1) with 1% outlier
   channels scaled by 20, W ~ N(0, 0.02^2), dY ~ N(0, (1e-3)^2);
   ``SeedSequence([0, 6, j, t])``.
+* ``muonh_matrix`` -- one MuonH-wrapped matrix [rows, cols] in binary32
+  (FP32 master weights and optimiser state): W ~ N(0, 0.02^2), the gradient
+  G ~ N(0, (1e-3)^2) and the momentum buffer ~ N(0, (1e-3)^2) (a state some
+  steps in); ``SeedSequence([0, 7, key, t])``. The wrapped matrices of a layer
+  are those of ``LAYER_LINEARS`` (the MLP's gate/up as one [17920, 1536]
+  matrix).
 """
 
 import numpy as np
@@ -169,6 +175,12 @@ def lm_head(M=8192, V=VOCAB, chunk=512):
         dY[r0:r1] = softmax_minus_onehot_rows(z, d["targets"][r0:r1])
     d["dY"] = dY
     return d
+
+
+def muonh_matrix(rows, cols, key=0):
+    """(W, G, buf) float32 [rows, cols] for one MuonH matrix."""
+    f = lambda t, std: (rng(0, 7, key, t).standard_normal((rows, cols)) * std).astype(np.float32)
+    return f(0, 0.02), f(1, 1e-3), f(2, 1e-3)
 
 
 # ---- small cases for tests -----------------------------------------------------

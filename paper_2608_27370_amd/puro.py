@@ -76,6 +76,14 @@ _SIGS = {
                              _p, _sz, _p]),
     "puro_linear_bwd": (_i, [_p, ctypes.POINTER(Saved), _i64, _i64, _i64, ctypes.POINTER(Recipe), _p, _p,
                              _i, _p, _sz, _p]),
+    "puro_lm_head_ce_workspace_size": (_sz, [_i64, _i64, _i64, _i, _i]),
+    "puro_lm_head_ce_fwd": (_i, [_p, _p, _p, _i64, _i64, _i64, _i, _p, _p, _p, _sz, _p]),
+    "puro_lm_head_ce_bwd": (_i, [_p, _p, _p, _p, _i64, _i64, _i64, _i, ctypes.c_float, _p, _p, _p, _sz, _p]),
+    "puro_muonh_workspace_size": (_sz, [_i64, _i64, _i64]),
+    "puro_muonh_step": (_i, [_i64, _i64, _i64, _p, _p, _p, _p, _p, ctypes.c_float, _i, ctypes.c_float, _i, _p,
+                             _p, _sz, _p]),
+    "puro_newton_schulz_workspace_size": (_sz, [_i64, _i64, _i64]),
+    "puro_newton_schulz_bf16": (_i, [_i64, _i64, _i64, _p, _i, _p, _p, _sz, _p]),
 }
 
 _lib = None
@@ -384,3 +392,122 @@ def linear_bwd(dY, saved, recipe, K, want_dx=True, want_dw=True, dX=None, dW=Non
         _ptr(dY), ctypes.byref(s), M, N, K, ctypes.byref(recipe.c()), _ptr(dX if want_dx else None),
         _ptr(dW if want_dw else None), int(bool(accumulate_dw)), _ptr(w), nb, _stream()))
     return (dX if want_dx else None), (dW if want_dw else None)
+
+
+class _LinearFn(torch.autograd.Function):
+    """Y = X W^T through puro_linear_fwd; the backward runs puro_linear_bwd
+    from the FP8 copies the forward saved (the BF16 X is not kept). With a
+    ``main_grad`` FP32 buffer on W, dW is accumulated into it by the Wgrad
+    GEMM and W gets no .grad; otherwise W's .grad is dW in W's dtype."""
+
+    @staticmethod
+    def forward(ctx, X, W, recipe):
+        if X.dtype != torch.bfloat16 or W.dtype != torch.bfloat16:
+            raise TypeError("the FP8 linear layer takes BF16 X and W")
+        Y, saved = linear_fwd(X.contiguous(), W.contiguous(), recipe)
+        ctx.saved, ctx.recipe, ctx.K = saved, recipe, X.shape[1]
+        ctx.main_grad = getattr(W, "main_grad", None)
+        return Y
+
+    @staticmethod
+    def backward(ctx, dY):
+        want_dx, want_dw = ctx.needs_input_grad[0], ctx.needs_input_grad[1]
+        mg = ctx.main_grad if want_dw else None
+        dX, dW = linear_bwd(dY.to(torch.bfloat16).contiguous(), ctx.saved, ctx.recipe, ctx.K, want_dx=want_dx,
+                            want_dw=want_dw, dW=mg, accumulate_dw=mg is not None)
+        ctx.saved = None
+        if mg is not None:
+            return dX, None, None
+        return dX, (dW.to(torch.bfloat16) if dW is not None else None), None
+
+
+def linear(X, W, recipe):
+    """The FP8 linear layer as an autograd operation: X [..., K], W [N, K]
+    (BF16); returns Y [..., N] (BF16)."""
+    shp = X.shape
+    Y = _LinearFn.apply(X.reshape(-1, shp[-1]), W, recipe)
+    return Y.reshape(*shp[:-1], Y.shape[-1])
+
+
+class Linear(torch.nn.Module):
+    """A bias-free linear layer whose forward and backward run the FP8 path
+    (default: the paper's blockwise recipe, E4M3 with power-of-two scales).
+    The weight is BF16, as the model's GEMM operands are (Appendix C); with
+    ``main_grad`` (default) its FP32 gradient is accumulated into
+    ``weight.main_grad`` across backward passes, for an optimiser that keeps
+    FP32 state (zero it after each step)."""
+
+    def __init__(self, in_features, out_features, recipe=None, main_grad=True, device=None):
+        super().__init__()
+        self.in_features, self.out_features = in_features, out_features
+        self.recipe = recipe if recipe is not None else LinearRecipe(E4M3, E4M3, E4M3, 1, SCALE_POW2)
+        self.weight = torch.nn.Parameter(torch.empty(out_features, in_features, dtype=torch.bfloat16,
+                                                     device=device))
+        with torch.no_grad():
+            self.weight.normal_(0.0, 0.02)
+        if main_grad:
+            self.weight.main_grad = torch.zeros(out_features, in_features, dtype=torch.float32,
+                                                device=self.weight.device)
+
+    def forward(self, x):
+        return linear(x, self.weight, self.recipe)
+
+
+# ------------------------------------------ LM head with cross-entropy loss
+LM_HEAD_BF16, LM_HEAD_FP8 = 0, 1
+
+
+def lm_head_ce_workspace_size(M, V, K, recipe, backward):
+    return lib().puro_lm_head_ce_workspace_size(M, V, K, recipe, int(bool(backward)))
+
+
+def lm_head_ce_fwd(X, W, targets, recipe=LM_HEAD_BF16, lse=None, loss=None, ws=None):
+    """lse [M] and loss [M] = lse - z_target of the logits X W^T (never
+    stored); X [M, K], W [V, K] BF16, targets [M] int32; returns (lse, loss)."""
+    M, K = X.shape
+    V = W.shape[0]
+    dev = X.device
+    lse = torch.empty(M, dtype=torch.float32, device=dev) if lse is None else lse
+    loss = torch.empty(M, dtype=torch.float32, device=dev) if loss is None else loss
+    w, nb = _ws(lm_head_ce_workspace_size(M, V, K, recipe, False), ws, dev)
+    _check("puro_lm_head_ce_fwd", lib().puro_lm_head_ce_fwd(
+        _ptr(X), _ptr(W), _ptr(targets), M, V, K, recipe, _ptr(lse), _ptr(loss), _ptr(w), nb, _stream()))
+    return lse, loss
+
+
+def lm_head_ce_bwd(X, W, targets, lse, recipe=LM_HEAD_BF16, grad_scale=1.0, dX=None, dW=None, ws=None):
+    """dX [M, K] (BF16) and dW [V, K] (FP32) of grad_scale * sum of the losses."""
+    M, K = X.shape
+    V = W.shape[0]
+    dev = X.device
+    dX = torch.empty(M, K, dtype=torch.bfloat16, device=dev) if dX is None else dX
+    dW = torch.empty(V, K, dtype=torch.float32, device=dev) if dW is None else dW
+    w, nb = _ws(lm_head_ce_workspace_size(M, V, K, recipe, True), ws, dev)
+    _check("puro_lm_head_ce_bwd", lib().puro_lm_head_ce_bwd(
+        _ptr(X), _ptr(W), _ptr(targets), _ptr(lse), M, V, K, recipe, float(grad_scale), _ptr(dX), _ptr(dW),
+        _ptr(w), nb, _stream()))
+    return dX, dW
+
+
+# ------------------------------------------------------------------- MuonH
+def muonh_step(W, G, buf, radius, eta, mu=0.95, nesterov=True, ns_steps=5, w_bf16=None, u_out=None, ws=None):
+    """One MuonH step of W [count, rows, cols] (or [rows, cols]) in place,
+    with buf (the momentum) updated in place; radius [count] FP32. Returns
+    (w_bf16, u_out) when asked for."""
+    shp = W.shape
+    count, rows, cols = (1,) + tuple(shp) if W.dim() == 2 else tuple(shp)
+    w, nb = _ws(lib().puro_muonh_workspace_size(count, rows, cols), ws, W.device)
+    _check("puro_muonh_step", lib().puro_muonh_step(
+        count, rows, cols, _ptr(W), _ptr(w_bf16), _ptr(G), _ptr(buf), _ptr(radius), float(mu), int(bool(nesterov)),
+        float(eta), int(ns_steps), _ptr(u_out), _ptr(w), nb, _stream()))
+    return w_bf16, u_out
+
+
+def newton_schulz_bf16(X, steps=5, out=None, ws=None):
+    """steps Newton-Schulz steps on X [count, r, c] (or [r, c]) BF16, r <= c."""
+    count, r, c = (1,) + tuple(X.shape) if X.dim() == 2 else tuple(X.shape)
+    out = torch.empty_like(X) if out is None else out
+    w, nb = _ws(lib().puro_newton_schulz_workspace_size(count, r, c), ws, X.device)
+    _check("puro_newton_schulz_bf16", lib().puro_newton_schulz_bf16(
+        count, r, c, _ptr(X), int(steps), _ptr(out), _ptr(w), nb, _stream()))
+    return out

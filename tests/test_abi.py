@@ -293,3 +293,57 @@ def test_gemm_epilogue_validation(puro):
     # a residual overlapping D without being D, and D itself with another pitch
     assert g(16, 16, 256, good, good, FAKE, 16, None, FAKE + 64, 16, FAKE, big, None) == ERR_SHAPE
     assert g(16, 16, 256, good, good, FAKE, 16, None, FAKE, 32, FAKE, big, None) == ERR_SHAPE
+
+
+def test_lm_head_validation(puro):
+    L = puro.lib()
+    big = 1 << 40
+    fwd = lambda M, V, K, r=0, X=FAKE, W=FAKE, t=FAKE, lse=FAKE, loss=FAKE, ws=FAKE, nb=big: L.puro_lm_head_ce_fwd(
+        X, W, t, M, V, K, r, lse, loss, ws, nb, None)
+    assert fwd(128, 256, 128, r=2) == ERR_UNSUPPORTED
+    assert fwd(0, 256, 128) == ERR_SHAPE
+    assert fwd(128, (1 << 21) + 128, 128) == ERR_SHAPE
+    assert fwd(128, 200, 128) == ERR_ALIGN
+    assert fwd(128, 256, 128, X=None) == ERR_NULL
+    assert fwd(128, 256, 128, t=FAKE + 2) == ERR_ALIGN
+    assert fwd(128, 256, 128, loss=None) == ERR_NULL
+    assert fwd(128, 256, 128, nb=16) == ERR_WORKSPACE
+    need = L.puro_lm_head_ce_workspace_size(128, 256, 128, 1, 1)
+    assert need > L.puro_lm_head_ce_workspace_size(128, 256, 128, 1, 0) > 0
+    assert L.puro_lm_head_ce_workspace_size(128, 200, 128, 0, 0) == 0
+    bwd = lambda g=1.0, dX=FAKE, nb=big: L.puro_lm_head_ce_bwd(FAKE, FAKE, FAKE, FAKE, 128, 256, 128, 1, g, dX, FAKE,
+                                                               FAKE, nb, None)
+    assert bwd(g=float("nan")) == ERR_UNSUPPORTED
+    assert bwd(g=float("inf")) == ERR_UNSUPPORTED
+    assert bwd(dX=None) == ERR_NULL
+    assert bwd(nb=need - 1) == ERR_WORKSPACE
+
+
+def test_muonh_validation(puro):
+    L = puro.lib()
+    big = 1 << 40
+    step = lambda cnt=2, rows=256, cols=384, W=FAKE, wb=None, G=FAKE, buf=FAKE, R=FAKE, mu=0.95, eta=0.01, st=5, \
+        u=None, ws=FAKE, nb=big: L.puro_muonh_step(cnt, rows, cols, W, wb, G, buf, R, mu, 1, eta, st, u, ws, nb, None)
+    assert step(cnt=0) == ERR_SHAPE
+    assert step(cnt=65536) == ERR_SHAPE
+    assert step(rows=(1 << 21) + 128) == ERR_SHAPE
+    assert step(cols=200) == ERR_ALIGN
+    assert step(G=None) == ERR_NULL
+    assert step(R=None) == ERR_NULL
+    assert step(W=FAKE + 8) == ERR_ALIGN
+    assert step(wb=FAKE + 8) == ERR_ALIGN
+    assert step(R=FAKE + 2) == ERR_ALIGN
+    assert step(mu=float("nan")) == ERR_UNSUPPORTED
+    assert step(eta=float("inf")) == ERR_UNSUPPORTED
+    assert step(st=-1) == ERR_UNSUPPORTED
+    need = L.puro_muonh_workspace_size(2, 256, 384)
+    assert need > 0 and L.puro_muonh_workspace_size(2, 384, 256) == need
+    assert step(nb=need - 1) == ERR_WORKSPACE
+    ns = lambda cnt=1, r=128, c=256, X=FAKE, steps=5, out=FAKE, nb=big: L.puro_newton_schulz_bf16(
+        cnt, r, c, X, steps, out, FAKE, nb, None)
+    assert ns(r=256, c=128) == ERR_SHAPE
+    assert ns(X=None) == ERR_NULL
+    assert ns(out=FAKE + 4) == ERR_ALIGN
+    assert ns(steps=65) == ERR_UNSUPPORTED
+    assert L.puro_newton_schulz_workspace_size(1, 256, 128) == 0
+    assert ns(nb=L.puro_newton_schulz_workspace_size(1, 128, 256) - 1) == ERR_WORKSPACE
