@@ -161,7 +161,9 @@ void launch_gemm(const GemmProblem& p, void* ws, hipStream_t stream);
 // ---- BF16 transpose (transpose.hip) -------------------------------------------
 
 // dst [C, R] (pitch ldd) = src [R, C] (pitch lds), for `batch` problems whose
-// source and destination start bs_src and bs_dst elements after the previous one's.
+// source and destination start bs_src and bs_dst elements after the previous
+// one's. R, C, the pitches and the strides are multiples of 8, the pointers
+// 16-byte aligned (every caller's shapes are multiples of 128).
 void transpose_bf16(const uint16_t* src, int64_t R, int64_t C, int64_t lds, uint16_t* dst, int64_t ldd,
                     hipStream_t stream, int batch = 1, int64_t bs_src = 0, int64_t bs_dst = 0);
 

@@ -11,27 +11,45 @@ namespace {
 
 constexpr int kT = 64;   // tile edge
 
-// dst [C, R] (pitch ldd) = src [R, C] (pitch lds) of problem blockIdx.z; 64 x
-// 64 tiles through LDS (one padding column keeps the column reads on distinct
-// banks), 256 threads, each moving 16 elements.
+// dst [C, R] (pitch ldd) = src [R, C] (pitch lds) of problem blockIdx.z, in
+// 64 x 64 tiles; R, C and both pitches are multiples of 8 (a 16-byte chunk
+// never straddles an edge). Each thread moves two 16-byte chunks in and two
+// out. The tile sits in LDS as 64 rows of 33 words (one padding word): a
+// wave's column reads (8 source rows x 8 columns, the lanes' chunks) then
+// fall on 32 distinct banks, two lanes sharing each word.
 __global__ __launch_bounds__(256) void transpose_bf16_kernel(const uint16_t* __restrict__ src, int64_t R, int64_t C,
                                                              int64_t lds, uint16_t* __restrict__ dst, int64_t ldd,
                                                              int64_t bs_src, int64_t bs_dst) {
-    __shared__ uint16_t t[kT][kT + 2];
+    constexpr int kW = kT / 2 + 1;       // words per LDS row
+    __shared__ uint32_t t[kT * kW];
     src += blockIdx.z * bs_src;
     dst += blockIdx.z * bs_dst;
     const int64_t r0 = (int64_t)blockIdx.y * kT, c0 = (int64_t)blockIdx.x * kT;
-    const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
 #pragma unroll
-    for (int i = 0; i < kT; i += 4) {
-        const int64_t r = r0 + ty + i, c = c0 + tx;
-        t[ty + i][tx] = (r < R && c < C) ? src[r * lds + c] : (uint16_t)0;
+    for (int k = 0; k < 2; ++k) {
+        const int q = threadIdx.x + 256 * k;
+        const int row = q >> 3, ch = q & 7;
+        const int64_t r = r0 + row, c = c0 + ch * 8;
+        uint4 v = make_uint4(0u, 0u, 0u, 0u);
+        if (r < R && c < C) v = *reinterpret_cast<const uint4*>(src + r * lds + c);
+        uint32_t* w = t + row * kW + ch * 4;
+        w[0] = v.x; w[1] = v.y; w[2] = v.z; w[3] = v.w;
     }
     __syncthreads();
 #pragma unroll
-    for (int i = 0; i < kT; i += 4) {
-        const int64_t c = c0 + ty + i, r = r0 + tx;
-        if (c < C && r < R) dst[c * ldd + r] = t[tx][ty + i];
+    for (int k = 0; k < 2; ++k) {
+        const int q = threadIdx.x + 256 * k;
+        const int cc = q >> 3, ch = q & 7;   // destination row c0 + cc, source rows r0 + 8 ch ..
+        const int64_t c = c0 + cc, r = r0 + ch * 8;
+        uint32_t e[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const uint32_t word = t[(ch * 8 + i) * kW + (cc >> 1)];
+            e[i] = (cc & 1) ? (word >> 16) : (word & 0xFFFFu);
+        }
+        if (c < C && r < R)
+            *reinterpret_cast<uint4*>(dst + c * ldd + r) =
+                make_uint4(e[0] | (e[1] << 16), e[2] | (e[3] << 16), e[4] | (e[5] << 16), e[6] | (e[7] << 16));
     }
 }
 
