@@ -43,6 +43,7 @@
 // (PURO_FA, PURO_FB, PURO_GROUPED), each object holding that variant's tile
 // configurations and output kinds.
 
+#include <climits>
 #include <type_traits>
 
 #include "device_common.h"
@@ -495,6 +496,24 @@ __global__ __launch_bounds__(WM * WN * 64 * (PROD ? 2 : 1)) void gemm_fp8_kernel
             eb[it] = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(
                 rb, (uint32_t)((ncol0 + ((it * 64 + lane) % ECPR) * 4) * 2), 0, 0));
     }
+    // LM-head epilogues: the per-row values (the target's column, lse) of the
+    // wave tile's rows, one global load per lane and 64 rows issued here;
+    // each iteration below takes its row's from the owning lane by a shuffle
+    // instead of waiting on a load of its own
+    constexpr int NRW = (WTM + 63) / 64;
+    int rtg[NRW];
+    float rls[NRW];
+    if constexpr (OUT == kOutLseStats || OUT == kOutSoftmaxGrad) {
+        static_assert(NRW <= 2 && (RPP <= 64 || WTM <= 64), "LM-head row values: a pass stays in one 64-row group");
+#pragma unroll
+        for (int j = 0; j < NRW; ++j) {
+            const int64_t m = (int64_t)mrow0 + 64 * j + lane;
+            const bool ok = 64 * j + lane < WTM && m < p.M;
+            rtg[j] = ok ? p.targets[m] - p.col0 : INT_MIN;
+            rls[j] = (OUT == kOutSoftmaxGrad && ok) ? p.lse[m] : 0.0f;
+        }
+    }
+    (void)rtg; (void)rls;
     __syncthreads();   // every wave is done with the last stage
     // one pass per constant: the accumulators are indexed by the pass, and a
     // loop the unroller leaves rolled would move them to scratch memory
@@ -519,13 +538,52 @@ __global__ __launch_bounds__(WM * WN * 64 * (PROD ? 2 : 1)) void gemm_fp8_kernel
         // writes only after this pass's reads have returned their data)
         asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
         constexpr int IT = RPP * ECPR / 64;
-        if constexpr (OUT == kOutLseStats || OUT == kOutSoftmaxGrad) {
-            // LM-head epilogues on the staged tile. A wave-tile row is 128
-            // columns = 32 chunks, so lanes 0-31 read one row and lanes 32-63
-            // the next; row reductions are butterflies within 32 lanes.
-            // Every lane takes part in every shuffle (no early exits); rows
-            // past M and columns past N are masked.
+        if constexpr (OUT == kOutLseStats) {
+            // The forward's per-block statistics: lane l owns wave-tile row
+            // pass * RPP + l and scans its 128 staged columns twice (the
+            // maximum, then the sum of exp(z - max)) with no cross-lane step;
+            // its row's target column comes from its own register. A wave
+            // tile wholly past N (the ragged last tile) has no block. The
+            // lanes of a 16-lane read phase hold 16 consecutive rows, whose
+            // swizzle keys differ: the reads are free of bank conflicts.
+            static_assert(ECPR == 32 && RPP == 64, "LM-head statistics: 64-row passes of 128 columns");
+            constexpr int RJ = (pass * RPP) / 64;
+            const int r = lane;
+            const int64_t m = mrow0 + pass * RPP + r;
+            if (ncol0 < p.N) {
+                const uint8_t* row = ep + r * ROWB;
+                float mx = -__builtin_inff();
+#pragma unroll 8
+                for (int c = 0; c < ECPR; ++c) {
+                    const float4 v = *reinterpret_cast<const float4*>(row + ((c ^ (r & SWZ)) << 4));
+                    mx = fmaxf(fmaxf(mx, fmaxf(v.x * alpha, v.y * alpha)), fmaxf(v.z * alpha, v.w * alpha));
+                }
+                float sum = 0.0f;
+#pragma unroll 8
+                for (int c = 0; c < ECPR; ++c) {
+                    const float4 v = *reinterpret_cast<const float4*>(row + ((c ^ (r & SWZ)) << 4));
+                    sum += (exp_f32(v.x * alpha - mx) + exp_f32(v.y * alpha - mx)) +
+                           (exp_f32(v.z * alpha - mx) + exp_f32(v.w * alpha - mx));
+                }
+                if (m < p.M) {
+                    p.stats[m * p.stats_ld + ncol0 / 128] = make_float2(mx, sum);
+                    const int tc = rtg[RJ] - ncol0;     // the target's column in this wave tile
+                    if (tc >= 0 && tc < WTN) {
+                        const float* f = reinterpret_cast<const float*>(row + (((tc >> 2) ^ (r & SWZ)) << 4));
+                        p.zt[m] = f[tc & 3] * alpha;
+                    }
+                }
+            }
+            return;
+        }
+        if constexpr (OUT == kOutSoftmaxGrad) {
+            // The backward's dz = g (exp(z - lse) - [column == target]) on
+            // the staged tile: a wave-tile row is 128 columns = 32 chunks, so
+            // lanes 0-31 take one row and lanes 32-63 the next, and store
+            // whole rows. The two rows' lse and target column are read from
+            // the lanes that loaded them (a uniform lane index: no LDS).
             static_assert(ECPR == 32, "LM-head epilogues take 128-column wave tiles");
+            constexpr int RJ = (pass * RPP) / 64;
 #pragma unroll 2
             for (int it = 0; it < IT; ++it) {
                 const int q = it * 64 + lane;
@@ -533,44 +591,26 @@ __global__ __launch_bounds__(WM * WN * 64 * (PROD ? 2 : 1)) void gemm_fp8_kernel
                 const float4 v = *reinterpret_cast<const float4*>(ep + r * ROWB + ((c ^ (r & SWZ)) << 4));
                 const int64_t m = mrow0 + pass * RPP + r;
                 const int n = ncol0 + c * 4;
-                const bool row_ok = m < p.M;
-                const int64_t mr = row_ok ? m : 0;
+                const int rw0 = (pass * RPP + 2 * it) & 63;             // row of lanes 0-31; lanes 32-63: + 1
+                const int t0 = __builtin_amdgcn_readlane(rtg[RJ], rw0);
+                const int t1 = __builtin_amdgcn_readlane(rtg[RJ], rw0 + 1);
+                const float l0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(rls[RJ]), rw0));
+                const float l1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(rls[RJ]), rw0 + 1));
+                const int tgt = (lane >> 5) ? t1 : t0;
+                const float l = (lane >> 5) ? l1 : l0;
                 const float e[4] = {v.x * alpha, v.y * alpha, v.z * alpha, v.w * alpha};
-                const int tgt = p.targets[mr] - p.col0;      // the target's column in this GEMM
-                if constexpr (OUT == kOutLseStats) {
-                    float mx = -__builtin_inff();
+                float d[4];
 #pragma unroll
-                    for (int t = 0; t < 4; ++t)
-                        if (n + t < p.N) mx = fmaxf(mx, e[t]);
+                for (int t = 0; t < 4; ++t)
+                    d[t] = p.grad_scale * (exp_f32(e[t] - l) - (n + t == tgt ? 1.0f : 0.0f));
+                if (m < p.M) {
+                    uint16_t* dst = reinterpret_cast<uint16_t*>(p.D) + m * p.ldd + n;
+                    if (n + 3 < p.N) {
+                        *reinterpret_cast<uint2*>(dst) = make_uint2(pack_bf16x2(d[0], d[1]), pack_bf16x2(d[2], d[3]));
+                    } else {
 #pragma unroll
-                    for (int o = 16; o >= 1; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 64));
-                    float sum = 0.0f;
-#pragma unroll
-                    for (int t = 0; t < 4; ++t)
-                        if (n + t < p.N) sum += exp_f32(e[t] - mx);
-#pragma unroll
-                    for (int o = 16; o >= 1; o >>= 1) sum += __shfl_xor(sum, o, 64);
-                    // a wave tile wholly past N (the ragged last tile) has no block
-                    if (row_ok && (lane & 31) == 0 && ncol0 < p.N)
-                        p.stats[m * p.stats_ld + ncol0 / 128] = make_float2(mx, sum);
-#pragma unroll
-                    for (int t = 0; t < 4; ++t)
-                        if (row_ok && n + t == tgt && n + t < p.N) p.zt[m] = e[t];
-                } else {
-                    const float l = p.lse[mr];
-                    float d[4];
-#pragma unroll
-                    for (int t = 0; t < 4; ++t)
-                        d[t] = p.grad_scale * (exp_f32(e[t] - l) - (n + t == tgt ? 1.0f : 0.0f));
-                    if (row_ok) {
-                        uint16_t* dst = reinterpret_cast<uint16_t*>(p.D) + m * p.ldd + n;
-                        if (n + 3 < p.N) {
-                            *reinterpret_cast<uint2*>(dst) = make_uint2(pack_bf16x2(d[0], d[1]), pack_bf16x2(d[2], d[3]));
-                        } else {
-#pragma unroll
-                            for (int t = 0; t < 4; ++t)
-                                if (n + t < p.N) dst[t] = to_bf16(d[t]);
-                        }
+                        for (int t = 0; t < 4; ++t)
+                            if (n + t < p.N) dst[t] = to_bf16(d[t]);
                     }
                 }
             }
