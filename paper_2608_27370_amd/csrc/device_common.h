@@ -185,16 +185,56 @@ __device__ __forceinline__ uint2 encode8(const uint32_t w[4], float r) {
     return out;
 }
 
+// Codes of the 8 BF16 values of w divided by the power of two s, one
+// v_cvt_scalef32_pk_{fp8,bf8}_bf16 per pair: the instruction rounds x / s
+// exactly as v_cvt_pk_{fp8,bf8}_f32 rounds it (the same codes as encode8
+// with r = 1 / s, verified bit for bit over every BF16 pattern on the
+// hardware), and like it does not saturate: for groups whose values stay
+// within the format after scaling. s must be a normal binary32 number.
+typedef short short2_t __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+template <int FMT, bool HI>
+__device__ __forceinline__ short2_t cvt_scaled_pk(short2_t old, uint32_t x, float s) {
+    const bf16x2_t v = __builtin_bit_cast(bf16x2_t, x);
+    if constexpr (FMT == kE4M3) return __builtin_amdgcn_cvt_scalef32_pk_fp8_bf16(old, v, s, HI);
+    else return __builtin_amdgcn_cvt_scalef32_pk_bf8_bf16(old, v, s, HI);
+}
+template <int FMT>
+__device__ __forceinline__ uint2 encode8_pow2(const uint32_t w[4], float s) {
+    short2_t a = cvt_scaled_pk<FMT, false>(short2_t{0, 0}, w[0], s);
+    a = cvt_scaled_pk<FMT, true>(a, w[1], s);
+    short2_t b = cvt_scaled_pk<FMT, false>(short2_t{0, 0}, w[2], s);
+    b = cvt_scaled_pk<FMT, true>(b, w[3], s);
+    return make_uint2(__builtin_bit_cast(uint32_t, a), __builtin_bit_cast(uint32_t, b));
+}
+
+// 8x8 transpose of 16-bit values: w[i] holds row i (word j = columns 2j and
+// 2j + 1, the low half first), wt[c] column c in the same form. One byte
+// permute per output word: a pair of rows' halves meet in one word.
+__device__ __forceinline__ void transpose8x8_b16(const uint32_t w[8][4], uint32_t wt[8][4]) {
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            wt[2 * j][k] = __builtin_amdgcn_perm(w[2 * k + 1][j], w[2 * k][j], 0x05040100u);      // low halves
+            wt[2 * j + 1][k] = __builtin_amdgcn_perm(w[2 * k + 1][j], w[2 * k][j], 0x07060302u);  // high halves
+        }
+}
+
+// Both halves' unsigned 16-bit maxima in one instruction (v_pk_max_u16).
+typedef unsigned short ushort2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t pk_max_u16(uint32_t a, uint32_t b) {
+    return __builtin_bit_cast(uint32_t, __builtin_elementwise_max(__builtin_bit_cast(ushort2_t, a),
+                                                                  __builtin_bit_cast(ushort2_t, b)));
+}
+// The two BF16 magnitude patterns of a word, in place.
+__device__ __forceinline__ uint32_t mag2(uint32_t w) { return w & 0x7FFF7FFFu; }
+
 // Largest BF16 magnitude pattern among 8 values (4 words); as integers the
 // magnitude patterns order like the magnitudes, and NaN patterns exceed Inf.
 __device__ __forceinline__ uint32_t absmax_bits8(const uint32_t w[4]) {
-    uint32_t m = 0;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        uint32_t lo = w[i] & 0x7FFFu, hi = (w[i] >> 16) & 0x7FFFu;
-        m = max(m, max(lo, hi));
-    }
-    return m;
+    const uint32_t m = pk_max_u16(pk_max_u16(mag2(w[0]), mag2(w[1])), pk_max_u16(mag2(w[2]), mag2(w[3])));
+    return max(m & 0xFFFFu, m >> 16);
 }
 
 // Power-of-two scale exponent; amax given as its BF16 magnitude pattern

@@ -307,10 +307,8 @@ __device__ __forceinline__ void store_rows(const QuantArgs& a, const Tile& t, co
 // 0, so a 16-byte run never crosses the end of a qT row. Ends with a barrier,
 // after which the LDS buffer may be reused. qT not 16-byte aligned: 8-byte
 // stores straight from registers.
-__device__ __forceinline__ void store_transposed(const QuantArgs& a, const Tile& t, int64_t row0, int64_t col0,
-                                                 const uint2 c[8], uint8_t* lds) {
-    uint2 ct[8];
-    transpose8x8(c, ct);
+__device__ __forceinline__ void store_transposed_ct(const QuantArgs& a, const Tile& t, int64_t row0, int64_t col0,
+                                                    const uint2 ct[8], uint8_t* lds) {
     if ((reinterpret_cast<uintptr_t>(a.qT) & 15) != 0) {
         if (!t.col_ok || t.row0 >= a.rows) return;
 #pragma unroll
@@ -336,6 +334,14 @@ __device__ __forceinline__ void store_transposed(const QuantArgs& a, const Tile&
     __syncthreads();
 }
 
+// The same from the codes of the thread's 8x8 block in row order.
+__device__ __forceinline__ void store_transposed(const QuantArgs& a, const Tile& t, int64_t row0, int64_t col0,
+                                                 const uint2 c[8], uint8_t* lds) {
+    uint2 ct[8];
+    transpose8x8(c, ct);
+    store_transposed_ct(a, t, row0, col0, ct, lds);
+}
+
 // Encode with one multiplier per column of the 8x8 block (column-grouped scales).
 template <int FMT, bool SAFE>
 __device__ __forceinline__ uint2 encode8_cols(const uint32_t w[4], const float r[8]) {
@@ -354,11 +360,6 @@ __device__ __forceinline__ uint2 encode8_cols(const uint32_t w[4], const float r
         out.y = encode4_fast<FMT>(v[4], v[5], v[6], v[7]);
     }
     return out;
-}
-
-__device__ __forceinline__ uint32_t elem_mag(const uint32_t w[8][4], int i, int j) {
-    const uint32_t word = w[i][j >> 1];
-    return ((j & 1) ? (word >> 16) : word) & 0x7FFFu;
 }
 
 // Scale of a per-tensor quantisation: s (stored) and the multiplier r, and
@@ -491,7 +492,7 @@ __global__ __launch_bounds__(kThreads) void quant_tensor_kernel(QuantArgs a0, Qu
 // 1x128 row groups (q, scale) and/or 128x1 column groups (qT, scaleT).
 template <int FMT, bool ROWS, bool COLS, int SRC>
 __global__ __launch_bounds__(kThreads) void quant_groups_kernel(QuantArgs a) {
-    __shared__ uint32_t colmax[4][kTile];
+    __shared__ uint32_t colmax[4][kTile / 2];     // packed pairs of column maxima per wave
     __shared__ __attribute__((aligned(16))) uint8_t tq[COLS ? kTile * kTile : 16];
     const Tile t = tile_coords(a.cols);
     uint32_t w[8][4];
@@ -510,6 +511,7 @@ __global__ __launch_bounds__(kThreads) void quant_groups_kernel(QuantArgs a) {
                 const int e = pow2_exponent_bf16<FMT>(m, floor_rule);
                 srow[i] = exp2i(e);
                 if (floor_rule && floor_rule_saturates(m)) c[i] = encode8<FMT, true>(w[i], exp2i(-e));
+                else if (e > -127) c[i] = encode8_pow2<FMT>(w[i], srow[i]);
                 else c[i] = encode8<FMT, false>(w[i], exp2i(-e));
             } else if (m == 0x7F80u) {               // an infinity: largest scale, saturate
                 srow[i] = exp2i(127);
@@ -530,34 +532,41 @@ __global__ __launch_bounds__(kThreads) void quant_groups_kernel(QuantArgs a) {
         }
     }
     if constexpr (COLS) {
-        // column maxima over the tile's 128 rows: 8 rows in-thread, 4 row
-        // groups per wave (lanes 16 apart), 4 waves through LDS
-        uint32_t cm[8];
+        // column maxima over the tile's 128 rows, two columns per word (the
+        // two magnitude patterns of a word in its halves): 8 rows in-thread,
+        // 4 row groups per wave (lanes 16 apart), 4 waves through LDS
+        uint32_t cm[4];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            uint32_t m = 0;
+        for (int j = 0; j < 4; ++j) {
+            uint32_t m = mag2(w[0][j]);
 #pragma unroll
-            for (int i = 0; i < 8; ++i) m = max(m, elem_mag(w, i, j));
-            m = max(m, (uint32_t)__shfl_xor((int)m, 16, 64));
-            m = max(m, (uint32_t)__shfl_xor((int)m, 32, 64));
+            for (int i = 1; i < 8; ++i) m = pk_max_u16(m, mag2(w[i][j]));
+            m = pk_max_u16(m, (uint32_t)__shfl_xor((int)m, 16, 64));
+            m = pk_max_u16(m, (uint32_t)__shfl_xor((int)m, 32, 64));
             cm[j] = m;
         }
         const int wv = threadIdx.x >> 6;
         if ((threadIdx.x & 63) < 16) {
 #pragma unroll
-            for (int j = 0; j < 8; ++j) colmax[wv][t.cc * 8 + j] = cm[j];
+            for (int j = 0; j < 4; ++j) colmax[wv][t.cc * 4 + j] = cm[j];
         }
         __syncthreads();
+        uint32_t cw[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int k = t.cc * 4 + j;
+            cw[j] = pk_max_u16(pk_max_u16(colmax[0][k], colmax[1][k]), pk_max_u16(colmax[2][k], colmax[3][k]));
+        }
         float rcol[8], scol[8];
-        bool finite = true;
+        bool finite = true, normal = true;
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
-            const int k = t.cc * 8 + j;
-            const uint32_t m = max(max(colmax[0][k], colmax[1][k]), max(colmax[2][k], colmax[3][k]));
+            const uint32_t m = (j & 1) ? (cw[j >> 1] >> 16) : (cw[j >> 1] & 0xFFFFu);
             if (m <= 0x7F7Fu) {
                 const int e = pow2_exponent_bf16<FMT>(m, floor_rule);
                 scol[j] = exp2i(e);
                 rcol[j] = exp2i(-e);
+                normal = normal && e > -127;
                 if (floor_rule && floor_rule_saturates(m)) finite = false;   // take the saturating path
             } else if (m == 0x7F80u) {
                 scol[j] = exp2i(127);
@@ -568,15 +577,26 @@ __global__ __launch_bounds__(kThreads) void quant_groups_kernel(QuantArgs a) {
                 finite = false;
             }
         }
-        uint2 c[8];
-        if (finite) {
+        uint2 ct[8];
+        if (finite && normal) {
+            // transpose the BF16 block first: each column then shares one
+            // scale, and its codes come out in the transposed copy's order
+            uint32_t wt[8][4];
+            transpose8x8_b16(w, wt);
 #pragma unroll
-            for (int i = 0; i < 8; ++i) c[i] = encode8_cols<FMT, false>(w[i], rcol);
+            for (int j = 0; j < 8; ++j) ct[j] = encode8_pow2<FMT>(wt[j], scol[j]);
         } else {
+            uint2 c[8];
+            if (finite) {
 #pragma unroll
-            for (int i = 0; i < 8; ++i) c[i] = encode8_cols<FMT, true>(w[i], rcol);
+                for (int i = 0; i < 8; ++i) c[i] = encode8_cols<FMT, false>(w[i], rcol);
+            } else {
+#pragma unroll
+                for (int i = 0; i < 8; ++i) c[i] = encode8_cols<FMT, true>(w[i], rcol);
+            }
+            transpose8x8(c, ct);
         }
-        store_transposed(a, t, (int64_t)blockIdx.y * kTile, (int64_t)blockIdx.x * kTile, c, tq);
+        store_transposed_ct(a, t, (int64_t)blockIdx.y * kTile, (int64_t)blockIdx.x * kTile, ct, tq);
         if (t.rg == 0 && t.col_ok) {
             const int64_t ng = a.rows / kTile;
 #pragma unroll
