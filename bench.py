@@ -603,9 +603,10 @@ class MuonH28:
     kind (QKV 2048x1536, O 1536x1536, gate/up 17920x1536, down 1536x8960) one
     call on the 28 matrices stored back to back (FP32 W, G, momentum; W ~
     N(0, 0.02^2), G and momentum ~ N(0, (1e-3)^2), drawn on the device). The
-    algorithmic work is the Newton-Schulz products: per matrix and step (r <=
-    c its oriented shape) 2 r^2 c for X X^T, 2 r^3 for A A^T, 2 r^2 c for B X,
-    five steps."""
+    algorithmic work is the Newton-Schulz products counted dense: per matrix
+    and step (r <= c its oriented shape) 2 r^2 c for X X^T, 2 r^3 for A A^T,
+    2 r^2 c for B X, five steps. The two symmetric products compute only the
+    tiles on or above the diagonal; the executed work is reported beside."""
 
     name = "muonh_28_layers_qwen2_1p5b"
 
@@ -630,13 +631,21 @@ class MuonH28:
             r, c = min(rows, cols), max(rows, cols)
             fl = L * 5 * (4.0 * r * r * c + 2.0 * r ** 3)
             self.flops += fl
+            t = -(-r // 256)                     # 256-wide tiles of the symmetric products
+            sym = t * (t + 1) / 2.0 / (t * t)    # the share of their tiles computed
+            self.executed_flops = getattr(self, "executed_flops", 0.0) + L * 5 * (
+                2.0 * r * r * c * sym + 2.0 * r ** 3 * sym + 2.0 * r * r * c)
             self.mats.append(dict(name=name, W=W, G=G, buf=buf, R=R, wb=wb, ws=ws, flops=fl, shape=(rows, cols)))
         self.peak = BF16_PEAK_TFLOPS
         self.dtype = "bf16"
-        self.metric = "MuonH optimiser step: Newton-Schulz TFLOP/s over the 28 layers' matrices (BF16 MFMA)"
+        self.metric = ("MuonH optimiser step: Newton-Schulz TFLOP/s over the 28 layers' matrices, dense-equivalent "
+                       "(BF16 MFMA)")
         self.config = {"workload": self.name, "layers": L, "matrices": {n: [r, c] for n, r, c in self.kinds},
                        "newton_schulz": "5 quintic steps in BF16, (a, b, c) = (3.4445, -4.7750, 2.0315)",
-                       "state": "FP32 W, G, momentum (mu 0.95, Nesterov); BF16 copy of W' written"}
+                       "state": "FP32 W, G, momentum (mu 0.95, Nesterov); BF16 copy of W' written",
+                       "flops_counted_per_step": self.flops, "flops_executed_per_step": self.executed_flops,
+                       "symmetric_products": "X X^T and b A + c A A^T: only the tiles on or above the diagonal, "
+                                             "then mirrored"}
 
     def _call(self, m):
         P = self.P

@@ -86,13 +86,15 @@ int per_cu(const TileCfg& t, bool grouped) {
 // waves of work units over the CUs, each a fixed cost plus a cost per k
 // slice (lower when part of the GPU idles and the clock rises; higher with
 // block scales), plus the split-K partial sums written and read back.
-Plan make_plan(int64_t M, int64_t N, int64_t K, bool grouped, int batch = 1) {
+Plan make_plan(int64_t M, int64_t N, int64_t K, bool grouped, int batch = 1, bool upper = false) {
     const int ksteps = (int)((K + kBK - 1) / kBK);
     Plan best{0, 1, ksteps};
     double best_cost = -1.0;
     for (int c = 0; c < kNumTiles; ++c) {
         const TileCfg t = kTiles[c];
-        const int64_t tiles = ((M + t.bm - 1) / t.bm) * ((N + t.bn - 1) / t.bn) * batch;
+        if (upper && t.bm != t.bn) continue;   // the upper-triangle walk takes square tiles
+        const int64_t tm_ = (M + t.bm - 1) / t.bm, tn_ = (N + t.bn - 1) / t.bn;
+        const int64_t tiles = (upper ? tm_ * (tm_ + 1) / 2 : tm_ * tn_) * batch;
         if (tiles == 0) return best;
         const int64_t slots = (int64_t)kCUs * per_cu(t, grouped);
         const int max_s = (N % 4 == 0) ? (ksteps / 4 < 16 ? ksteps / 4 : 16) : 1;
@@ -173,6 +175,7 @@ void run_plan(const GemmProblem& g, const Plan& pl, void* ws, hipStream_t stream
     prm.residual = g.residual;
     prm.ldr = g.ldr;
     prm.res_scale = g.res_scale;
+    prm.upper = g.upper;
     const int ob = g.out == kOutF32 ? 4 : 2;
     prm.batch = g.batch;
     prm.bsa = g.bsa * eb; prm.bsb = g.bsb * eb; prm.bsd = g.bsd * ob; prm.bsr = g.bsr;
@@ -181,7 +184,7 @@ void run_plan(const GemmProblem& g, const Plan& pl, void* ws, hipStream_t stream
     prm.lse = g.lse; prm.grad_scale = g.grad_scale;
     const bool grouped = grouped_scales(g);
     const int out = pl.splits > 1 ? 2 : g.out;
-    const int grid = prm.tiles_m * prm.tiles_n * pl.splits * g.batch;
+    const int grid = (g.upper ? prm.tiles_m * (prm.tiles_m + 1) / 2 : prm.tiles_m * prm.tiles_n) * pl.splits * g.batch;
     auto launch = [&](auto fa, auto fb) {
         constexpr int FA = decltype(fa)::value, FB = decltype(fb)::value;
         if (grouped) launch_variant<FA, FB, true>(prm, pl.cfg, out, grid, stream);
@@ -220,9 +223,15 @@ void run_plan(const GemmProblem& g, const Plan& pl, void* ws, hipStream_t stream
 size_t gemm_workspace_bytes(int64_t M, int64_t N, int64_t K, int out, int batch) {
     // enough for the plan with or without block scales
     (void)out;
-    const size_t a = plan_workspace_bytes(M, N, make_plan(M, N, K, false, batch), batch);
-    const size_t b = plan_workspace_bytes(M, N, make_plan(M, N, K, true, batch), batch);
-    return a > b ? a : b;
+    // enough for the plans with or without block scales, and (square
+    // problems) for the upper-triangle plans
+    size_t w = 0;
+    for (int u = 0; u < (M == N ? 2 : 1); ++u)
+        for (int gr = 0; gr < 2; ++gr) {
+            const size_t v = plan_workspace_bytes(M, N, make_plan(M, N, K, gr != 0, batch, u != 0), batch);
+            w = v > w ? v : w;
+        }
+    return w;
 }
 
 void gemm_plan(int64_t M, int64_t N, int64_t K, bool grouped, int* tile_m, int* tile_n, int* stages,
@@ -242,7 +251,12 @@ void launch_gemm(const GemmProblem& g, void* ws, hipStream_t stream) {
         run_plan(g, Plan{0, 1, (int)((kb + kBK - 1) / kBK)}, ws, stream);
         return;
     }
-    run_plan(g, make_plan(g.M, g.N, kb, grouped_scales(g), g.batch), ws, stream);
+    run_plan(g, make_plan(g.M, g.N, kb, grouped_scales(g), g.batch, g.upper != 0), ws, stream);
+}
+
+int gemm_tile(const GemmProblem& g) {
+    if (g.out == kOutLseStats || g.out == kOutSoftmaxGrad) return kTiles[0].bm;
+    return kTiles[make_plan(g.M, g.N, g.K * elem_bytes(g), grouped_scales(g), g.batch, g.upper != 0).cfg].bm;
 }
 
 }  // namespace puro

@@ -167,7 +167,8 @@ __global__ __launch_bounds__(WM * WN * 64 * (PROD ? 2 : 1)) void gemm_fp8_kernel
     const int T = gridDim.x;
     const int b = blockIdx.x;
     int lt = (T % 8 == 0) ? (b % 8) * (T / 8) + b / 8 : b;
-    const int per_split = p.tiles_m * p.tiles_n;
+    // a symmetric product computes only the tiles on or above the diagonal
+    const int per_split = p.upper ? p.tiles_m * (p.tiles_m + 1) / 2 : p.tiles_m * p.tiles_n;
     if (p.batch > 1) {
         // problem bi of a batched launch: its operands, output and partials
         const int bi = lt / (per_split * p.splits);
@@ -180,11 +181,24 @@ __global__ __launch_bounds__(WM * WN * 64 * (PROD ? 2 : 1)) void gemm_fp8_kernel
     }
     const int ks = lt / per_split;
     const int rem = lt - ks * per_split;
-    const int group = rem / (p.gm * p.tiles_n);
-    const int first_m = group * p.gm;
-    const int gsz = min(p.gm, p.tiles_m - first_m);
-    const int r2 = rem - group * p.gm * p.tiles_n;
-    const int tm = first_m + r2 % gsz, tn = r2 / gsz;
+    int tm, tn;
+    if (p.upper) {
+        // row tm of the upper triangle holds tiles_n - tm tiles (a uniform scalar walk)
+        int r = rem;
+        tm = 0;
+        while (r >= p.tiles_n - tm) {
+            r -= p.tiles_n - tm;
+            ++tm;
+        }
+        tn = tm + r;
+    } else {
+        const int group = rem / (p.gm * p.tiles_n);
+        const int first_m = group * p.gm;
+        const int gsz = min(p.gm, p.tiles_m - first_m);
+        const int r2 = rem - group * p.gm * p.tiles_n;
+        tm = first_m + r2 % gsz;
+        tn = r2 / gsz;
+    }
     const int m0 = tm * BM, n0 = tn * BN;
     // per-tensor scales, applied to the FP32 sums in the epilogue (loaded
     // here so that their latency hides behind the main loop)

@@ -131,6 +131,10 @@ struct GemmProblem {
     const uint16_t* residual;
     int64_t ldr;
     float alpha = 1.0f, res_scale = 1.0f;
+    // a symmetric product (M == N, D = D^T): compute only the tiles on or
+    // above the diagonal (square tiles); the tiles below are left unwritten
+    // (gemm_tile returns the tile edge for filling them in)
+    int upper = 0;
     // `batch` independent problems of the same shape and scales: operand,
     // output and residual b start bsa, bsb, bsd, bsr elements after those of
     // problem 0
@@ -157,6 +161,8 @@ void gemm_plan(int64_t M, int64_t N, int64_t K, bool grouped, int* tile_m, int* 
                int* splits);
 // Enqueue the GEMM; `ws` must hold gemm_workspace_bytes(...) bytes.
 void launch_gemm(const GemmProblem& p, void* ws, hipStream_t stream);
+// The output tile edge (rows) of the plan launch_gemm takes for `p`.
+int gemm_tile(const GemmProblem& p);
 
 // ---- BF16 transpose (transpose.hip) -------------------------------------------
 
@@ -166,6 +172,10 @@ void launch_gemm(const GemmProblem& p, void* ws, hipStream_t stream);
 // 16-byte aligned (every caller's shapes are multiples of 128).
 void transpose_bf16(const uint16_t* src, int64_t R, int64_t C, int64_t lds, uint16_t* dst, int64_t ldd,
                     hipStream_t stream, int batch = 1, int64_t bs_src = 0, int64_t bs_dst = 0);
+// The lower triangle of tiles of a symmetric A [R, R] (pitch ld, R a
+// multiple of 64 and of tg) from the upper one: element (i, j) = (j, i)
+// wherever i / tg > j / tg; `batch` matrices bs elements apart.
+void mirror_lower_bf16(uint16_t* A, int64_t R, int64_t ld, int tg, hipStream_t stream, int batch, int64_t bs);
 
 // ---- LM head with cross-entropy (lm_head.hip) ---------------------------------
 

@@ -251,7 +251,9 @@ int ns_steps(uint8_t* w8, const NsLayout& l, int64_t count, int64_t r, int64_t c
         gram.B = reinterpret_cast<const uint8_t*>(X[cur]); gram.ldb = c; gram.fb = kBF16; gram.sb_mode = kSNone;
         gram.D = A; gram.ldd = r; gram.out = kOutBF16;
         gram.batch = bt; gram.bsa = r * c; gram.bsb = r * c; gram.bsd = r * r;
+        gram.upper = 1;   // X X^T is symmetric: the upper tiles, then their mirror
         launch_gemm(gram, gws, stream);
+        mirror_lower_bf16(A, r, r, gemm_tile(gram), stream, bt, r * r);
         GemmProblem poly{};
         poly.M = r; poly.N = r; poly.K = r;
         poly.A = reinterpret_cast<const uint8_t*>(A); poly.lda = r; poly.fa = kBF16; poly.sa_mode = kSNone;
@@ -259,7 +261,9 @@ int ns_steps(uint8_t* w8, const NsLayout& l, int64_t count, int64_t r, int64_t c
         poly.D = B; poly.ldd = r; poly.out = kOutBF16Epi;
         poly.residual = A; poly.ldr = r; poly.alpha = kNsC; poly.res_scale = kNsB;
         poly.batch = bt; poly.bsa = r * r; poly.bsb = r * r; poly.bsd = r * r; poly.bsr = r * r;
+        poly.upper = 1;   // b A + c A A^T is symmetric too
         launch_gemm(poly, gws, stream);
+        mirror_lower_bf16(B, r, r, gemm_tile(poly), stream, bt, r * r);
         GemmProblem upd{};
         upd.M = r; upd.N = c; upd.K = r;
         upd.A = reinterpret_cast<const uint8_t*>(B); upd.lda = r; upd.fa = kBF16; upd.sa_mode = kSNone;
