@@ -995,7 +995,7 @@ def breakdown(args, torch, W, stream):
 def main():
     args = parse()
     if args.gpus != 1:
-        print("bench.py runs on one GPU only: this build measures the single-GPU share of the data-"
+        print("bench.py runs on one GPU only: it measures the single-GPU share of the data-"
               "parallel path (every rank runs the same layers on its own tokens); --gpus %d is not "
               "supported" % args.gpus, file=sys.stderr)
         sys.exit(2)

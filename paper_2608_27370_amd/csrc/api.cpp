@@ -396,6 +396,9 @@ puro_status gemm_impl(int64_t M, int64_t N, int64_t K, const puro_fp8_operand* A
     g.D = D; g.ldd = ldd; g.out = out; g.accumulate = accumulate != 0;
     g.sa_kmajor = a_kmajor; g.sb_kmajor = b_kmajor;
     g.bias = bias; g.residual = residual; g.ldr = ldr;
+    // a linear layer's outputs (Y, dX, dW) are far larger than the L2 and
+    // are next read by another kernel: stream them past the caches
+    g.nt_out = 1;
     launch_gemm(g, ws, stream);
     return launched();
 }

@@ -176,6 +176,7 @@ void run_plan(const GemmProblem& g, const Plan& pl, void* ws, hipStream_t stream
     prm.ldr = g.ldr;
     prm.res_scale = g.res_scale;
     prm.upper = g.upper;
+    prm.nt_out = g.nt_out;
     const int ob = g.out == kOutF32 ? 4 : 2;
     prm.batch = g.batch;
     prm.bsa = g.bsa * eb; prm.bsb = g.bsb * eb; prm.bsd = g.bsd * ob; prm.bsr = g.bsr;

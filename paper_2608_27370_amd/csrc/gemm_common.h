@@ -36,6 +36,7 @@ struct Params {
     int64_t ldr;
     float res_scale;           // factor of the residual
     int upper;                 // only the tiles on or above the diagonal (square tiles, M == N)
+    int nt_out;                // interior tiles store D with non-temporal (streaming) stores
     int batch;                 // problems of one launch: A, B, D advance by bsa, bsb, bsd bytes,
     int64_t bsa, bsb, bsd;     // the residual by bsr elements, the split-K partials by
     int64_t bsr;               // splits * M * N floats

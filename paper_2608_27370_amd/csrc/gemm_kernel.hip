@@ -688,11 +688,24 @@ __global__ __launch_bounds__(WM * WN * 64 * (PROD ? 2 : 1)) void gemm_fp8_kernel
                                 w.z = fmaf(rs, bf16lo(rv.y), w.z); w.w = fmaf(rs, bf16hi(rv.y), w.w);
                             }
                         }
-                        if constexpr (OUT == kOutF32)
-                            *reinterpret_cast<float4*>(reinterpret_cast<float*>(p.D) + m * p.ldd + n) = w;
-                        else
-                            *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(p.D) + m * p.ldd + n) =
-                                make_uint2(pack_bf16x2(w.x, w.y), pack_bf16x2(w.z, w.w));
+                        if constexpr (OUT == kOutF32) {
+                            float* dst = reinterpret_cast<float*>(p.D) + m * p.ldd + n;
+                            if (p.nt_out) {
+                                typedef float v4f __attribute__((ext_vector_type(4)));
+                                __builtin_nontemporal_store(v4f{w.x, w.y, w.z, w.w}, reinterpret_cast<v4f*>(dst));
+                            } else {
+                                *reinterpret_cast<float4*>(dst) = w;
+                            }
+                        } else {
+                            uint16_t* dst = reinterpret_cast<uint16_t*>(p.D) + m * p.ldd + n;
+                            const uint32_t lo = pack_bf16x2(w.x, w.y), hi = pack_bf16x2(w.z, w.w);
+                            if (p.nt_out) {
+                                typedef unsigned int v2u __attribute__((ext_vector_type(2)));
+                                __builtin_nontemporal_store(v2u{lo, hi}, reinterpret_cast<v2u*>(dst));
+                            } else {
+                                *reinterpret_cast<uint2*>(dst) = make_uint2(lo, hi);
+                            }
+                        }
                     }
                 }
             }

@@ -135,6 +135,9 @@ struct GemmProblem {
     // above the diagonal (square tiles); the tiles below are left unwritten
     // (gemm_tile returns the tile edge for filling them in)
     int upper = 0;
+    // D is not read back soon: interior tiles store it with non-temporal
+    // (streaming) stores, which shorten the output-heavy epilogues
+    int nt_out = 0;
     // `batch` independent problems of the same shape and scales: operand,
     // output and residual b start bsa, bsb, bsd, bsr elements after those of
     // problem 0
