@@ -149,10 +149,11 @@ class ClockSampler:
     """The GFX clock sampled through amdsmi every few milliseconds while
     running: the mean over the XCDs of the metrics table's current GFX
     clocks, or (where the table has none) the clock-info reading; None when
-    amdsmi is unavailable."""
+    amdsmi is unavailable. The socket power is sampled beside it."""
 
     def __init__(self, period_s=0.005):
         self.samples, self.period, self._stop = [], period_s, threading.Event()
+        self.power = []
         self.handle, self.source = None, None
         try:
             import amdsmi
@@ -177,12 +178,26 @@ class ClockSampler:
         self.source = "amdsmi clock info GFX"
         return float(info["clk"])
 
+    def read_power(self):
+        try:
+            info = self.amdsmi.amdsmi_get_power_info(self.handle)
+            for k in ("current_socket_power", "average_socket_power", "socket_power"):
+                v = info.get(k)
+                if isinstance(v, (int, float)) and 0 < v < 65535:
+                    return float(v)
+        except Exception:
+            pass
+        return None
+
     def _run(self):
         while not self._stop.is_set():
             try:
                 self.samples.append(self.read())
             except Exception:
                 return
+            w = self.read_power()
+            if w is not None:
+                self.power.append(w)
             time.sleep(self.period)
 
     def __enter__(self):
@@ -201,8 +216,11 @@ class ClockSampler:
         if not self.samples:
             return None
         s = np.array(self.samples)
-        return {"median_mhz": float(np.median(s)), "p10_mhz": float(np.percentile(s, 10)),
-                "p90_mhz": float(np.percentile(s, 90)), "samples": int(s.size), "source": self.source}
+        out = {"median_mhz": float(np.median(s)), "p10_mhz": float(np.percentile(s, 10)),
+               "p90_mhz": float(np.percentile(s, 90)), "samples": int(s.size), "source": self.source}
+        if self.power:
+            out["median_socket_power_w"] = float(np.median(self.power))
+        return out
 
 
 SWIGLU_CALLS = ("swiglu_tensor", "swiglu_groups", "swiglu_bwd_groups")
@@ -931,17 +949,25 @@ def run_only(args, torch, W):
             sys.exit("unknown --only %r; calls of %s: %s" % (args.only, W.name,
                                                              ", ".join(c.key for c in W.calls())))
         fn, label = rows[0].fn, rows[0].label
+        # the call's operands are what the kind's earlier calls write (its
+        # quantisations): run every call of the kind once, in order, first
+        kind = args.only.split(".")[0]
+        for c in W.calls():
+            if c.key.split(".")[0] == kind:
+                c.fn()
     for _ in range(args.warmup):
         fn()
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record(stream)
-    for _ in range(args.steps):
-        fn()
-    e1.record(stream)
-    torch.cuda.synchronize()
+    with ClockSampler() as clock:
+        e0.record(stream)
+        for _ in range(args.steps):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
     print(json.dumps({"only": args.only, "call": label, "launches": args.steps,
-                      "us_per_call": round(e0.elapsed_time(e1) / max(1, args.steps) * 1e3, 2)}), flush=True)
+                      "us_per_call": round(e0.elapsed_time(e1) / max(1, args.steps) * 1e3, 2),
+                      "clock": clock.summary()}), flush=True)
 
 
 def breakdown(args, torch, W, stream):

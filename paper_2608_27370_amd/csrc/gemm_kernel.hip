@@ -79,6 +79,8 @@ __device__ __forceinline__ void static_for(F&& f) {
     }
 }
 
+constexpr int cgcd(int a, int b) { return b == 0 ? a : cgcd(b, a % b); }
+
 __device__ __forceinline__ uint32_t e8m0_of(float s) { return (__float_as_uint(s) >> 23) & 0xFFu; }
 
 
@@ -497,7 +499,13 @@ __global__ __launch_bounds__(WM * WN * 64 * (PROD ? 2 : 1)) void gemm_fp8_kernel
     // a tile inside the matrix whose sums overwrite the output stores whole
     // 4-column vectors everywhere: a branch-free path that issues all of a
     // pass's LDS reads before its stores
-    const bool fast = m0 + BM <= p.M && n0 + BN <= p.N && (OUT == 2 || !p.accumulate);
+    constexpr int ES = (OUT == kOutF32 || OUT == 2) ? 4 : 2;    // bytes per output element
+    const int64_t ldo = OUT == 2 ? (int64_t)p.N : p.ldd;          // output pitch (elements)
+    // (and whose rows, and residual rows, lie within 2^31 bytes of its first:
+    // the fast path addresses them with 32-bit buffer offsets)
+    const bool fast = m0 + BM <= p.M && n0 + BN <= p.N && (OUT == 2 || !p.accumulate) &&
+                      (int64_t)WTM * ldo * ES <= INT32_MAX &&
+                      (OUT != kOutBF16Epi || (int64_t)WTM * p.ldr * 2 <= INT32_MAX);
     // the bias of the lane's columns in the fast path below: lane chunk
     // (it * 64 + lane) % ECPR repeats with period ECPR / gcd(64, ECPR) in it
     constexpr int EP = ECPR / ((ECPR & -ECPR) < 64 ? (ECPR & -ECPR) : 64);
@@ -528,6 +536,42 @@ __global__ __launch_bounds__(WM * WN * 64 * (PROD ? 2 : 1)) void gemm_fp8_kernel
         }
     }
     (void)rtg; (void)rls;
+    // Fast-path addressing. Iteration it of a pass covers staged row r and
+    // chunk c with it * 64 + lane = r * ECPR + c. That map repeats every FP
+    // iterations, FR rows further on, and the rows' chunk swizzle every NPH
+    // such periods. So the lane parts of the LDS addresses (NPH x FP) and of
+    // the output and residual offsets (FP) are computed here, once per tile;
+    // an iteration adds a compile-time LDS offset and a wave-uniform row
+    // offset (the buffer access's scalar operand). No store then computes a
+    // 64-bit address.
+    constexpr int FP = EP;
+    constexpr int FR = 64 * FP / ECPR;
+    constexpr int NPH = (SWZ + 1) / cgcd(FR, SWZ + 1);
+    const uint32_t row_bytes = (uint32_t)(ldo * ES);
+    const uint32_t rrow_bytes = OUT == kOutBF16Epi ? (uint32_t)(p.ldr * 2) : 0u;
+    uint32_t laddr[NPH][FP], goff[FP], roff[FP];
+#pragma unroll
+    for (int vv = 0; vv < FP; ++vv) {
+        const int q = vv * 64 + lane;
+        const int rv = q / ECPR, cv = q % ECPR;
+        goff[vv] = rv * row_bytes + cv * 4 * ES;
+        roff[vv] = rv * rrow_bytes + cv * 8;
+#pragma unroll
+        for (int ph = 0; ph < NPH; ++ph) {
+            const int r = ph * FR + rv;
+            laddr[ph][vv] = r * ROWB + ((cv ^ (r & SWZ)) << 4);
+        }
+    }
+    // the wave tile's output (and residual) rows as buffers: base at its
+    // first element, range over its last row's WTN elements
+    const __amdgpu_buffer_rsrc_t rd = __builtin_amdgcn_make_buffer_rsrc(
+        OUT == 2 ? (void*)(part + (int64_t)mrow0 * p.N + ncol0)
+                 : (void*)(reinterpret_cast<uint8_t*>(p.D) + ((int64_t)mrow0 * p.ldd + ncol0) * ES),
+        0, fast ? (int)((WTM - 1) * row_bytes + WTN * ES) : 0, 0x00020000);
+    const __amdgpu_buffer_rsrc_t rres = __builtin_amdgcn_make_buffer_rsrc(
+        OUT == kOutBF16Epi && p.residual ? const_cast<uint16_t*>(p.residual + (int64_t)mrow0 * p.ldr + ncol0) : nullptr,
+        0, OUT == kOutBF16Epi && p.residual && fast ? (int)((WTM - 1) * rrow_bytes + WTN * 2) : 0, 0x00020000);
+    (void)laddr; (void)goff; (void)roff; (void)rd; (void)rres;
     __syncthreads();   // every wave is done with the last stage
     // one pass per constant: the accumulators are indexed by the pass, and a
     // loop the unroller leaves rolled would move them to scratch memory
@@ -631,54 +675,52 @@ __global__ __launch_bounds__(WM * WN * 64 * (PROD ? 2 : 1)) void gemm_fp8_kernel
             return;
         }
         if (fast) {
-            // the epilogue terms are loaded before the LDS reads of their
-            // group of iterations, so that their latency overlaps those reads
-            // and the group's stores wait once (a load issued after stores
-            // waits for them); buffer loads, so an absent term costs no
-            // branch and no traffic. Groups of at most 16 iterations keep the
-            // residual and the staged values in registers beside the
-            // accumulators of the passes still to come.
+            // the residual is loaded before the LDS reads of its group of
+            // iterations, so that its latency overlaps those reads and the
+            // group's stores wait once (a load issued after stores waits for
+            // them); an absent residual is a zero-range buffer (no branch, no
+            // traffic). Groups of at most 16 iterations keep the residual and
+            // the staged values in registers beside the accumulators of the
+            // passes still to come.
             constexpr int EG = (OUT == kOutBF16Epi && IT > 16) ? IT / 2 : IT;
-            static_assert(IT % EG == 0, "epilogue groups");
+            static_assert(IT % EG == 0 && EG % FP == 0, "epilogue groups");
 #pragma unroll
             for (int g0 = 0; g0 < IT; g0 += EG) {
                 uint2 er[OUT == kOutBF16Epi ? EG : 1];
                 if constexpr (OUT == kOutBF16Epi) {
-                    const int64_t mt = mrow0 + pass * RPP;           // the pass's first row
-                    const __amdgpu_buffer_rsrc_t rr = __builtin_amdgcn_make_buffer_rsrc(
-                        const_cast<uint16_t*>(p.residual ? p.residual + mt * p.ldr : p.residual), 0,
-                        p.residual ? (int)((RPP - 1) * p.ldr * 2 + (int64_t)(ncol0 + WTN) * 2) : 0, 0x00020000);
 #pragma unroll
                     for (int e = 0; e < EG; ++e) {
-                        const int q = (g0 + e) * 64 + lane;
-                        const int r = q / ECPR, c = q % ECPR;
+                        const int u = (g0 + e) / FP, vv = (g0 + e) % FP;
                         er[e] = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(
-                            rr, (uint32_t)((r * p.ldr + ncol0 + c * 4) * 2), 0, 0));
+                            rres, (int)roff[vv], (int)((pass * RPP + u * FR) * rrow_bytes), 0));
                     }
                 }
                 float4 v[EG];
 #pragma unroll
                 for (int e = 0; e < EG; ++e) {
-                    const int q = (g0 + e) * 64 + lane;
-                    const int r = q / ECPR, c = q % ECPR;
-                    v[e] = *reinterpret_cast<const float4*>(ep + r * ROWB + ((c ^ (r & SWZ)) << 4));
+                    const int u = (g0 + e) / FP, vv = (g0 + e) % FP, ph = u % NPH;
+                    v[e] = *reinterpret_cast<const float4*>(ep + laddr[ph][vv] + (u - ph) * FR * ROWB);
                 }
+                if constexpr (OUT != 2) {
+                    if (alpha != 1.0f) {
 #pragma unroll
-                for (int e = 0; e < EG; ++e) {
-                    const int it = g0 + e;
-                    const int q = it * 64 + lane;
-                    const int r = q / ECPR, c = q % ECPR;
-                    const int64_t m = mrow0 + pass * RPP + r;
-                    const int n = ncol0 + c * 4;
-                    float4 w = v[e];
-                    if constexpr (OUT == 2) {
-                        *reinterpret_cast<float4*>(part + m * p.N + n) = w;
-                    } else {
-                        w.x *= alpha; w.y *= alpha; w.z *= alpha; w.w *= alpha;
+                        for (int e = 0; e < EG; ++e) {
+                            v[e].x *= alpha; v[e].y *= alpha; v[e].z *= alpha; v[e].w *= alpha;
+                        }
+                    }
+                }
+                // AUX 2 is the buffer store's non-temporal bit
+                auto store_group = [&](auto nt_c) __attribute__((always_inline)) {
+                    constexpr int AUX = decltype(nt_c)::value ? 2 : 0;
+#pragma unroll
+                    for (int e = 0; e < EG; ++e) {
+                        const int u = (g0 + e) / FP, vv = (g0 + e) % FP;
+                        const int soff = (int)((pass * RPP + u * FR) * row_bytes);
+                        float4 w = v[e];
                         if constexpr (OUT == kOutBF16Epi) {
                             // each term only when given: adding +0 would turn a -0 sum into +0
                             if (p.bias) {
-                                const uint2 b = eb[it % EP];
+                                const uint2 b = eb[vv];
                                 w.x += bf16lo(b.x); w.y += bf16hi(b.x); w.z += bf16lo(b.y); w.w += bf16hi(b.y);
                             }
                             if (p.residual) {
@@ -688,26 +730,18 @@ __global__ __launch_bounds__(WM * WN * 64 * (PROD ? 2 : 1)) void gemm_fp8_kernel
                                 w.z = fmaf(rs, bf16lo(rv.y), w.z); w.w = fmaf(rs, bf16hi(rv.y), w.w);
                             }
                         }
-                        if constexpr (OUT == kOutF32) {
-                            float* dst = reinterpret_cast<float*>(p.D) + m * p.ldd + n;
-                            if (p.nt_out) {
-                                typedef float v4f __attribute__((ext_vector_type(4)));
-                                __builtin_nontemporal_store(v4f{w.x, w.y, w.z, w.w}, reinterpret_cast<v4f*>(dst));
-                            } else {
-                                *reinterpret_cast<float4*>(dst) = w;
-                            }
+                        if constexpr (ES == 4) {
+                            typedef unsigned int v4u __attribute__((ext_vector_type(4)));
+                            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4u, w), rd, (int)goff[vv], soff, AUX);
                         } else {
-                            uint16_t* dst = reinterpret_cast<uint16_t*>(p.D) + m * p.ldd + n;
-                            const uint32_t lo = pack_bf16x2(w.x, w.y), hi = pack_bf16x2(w.z, w.w);
-                            if (p.nt_out) {
-                                typedef unsigned int v2u __attribute__((ext_vector_type(2)));
-                                __builtin_nontemporal_store(v2u{lo, hi}, reinterpret_cast<v2u*>(dst));
-                            } else {
-                                *reinterpret_cast<uint2*>(dst) = make_uint2(lo, hi);
-                            }
+                            typedef unsigned int v2u __attribute__((ext_vector_type(2)));
+                            __builtin_amdgcn_raw_buffer_store_b64(v2u{pack_bf16x2(w.x, w.y), pack_bf16x2(w.z, w.w)}, rd,
+                                                                  (int)goff[vv], soff, AUX);
                         }
                     }
-                }
+                };
+                if (OUT != 2 && p.nt_out) store_group(std::true_type{});
+                else store_group(std::false_type{});
             }
             return;
         }
