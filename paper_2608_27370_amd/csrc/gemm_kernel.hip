@@ -81,7 +81,6 @@ __device__ __forceinline__ void static_for(F&& f) {
 
 constexpr int cgcd(int a, int b) { return b == 0 ? a : cgcd(b, a % b); }
 
-__device__ __forceinline__ uint32_t e8m0_of(float s) { return (__float_as_uint(s) >> 23) & 0xFFu; }
 
 
 typedef int v4i __attribute__((ext_vector_type(4)));
@@ -343,7 +342,9 @@ __global__ __launch_bounds__(WM * WN * 64 * (PROD ? 2 : 1)) void gemm_fp8_kernel
         sc_on[fi] = mode != kSTensor;
     }
     // read piece t of k step h of the slice in stage st: t < FM + FN are
-    // the operand fragments, the rest the scales
+    // the operand fragments, the rest the scales (their raw binary32 bits:
+    // scales_e8m0 turns them into the instruction's operands once they have
+    // landed, so that no read waits on its own result)
     constexpr int NPIECE = (FM + FN) * (GROUPED ? 2 : 1);
     auto read_piece = [&](Frags& f, int st, int h, int t) __attribute__((always_inline)) {
         if (t < FM + FN) {
@@ -355,8 +356,15 @@ __global__ __launch_bounds__(WM * WN * 64 * (PROD ? 2 : 1)) void gemm_fp8_kernel
             f.f[t] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
         } else {
             const int fi = t - (FM + FN);
-            const uint32_t e = e8m0_of(ssc[st * (BM + BN) + sc_off[fi]]);
-            f.sc[fi] = sc_on[fi] ? e : 127u;
+            f.sc[fi] = __float_as_uint(ssc[st * (BM + BN) + sc_off[fi]]);
+        }
+    };
+    // the E8M0 exponent of each scale (127, a factor of 1, for a per-tensor
+    // scaled operand, whose factor the epilogue applies)
+    auto scales_e8m0 = [&](Frags& f) __attribute__((always_inline)) {
+        if constexpr (GROUPED) {
+#pragma unroll
+            for (int fi = 0; fi < FM + FN; ++fi) f.sc[fi] = sc_on[fi] ? (f.sc[fi] >> 23) & 0xFFu : 127u;
         }
     };
     auto mfma_one = [&](const Frags& f, int t) __attribute__((always_inline)) {
@@ -409,15 +417,30 @@ __global__ __launch_bounds__(WM * WN * 64 * (PROD ? 2 : 1)) void gemm_fp8_kernel
         const int rst = last ? (sl + 1 - s0) % NST : st;   // stage and k step read into nxt
         const int rh = last ? 0 : h + 1;
         const bool refill = sl + NST < s1;
-        // read piece u goes after MFMA u * NMFMA / NPIECE, DMA load q after
-        // MFMA q * NMFMA / LOADS (constant loop bounds, so that everything
-        // unrolls and the fragments stay in registers)
+        // fragment read u goes after MFMA u * NMFMA / NPIECE (the first half
+        // of the step), DMA load q after MFMA q * NMFMA / LOADS (constant loop
+        // bounds, so that everything unrolls and the fragments stay in
+        // registers). A slice's k steps share its scales (one 128-wide k
+        // block): the last step reads the next slice's, two after each of
+        // MFMAs NMFMA / 2 .. NMFMA / 2 + 3, and makes them operands after its
+        // last MFMA; the other steps pass theirs on.
+        if constexpr (GROUPED) {
+            if (!last) {
+#pragma unroll
+                for (int fi = 0; fi < FM + FN; ++fi) nxt.sc[fi] = cur.sc[fi];
+            }
+        }
 #pragma unroll
         for (int t = 0; t < NMFMA; ++t) {
             mfma_one(cur, t);
 #pragma unroll
-            for (int u = 0; u < NPIECE; ++u)
+            for (int u = 0; u < FM + FN; ++u)
                 if (u * NMFMA / NPIECE == t) read_piece(nxt, rst, rh, u);
+            if (last) {
+#pragma unroll
+                for (int u = FM + FN; u < NPIECE; ++u)
+                    if (NMFMA / 2 + (u - FM - FN) / 2 == t) read_piece(nxt, rst, rh, u);
+            }
             if (last && !PROD) {
 #pragma unroll
                 for (int q = 0; q < LOADS; ++q)
@@ -425,6 +448,7 @@ __global__ __launch_bounds__(WM * WN * 64 * (PROD ? 2 : 1)) void gemm_fp8_kernel
             }
             __builtin_amdgcn_sched_barrier(0);
         }
+        if (last) scales_e8m0(nxt);
     };
 
     // prologue: slices s0 .. s0 + NST - 1 in flight, then k step 0 of slice s0 read
@@ -457,6 +481,7 @@ __global__ __launch_bounds__(WM * WN * 64 * (PROD ? 2 : 1)) void gemm_fp8_kernel
     Frags F0, F1;
 #pragma unroll
     for (int t = 0; t < NPIECE; ++t) read_piece(F0, 0, 0, t);
+    scales_e8m0(F0);
     if constexpr (KH == 2) {
         for (int sl = s0; sl < s1; ++sl) {
             step(sl, 0, F0, F1);
