@@ -118,14 +118,12 @@ Plan make_plan(int64_t M, int64_t N, int64_t K, bool grouped, int batch = 1, boo
 }
 
 // Tile rows per group of an XCD's contiguous range of tiles (the order in
-// which that XCD's CUs take them): 4 by default (the QKV Wgrad's 24-tile
-// ranges become 4 x 6 tiles, 10 operand panels per XCD instead of 11 at 8).
-// Short reductions over many tile columns take 2: their K panels are small,
-// and the gate/up projection's Fprop (16384 x 17920 x 1536) measured 10%
-// faster than at 4 (1 to 8 and 16 rows measured, results bitwise the same).
-int plan_group_rows(int64_t K, int tiles_n) {
-    return (K <= 2048 && tiles_n >= 32) ? 2 : 4;
-}
+// which that XCD's CUs take them): 4 (the QKV Wgrad's 24-tile ranges become
+// 4 x 6 tiles, 10 operand panels per XCD instead of 11 at 8). On the
+// 28-layer step with the workload's operands, groups of 2 and 8 rows for
+// the short reductions over many tile columns (the gate/up Fprop, the down
+// Dgrad) measured 1% slower than 4 (results bitwise the same).
+constexpr int kGroupRows = 4;
 
 size_t plan_workspace_bytes(int64_t M, int64_t N, const Plan& pl, int batch = 1) {
     if (pl.splits <= 1) return 0;
@@ -169,7 +167,7 @@ void run_plan(const GemmProblem& g, const Plan& pl, void* ws, hipStream_t stream
     prm.tiles_m = (int)((g.M + t.bm - 1) / t.bm);
     prm.tiles_n = (int)((g.N + t.bn - 1) / t.bn);
     prm.accumulate = g.accumulate;
-    prm.gm = plan_group_rows(g.K * eb, prm.tiles_n);
+    prm.gm = kGroupRows;
     prm.alpha = g.alpha;
     prm.bias = g.bias;
     prm.residual = g.residual;
