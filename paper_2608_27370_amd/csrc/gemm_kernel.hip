@@ -561,6 +561,89 @@ __global__ __launch_bounds__(WM * WN * 64 * (PROD ? 2 : 1)) void gemm_fp8_kernel
         }
     }
     (void)rtg; (void)rls;
+    __syncthreads();   // every wave is done with the last stage
+    // A plain BF16 output of a tile inside the matrix, 128-column wave tiles:
+    // the lane rounds its sums to BF16 first and stages those, half the LDS
+    // bytes of the binary32 staging below, and the whole wave tile fits its
+    // region in one pass. Staged row r is 256 bytes, 32 units of 8 bytes
+    // (four columns), and unit u sits at position u ^ 2 (r & 15): the two
+    // units of each 16-byte chunk stay side by side and in order, so a chunk
+    // reads back with one 16-byte load and leaves with one 16-byte store (a
+    // store covers four whole rows); a chunk's position in its row depends
+    // on r & 15, so the 16 lanes of a read phase, one row's 16 chunks, hit
+    // distinct banks.
+    if constexpr (OUT == kOutBF16 && ECPR == 32 && WTM * 256 <= REGION) {
+        if (fast) {
+            auto stage = [&](auto scaled) __attribute__((always_inline)) {
+#pragma unroll
+                for (int i = 0; i < FM; ++i) {
+                    const int r = i * 32 + (lane & 31);
+#pragma unroll
+                    for (int j = 0; j < FN; ++j) {
+#pragma unroll
+                        for (int g = 0; g < 4; ++g) {
+                            // read at the point of use (a copy the compiler
+                            // may not hoist): otherwise it moves accumulators
+                            // to VGPRs ahead of the branch, and spills
+                            float v0, v1, v2, v3;
+                            asm volatile("v_accvgpr_read_b32 %0, %1" : "=v"(v0) : "a"(acc[i][j][4 * g]));
+                            asm volatile("v_accvgpr_read_b32 %0, %1" : "=v"(v1) : "a"(acc[i][j][4 * g + 1]));
+                            asm volatile("v_accvgpr_read_b32 %0, %1" : "=v"(v2) : "a"(acc[i][j][4 * g + 2]));
+                            asm volatile("v_accvgpr_read_b32 %0, %1" : "=v"(v3) : "a"(acc[i][j][4 * g + 3]));
+                            if constexpr (decltype(scaled)::value) {
+                                v0 *= alpha; v1 *= alpha; v2 *= alpha; v3 *= alpha;
+                            }
+                            const int u = j * 8 + 2 * g + (lane >> 5);
+                            *reinterpret_cast<uint2*>(ep + r * 256 + ((u ^ (2 * (r & 15))) << 3)) =
+                                make_uint2(pack_bf16x2(v0, v1), pack_bf16x2(v2, v3));
+                        }
+                        // one fragment at a time: otherwise every accumulator
+                        // is read into VGPRs before the first write
+                        __builtin_amdgcn_sched_barrier(0);
+                    }
+                }
+            };
+            if (alpha == 1.0f) stage(std::false_type{});
+            else stage(std::true_type{});
+            // the region belongs to this wave alone
+            asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+            // iteration it: lane l takes chunk l & 15 of staged row 4 it + (l >> 4);
+            // (r & 15) repeats every 4 iterations, so four lane addresses serve
+            // all of them with compile-time offsets
+            typedef unsigned int v4u __attribute__((ext_vector_type(4)));
+            const int rl = lane >> 4, cl = lane & 15;
+            uint32_t la[4];
+#pragma unroll
+            for (int ph = 0; ph < 4; ++ph) {
+                const int r = 4 * ph + rl;
+                la[ph] = r * 256 + ((cl ^ (r & 15)) << 4);
+            }
+            const uint32_t row_bytes = (uint32_t)(p.ldd * 2);
+            const __amdgpu_buffer_rsrc_t rd = __builtin_amdgcn_make_buffer_rsrc(
+                reinterpret_cast<uint8_t*>(p.D) + ((int64_t)mrow0 * p.ldd + ncol0) * 2, 0,
+                (int)((WTM - 1) * row_bytes + WTN * 2), 0x00020000);
+            const int voff = (int)(rl * row_bytes + cl * 16);
+            constexpr int IT16 = WTM / 4, EG16 = 4;
+            auto store_all = [&](auto nt_c) __attribute__((always_inline)) {
+                constexpr int AUX = decltype(nt_c)::value ? 2 : 0;   // 2: the non-temporal bit
+#pragma unroll
+                for (int g0 = 0; g0 < IT16; g0 += EG16) {
+                    v4u d[EG16];
+#pragma unroll
+                    for (int e = 0; e < EG16; ++e) {
+                        const int it = g0 + e, ph = it % 4;
+                        d[e] = *reinterpret_cast<const v4u*>(ep + la[ph] + (it - ph) * 4 * 256);
+                    }
+#pragma unroll
+                    for (int e = 0; e < EG16; ++e)
+                        __builtin_amdgcn_raw_buffer_store_b128(d[e], rd, voff, (int)((g0 + e) * 4 * row_bytes), AUX);
+                }
+            };
+            if (p.nt_out) store_all(std::true_type{});
+            else store_all(std::false_type{});
+            return;
+        }
+    }
     // Fast-path addressing. Iteration it of a pass covers staged row r and
     // chunk c with it * 64 + lane = r * ECPR + c. That map repeats every FP
     // iterations, FR rows further on, and the rows' chunk swizzle every NPH
@@ -597,7 +680,6 @@ __global__ __launch_bounds__(WM * WN * 64 * (PROD ? 2 : 1)) void gemm_fp8_kernel
         OUT == kOutBF16Epi && p.residual ? const_cast<uint16_t*>(p.residual + (int64_t)mrow0 * p.ldr + ncol0) : nullptr,
         0, OUT == kOutBF16Epi && p.residual && fast ? (int)((WTM - 1) * rrow_bytes + WTN * 2) : 0, 0x00020000);
     (void)laddr; (void)goff; (void)roff; (void)rd; (void)rres;
-    __syncthreads();   // every wave is done with the last stage
     // one pass per constant: the accumulators are indexed by the pass, and a
     // loop the unroller leaves rolled would move them to scratch memory
     static_for<WTM / RPP>([&](auto pass_c) __attribute__((always_inline)) {
