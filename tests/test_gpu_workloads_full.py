@@ -102,7 +102,9 @@ def check_entries(D, out, ms, ns, A, B, what, strict=False):
     op = A[:4] + B[:4]
     K = A[0].shape[1]
     ref, den = gemm.gemm_entries(am, bn, *op)
-    slack = mfma_model.truncation_loss(am, bn, *op, chunk=max(16, (1 << 24) // max(K, 1)))
+    # with ``strict`` the plain bound is asserted, which implies the widened
+    # one: the truncation model (the costly part over long reductions) is skipped
+    slack = 0.0 if strict else mfma_model.truncation_loss(am, bn, *op, chunk=max(16, (1 << 24) // max(K, 1)))
     if out == "fp32":
         check_fp32(host(D)[ms, ns], ref, den, what=what, slack=slack, strict=strict)
     else:
@@ -113,7 +115,7 @@ def uniq(a):
     return np.unique(np.asarray(a, dtype=np.int64))
 
 
-def run_tensor_layer(P, X, W, dY, dyf, what, full_limit=9000, strict=()):
+def run_tensor_layer(P, X, W, dY, dyf, what, full_limit=20000, strict=()):
     """Per-tensor linear fwd + bwd on the GPU, checked against the oracle on
     samples. X [M, K], W [N, K], dY [M, N] BF16 bits. ``strict`` names the
     outputs ("Y", "dX", "dW") on which the plain bound max|err| / sum|ab| <=
@@ -197,7 +199,9 @@ def test_lm_head_8192x151936x1536(P):
 def run_block_layer(P, X, W, dY, what, rule="pow2", strict=False):
     """Blockwise linear fwd + bwd (E4M3 throughout, power-of-two `rule`) on
     the GPU, checked against the oracle: W's blocks whole, X's column groups
-    and dY's row and column groups on sampled rows, GEMM outputs on samples."""
+    and dY's row and column groups on sampled rows, GEMM outputs on samples
+    (with ``strict`` also every entry of each output's first and last
+    256 x 256 block)."""
     M, K = X.shape
     N = W.shape[0]
     rnd = P.SCALE_POW2 if rule == "pow2" else P.SCALE_POW2_FLOOR
@@ -232,13 +236,13 @@ def run_block_layer(P, X, W, dY, what, rule="pow2", strict=False):
     Wb = (wq, "e4m3", ws, "block", None)
     WbT = (wqT, "e4m3", wsT, "block", None)
     # Fprop Y [M, N] = Xq(1x128) Wq(128x128)^T
-    ms, ns = sample_sparse(M, N, g, full=False)
+    ms, ns = sample_sparse(M, N, g, full=bool(strict))
     check_entries(Y, "bf16", ms, ns, group_rows(X, uniq(ms), "e4m3", rule), Wb, what + " Y", strict)
     # Dgrad dX [M, K] = dYq(1x128) WqT(128x128)^T
-    ms, ks = sample_sparse(M, K, g, full=False)
+    ms, ks = sample_sparse(M, K, g, full=bool(strict))
     check_entries(dX, "bf16", ms, ks, group_rows(dY, uniq(ms), "e4m3", rule), WbT, what + " dX", strict)
     # Wgrad dW [N, K] = dYqT(128x1) XqT(128x1)^T
-    ns, ks = sample_sparse(N, K, g, full=False)
+    ns, ks = sample_sparse(N, K, g, full=bool(strict))
     check_entries(dW, "fp32", ns, ks, group_cols(dY, uniq(ns), "e4m3", rule),
                   group_cols(X, uniq(ks), "e4m3", rule), what + " dW", strict)
 
