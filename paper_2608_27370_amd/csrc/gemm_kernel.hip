@@ -572,8 +572,23 @@ __global__ __launch_bounds__(WM * WN * 64 * (PROD ? 2 : 1)) void gemm_fp8_kernel
     // store covers four whole rows); a chunk's position in its row depends
     // on r & 15, so the 16 lanes of a read phase, one row's 16 chunks, hit
     // distinct banks.
-    if constexpr (OUT == kOutBF16 && ECPR == 32 && WTM * 256 <= REGION) {
+    // The LM head's backward output (dz of the logits) takes the same path:
+    // each lane forms dz = g (exp(z - lse) - [column == target]) from its
+    // sums directly, with the lse and target column of its FM rows loaded
+    // first, and rounds it to BF16, as the per-row path below does.
+    if constexpr ((OUT == kOutBF16 || OUT == kOutSoftmaxGrad) && ECPR == 32 && WTM * 256 <= REGION) {
         if (fast) {
+            float row_lse[OUT == kOutSoftmaxGrad ? FM : 1];
+            int row_tgt[OUT == kOutSoftmaxGrad ? FM : 1];
+            if constexpr (OUT == kOutSoftmaxGrad) {
+#pragma unroll
+                for (int i = 0; i < FM; ++i) {
+                    const int64_t m = (int64_t)mrow0 + i * 32 + (lane & 31);
+                    row_tgt[i] = p.targets[m] - p.col0;
+                    row_lse[i] = p.lse[m];
+                }
+            }
+            (void)row_lse; (void)row_tgt;
             auto stage = [&](auto scaled) __attribute__((always_inline)) {
 #pragma unroll
                 for (int i = 0; i < FM; ++i) {
@@ -592,6 +607,16 @@ __global__ __launch_bounds__(WM * WN * 64 * (PROD ? 2 : 1)) void gemm_fp8_kernel
                             asm volatile("v_accvgpr_read_b32 %0, %1" : "=v"(v3) : "a"(acc[i][j][4 * g + 3]));
                             if constexpr (decltype(scaled)::value) {
                                 v0 *= alpha; v1 *= alpha; v2 *= alpha; v3 *= alpha;
+                            }
+                            if constexpr (OUT == kOutSoftmaxGrad) {
+                                // the columns of these four sums, in the chunk
+                                const int n = ncol0 + j * 32 + 8 * g + 4 * (lane >> 5);
+                                const float l = row_lse[i], gs = p.grad_scale;
+                                const int tc = row_tgt[i];
+                                v0 = gs * (exp_f32(v0 - l) - (n == tc ? 1.0f : 0.0f));
+                                v1 = gs * (exp_f32(v1 - l) - (n + 1 == tc ? 1.0f : 0.0f));
+                                v2 = gs * (exp_f32(v2 - l) - (n + 2 == tc ? 1.0f : 0.0f));
+                                v3 = gs * (exp_f32(v3 - l) - (n + 3 == tc ? 1.0f : 0.0f));
                             }
                             const int u = j * 8 + 2 * g + (lane >> 5);
                             *reinterpret_cast<uint2*>(ep + r * 256 + ((u ^ (2 * (r & 15))) << 3)) =
