@@ -374,8 +374,10 @@ puro_status puro_linear_bwd(const uint16_t* dY, const puro_linear_saved* saved,
  * The logits are never stored: the forward reduces each 128-column block of
  * the GEMM's output tile to (max, sum exp) in its epilogue; the backward
  * recomputes the logits in chunks of 16384 vocabulary columns and writes only
- * the chunk's dz (BF16) to the workspace. g is the loss's upstream gradient
- * (1 for the sum over tokens, 1/M for their mean).
+ * the chunk's dz to the workspace (BF16; under PURO_LM_HEAD_FP8 its E4M3
+ * copies, in 1x128 row and 128x1 column groups, made in the same epilogue).
+ * g is the loss's upstream gradient (1 for the sum over tokens, 1/M for
+ * their mean).
  * Recipes: PURO_LM_HEAD_BF16 (BF16 GEMMs with binary32 accumulation, dz
  * rounded to BF16), PURO_LM_HEAD_FP8 (Section 3.2's blockwise recipe: X in
  * 1x128 groups, W in 128x128 blocks, each dz chunk rounded to BF16 and then

@@ -185,6 +185,26 @@ __device__ __forceinline__ uint2 encode8(const uint32_t w[4], float r) {
     return out;
 }
 
+// Encode with one multiplier per column of the 8x8 block (column-grouped scales).
+template <int FMT, bool SAFE>
+__device__ __forceinline__ uint2 encode8_cols(const uint32_t w[4], const float r[8]) {
+    float v[8];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        v[2 * i] = bf16lo(w[i]) * r[2 * i];
+        v[2 * i + 1] = bf16hi(w[i]) * r[2 * i + 1];
+    }
+    uint2 out;
+    if constexpr (SAFE) {
+        out.x = encode4_safe<FMT>(v[0], v[1], v[2], v[3]);
+        out.y = encode4_safe<FMT>(v[4], v[5], v[6], v[7]);
+    } else {
+        out.x = encode4_fast<FMT>(v[0], v[1], v[2], v[3]);
+        out.y = encode4_fast<FMT>(v[4], v[5], v[6], v[7]);
+    }
+    return out;
+}
+
 // Codes of the 8 BF16 values of w divided by the power of two s, one
 // v_cvt_scalef32_pk_{fp8,bf8}_bf16 per pair: the instruction rounds x / s
 // exactly as v_cvt_pk_{fp8,bf8}_f32 rounds it (the same codes as encode8

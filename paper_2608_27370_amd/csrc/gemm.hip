@@ -181,6 +181,7 @@ void run_plan(const GemmProblem& g, const Plan& pl, void* ws, hipStream_t stream
     prm.targets = g.targets; prm.col0 = g.col0;
     prm.stats = g.stats; prm.stats_ld = g.stats_ld; prm.zt = g.zt;
     prm.lse = g.lse; prm.grad_scale = g.grad_scale;
+    prm.q8 = g.q8; prm.q8_scale = g.q8_scale; prm.q8t = g.q8t; prm.q8t_scale = g.q8t_scale;
     const bool grouped = grouped_scales(g);
     const int out = pl.splits > 1 ? 2 : g.out;
     const int grid = (g.upper ? prm.tiles_m * (prm.tiles_m + 1) / 2 : prm.tiles_m * prm.tiles_n) * pl.splits * g.batch;
@@ -244,7 +245,7 @@ void gemm_plan(int64_t M, int64_t N, int64_t K, bool grouped, int* tile_m, int* 
 
 void launch_gemm(const GemmProblem& g, void* ws, hipStream_t stream) {
     const int64_t kb = g.K * elem_bytes(g);
-    if (g.out == kOutLseStats || g.out == kOutSoftmaxGrad) {
+    if (g.out == kOutLseStats || g.out == kOutSoftmaxGrad || g.out == kOutSoftmaxGradQ) {
         // the LM-head epilogues reduce over 128-column wave tiles: the
         // 256 x 256 configuration, unsplit
         run_plan(g, Plan{0, 1, (int)((kb + kBK - 1) / kBK)}, ws, stream);
@@ -254,7 +255,7 @@ void launch_gemm(const GemmProblem& g, void* ws, hipStream_t stream) {
 }
 
 int gemm_tile(const GemmProblem& g) {
-    if (g.out == kOutLseStats || g.out == kOutSoftmaxGrad) return kTiles[0].bm;
+    if (g.out == kOutLseStats || g.out == kOutSoftmaxGrad || g.out == kOutSoftmaxGradQ) return kTiles[0].bm;
     return kTiles[make_plan(g.M, g.N, g.K * elem_bytes(g), grouped_scales(g), g.batch, g.upper != 0).cfg].bm;
 }
 

@@ -49,6 +49,10 @@ struct Params {
     float* zt;                 // [M]: the target's logit
     const float* lse;          // [M]
     float grad_scale;
+    uint8_t* q8;               // kOutSoftmaxGradQ: dz's FP8 copies (the GemmProblem fields)
+    float* q8_scale;
+    uint8_t* q8t;
+    float* q8t_scale;
 };
 
 struct TileCfg {

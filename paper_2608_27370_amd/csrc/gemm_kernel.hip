@@ -124,6 +124,139 @@ __device__ __forceinline__ void dma_to_lds(v4i rsrc, uint32_t lds, uint32_t voff
                      : "=&s"(saved) : "s"(lds), "v"(voff), "s"(rsrc) : "memory");
 }
 
+// dz's E4M3 copies from a wave's staged 128 x 128 BF16 tile (row r at
+// ep + 256 r, its 16-byte chunk c at position c ^ (r & 15)), for the LM
+// head's backward: the same codes and power-of-two scales as the 1x128 +
+// 128x1 quantiser gives for that BF16 dz (its groups are 128-aligned, so
+// each lies in one wave tile), written where the dX and dW GEMMs read them.
+//  * rows: lane l quantises staged rows l and l + 64, each one 1x128 group;
+//  * columns: lane l takes 8 columns (chunk c = l & 15) over the row blocks
+//    of 8 rows b = (l >> 4) + 4 k; the 4 lanes of a chunk share the column
+//    maxima through two shuffles, each 8 x 8 block is transposed in
+//    registers and its 8 columns' codes go to the transposed copy.
+__device__ __forceinline__ void quantize_staged_dz(const Params& p, const uint8_t* ep, int64_t mrow0, int64_t ncol0,
+                                                   int lane) {
+    typedef unsigned int v4u __attribute__((ext_vector_type(4)));
+    constexpr int F = kE4M3;
+    const int64_t M = p.M, N = p.N;
+    auto chunk = [&](int r, int c) __attribute__((always_inline)) {
+        return *reinterpret_cast<const v4u*>(ep + r * 256 + ((c ^ (r & 15)) << 4));
+    };
+    // ---- rows
+    const __amdgpu_buffer_rsrc_t rq =
+        __builtin_amdgcn_make_buffer_rsrc(p.q8 + mrow0 * N + ncol0, 0, (int)(127 * N + 128), 0x00020000);
+#pragma unroll
+    for (int rr = 0; rr < 2; ++rr) {
+        const int r = lane + 64 * rr;
+        uint32_t w[16][4];
+        uint32_t m = 0;
+#pragma unroll
+        for (int c = 0; c < 16; ++c) {
+            const v4u v = chunk(r, c);
+            w[c][0] = v.x; w[c][1] = v.y; w[c][2] = v.z; w[c][3] = v.w;
+            m = max(m, absmax_bits8(w[c]));
+        }
+        float s;
+        uint2 q[16];
+        if (m <= 0x7F7Fu) {
+            const int e = pow2_exponent_bf16<F>(m);
+            s = exp2i(e);
+            if (e > -127) {
+#pragma unroll
+                for (int c = 0; c < 16; ++c) q[c] = encode8_pow2<F>(w[c], s);
+            } else {
+#pragma unroll
+                for (int c = 0; c < 16; ++c) q[c] = encode8<F, false>(w[c], exp2i(-e));
+            }
+        } else {
+            // an infinity: the largest scale, saturated codes; a NaN: NaN scale and codes
+            const bool inf = m == 0x7F80u;
+            s = inf ? exp2i(127) : __uint_as_float(0x7FC00000u);
+            const float rinv = inf ? exp2i(-127) : s;
+#pragma unroll
+            for (int c = 0; c < 16; ++c) q[c] = encode8<F, true>(w[c], rinv);
+        }
+#pragma unroll
+        for (int c = 0; c < 16; c += 2)
+            __builtin_amdgcn_raw_buffer_store_b128(v4u{q[c].x, q[c].y, q[c + 1].x, q[c + 1].y}, rq,
+                                                   (int)(r * N + c * 8), 0, 0);
+        p.q8_scale[(ncol0 / 128) * M + mrow0 + r] = s;
+    }
+    // ---- columns
+    const int cb = lane & 15, b0 = lane >> 4;
+    uint32_t cm[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const v4u v = chunk((b0 + 4 * k) * 8 + i, cb);
+            cm[0] = pk_max_u16(cm[0], mag2(v.x)); cm[1] = pk_max_u16(cm[1], mag2(v.y));
+            cm[2] = pk_max_u16(cm[2], mag2(v.z)); cm[3] = pk_max_u16(cm[3], mag2(v.w));
+        }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        cm[j] = pk_max_u16(cm[j], (uint32_t)__shfl_xor((int)cm[j], 16, 64));
+        cm[j] = pk_max_u16(cm[j], (uint32_t)__shfl_xor((int)cm[j], 32, 64));
+    }
+    float scol[8], rcol[8];
+    bool finite = true, normal = true;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        const uint32_t m = (j & 1) ? (cm[j >> 1] >> 16) : (cm[j >> 1] & 0xFFFFu);
+        if (m <= 0x7F7Fu) {
+            const int e = pow2_exponent_bf16<F>(m);
+            scol[j] = exp2i(e);
+            rcol[j] = exp2i(-e);
+            normal = normal && e > -127;
+        } else if (m == 0x7F80u) {
+            scol[j] = exp2i(127);
+            rcol[j] = exp2i(-127);
+            finite = false;
+        } else {
+            scol[j] = rcol[j] = __uint_as_float(0x7FC00000u);
+            finite = false;
+        }
+    }
+    // the transposed copy's rows ncol0 + 8 cb + j hold columns mrow0 + 8 b + (0..7)
+    const __amdgpu_buffer_rsrc_t rt =
+        __builtin_amdgcn_make_buffer_rsrc(p.q8t + ncol0 * M + mrow0, 0, (int)(127 * M + 128), 0x00020000);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        const int b = b0 + 4 * k;
+        uint32_t w[8][4];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const v4u v = chunk(b * 8 + i, cb);
+            w[i][0] = v.x; w[i][1] = v.y; w[i][2] = v.z; w[i][3] = v.w;
+        }
+        uint2 ct[8];
+        if (finite && normal) {
+            uint32_t wt[8][4];
+            transpose8x8_b16(w, wt);
+#pragma unroll
+            for (int j = 0; j < 8; ++j) ct[j] = encode8_pow2<F>(wt[j], scol[j]);
+        } else {
+            uint2 c[8];
+            if (finite) {
+#pragma unroll
+                for (int i = 0; i < 8; ++i) c[i] = encode8_cols<F, false>(w[i], rcol);
+            } else {
+#pragma unroll
+                for (int i = 0; i < 8; ++i) c[i] = encode8_cols<F, true>(w[i], rcol);
+            }
+            transpose8x8(c, ct);
+        }
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+            __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(unsigned int __attribute__((ext_vector_type(2))), ct[j]),
+                                                  rt, (int)((cb * 8 + j) * M + b * 8), 0, 0);
+    }
+    if (b0 == 0) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) p.q8t_scale[(mrow0 / 128) * N + ncol0 + cb * 8 + j] = scol[j];
+    }
+}
+
 // PROD: the workgroup has NW more waves that only issue the global->LDS
 // loads (producers); the NW MFMA waves (consumers) then only read LDS and
 // multiply, so a load that cannot issue (the texture unit's queue full)
@@ -576,11 +709,18 @@ __global__ __launch_bounds__(WM * WN * 64 * (PROD ? 2 : 1)) void gemm_fp8_kernel
     // each lane forms dz = g (exp(z - lse) - [column == target]) from its
     // sums directly, with the lse and target column of its FM rows loaded
     // first, and rounds it to BF16, as the per-row path below does.
-    if constexpr ((OUT == kOutBF16 || OUT == kOutSoftmaxGrad) && ECPR == 32 && WTM * 256 <= REGION) {
-        if (fast) {
-            float row_lse[OUT == kOutSoftmaxGrad ? FM : 1];
-            int row_tgt[OUT == kOutSoftmaxGrad ? FM : 1];
-            if constexpr (OUT == kOutSoftmaxGrad) {
+    // kOutSoftmaxGradQ stages dz the same way and quantises the staged tile
+    // (below); M and N are multiples of 128, so a wave tile lies wholly
+    // inside the output or wholly outside it.
+    constexpr bool kDz = OUT == kOutSoftmaxGrad || OUT == kOutSoftmaxGradQ;
+    if constexpr ((OUT == kOutBF16 || kDz) && ECPR == 32 && WTM * 256 <= REGION) {
+        if constexpr (OUT == kOutSoftmaxGradQ) {
+            if (mrow0 + WTM > p.M || ncol0 + WTN > p.N) return;
+        }
+        if (OUT == kOutSoftmaxGradQ || fast) {
+            float row_lse[kDz ? FM : 1];
+            int row_tgt[kDz ? FM : 1];
+            if constexpr (kDz) {
 #pragma unroll
                 for (int i = 0; i < FM; ++i) {
                     const int64_t m = (int64_t)mrow0 + i * 32 + (lane & 31);
@@ -608,7 +748,7 @@ __global__ __launch_bounds__(WM * WN * 64 * (PROD ? 2 : 1)) void gemm_fp8_kernel
                             if constexpr (decltype(scaled)::value) {
                                 v0 *= alpha; v1 *= alpha; v2 *= alpha; v3 *= alpha;
                             }
-                            if constexpr (OUT == kOutSoftmaxGrad) {
+                            if constexpr (kDz) {
                                 // the columns of these four sums, in the chunk
                                 const int n = ncol0 + j * 32 + 8 * g + 4 * (lane >> 5);
                                 const float l = row_lse[i], gs = p.grad_scale;
@@ -632,6 +772,10 @@ __global__ __launch_bounds__(WM * WN * 64 * (PROD ? 2 : 1)) void gemm_fp8_kernel
             else stage(std::true_type{});
             // the region belongs to this wave alone
             asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+            if constexpr (OUT == kOutSoftmaxGradQ) {
+                quantize_staged_dz(p, ep, mrow0, ncol0, lane);
+                return;
+            }
             // iteration it: lane l takes chunk l & 15 of staged row 4 it + (l >> 4);
             // (r & 15) repeats every 4 iterations, so four lane addresses serve
             // all of them with compile-time offsets
@@ -949,6 +1093,10 @@ void launch_tile(const Params& prm, int out, int grid, hipStream_t stream) {
             if (out == kOutLseStats) launch_cfg<BM, BN, WM, WN, SL, NST, PROD, FA, FB, GROUPED, kOutLseStats>(prm, grid, stream);
             else launch_cfg<BM, BN, WM, WN, SL, NST, PROD, FA, FB, GROUPED, kOutSoftmaxGrad>(prm, grid, stream);
         }
+    } else if (out == kOutSoftmaxGradQ) {
+        // the blockwise E4M3 recipe's backward, 128 x 128 wave tiles
+        if constexpr (FA == kE4M3 && FB == kE4M3 && GROUPED && BM / WM == 128 && BN / WN == 128)
+            launch_cfg<BM, BN, WM, WN, SL, NST, PROD, FA, FB, GROUPED, kOutSoftmaxGradQ>(prm, grid, stream);
     } else launch_cfg<BM, BN, WM, WN, SL, NST, PROD, FA, FB, GROUPED, kOutBF16>(prm, grid, stream);
 }
 

@@ -101,8 +101,12 @@ enum ScaleMode : int { kSTensor = 0, kSRow = 1, kSBlock = 2, kSNone = 3 };
 // sums of a split-K plan are kind 2, internal to the GEMM). The LM-head
 // kinds replace the output store: kOutLseStats writes per row and 128-column
 // block (max, sum of exp(z - max)) and the target's logit; kOutSoftmaxGrad
-// writes BF16 dz = g (exp(z - lse) - [column == target]).
-enum OutKind : int { kOutBF16 = 0, kOutF32 = 1, kOutBF16Epi = 3, kOutLseStats = 4, kOutSoftmaxGrad = 5 };
+// writes BF16 dz = g (exp(z - lse) - [column == target]); kOutSoftmaxGradQ
+// writes that dz's E4M3 copies instead, in 1x128 row groups and (transposed)
+// 128x1 column groups with power-of-two scales, as the quantiser makes them
+// from the BF16 dz (E4M3 block-scaled operands; M and N multiples of 128).
+enum OutKind : int { kOutBF16 = 0, kOutF32 = 1, kOutBF16Epi = 3, kOutLseStats = 4, kOutSoftmaxGrad = 5,
+                     kOutSoftmaxGradQ = 6 };
 
 // K, lda and ldb count operand elements (FP8 codes, or BF16 values when fa
 // and fb are kBF16, with scale modes kSNone).
@@ -154,6 +158,13 @@ struct GemmProblem {
     float* zt;
     const float* lse;
     float grad_scale;
+    // kOutSoftmaxGradQ: dz's row-grouped codes [M, N] (ld N) with scales
+    // [N / 128][M], and its transposed column-grouped codes [N, M] (ld M)
+    // with scales [M / 128][N] (scale arrays k-block-major)
+    uint8_t* q8 = nullptr;
+    float* q8_scale = nullptr;
+    uint8_t* q8t = nullptr;
+    float* q8t_scale = nullptr;
 };
 
 // Workspace the GEMM needs for split-K partial sums (0 when it runs unsplit);

@@ -20,8 +20,9 @@
 // GEMMs read, X^T and W^T, are made once per call), or the blockwise FP8
 // recipe of Section 3.2: X in 1x128 groups (rows for the logits, columns for
 // dW), W in 128x128 blocks (the transposed copy for dX shares the block
-// scales), and each dz chunk quantised in 1x128 + 128x1 groups by the
-// quantiser; E4M3 with power-of-two scales.
+// scales), and each dz chunk quantised in 1x128 + 128x1 groups (by the
+// chunk GEMM's epilogue, from the BF16 dz it forms, as the quantiser would);
+// E4M3 with power-of-two scales.
 
 #include <math.h>
 
@@ -126,7 +127,8 @@ static LmLayout lm_layout(int64_t M, int64_t V, int64_t K, int fp8, bool bwd) {
     }
     size_t g = 0;
     if (bwd) {
-        l.dz = c.take((size_t)M * Vc * 2);
+        // the FP8 recipe's chunk GEMM writes dz's E4M3 copies directly
+        if (!fp8) l.dz = c.take((size_t)M * Vc * 2);
         if (fp8) {
             l.dzq = c.take((size_t)M * Vc);
             l.dzs = c.take((size_t)M * (Vc / 128) * 4);
@@ -232,24 +234,23 @@ void launch_lm_head_bwd(const uint16_t* X, const uint16_t* W, const int32_t* tar
     void* gws = w8 + l.gemm;
     for (int64_t c0 = 0; c0 < V; c0 += Vc) {
         const int64_t n = (V - c0) < Vc ? (V - c0) : Vc;
-        // dz of the chunk's columns: the logits recomputed, the gradient written as BF16 [M, n]
-        GemmProblem g = logits_problem(X, W, M, K, c0, n, fp8, w8, l, kOutSoftmaxGrad);
+        // dz of the chunk's columns: the logits recomputed, the gradient
+        // written as BF16 [M, n] or (FP8) as its E4M3 copies in 1x128 rows
+        // (for dX) and 128x1 columns (for dW), k-major scales
+        GemmProblem g = logits_problem(X, W, M, K, c0, n, fp8, w8, l, fp8 ? kOutSoftmaxGradQ : kOutSoftmaxGrad);
         g.targets = targets;
         g.lse = lse;
         g.grad_scale = grad_scale;
-        g.D = dz; g.ldd = n;
+        g.D = fp8 ? nullptr : dz; g.ldd = n;
+        if (fp8) {
+            g.q8 = w8 + l.dzq; g.q8_scale = reinterpret_cast<float*>(w8 + l.dzs);
+            g.q8t = w8 + l.dzqt; g.q8t_scale = reinterpret_cast<float*>(w8 + l.dzst);
+        }
         launch_gemm(g, nullptr, stream);
         GemmProblem gx{}, gw{};
         gx.M = M; gx.N = K; gx.K = n; gx.out = kOutF32; gx.D = dxacc; gx.ldd = K; gx.accumulate = c0 > 0;
         gw.M = n; gw.N = K; gw.K = M; gw.out = kOutF32; gw.D = dW + c0 * K; gw.ldd = K;
         if (fp8) {
-            // the chunk's dz in 1x128 rows (for dX) and 128x1 columns (for dW), k-major scales
-            QuantArgs a{};
-            a.x = dz; a.rows = M; a.cols = n; a.ld = n;
-            a.q = w8 + l.dzq; a.scale = reinterpret_cast<float*>(w8 + l.dzs);
-            a.qT = w8 + l.dzqt; a.scaleT = reinterpret_cast<float*>(w8 + l.dzst);
-            a.pow2 = 1; a.kmajor = 1;
-            launch_quantize(kE4M3, kQRow, a, stream);
             // dX += dzq [M, n] (WqT columns [c0, c0 + n)), block scales k-major
             gx.A = w8 + l.dzq; gx.lda = n; gx.fa = kE4M3; gx.sa_mode = kSRow; gx.sa_kmajor = 1;
             gx.sa = reinterpret_cast<const float*>(w8 + l.dzs);

@@ -342,25 +342,6 @@ __device__ __forceinline__ void store_transposed(const QuantArgs& a, const Tile&
     store_transposed_ct(a, t, row0, col0, ct, lds);
 }
 
-// Encode with one multiplier per column of the 8x8 block (column-grouped scales).
-template <int FMT, bool SAFE>
-__device__ __forceinline__ uint2 encode8_cols(const uint32_t w[4], const float r[8]) {
-    float v[8];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        v[2 * i] = bf16lo(w[i]) * r[2 * i];
-        v[2 * i + 1] = bf16hi(w[i]) * r[2 * i + 1];
-    }
-    uint2 out;
-    if constexpr (SAFE) {
-        out.x = encode4_safe<FMT>(v[0], v[1], v[2], v[3]);
-        out.y = encode4_safe<FMT>(v[4], v[5], v[6], v[7]);
-    } else {
-        out.x = encode4_fast<FMT>(v[0], v[1], v[2], v[3]);
-        out.y = encode4_fast<FMT>(v[4], v[5], v[6], v[7]);
-    }
-    return out;
-}
 
 // Scale of a per-tensor quantisation: s (stored) and the multiplier r, and
 // whether encoding must take the saturating path (the amax was supplied and
