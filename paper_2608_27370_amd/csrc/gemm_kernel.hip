@@ -676,24 +676,21 @@ __global__ __launch_bounds__(WM * WN * 64 * (PROD ? 2 : 1)) void gemm_fp8_kernel
             eb[it] = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(
                 rb, (uint32_t)((ncol0 + ((it * 64 + lane) % ECPR) * 4) * 2), 0, 0));
     }
-    // LM-head epilogues: the per-row values (the target's column, lse) of the
-    // wave tile's rows, one global load per lane and 64 rows issued here;
-    // each iteration below takes its row's from the owning lane by a shuffle
-    // instead of waiting on a load of its own
+    // The forward statistics' per-row target column: lane l loads that of
+    // the wave tile's row 64 j + l, which the statistics pass (one lane per
+    // row) then finds in its own register
     constexpr int NRW = (WTM + 63) / 64;
     int rtg[NRW];
-    float rls[NRW];
-    if constexpr (OUT == kOutLseStats || OUT == kOutSoftmaxGrad) {
+    if constexpr (OUT == kOutLseStats) {
         static_assert(NRW <= 2 && (RPP <= 64 || WTM <= 64), "LM-head row values: a pass stays in one 64-row group");
 #pragma unroll
         for (int j = 0; j < NRW; ++j) {
             const int64_t m = (int64_t)mrow0 + 64 * j + lane;
             const bool ok = 64 * j + lane < WTM && m < p.M;
             rtg[j] = ok ? p.targets[m] - p.col0 : INT_MIN;
-            rls[j] = (OUT == kOutSoftmaxGrad && ok) ? p.lse[m] : 0.0f;
         }
     }
-    (void)rtg; (void)rls;
+    (void)rtg;
     __syncthreads();   // every wave is done with the last stage
     // A plain BF16 output of a tile inside the matrix, 128-column wave tiles:
     // the lane rounds its sums to BF16 first and stages those, half the LDS
@@ -709,15 +706,16 @@ __global__ __launch_bounds__(WM * WN * 64 * (PROD ? 2 : 1)) void gemm_fp8_kernel
     // each lane forms dz = g (exp(z - lse) - [column == target]) from its
     // sums directly, with the lse and target column of its FM rows loaded
     // first, and rounds it to BF16, as the per-row path below does.
-    // kOutSoftmaxGradQ stages dz the same way and quantises the staged tile
-    // (below); M and N are multiples of 128, so a wave tile lies wholly
-    // inside the output or wholly outside it.
+    // Its dz kinds take every wave tile this way (M and N are multiples of
+    // 128, so a wave tile lies wholly inside the output or wholly outside):
+    // kOutSoftmaxGradQ quantises the staged tile (below).
     constexpr bool kDz = OUT == kOutSoftmaxGrad || OUT == kOutSoftmaxGradQ;
+    static_assert(!kDz || (ECPR == 32 && WTM == 128 && WTM * 256 <= REGION), "dz kinds: 128 x 128 wave tiles");
     if constexpr ((OUT == kOutBF16 || kDz) && ECPR == 32 && WTM * 256 <= REGION) {
-        if constexpr (OUT == kOutSoftmaxGradQ) {
+        if constexpr (kDz) {
             if (mrow0 + WTM > p.M || ncol0 + WTN > p.N) return;
         }
-        if (OUT == kOutSoftmaxGradQ || fast) {
+        if (kDz || fast) {
             float row_lse[kDz ? FM : 1];
             int row_tgt[kDz ? FM : 1];
             if constexpr (kDz) {
@@ -905,46 +903,6 @@ __global__ __launch_bounds__(WM * WN * 64 * (PROD ? 2 : 1)) void gemm_fp8_kernel
                     if (tc >= 0 && tc < WTN) {
                         const float* f = reinterpret_cast<const float*>(row + (((tc >> 2) ^ (r & SWZ)) << 4));
                         p.zt[m] = f[tc & 3] * alpha;
-                    }
-                }
-            }
-            return;
-        }
-        if constexpr (OUT == kOutSoftmaxGrad) {
-            // The backward's dz = g (exp(z - lse) - [column == target]) on
-            // the staged tile: a wave-tile row is 128 columns = 32 chunks, so
-            // lanes 0-31 take one row and lanes 32-63 the next, and store
-            // whole rows. The two rows' lse and target column are read from
-            // the lanes that loaded them (a uniform lane index: no LDS).
-            static_assert(ECPR == 32, "LM-head epilogues take 128-column wave tiles");
-            constexpr int RJ = (pass * RPP) / 64;
-#pragma unroll 2
-            for (int it = 0; it < IT; ++it) {
-                const int q = it * 64 + lane;
-                const int r = q / ECPR, c = q % ECPR;
-                const float4 v = *reinterpret_cast<const float4*>(ep + r * ROWB + ((c ^ (r & SWZ)) << 4));
-                const int64_t m = mrow0 + pass * RPP + r;
-                const int n = ncol0 + c * 4;
-                const int rw0 = (pass * RPP + 2 * it) & 63;             // row of lanes 0-31; lanes 32-63: + 1
-                const int t0 = __builtin_amdgcn_readlane(rtg[RJ], rw0);
-                const int t1 = __builtin_amdgcn_readlane(rtg[RJ], rw0 + 1);
-                const float l0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(rls[RJ]), rw0));
-                const float l1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(rls[RJ]), rw0 + 1));
-                const int tgt = (lane >> 5) ? t1 : t0;
-                const float l = (lane >> 5) ? l1 : l0;
-                const float e[4] = {v.x * alpha, v.y * alpha, v.z * alpha, v.w * alpha};
-                float d[4];
-#pragma unroll
-                for (int t = 0; t < 4; ++t)
-                    d[t] = p.grad_scale * (exp_f32(e[t] - l) - (n + t == tgt ? 1.0f : 0.0f));
-                if (m < p.M) {
-                    uint16_t* dst = reinterpret_cast<uint16_t*>(p.D) + m * p.ldd + n;
-                    if (n + 3 < p.N) {
-                        *reinterpret_cast<uint2*>(dst) = make_uint2(pack_bf16x2(d[0], d[1]), pack_bf16x2(d[2], d[3]));
-                    } else {
-#pragma unroll
-                        for (int t = 0; t < 4; ++t)
-                            if (n + t < p.N) dst[t] = to_bf16(d[t]);
                     }
                 }
             }

@@ -104,7 +104,8 @@ enum ScaleMode : int { kSTensor = 0, kSRow = 1, kSBlock = 2, kSNone = 3 };
 // writes BF16 dz = g (exp(z - lse) - [column == target]); kOutSoftmaxGradQ
 // writes that dz's E4M3 copies instead, in 1x128 row groups and (transposed)
 // 128x1 column groups with power-of-two scales, as the quantiser makes them
-// from the BF16 dz (E4M3 block-scaled operands; M and N multiples of 128).
+// from the BF16 dz (E4M3 block-scaled operands). Both dz kinds need M and N
+// to be multiples of 128.
 enum OutKind : int { kOutBF16 = 0, kOutF32 = 1, kOutBF16Epi = 3, kOutLseStats = 4, kOutSoftmaxGrad = 5,
                      kOutSoftmaxGradQ = 6 };
 

@@ -17,7 +17,8 @@
 // binary32) and the dW GEMM of the chunk's rows of W.
 //
 // Recipes: BF16 operands throughout (the transposed copies that the backward
-// GEMMs read, X^T and W^T, are made once per call), or the blockwise FP8
+// GEMMs read, X^T and W^T, are made once per call, and each dz chunk's),
+// or the blockwise FP8
 // recipe of Section 3.2: X in 1x128 groups (rows for the logits, columns for
 // dW), W in 128x128 blocks (the transposed copy for dX shares the block
 // scales), and each dz chunk quantised in 1x128 + 128x1 groups (by the
