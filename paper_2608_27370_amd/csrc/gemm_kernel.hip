@@ -632,6 +632,70 @@ __global__ __launch_bounds__(WM * WN * 64 * (PROD ? 2 : 1)) void gemm_fp8_kernel
     // which the epilogue reuses: let them land first
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 
+    // ---- The LM head's forward statistics, straight from the accumulators.
+    // Of each of its rows i*32 + (l & 31), lane l holds the 64 columns
+    // j*32 + 8g + 4(l >> 5) + {0..3} of the wave tile; lane l ^ 32 holds the
+    // other 64. A row's maximum and its sum of e^(z - max) over the 128
+    // columns are the lane's over its 64 sums, combined with the partner's by
+    // one exchange each: no staging, every logit read once. The exponent is
+    // one FMA, z log2(e) - max log2(e), fed to the exp2 instruction. Its
+    // rounding errs by a relative 2^-24 of |z| on each term and of |max| on
+    // all of them alike, far inside the error of a binary32 log-sum-exp.
+    if constexpr (OUT == kOutLseStats) {
+        static_assert(!PROD && FN == 4 && WTN == 128, "LM-head statistics: 128-column wave tiles");
+        const int mrow0 = m0 + wm * WTM, ncol0 = n0 + wn * WTN;
+        if (ncol0 >= p.N) return;      // a wave tile wholly past N (the ragged last tile) has no block
+        const int hl = lane >> 5;
+        // each row's target column, relative to the lane's first column of
+        // the wave tile (4 hl), or out of range
+        int tcol[FM];
+#pragma unroll
+        for (int i = 0; i < FM; ++i) {
+            const int64_t m = (int64_t)mrow0 + i * 32 + (lane & 31);
+            tcol[i] = m < p.M ? p.targets[m] - p.col0 - ncol0 - 4 * hl : INT_MIN;
+        }
+        constexpr float kLog2e = 1.44269504088896340736f;
+        static_for<FM>([&](auto i_c) __attribute__((always_inline)) {
+            constexpr int i = decltype(i_c)::value;
+            float v[FN * 16];
+#pragma unroll
+            for (int e = 0; e < FN * 16; ++e)
+                asm volatile("v_accvgpr_read_b32 %0, %1" : "=v"(v[e]) : "a"(acc[i][e / 16][e % 16]));
+            if (alpha != 1.0f) {
+#pragma unroll
+                for (int e = 0; e < FN * 16; ++e) v[e] *= alpha;
+            }
+            float mq[4] = {v[0], v[1], v[2], v[3]};
+#pragma unroll
+            for (int e = 4; e < FN * 16; ++e) mq[e % 4] = fmaxf(mq[e % 4], v[e]);
+            float mx = fmaxf(fmaxf(mq[0], mq[1]), fmaxf(mq[2], mq[3]));
+            mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+            const float m2 = mx * kLog2e;
+            float sq[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+            for (int e = 0; e < FN * 16; ++e) sq[e % 4] += __builtin_amdgcn_exp2f(fmaf(v[e], kLog2e, -m2));
+            float sum = (sq[0] + sq[1]) + (sq[2] + sq[3]);
+            sum += __shfl_xor(sum, 32, 64);
+            const int64_t m = (int64_t)mrow0 + i * 32 + (lane & 31);
+            if (hl == 0 && m < p.M) p.stats[m * p.stats_ld + ncol0 / 128] = make_float2(mx, sum);
+            // the target's logit, where this wave tile holds it: entry
+            // (j, g, t) of fragment row i is column j*32 + 8g + t past the
+            // lane's first (rare: a branch taken by the whole wave or not)
+            const int tc = tcol[i];
+            const bool mine = tc >= 0 && tc < WTN && ((tc >> 2) & 1) == 0;
+            if (__builtin_amdgcn_ballot_w64(mine)) {
+                float zt = 0.0f;
+#pragma unroll
+                for (int e = 0; e < FN * 16; ++e) {
+                    const int j = e / 16, g = (e % 16) / 4, t = e % 4;
+                    zt = tc == j * 32 + 8 * g + t ? v[e] : zt;
+                }
+                if (mine) p.zt[m] = zt;
+            }
+        });
+        return;
+    }
+
     // ---- epilogue. Lane l holds, for fragment (i, j), wave-tile row
     // i*32 + (l & 31) and columns j*32 + 8g + 4(l >> 5) + {0..3}, g = 0..3.
     // Written straight to memory that would scatter 16-byte pieces over 32
@@ -676,21 +740,6 @@ __global__ __launch_bounds__(WM * WN * 64 * (PROD ? 2 : 1)) void gemm_fp8_kernel
             eb[it] = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(
                 rb, (uint32_t)((ncol0 + ((it * 64 + lane) % ECPR) * 4) * 2), 0, 0));
     }
-    // The forward statistics' per-row target column: lane l loads that of
-    // the wave tile's row 64 j + l, which the statistics pass (one lane per
-    // row) then finds in its own register
-    constexpr int NRW = (WTM + 63) / 64;
-    int rtg[NRW];
-    if constexpr (OUT == kOutLseStats) {
-        static_assert(NRW <= 2 && (RPP <= 64 || WTM <= 64), "LM-head row values: a pass stays in one 64-row group");
-#pragma unroll
-        for (int j = 0; j < NRW; ++j) {
-            const int64_t m = (int64_t)mrow0 + 64 * j + lane;
-            const bool ok = 64 * j + lane < WTM && m < p.M;
-            rtg[j] = ok ? p.targets[m] - p.col0 : INT_MIN;
-        }
-    }
-    (void)rtg;
     __syncthreads();   // every wave is done with the last stage
     // A plain BF16 output of a tile inside the matrix, 128-column wave tiles:
     // the lane rounds its sums to BF16 first and stages those, half the LDS
@@ -870,44 +919,6 @@ __global__ __launch_bounds__(WM * WN * 64 * (PROD ? 2 : 1)) void gemm_fp8_kernel
         // writes only after this pass's reads have returned their data)
         asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
         constexpr int IT = RPP * ECPR / 64;
-        if constexpr (OUT == kOutLseStats) {
-            // The forward's per-block statistics: lane l owns wave-tile row
-            // pass * RPP + l and scans its 128 staged columns twice (the
-            // maximum, then the sum of exp(z - max)) with no cross-lane step;
-            // its row's target column comes from its own register. A wave
-            // tile wholly past N (the ragged last tile) has no block. The
-            // lanes of a 16-lane read phase hold 16 consecutive rows, whose
-            // swizzle keys differ: the reads are free of bank conflicts.
-            static_assert(ECPR == 32 && RPP == 64, "LM-head statistics: 64-row passes of 128 columns");
-            constexpr int RJ = (pass * RPP) / 64;
-            const int r = lane;
-            const int64_t m = mrow0 + pass * RPP + r;
-            if (ncol0 < p.N) {
-                const uint8_t* row = ep + r * ROWB;
-                float mx = -__builtin_inff();
-#pragma unroll 8
-                for (int c = 0; c < ECPR; ++c) {
-                    const float4 v = *reinterpret_cast<const float4*>(row + ((c ^ (r & SWZ)) << 4));
-                    mx = fmaxf(fmaxf(mx, fmaxf(v.x * alpha, v.y * alpha)), fmaxf(v.z * alpha, v.w * alpha));
-                }
-                float sum = 0.0f;
-#pragma unroll 8
-                for (int c = 0; c < ECPR; ++c) {
-                    const float4 v = *reinterpret_cast<const float4*>(row + ((c ^ (r & SWZ)) << 4));
-                    sum += (exp_f32(v.x * alpha - mx) + exp_f32(v.y * alpha - mx)) +
-                           (exp_f32(v.z * alpha - mx) + exp_f32(v.w * alpha - mx));
-                }
-                if (m < p.M) {
-                    p.stats[m * p.stats_ld + ncol0 / 128] = make_float2(mx, sum);
-                    const int tc = rtg[RJ] - ncol0;     // the target's column in this wave tile
-                    if (tc >= 0 && tc < WTN) {
-                        const float* f = reinterpret_cast<const float*>(row + (((tc >> 2) ^ (r & SWZ)) << 4));
-                        p.zt[m] = f[tc & 3] * alpha;
-                    }
-                }
-            }
-            return;
-        }
         if (fast) {
             // the residual is loaded before the LDS reads of its group of
             // iterations, so that its latency overlaps those reads and the
