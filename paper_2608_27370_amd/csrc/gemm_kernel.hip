@@ -754,7 +754,10 @@ __global__ __launch_bounds__(WM * WN * 64 * (PROD ? 2 : 1)) void gemm_fp8_kernel
     // The LM head's backward output (dz of the logits) takes the same path:
     // each lane forms dz = g (exp(z - lse) - [column == target]) from its
     // sums directly, with the lse and target column of its FM rows loaded
-    // first, and rounds it to BF16, as the per-row path below does.
+    // first, and rounds it to BF16. The exponential is 2^t (1 + c): with
+    // lse log2(e) split per row into its binary32 rounding P and the rest,
+    // t = z log2(e)_hi - P is one FMA, which rounds once as z - lse would,
+    // and 1 + c, the rest of the exponent times ln 2, is another.
     // Its dz kinds take every wave tile this way (M and N are multiples of
     // 128, so a wave tile lies wholly inside the output or wholly outside):
     // kOutSoftmaxGradQ quantises the staged tile (below).
@@ -765,17 +768,26 @@ __global__ __launch_bounds__(WM * WN * 64 * (PROD ? 2 : 1)) void gemm_fp8_kernel
             if (mrow0 + WTM > p.M || ncol0 + WTN > p.N) return;
         }
         if (kDz || fast) {
-            float row_lse[kDz ? FM : 1];
+            // per row: P = lse log2(e)_hi rounded, K = 1 - (the rest of
+            // lse log2(e)) ln 2 (rounded once), and the target's column
+            // relative to the lane's first column of the wave tile
+            constexpr float kL2eHi = 1.44269502162933349609375f;     // log2(e) rounded to binary32
+            constexpr float kL2eLo = 1.925962989e-8f;                // log2(e) - kL2eHi
+            constexpr float kLn2 = 0.693147180559945309f;
+            constexpr float kL2eLoLn2 = kL2eLo * kLn2;
+            float row_p[kDz ? FM : 1], row_k[kDz ? FM : 1];
             int row_tgt[kDz ? FM : 1];
             if constexpr (kDz) {
 #pragma unroll
                 for (int i = 0; i < FM; ++i) {
                     const int64_t m = (int64_t)mrow0 + i * 32 + (lane & 31);
-                    row_tgt[i] = p.targets[m] - p.col0;
-                    row_lse[i] = p.lse[m];
+                    row_tgt[i] = p.targets[m] - p.col0 - ncol0 - 4 * (lane >> 5);
+                    const float l = p.lse[m];
+                    row_p[i] = l * kL2eHi;
+                    row_k[i] = 1.0f - (fmaf(l, kL2eHi, -row_p[i]) + l * kL2eLo) * kLn2;
                 }
             }
-            (void)row_lse; (void)row_tgt;
+            (void)row_p; (void)row_k; (void)row_tgt;
             auto stage = [&](auto scaled) __attribute__((always_inline)) {
 #pragma unroll
                 for (int i = 0; i < FM; ++i) {
@@ -796,14 +808,16 @@ __global__ __launch_bounds__(WM * WN * 64 * (PROD ? 2 : 1)) void gemm_fp8_kernel
                                 v0 *= alpha; v1 *= alpha; v2 *= alpha; v3 *= alpha;
                             }
                             if constexpr (kDz) {
-                                // the columns of these four sums, in the chunk
-                                const int n = ncol0 + j * 32 + 8 * g + 4 * (lane >> 5);
-                                const float l = row_lse[i], gs = p.grad_scale;
-                                const int tc = row_tgt[i];
-                                v0 = gs * (exp_f32(v0 - l) - (n == tc ? 1.0f : 0.0f));
-                                v1 = gs * (exp_f32(v1 - l) - (n + 1 == tc ? 1.0f : 0.0f));
-                                v2 = gs * (exp_f32(v2 - l) - (n + 2 == tc ? 1.0f : 0.0f));
-                                v3 = gs * (exp_f32(v3 - l) - (n + 3 == tc ? 1.0f : 0.0f));
+                                // the four sums are columns j*32 + 8g + {0..3} past the
+                                // lane's first: tr is the target's position among them
+                                const int tr = row_tgt[i] - (j * 32 + 8 * g);
+                                const float P = row_p[i], K = row_k[i], gs = p.grad_scale;
+                                auto dz = [&](float z, int c) __attribute__((always_inline)) {
+                                    // 2^(z log2 e - lse log2 e) = 2^t (1 + c)
+                                    const float e = __builtin_amdgcn_exp2f(fmaf(z, kL2eHi, -P)) * fmaf(z, kL2eLoLn2, K);
+                                    return fmaf(gs, e, c == tr ? -gs : 0.0f);
+                                };
+                                v0 = dz(v0, 0); v1 = dz(v1, 1); v2 = dz(v2, 2); v3 = dz(v3, 3);
                             }
                             const int u = j * 8 + 2 * g + (lane >> 5);
                             *reinterpret_cast<uint2*>(ep + r * 256 + ((u ^ (2 * (r & 15))) << 3)) =
