@@ -788,9 +788,11 @@ __global__ __launch_bounds__(WM * WN * 64 * (PROD ? 2 : 1)) void gemm_fp8_kernel
                 }
             }
             (void)row_p; (void)row_k; (void)row_tgt;
-            auto stage = [&](auto scaled) __attribute__((always_inline)) {
-#pragma unroll
-                for (int i = 0; i < FM; ++i) {
+            // one fragment row i of the wave tile; `onehot` when some lane's
+            // row has its target among the lane's columns of this wave tile
+            // (a few rows in a hundred), else dz is g e throughout
+            auto stage_row = [&](auto scaled, auto onehot, int i) __attribute__((always_inline)) {
+                {
                     const int r = i * 32 + (lane & 31);
 #pragma unroll
                     for (int j = 0; j < FN; ++j) {
@@ -815,7 +817,8 @@ __global__ __launch_bounds__(WM * WN * 64 * (PROD ? 2 : 1)) void gemm_fp8_kernel
                                 auto dz = [&](float z, int c) __attribute__((always_inline)) {
                                     // 2^(z log2 e - lse log2 e) = 2^t (1 + c)
                                     const float e = __builtin_amdgcn_exp2f(fmaf(z, kL2eHi, -P)) * fmaf(z, kL2eLoLn2, K);
-                                    return fmaf(gs, e, c == tr ? -gs : 0.0f);
+                                    if constexpr (decltype(onehot)::value) return fmaf(gs, e, c == tr ? -gs : 0.0f);
+                                    else return gs * e;
                                 };
                                 v0 = dz(v0, 0); v1 = dz(v1, 1); v2 = dz(v2, 2); v3 = dz(v3, 3);
                             }
@@ -826,6 +829,21 @@ __global__ __launch_bounds__(WM * WN * 64 * (PROD ? 2 : 1)) void gemm_fp8_kernel
                         // one fragment at a time: otherwise every accumulator
                         // is read into VGPRs before the first write
                         __builtin_amdgcn_sched_barrier(0);
+                    }
+                }
+            };
+            auto stage = [&](auto scaled) __attribute__((always_inline)) {
+#pragma unroll
+                for (int i = 0; i < FM; ++i) {
+                    if constexpr (kDz) {
+                        // set for the lane that holds its row's target (and
+                        // maybe for its partner lane): a wave-uniform branch
+                        if (__builtin_amdgcn_ballot_w64((unsigned)row_tgt[i] < (unsigned)WTN))
+                            stage_row(scaled, std::true_type{}, i);
+                        else
+                            stage_row(scaled, std::false_type{}, i);
+                    } else {
+                        stage_row(scaled, std::false_type{}, i);
                     }
                 }
             };
