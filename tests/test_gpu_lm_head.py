@@ -128,15 +128,9 @@ def run(P, X, W, t, recipe, g=1.0, lse_in=None):
     return host(lse), host(loss), dX, dW
 
 
-@pytest.mark.parametrize("recipe", [BF16, FP8], ids=["bf16", "fp8"])
-@pytest.mark.parametrize("M,V,K", [(256, 1152, 256), (128, 256, 384)])
-def test_lm_head_small(P, recipe, M, V, K):
-    """Every output of a small case; V = 1152 leaves the last 256-wide tile
-    half empty."""
-    X = inputs.case(81, (M, K), kind="student_t")
-    W = inputs.case(82, (V, K), std=0.05)
-    t = inputs.rng(0, 99, 83).integers(0, V, M)
-    g = 1.0 / M
+def check_small(P, X, W, t, recipe, g):
+    """lse and loss of every row, and every entry of dX and dW, against the
+    oracle's float64 values within the allowances of a binary32 evaluation."""
     lse_k, loss_k, dX, dW = run(P, X, W, t, recipe, g)
     ops = Operands(X, W, recipe)
     z, S, slack = ops.logits()
@@ -158,6 +152,40 @@ def test_lm_head_small(P, recipe, M, V, K):
     extra = ww @ np.abs(ops.xt) + truncation_max(cw, lambda q, s: mfma_model.truncation_loss_full(
         q, fp8.E4M3, s, "row", ops.xqT, fp8.E4M3, ops.xsT, "row"))
     check_fp32(host(dW), ref, den, what="lm_head %s dW" % name, slack=extra)
+
+
+@pytest.mark.parametrize("recipe", [BF16, FP8], ids=["bf16", "fp8"])
+@pytest.mark.parametrize("M,V,K", [(256, 1152, 256), (128, 256, 384)])
+def test_lm_head_small(P, recipe, M, V, K):
+    """Every output of a small case; V = 1152 leaves the last 256-wide tile
+    half empty."""
+    X = inputs.case(81, (M, K), kind="student_t")
+    W = inputs.case(82, (V, K), std=0.05)
+    t = inputs.rng(0, 99, 83).integers(0, V, M)
+    check_small(P, X, W, t, recipe, 1.0 / M)
+
+
+@pytest.mark.parametrize("recipe", [BF16, FP8], ids=["bf16", "fp8"])
+def test_lm_head_target_positions(P, recipe):
+    """Targets placed at every kind of column position rather than at random:
+    in each 8-column group the first and last column of both 4-column halves
+    (the two lanes that hold a row's columns), the first and last column of a
+    128-column block, of a 256-column tile and of the vocabulary, and every
+    column of one 8-column group. Rows 0-127 spread their targets over all
+    blocks; rows 128-255 put the targets of a whole 32-row fragment into one
+    block (so several rows of a fragment meet their target in the same place)
+    and leave other fragments with none in most blocks."""
+    M, V, K = 256, 640, 128
+    X = inputs.case(86, (M, K), kind="student_t")
+    W = inputs.case(87, (V, K), std=0.05)
+    pos = [0, 3, 4, 7, 8, 11, 12, 15, 120, 123, 124, 127, 128, 131, 132, 255, 256, 259, 260, 383, 384,
+           511, 512, 636, 637, 638, 639] + list(range(136, 144))
+    t = np.empty(M, np.int64)
+    t[:128] = [pos[i % len(pos)] for i in range(128)]
+    for f in range(4):                       # rows 128 + 32 f .. : one block per fragment
+        base = (f % 5) * 128
+        t[128 + 32 * f: 160 + 32 * f] = base + (np.arange(32) * 5) % 128
+    check_small(P, X, W, t, recipe, 1.0 / M)
 
 
 def test_lm_head_targets_outside_give_nan(P):
