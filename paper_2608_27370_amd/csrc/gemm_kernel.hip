@@ -763,7 +763,7 @@ __global__ __launch_bounds__(WM * WN * 64 * (PROD ? 2 : 1)) void gemm_fp8_kernel
     // kOutSoftmaxGradQ quantises the staged tile (below).
     constexpr bool kDz = OUT == kOutSoftmaxGrad || OUT == kOutSoftmaxGradQ;
     static_assert(!kDz || (ECPR == 32 && WTM == 128 && WTM * 256 <= REGION), "dz kinds: 128 x 128 wave tiles");
-    if constexpr ((OUT == kOutBF16 || kDz) && ECPR == 32 && WTM * 256 <= REGION) {
+    if constexpr ((OUT == kOutBF16 || OUT == kOutBF16Epi || kDz) && ECPR == 32 && WTM * 256 <= REGION) {
         if constexpr (kDz) {
             if (mrow0 + WTM > p.M || ncol0 + WTN > p.N) return;
         }
@@ -788,10 +788,42 @@ __global__ __launch_bounds__(WM * WN * 64 * (PROD ? 2 : 1)) void gemm_fp8_kernel
                 }
             }
             (void)row_p; (void)row_k; (void)row_tgt;
+            // The bias / residual epilogue in the same one pass: the wave's
+            // residual block arrives in its LDS region by DMA, each 16-byte
+            // chunk already where the staged output chunk will sit (the lane
+            // that lands chunk position q of row r loads the residual's chunk
+            // q ^ (r & 15)); the lane then reads the four residual values of
+            // each of its output units there, forms alpha acc + bias + rs
+            // residual in binary32 with one rounding to BF16, and writes the
+            // result over them. The bias of the lane's 64 columns is loaded
+            // into registers once.
+            uint2 bq[OUT == kOutBF16Epi ? FN * 4 : 1];
+            if constexpr (OUT == kOutBF16Epi) {
+                if (p.bias) {
+                    const __amdgpu_buffer_rsrc_t rbq = __builtin_amdgcn_make_buffer_rsrc(
+                        const_cast<uint16_t*>(p.bias), 0, p.N * 2, 0x00020000);
+#pragma unroll
+                    for (int e = 0; e < FN * 4; ++e)
+                        bq[e] = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(
+                            rbq, (uint32_t)((ncol0 + (e / 4) * 32 + 8 * (e % 4) + 4 * (lane >> 5)) * 2), 0, 0));
+                }
+                if (p.residual) {
+                    const v4i rr = make_rsrc(p.residual + (int64_t)mrow0 * p.ldr + ncol0,
+                                             (uint32_t)((WTM - 1) * p.ldr * 2 + WTN * 2));
+                    const uint32_t ep_lds = smem_lds + wave * REGION;
+#pragma unroll
+                    for (int q = 0; q < WTM / 4; ++q) {          // 1 KB: four rows of 256 bytes
+                        const int r = q * 4 + (lane >> 4), c = (lane & 15) ^ (r & 15);
+                        dma_to_lds<16>(rr, ep_lds + q * 1024, (uint32_t)((r * p.ldr + c * 8) * 2));
+                    }
+                }
+                asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+            }
+            (void)bq;
             // one fragment row i of the wave tile; `onehot` when some lane's
             // row has its target among the lane's columns of this wave tile
             // (a few rows in a hundred), else dz is g e throughout
-            auto stage_row = [&](auto scaled, auto onehot, int i) __attribute__((always_inline)) {
+            auto stage_row = [&](auto scaled, auto onehot, auto epi, int i) __attribute__((always_inline)) {
                 {
                     const int r = i * 32 + (lane & 31);
 #pragma unroll
@@ -823,8 +855,21 @@ __global__ __launch_bounds__(WM * WN * 64 * (PROD ? 2 : 1)) void gemm_fp8_kernel
                                 v0 = dz(v0, 0); v1 = dz(v1, 1); v2 = dz(v2, 2); v3 = dz(v3, 3);
                             }
                             const int u = j * 8 + 2 * g + (lane >> 5);
-                            *reinterpret_cast<uint2*>(ep + r * 256 + ((u ^ (2 * (r & 15))) << 3)) =
-                                make_uint2(pack_bf16x2(v0, v1), pack_bf16x2(v2, v3));
+                            uint2* const pos = reinterpret_cast<uint2*>(ep + r * 256 + ((u ^ (2 * (r & 15))) << 3));
+                            if constexpr (OUT == kOutBF16Epi) {
+                                // each term only when given: adding +0 would turn a -0 sum into +0
+                                if constexpr ((decltype(epi)::value & 1) != 0) {
+                                    const uint2 b = bq[j * 4 + g];
+                                    v0 += bf16lo(b.x); v1 += bf16hi(b.x); v2 += bf16lo(b.y); v3 += bf16hi(b.y);
+                                }
+                                if constexpr ((decltype(epi)::value & 2) != 0) {
+                                    const uint2 rv = *pos;
+                                    const float rs = p.res_scale;
+                                    v0 = fmaf(rs, bf16lo(rv.x), v0); v1 = fmaf(rs, bf16hi(rv.x), v1);
+                                    v2 = fmaf(rs, bf16lo(rv.y), v2); v3 = fmaf(rs, bf16hi(rv.y), v3);
+                                }
+                            }
+                            *pos = make_uint2(pack_bf16x2(v0, v1), pack_bf16x2(v2, v3));
                         }
                         // one fragment at a time: otherwise every accumulator
                         // is read into VGPRs before the first write
@@ -832,23 +877,35 @@ __global__ __launch_bounds__(WM * WN * 64 * (PROD ? 2 : 1)) void gemm_fp8_kernel
                     }
                 }
             };
-            auto stage = [&](auto scaled) __attribute__((always_inline)) {
+            auto stage = [&](auto scaled, auto epi) __attribute__((always_inline)) {
 #pragma unroll
                 for (int i = 0; i < FM; ++i) {
                     if constexpr (kDz) {
                         // set for the lane that holds its row's target (and
                         // maybe for its partner lane): a wave-uniform branch
                         if (__builtin_amdgcn_ballot_w64((unsigned)row_tgt[i] < (unsigned)WTN))
-                            stage_row(scaled, std::true_type{}, i);
+                            stage_row(scaled, std::true_type{}, epi, i);
                         else
-                            stage_row(scaled, std::false_type{}, i);
+                            stage_row(scaled, std::false_type{}, epi, i);
                     } else {
-                        stage_row(scaled, std::false_type{}, i);
+                        stage_row(scaled, std::false_type{}, epi, i);
                     }
                 }
             };
-            if (alpha == 1.0f) stage(std::false_type{});
-            else stage(std::true_type{});
+            // epi: bit 0 a bias, bit 1 a residual (bias / residual epilogue only)
+            auto stage_epi = [&](auto epi) __attribute__((always_inline)) {
+                if (alpha == 1.0f) stage(std::false_type{}, epi);
+                else stage(std::true_type{}, epi);
+            };
+            if constexpr (OUT == kOutBF16Epi) {
+                const int which = (p.bias ? 1 : 0) | (p.residual ? 2 : 0);
+                if (which == 3) stage_epi(std::integral_constant<int, 3>{});
+                else if (which == 2) stage_epi(std::integral_constant<int, 2>{});
+                else if (which == 1) stage_epi(std::integral_constant<int, 1>{});
+                else stage_epi(std::integral_constant<int, 0>{});
+            } else {
+                stage_epi(std::integral_constant<int, 0>{});
+            }
             // the region belongs to this wave alone
             asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
             if constexpr (OUT == kOutSoftmaxGradQ) {
