@@ -718,14 +718,14 @@ __global__ __launch_bounds__(WM * WN * 64 * (PROD ? 2 : 1)) void gemm_fp8_kernel
     const int mrow0 = m0 + wm * WTM;
     const int ncol0 = n0 + wn * WTN;
     float* const part = p.partial + (int64_t)ks * p.M * p.N;
-    // a tile inside the matrix whose sums overwrite the output stores whole
-    // 4-column vectors everywhere: a branch-free path that issues all of a
-    // pass's LDS reads before its stores
+    // a tile inside the matrix whose sums overwrite the output (or, binary32,
+    // add to it) stores whole 4-column vectors everywhere: a branch-free path
+    // that issues all of a pass's LDS reads before its stores
     constexpr int ES = (OUT == kOutF32 || OUT == 2) ? 4 : 2;    // bytes per output element
     const int64_t ldo = OUT == 2 ? (int64_t)p.N : p.ldd;          // output pitch (elements)
     // (and whose rows, and residual rows, lie within 2^31 bytes of its first:
     // the fast path addresses them with 32-bit buffer offsets)
-    const bool fast = m0 + BM <= p.M && n0 + BN <= p.N && (OUT == 2 || !p.accumulate) &&
+    const bool fast = m0 + BM <= p.M && n0 + BN <= p.N && (OUT == 2 || OUT == kOutF32 || !p.accumulate) &&
                       (int64_t)WTM * ldo * ES <= INT32_MAX &&
                       (OUT != kOutBF16Epi || (int64_t)WTM * p.ldr * 2 <= INT32_MAX);
     // the bias of the lane's columns in the fast path below: lane chunk
@@ -1016,66 +1016,93 @@ __global__ __launch_bounds__(WM * WN * 64 * (PROD ? 2 : 1)) void gemm_fp8_kernel
             // traffic). Groups of at most 16 iterations keep the residual and
             // the staged values in registers beside the accumulators of the
             // passes still to come.
-            constexpr int EG = (OUT == kOutBF16Epi && IT > 16) ? IT / 2 : IT;
-            static_assert(IT % EG == 0 && EG % FP == 0, "epilogue groups");
+            // With ACC (binary32 output added to what D holds) each group
+            // first loads the outputs it replaces, with the stores' own
+            // addressing, in the same place as the residual.
+            auto run_groups = [&](auto acc_c) __attribute__((always_inline)) {
+                constexpr bool ACC = decltype(acc_c)::value;
+                constexpr int EG = ((OUT == kOutBF16Epi || ACC) && IT > 16) ? IT / 2 : IT;
+                static_assert(IT % EG == 0 && EG % FP == 0, "epilogue groups");
+                typedef unsigned int v4a __attribute__((ext_vector_type(4)));
 #pragma unroll
-            for (int g0 = 0; g0 < IT; g0 += EG) {
-                uint2 er[OUT == kOutBF16Epi ? EG : 1];
-                if constexpr (OUT == kOutBF16Epi) {
-#pragma unroll
-                    for (int e = 0; e < EG; ++e) {
-                        const int u = (g0 + e) / FP, vv = (g0 + e) % FP;
-                        er[e] = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(
-                            rres, (int)roff[vv], (int)((pass * RPP + u * FR) * rrow_bytes), 0));
-                    }
-                }
-                float4 v[EG];
-#pragma unroll
-                for (int e = 0; e < EG; ++e) {
-                    const int u = (g0 + e) / FP, vv = (g0 + e) % FP, ph = u % NPH;
-                    v[e] = *reinterpret_cast<const float4*>(ep + laddr[ph][vv] + (u - ph) * FR * ROWB);
-                }
-                if constexpr (OUT != 2) {
-                    if (alpha != 1.0f) {
+                for (int g0 = 0; g0 < IT; g0 += EG) {
+                    v4a ea[ACC ? EG : 1];
+                    if constexpr (ACC) {
 #pragma unroll
                         for (int e = 0; e < EG; ++e) {
-                            v[e].x *= alpha; v[e].y *= alpha; v[e].z *= alpha; v[e].w *= alpha;
+                            const int u = (g0 + e) / FP, vv = (g0 + e) % FP;
+                            ea[e] = __builtin_bit_cast(v4a, __builtin_amdgcn_raw_buffer_load_b128(
+                                rd, (int)goff[vv], (int)((pass * RPP + u * FR) * row_bytes), 0));
                         }
                     }
-                }
-                // AUX 2 is the buffer store's non-temporal bit
-                auto store_group = [&](auto nt_c) __attribute__((always_inline)) {
-                    constexpr int AUX = decltype(nt_c)::value ? 2 : 0;
+                    (void)ea;
+                    uint2 er[OUT == kOutBF16Epi ? EG : 1];
+                    if constexpr (OUT == kOutBF16Epi) {
+#pragma unroll
+                        for (int e = 0; e < EG; ++e) {
+                            const int u = (g0 + e) / FP, vv = (g0 + e) % FP;
+                            er[e] = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(
+                                rres, (int)roff[vv], (int)((pass * RPP + u * FR) * rrow_bytes), 0));
+                        }
+                    }
+                    float4 v[EG];
 #pragma unroll
                     for (int e = 0; e < EG; ++e) {
-                        const int u = (g0 + e) / FP, vv = (g0 + e) % FP;
-                        const int soff = (int)((pass * RPP + u * FR) * row_bytes);
-                        float4 w = v[e];
-                        if constexpr (OUT == kOutBF16Epi) {
-                            // each term only when given: adding +0 would turn a -0 sum into +0
-                            if (p.bias) {
-                                const uint2 b = eb[vv];
-                                w.x += bf16lo(b.x); w.y += bf16hi(b.x); w.z += bf16lo(b.y); w.w += bf16hi(b.y);
+                        const int u = (g0 + e) / FP, vv = (g0 + e) % FP, ph = u % NPH;
+                        v[e] = *reinterpret_cast<const float4*>(ep + laddr[ph][vv] + (u - ph) * FR * ROWB);
+                    }
+                    if constexpr (OUT != 2) {
+                        if (alpha != 1.0f) {
+#pragma unroll
+                            for (int e = 0; e < EG; ++e) {
+                                v[e].x *= alpha; v[e].y *= alpha; v[e].z *= alpha; v[e].w *= alpha;
                             }
-                            if (p.residual) {
-                                const uint2 rv = er[e];
-                                const float rs = p.res_scale;
-                                w.x = fmaf(rs, bf16lo(rv.x), w.x); w.y = fmaf(rs, bf16hi(rv.x), w.y);
-                                w.z = fmaf(rs, bf16lo(rv.y), w.z); w.w = fmaf(rs, bf16hi(rv.y), w.w);
-                            }
-                        }
-                        if constexpr (ES == 4) {
-                            typedef unsigned int v4u __attribute__((ext_vector_type(4)));
-                            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4u, w), rd, (int)goff[vv], soff, AUX);
-                        } else {
-                            typedef unsigned int v2u __attribute__((ext_vector_type(2)));
-                            __builtin_amdgcn_raw_buffer_store_b64(v2u{pack_bf16x2(w.x, w.y), pack_bf16x2(w.z, w.w)}, rd,
-                                                                  (int)goff[vv], soff, AUX);
                         }
                     }
-                };
-                if (OUT != 2 && p.nt_out) store_group(std::true_type{});
-                else store_group(std::false_type{});
+                    // AUX 2 is the buffer store's non-temporal bit
+                    auto store_group = [&](auto nt_c) __attribute__((always_inline)) {
+                        constexpr int AUX = decltype(nt_c)::value ? 2 : 0;
+#pragma unroll
+                        for (int e = 0; e < EG; ++e) {
+                            const int u = (g0 + e) / FP, vv = (g0 + e) % FP;
+                            const int soff = (int)((pass * RPP + u * FR) * row_bytes);
+                            float4 w = v[e];
+                            if constexpr (OUT == kOutBF16Epi) {
+                                // each term only when given: adding +0 would turn a -0 sum into +0
+                                if (p.bias) {
+                                    const uint2 b = eb[vv];
+                                    w.x += bf16lo(b.x); w.y += bf16hi(b.x); w.z += bf16lo(b.y); w.w += bf16hi(b.y);
+                                }
+                                if (p.residual) {
+                                    const uint2 rv = er[e];
+                                    const float rs = p.res_scale;
+                                    w.x = fmaf(rs, bf16lo(rv.x), w.x); w.y = fmaf(rs, bf16hi(rv.x), w.y);
+                                    w.z = fmaf(rs, bf16lo(rv.y), w.z); w.w = fmaf(rs, bf16hi(rv.y), w.w);
+                                }
+                            }
+                            if constexpr (ES == 4) {
+                                if constexpr (ACC) {
+                                    const float4 o = __builtin_bit_cast(float4, ea[e]);
+                                    w.x += o.x; w.y += o.y; w.z += o.z; w.w += o.w;
+                                }
+                                typedef unsigned int v4u __attribute__((ext_vector_type(4)));
+                                __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4u, w), rd, (int)goff[vv], soff, AUX);
+                            } else {
+                                typedef unsigned int v2u __attribute__((ext_vector_type(2)));
+                                __builtin_amdgcn_raw_buffer_store_b64(v2u{pack_bf16x2(w.x, w.y), pack_bf16x2(w.z, w.w)}, rd,
+                                                                      (int)goff[vv], soff, AUX);
+                            }
+                        }
+                    };
+                    if (OUT != 2 && p.nt_out) store_group(std::true_type{});
+                    else store_group(std::false_type{});
+                }
+            };
+            if constexpr (OUT == kOutF32) {
+                if (p.accumulate) run_groups(std::true_type{});
+                else run_groups(std::false_type{});
+            } else {
+                run_groups(std::false_type{});
             }
             return;
         }
