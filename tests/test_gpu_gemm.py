@@ -319,10 +319,13 @@ def test_gemm_epilogue(P, shape, terms):
 
 
 # The epilogue on the tile configurations the shapes above do not reach:
-# 256x192 (bias repeating with period 3 over a lane's store iterations), and
-# 128x128 with a 4-deep ring and producer waves, alone and split over K.
+# 256x256 (the one-pass BF16 staging, whose residual block arrives in LDS by
+# DMA before the tile's stores: here in place on D), 256x192 (bias repeating
+# with period 3 over a lane's store iterations), and 128x128 with a 4-deep
+# ring and producer waves, alone and split over K.
 EPI_TILE_CASES = [
     # (M, N, K, tile_m, tile_n, stages, splits, in_place, full_tiles)
+    (4096, 4096, 512, 256, 256, 2, 1, True, True),
     (8192, 1536, 1536, 256, 192, 2, 1, True, True),
     (2048, 1536, 2048, 128, 128, 4, 1, False, True),
     (1024, 768, 8192, 128, 128, 4, 4, True, False),
