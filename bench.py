@@ -592,7 +592,7 @@ class LmHead:
                                   "1x128 + 128x1, E4M3, power-of-two scales" if fp8 else
                                   "BF16 operands, binary32 accumulation, dz BF16"),
                        "logits": "never stored: forward reduces them to (max, sum exp) per 128-column block in "
-                                 "the GEMM epilogue; backward recomputes them per 16384-column chunk"}
+                                 "the GEMM epilogue; backward recomputes them per 8192-column chunk"}
 
     def step(self):
         P = self.P
@@ -608,7 +608,7 @@ class LmHead:
                  (", X and W quantised" if self.dtype == "fp8" else ""),
                  lambda: P.lm_head_ce_fwd(self.X, self.W, self.t, self.recipe, lse=self.lse, loss=self.loss,
                                           ws=self.wsf), flops=fl, launches=0, peak=self.peak),
-            Call("bwd", "backward: per 16384-column chunk the logits GEMM with the softmax-gradient epilogue, "
+            Call("bwd", "backward: per 8192-column chunk the logits GEMM with the softmax-gradient epilogue, "
                  "then dX and dW GEMMs (4 M V K executed, 4 M V K counted)",
                  lambda: P.lm_head_ce_bwd(self.X, self.W, self.t, self.lse, self.recipe, grad_scale=1.0 / M,
                                           dX=self.dX, dW=self.dW, ws=self.wsb), flops=2 * fl, launches=0,

@@ -373,7 +373,7 @@ puro_status puro_linear_bwd(const uint16_t* dY, const puro_linear_saved* saved,
  *             dW = dz^T X (FP32 [V, K], overwritten)
  * The logits are never stored: the forward reduces each 128-column block of
  * the GEMM's output tile to (max, sum exp) in its epilogue; the backward
- * recomputes the logits in chunks of 16384 vocabulary columns and writes only
+ * recomputes the logits in chunks of 8192 vocabulary columns and writes only
  * the chunk's dz to the workspace (BF16; under PURO_LM_HEAD_FP8 its E4M3
  * copies, in 1x128 row and 128x1 column groups, made in the same epilogue).
  * g is the loss's upstream gradient (1 for the sum over tokens, 1/M for

@@ -194,8 +194,11 @@ void mirror_lower_bf16(uint16_t* A, int64_t R, int64_t ld, int tg, hipStream_t s
 
 // ---- LM head with cross-entropy (lm_head.hip) ---------------------------------
 
-// Vocabulary columns per chunk of the backward pass.
-constexpr int64_t kLmChunk = 16384;
+// Vocabulary columns per chunk of the backward pass: a chunk's dz copies
+// (2 bytes per logit under FP8, at M 8192 128 MB) then stay within the 256 MB
+// last-level cache between the epilogue that writes them and the dX and dW
+// GEMMs that read them.
+constexpr int64_t kLmChunk = 8192;
 int64_t lm_head_chunk(int64_t V);
 // Workspace of the forward (bwd false) or backward pass; fp8: the blockwise
 // FP8 recipe, else BF16 operands. M, V, K multiples of 128.

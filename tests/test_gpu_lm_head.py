@@ -203,7 +203,7 @@ def test_lm_head_targets_outside_give_nan(P):
 @pytest.mark.timeout(1500)
 @pytest.mark.parametrize("recipe", [BF16, FP8], ids=["bf16", "fp8"])
 def test_lm_head_full_size(P, recipe):
-    """M 8192 tokens, V 151936, K 1536 (the vocabulary walked in nine full
+    """M 8192 tokens, V 151936, K 1536 (the vocabulary walked in 18 full
     chunks and a narrower last one): X Student-t(3), W ~ N(0, 0.02^2),
     uniform targets, grad_scale 1 (the sum over tokens).
 
